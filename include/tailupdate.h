@@ -1,0 +1,245 @@
+/*
+ * tailupdate.h - C ABI of the true-tail hybrid-state update for MI355X (gfx950).
+ *
+ * A character context is the state (A_t, R_t, p_t) of the paper's Section 4.1:
+ * the live attention KV cache of every attention layer, the recurrent state of
+ * every gated delta-rule layer, and the next position id (the cursor). An
+ * update removes the direct KV of superseded records (Eq. 2) and runs the
+ * replacement tokens at the true tail: rotary positions p_t, p_t + 1, ...,
+ * attention over the surviving plus new KV, and the recurrence continuing from
+ * the carried state (Eq. 3). Section 4.2 fixes the bookkeeping: deletion ranges
+ * are verified against the live spans first, removed positions become holes
+ * (no placeholder rows), keys are never rotated back, and the cursor keeps
+ * growing independently of the live length.
+ *
+ * Conventions for every call below
+ *  - Device buffers are caller-owned; the library never allocates or frees
+ *    device memory. Scratch memory is a caller-supplied workspace of at least
+ *    the size returned by the matching *_workspace_size function (256-byte
+ *    aligned), reused freely by the library within a call.
+ *  - bf16 tensors are passed as `void*` to 16-bit bfloat16 storage.
+ *  - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued
+ *    asynchronously; calls on one context must be ordered by the caller's
+ *    stream. Nothing here synchronises the device.
+ *  - Every check happens on the host before anything is enqueued: an error
+ *    return leaves all device buffers and all host metadata unchanged.
+ *  - Status codes: TU_OK (0) or a negative TU_ERR_*; tu_last_error() returns a
+ *    thread-local message for the last failure of the calling thread.
+ */
+#ifndef TAILUPDATE_H
+#define TAILUPDATE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TU_ABI_VERSION 1
+
+#define TU_OK 0
+#define TU_ERR_ARG (-1)       /* null pointer, unsupported or inconsistent shape */
+#define TU_ERR_RANGE (-2)     /* deletion range not sorted/disjoint/non-empty/live/below cursor */
+#define TU_ERR_CAPACITY (-3)  /* surviving + tail rows exceed the cache capacity, or interval list full */
+#define TU_ERR_WORKSPACE (-4) /* workspace missing or smaller than required */
+#define TU_ERR_HIP (-5)       /* a HIP launch failed */
+
+#define TU_MAX_RANGES 128     /* deletion ranges per context per call */
+
+#define TU_LAYER_ATTN 0
+#define TU_LAYER_DELTA 1
+
+/* Half-open interval [begin, end) of position ids. */
+typedef struct tu_interval {
+  int64_t begin;
+  int64_t end;
+} tu_interval;
+
+/*
+ * One character context (Section 4.1 state; D3/D4 bookkeeping of Section 4.2).
+ * Host-side metadata plus the device position array. Cache rows [0, len) hold
+ * the live tokens in increasing position order; `live` lists their positions
+ * as sorted, disjoint, non-adjacent intervals whose total length is `len`.
+ */
+typedef struct tu_seq {
+  int64_t len;        /* live rows */
+  int64_t capacity;   /* rows allocated in d_pos and in each K/V buffer of this context */
+  int64_t next_pos;   /* cursor p_t; every live position is below it */
+  tu_interval* live;  /* host array [live_cap] */
+  int32_t n_live;     /* intervals in use */
+  int32_t live_cap;   /* intervals allocated */
+  int32_t* d_pos;     /* device int32 [capacity]: position id of each cache row */
+} tu_seq;
+
+/*
+ * Attention-layer shape. Query head h reads KV head h / (n_q_heads / n_kv_heads).
+ * head_dim must be 64 or 256; rotary_dim even, 0 <= rotary_dim <= head_dim
+ * (rotate-half pairs (j, j + rotary_dim/2), angle pos * rope_theta^(-2j/rotary_dim)).
+ * kv_splits = 0 lets the library split the key range for occupancy; a positive
+ * value forces that many splits (results are the same up to rounding).
+ */
+typedef struct tu_attn_params {
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t rotary_dim;
+  double rope_theta;
+  float softmax_scale;
+  int32_t kv_splits;
+} tu_attn_params;
+
+/*
+ * Gated delta-rule layer shape (Gated DeltaNet, cited in Section 4.1).
+ * Value head h reads key/query head h / (n_v_heads / n_k_heads).
+ * d_k = d_v in {64, 128}; chunk in {16, 32, 64}. `scale` multiplies S q.
+ */
+typedef struct tu_delta_params {
+  int32_t n_k_heads;
+  int32_t n_v_heads;
+  int32_t d_k;
+  int32_t d_v;
+  int32_t chunk;
+  float scale;
+} tu_delta_params;
+
+/* ABI version (TU_ABI_VERSION) and the calling thread's last error message. */
+int tu_abi_version(void);
+const char* tu_last_error(void);
+
+/*
+ * Range verification (Section 4.2; host only, no device access).
+ * ranges: host int64 [n_ranges][2] half-open position ranges. Accepts iff the
+ * ranges are non-empty, sorted, pairwise disjoint, below seq->next_pos and each
+ * lies entirely inside the live positions of `seq`. Writes the number of
+ * removed rows to *n_removed (may be NULL). Returns TU_OK or TU_ERR_RANGE /
+ * TU_ERR_ARG.
+ */
+int tu_validate_ranges(const tu_seq* seq, const int64_t* ranges, int32_t n_ranges,
+                       int64_t* n_removed);
+
+/*
+ * KV invalidation, Eq. 2 (Section 4.1) with the Section 4.2 bookkeeping.
+ * Removes the rows whose positions fall in `ranges` from every attention layer
+ * of one context, keeping the surviving rows in order and bit-identical.
+ *  k_layers, v_layers: host arrays [n_layers] of device bf16 [capacity][n_kv_heads][head_dim].
+ *  src_index: optional device int32 [>= seq->len]; on success entry j (< new len)
+ *             holds the old row index of the j-th surviving row. May be NULL.
+ * On success seq->len and seq->live are updated; seq->next_pos is unchanged.
+ * The device kernels compute the keep mask from d_pos, turn it into offsets by
+ * wavefront prefix sums, and move only the rows behind the first hole, in place.
+ */
+size_t compact_kv_workspace_size(int64_t len, int32_t n_layers, int32_t n_kv_heads, int32_t head_dim);
+int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_t n_layers,
+               int32_t n_kv_heads, int32_t head_dim, const int64_t* ranges, int32_t n_ranges,
+               int32_t* src_index, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * True-tail attention of one layer, Eq. 3 (Section 4.1): rotary embedding of the
+ * T tail tokens at positions seq->next_pos + i (angles in float64, results
+ * rounded to bf16 round-to-nearest-even), append of the rotated keys and the
+ * values at cache rows [seq->len, seq->len + T) (and their positions in d_pos),
+ * then causal grouped-query softmax attention: tail row i attends to cache rows
+ * 0 .. seq->len + i.
+ *  q: device bf16 [T][n_q_heads][head_dim]; k, v: device bf16 [T][n_kv_heads][head_dim]
+ *     (k before rotation).
+ *  out: device fp32 [T][n_q_heads][head_dim].
+ *  q_hat: optional device bf16 [T][n_q_heads][head_dim] receiving the rotated queries.
+ * Does not change `seq` (several layers share one context): call commit_tail once
+ * after the last layer, or use update_layer_stack.
+ */
+size_t tail_prefill_attention_workspace_size(const tu_attn_params* p, int64_t T, int64_t len);
+int tail_prefill_attention(const tu_seq* seq, void* k_cache, void* v_cache, const tu_attn_params* p,
+                           const void* q, const void* k, const void* v, int64_t T, float* out,
+                           void* q_hat, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Advance a context by T appended tokens: len += T, live gains [next_pos, next_pos+T),
+ * next_pos += T (Section 4.2: the cursor grows by every appended token). Host only. */
+int commit_tail(tu_seq* seq, int64_t T);
+
+/*
+ * Recurrence continuation, Eq. 3 for a gated delta-rule layer: from the carried
+ * state, for each tail token t
+ *   S <- g_t * S (I - beta_t k_t k_t^T) + beta_t v_t k_t^T,   o_t = scale * S q_t,
+ * evaluated in chunks of p->chunk tokens (chunk-parallel WY preparation, then a
+ * sequential chain over chunks with the fp32 state held on chip).
+ *  state: device fp32 [n_v_heads][d_v][d_k], updated in place.
+ *  q, k:  device bf16 [T][n_k_heads][d_k];  v: device bf16 [T][n_v_heads][d_v].
+ *  beta, g: device fp32 [T][n_v_heads];  out: device fp32 [T][n_v_heads][d_v].
+ */
+size_t delta_rule_continue_workspace_size(const tu_delta_params* p, int64_t T);
+int delta_rule_continue(float* state, const void* q, const void* k, const void* v, const float* beta,
+                        const float* g, int64_t T, const tu_delta_params* p, float* out,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* One context's part of a stack update. */
+typedef struct tu_seq_update {
+  tu_seq* seq;
+  const int64_t* ranges;  /* host int64 [n_ranges][2], may be NULL when n_ranges == 0 */
+  int32_t n_ranges;
+  int64_t T;              /* tail tokens */
+  int32_t* src_index;     /* optional device int32 [>= seq->len] (see compact_kv) */
+} tu_seq_update;
+
+/*
+ * One layer of the stack. Tail inputs of all contexts are packed in context
+ * order: context s owns rows [sum of earlier T, + T_s).
+ *  attention: k_cache[s], v_cache[s] device bf16 caches; q, k, v, out as in
+ *             tail_prefill_attention; beta, g, state unused.
+ *  delta:     state[s] device fp32 [Hv][d_v][d_k]; q, k, v, beta, g, out as in
+ *             delta_rule_continue; k_cache, v_cache unused.
+ */
+typedef struct tu_layer_io {
+  int32_t kind;                /* TU_LAYER_ATTN or TU_LAYER_DELTA */
+  void* const* k_cache;        /* host array [n_seq] of device pointers */
+  void* const* v_cache;
+  float* const* state;         /* host array [n_seq] of device pointers */
+  const void* q;
+  const void* k;
+  const void* v;
+  const float* beta;
+  const float* g;
+  float* out;
+} tu_layer_io;
+
+typedef struct tu_update {
+  int32_t n_seq;
+  tu_seq_update* seqs;         /* host array [n_seq] */
+  int32_t n_layers;
+  const tu_layer_io* layers;   /* host array [n_layers], in model order */
+  tu_attn_params attn;
+  tu_delta_params delta;
+} tu_update;
+
+/*
+ * Whole update of a hybrid layer stack for n_seq contexts (Eq. 1-3): verify every
+ * context's ranges and capacity; compact every attention layer's cache once per
+ * context (one index list per context, reused by all attention layers); then, in
+ * layer order, tail attention for attention layers and recurrence continuation
+ * for delta layers, batched over the contexts; finally commit each context's
+ * metadata (len = survivors + T, live intervals, cursor += T). A full refill is
+ * the same call on empty contexts (len 0) with zero states.
+ * tu_validate_update performs only the host checks (no device access).
+ */
+size_t update_layer_stack_workspace_size(const tu_update* u);
+int tu_validate_update(const tu_update* u);
+int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Kernel timing (diagnostics, not part of the update). While enabled for the
+ * calling thread, every kernel the library launches is bracketed by two HIP
+ * events recorded on the launch's stream. tu_profile_collect waits for those
+ * events, then reports per kernel name (NUL-terminated, `name_stride` bytes per
+ * entry in `names`) the launch count and the summed duration in milliseconds,
+ * for at most `max_entries` kernels; it returns the number of entries written
+ * (or a negative status) and clears the records. Kernel names: keep_scan,
+ * gather, rope_append, attention, attention_merge, delta_prep, delta_chain.
+ */
+int tu_profile_enable(int on);
+int tu_profile_collect(char* names, int32_t name_stride, int32_t* counts, double* total_ms, int32_t max_entries);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TAILUPDATE_H */

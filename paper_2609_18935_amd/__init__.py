@@ -1,0 +1,24 @@
+"""True-tail hybrid-state update on MI355X (gfx950).
+
+The HIP library libtailupdate.so (built from csrc/ by `build.py`) implements the
+update of a hybrid recurrent-attention context (paper Section 4.1, Eq. 2-3): KV
+compaction, rotary append at the true tail, causal GQA attention over surviving
++ new KV, and the gated delta-rule continuation from the carried state.
+`binding` is the ctypes layer over its C ABI (include/tailupdate.h).
+"""
+from .binding import (  # noqa: F401
+    Context,
+    LayerIO,
+    StackUpdate,
+    TailUpdateError,
+    attn_params,
+    commit_tail,
+    compact_kv,
+    delta_params,
+    delta_rule_continue,
+    lib,
+    tail_prefill_attention,
+    update_layer_stack,
+    TU_LAYER_ATTN,
+    TU_LAYER_DELTA,
+)

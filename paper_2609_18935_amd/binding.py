@@ -1,0 +1,316 @@
+"""Python binding of libtailupdate.so (argument marshalling only).
+
+Every step of the update runs in the HIP library; this module only turns torch
+device tensors into pointers, keeps the host metadata of each context in the
+C structs the library reads and writes, and raises on non-zero status. PyTorch
+is used for device memory and streams.
+
+If the shared library is missing the import fails loudly: there is no CPU
+fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtailupdate.so")
+
+TU_OK = 0
+TU_ERR_ARG = -1
+TU_ERR_RANGE = -2
+TU_ERR_CAPACITY = -3
+TU_ERR_WORKSPACE = -4
+TU_ERR_HIP = -5
+TU_LAYER_ATTN = 0
+TU_LAYER_DELTA = 1
+TU_MAX_RANGES = 128
+
+_i32, _i64, _f32, _f64, _vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
+
+
+class tu_interval(ctypes.Structure):
+    _fields_ = [("begin", _i64), ("end", _i64)]
+
+
+class tu_seq(ctypes.Structure):
+    _fields_ = [("len", _i64), ("capacity", _i64), ("next_pos", _i64),
+                ("live", ctypes.POINTER(tu_interval)), ("n_live", _i32), ("live_cap", _i32),
+                ("d_pos", _vp)]
+
+
+class tu_attn_params(ctypes.Structure):
+    _fields_ = [("n_q_heads", _i32), ("n_kv_heads", _i32), ("head_dim", _i32), ("rotary_dim", _i32),
+                ("rope_theta", _f64), ("softmax_scale", _f32), ("kv_splits", _i32)]
+
+
+class tu_delta_params(ctypes.Structure):
+    _fields_ = [("n_k_heads", _i32), ("n_v_heads", _i32), ("d_k", _i32), ("d_v", _i32), ("chunk", _i32),
+                ("scale", _f32)]
+
+
+class tu_seq_update(ctypes.Structure):
+    _fields_ = [("seq", ctypes.POINTER(tu_seq)), ("ranges", ctypes.POINTER(_i64)), ("n_ranges", _i32),
+                ("T", _i64), ("src_index", _vp)]
+
+
+class tu_layer_io(ctypes.Structure):
+    _fields_ = [("kind", _i32), ("k_cache", ctypes.POINTER(_vp)), ("v_cache", ctypes.POINTER(_vp)),
+                ("state", ctypes.POINTER(_vp)), ("q", _vp), ("k", _vp), ("v", _vp), ("beta", _vp), ("g", _vp),
+                ("out", _vp)]
+
+
+class tu_update(ctypes.Structure):
+    _fields_ = [("n_seq", _i32), ("seqs", ctypes.POINTER(tu_seq_update)), ("n_layers", _i32),
+                ("layers", ctypes.POINTER(tu_layer_io)), ("attn", tu_attn_params), ("delta", tu_delta_params)]
+
+
+# exported symbols and their signatures (mirrors include/tailupdate.h)
+_SIGNATURES = {
+    "tu_abi_version": (_i32, []),
+    "tu_last_error": (ctypes.c_char_p, []),
+    "tu_validate_ranges": (_i32, [ctypes.POINTER(tu_seq), ctypes.POINTER(_i64), _i32, ctypes.POINTER(_i64)]),
+    "compact_kv_workspace_size": (ctypes.c_size_t, [_i64, _i32, _i32, _i32]),
+    "compact_kv": (_i32, [ctypes.POINTER(tu_seq), ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _i32, _i32,
+                          ctypes.POINTER(_i64), _i32, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tail_prefill_attention_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_attn_params), _i64, _i64]),
+    "tail_prefill_attention": (_i32, [ctypes.POINTER(tu_seq), _vp, _vp, ctypes.POINTER(tu_attn_params), _vp, _vp,
+                                      _vp, _i64, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "commit_tail": (_i32, [ctypes.POINTER(tu_seq), _i64]),
+    "delta_rule_continue_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_delta_params), _i64]),
+    "delta_rule_continue": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i64, ctypes.POINTER(tu_delta_params), _vp, _vp,
+                                   ctypes.c_size_t, _vp]),
+    "update_layer_stack_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_update)]),
+    "tu_validate_update": (_i32, [ctypes.POINTER(tu_update)]),
+    "update_layer_stack": (_i32, [ctypes.POINTER(tu_update), _vp, ctypes.c_size_t, _vp]),
+}
+
+_lib_handle = None
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib_handle
+    if _lib_handle is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_18935_amd.build`")
+        h = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(h, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib_handle = h
+    return _lib_handle
+
+
+class TailUpdateError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"[{code}] {message}")
+        self.code = code
+
+
+def _check(code: int):
+    if code != TU_OK:
+        raise TailUpdateError(code, lib().tu_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the library must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        # NULL is the default stream; torch's current stream when a GPU is present
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]) -> torch.Tensor:
+    if workspace is not None:
+        return workspace
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def _ranges_array(ranges) -> tuple:
+    import numpy as np
+    r = np.ascontiguousarray(np.asarray(ranges, dtype=np.int64).reshape(-1, 2))
+    arr = (_i64 * max(1, r.size))(*r.reshape(-1).tolist())
+    return arr, int(r.shape[0])
+
+
+# ----------------------------------------------------------------------------- parameters
+
+def attn_params(n_q_heads: int, n_kv_heads: int, head_dim: int, rotary_dim: Optional[int] = None,
+                rope_theta: float = 1.0e7, softmax_scale: Optional[float] = None, kv_splits: int = 0):
+    return tu_attn_params(n_q_heads, n_kv_heads, head_dim, head_dim if rotary_dim is None else rotary_dim,
+                          float(rope_theta), float(head_dim ** -0.5 if softmax_scale is None else softmax_scale),
+                          int(kv_splits))
+
+
+def delta_params(n_k_heads: int, n_v_heads: int, d_k: int, d_v: int, chunk: int, scale: Optional[float] = None):
+    return tu_delta_params(n_k_heads, n_v_heads, d_k, d_v, chunk, float(d_k ** -0.5 if scale is None else scale))
+
+
+# ----------------------------------------------------------------------------- contexts
+
+class Context:
+    """A character context: host metadata (tu_seq) plus the device position array.
+
+    The caller owns the K/V caches of every attention layer ([capacity][Hkv][D]
+    bf16) and the fp32 states of every delta layer.
+    """
+
+    def __init__(self, capacity: int, device="cuda", live_cap: int = 4096):
+        self.pos = torch.zeros(max(1, capacity), dtype=torch.int32, device=device)
+        self._live = (tu_interval * live_cap)()
+        self.c = tu_seq(0, int(capacity), 0, self._live, 0, int(live_cap), self.pos.data_ptr())
+
+    @property
+    def len(self) -> int:
+        return int(self.c.len)
+
+    @property
+    def capacity(self) -> int:
+        return int(self.c.capacity)
+
+    @property
+    def next_pos(self) -> int:
+        return int(self.c.next_pos)
+
+    def intervals(self) -> List[tuple]:
+        return [(int(self._live[i].begin), int(self._live[i].end)) for i in range(self.c.n_live)]
+
+    def set_metadata(self, intervals: Sequence[tuple], next_pos: int):
+        """Declare the live positions of a cache the caller filled (pos must match)."""
+        if len(intervals) > self.c.live_cap:
+            raise ValueError("too many intervals")
+        n = 0
+        for i, (a, b) in enumerate(intervals):
+            self._live[i] = tu_interval(int(a), int(b))
+            n += int(b) - int(a)
+        self.c.n_live = len(intervals)
+        self.c.len = n
+        self.c.next_pos = int(next_pos)
+
+    def snapshot(self):
+        return (self.intervals(), self.next_pos, self.pos.clone())
+
+    def restore(self, snap):
+        iv, nxt, pos = snap
+        self.pos.copy_(pos)
+        self.set_metadata(iv, nxt)
+
+    def validate_ranges(self, ranges) -> int:
+        arr, n = _ranges_array(ranges)
+        removed = _i64(0)
+        _check(lib().tu_validate_ranges(ctypes.byref(self.c), arr, n, ctypes.byref(removed)))
+        return int(removed.value)
+
+
+# ----------------------------------------------------------------------------- entry points
+
+def compact_kv(ctx: Context, k_layers: Sequence[torch.Tensor], v_layers: Sequence[torch.Tensor], ranges,
+               src_index: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None, stream=None):
+    n = len(k_layers)
+    Hkv, D = int(k_layers[0].shape[1]), int(k_layers[0].shape[2])
+    ks = (_vp * max(1, n))(*[_ptr(t) for t in k_layers])
+    vs = (_vp * max(1, n))(*[_ptr(t) for t in v_layers])
+    arr, nr = _ranges_array(ranges)
+    nbytes = lib().compact_kv_workspace_size(ctx.len, n, Hkv, D)
+    ws = _workspace(nbytes, ctx.pos.device, workspace)
+    _check(lib().compact_kv(ctypes.byref(ctx.c), ks, vs, n, Hkv, D, arr, nr, _ptr(src_index), _ptr(ws),
+                            ws.numel(), _stream(stream)))
+
+
+def tail_prefill_attention(ctx: Context, k_cache: torch.Tensor, v_cache: torch.Tensor, params: tu_attn_params,
+                           q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: torch.Tensor,
+                           q_hat: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                           stream=None):
+    T = int(q.shape[0])
+    nbytes = lib().tail_prefill_attention_workspace_size(ctypes.byref(params), T, ctx.len)
+    ws = _workspace(nbytes, q.device, workspace)
+    _check(lib().tail_prefill_attention(ctypes.byref(ctx.c), _ptr(k_cache), _ptr(v_cache), ctypes.byref(params),
+                                        _ptr(q), _ptr(k), _ptr(v), T, _ptr(out), _ptr(q_hat), _ptr(ws), ws.numel(),
+                                        _stream(stream)))
+
+
+def commit_tail(ctx: Context, T: int):
+    _check(lib().commit_tail(ctypes.byref(ctx.c), int(T)))
+
+
+def delta_rule_continue(state: torch.Tensor, q, k, v, beta, g, params: tu_delta_params, out: torch.Tensor,
+                        workspace: Optional[torch.Tensor] = None, stream=None):
+    T = int(q.shape[0])
+    nbytes = lib().delta_rule_continue_workspace_size(ctypes.byref(params), T)
+    ws = _workspace(nbytes, state.device, workspace)
+    _check(lib().delta_rule_continue(_ptr(state), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(g), T,
+                                     ctypes.byref(params), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+class LayerIO:
+    """Inputs and outputs of one layer of a stack update (tail rows packed over contexts)."""
+
+    def __init__(self, kind: int, q, k, v, out, k_cache=None, v_cache=None, state=None, beta=None, g=None):
+        self.kind = kind
+        self.q, self.k, self.v, self.out = q, k, v, out
+        self.k_cache, self.v_cache, self.state = k_cache, v_cache, state
+        self.beta, self.g = beta, g
+
+
+class StackUpdate:
+    """A prepared update_layer_stack call (ctypes structs built once, reusable)."""
+
+    def __init__(self, contexts: Sequence[Context], ranges: Sequence, tails: Sequence[int], layers: Sequence[LayerIO],
+                 attn: Optional[tu_attn_params] = None, delta: Optional[tu_delta_params] = None,
+                 src_index: Optional[Sequence[Optional[torch.Tensor]]] = None):
+        n = len(contexts)
+        self.contexts = list(contexts)
+        self._keep = []
+        self._seq_arr = (tu_seq_update * max(1, n))()
+        for s, ctx in enumerate(contexts):
+            arr, nr = _ranges_array(ranges[s])
+            self._keep.append(arr)
+            si = None if src_index is None else src_index[s]
+            self._seq_arr[s] = tu_seq_update(ctypes.pointer(ctx.c), arr, nr, int(tails[s]), _ptr(si))
+        self._layer_arr = (tu_layer_io * max(1, len(layers)))()
+        for l, L in enumerate(layers):
+            def plist(ts):
+                if ts is None:
+                    return None
+                a = (_vp * max(1, n))(*[_ptr(t) for t in ts])
+                self._keep.append(a)
+                return a
+            self._layer_arr[l] = tu_layer_io(L.kind, plist(L.k_cache), plist(L.v_cache), plist(L.state), _ptr(L.q),
+                                             _ptr(L.k), _ptr(L.v), _ptr(L.beta), _ptr(L.g), _ptr(L.out))
+        self.u = tu_update(n, self._seq_arr, len(layers), self._layer_arr,
+                           attn if attn is not None else tu_attn_params(),
+                           delta if delta is not None else tu_delta_params())
+
+    def validate(self):
+        _check(lib().tu_validate_update(ctypes.byref(self.u)))
+
+    def workspace_size(self) -> int:
+        n = lib().update_layer_stack_workspace_size(ctypes.byref(self.u))
+        if n == 0:
+            self.validate()
+        return int(n)
+
+    def run(self, workspace: torch.Tensor, stream=None):
+        _check(lib().update_layer_stack(ctypes.byref(self.u), _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def update_layer_stack(contexts, ranges, tails, layers, attn=None, delta=None, workspace=None, stream=None,
+                       src_index=None):
+    up = StackUpdate(contexts, ranges, tails, layers, attn, delta, src_index)
+    nbytes = up.workspace_size()
+    dev = contexts[0].pos.device if contexts else "cuda"
+    ws = _workspace(nbytes, dev, workspace)
+    up.run(ws, stream)
+    return up

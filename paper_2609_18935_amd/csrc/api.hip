@@ -1,0 +1,919 @@
+// Host side of the tail-update library: argument and range verification, launch
+// planning, workspace carving and the C ABI declared in include/tailupdate.h.
+//
+// Every check runs before the first launch, so an error leaves device buffers and
+// host metadata untouched (Section 4.2 of the paper: deletion ranges are verified
+// against the live spans before anything is removed).
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "tailupdate.h"
+
+namespace tu {
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return TU_OK;
+}
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+// Carves aligned regions out of a workspace; with base == nullptr it only measures.
+struct Arena {
+  char* base;
+  size_t used = 0;
+  explicit Arena(void* b) : base(static_cast<char*>(b)) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + used : nullptr;
+    used += align_up(bytes);
+    return p;
+  }
+};
+
+// ------------------------------------------------------------------ metadata checks
+
+int check_seq(const tu_seq* s) {
+  if (!s) return fail(TU_ERR_ARG, "null context");
+  if (s->len < 0 || s->capacity < s->len) return fail(TU_ERR_ARG, "len %lld outside [0, capacity %lld]",
+                                                      (long long)s->len, (long long)s->capacity);
+  if (s->n_live < 0 || s->n_live > s->live_cap) return fail(TU_ERR_ARG, "n_live outside [0, live_cap]");
+  if (s->n_live > 0 && !s->live) return fail(TU_ERR_ARG, "null live-interval array");
+  if (s->capacity > 0 && !s->d_pos) return fail(TU_ERR_ARG, "null d_pos");
+  if (s->next_pos < 0 || s->next_pos > INT32_MAX) return fail(TU_ERR_ARG, "cursor outside the int32 position range");
+  int64_t total = 0, prev_end = -1;
+  for (int i = 0; i < s->n_live; ++i) {
+    const tu_interval& iv = s->live[i];
+    if (iv.end <= iv.begin) return fail(TU_ERR_ARG, "empty live interval");
+    if (iv.begin <= prev_end) return fail(TU_ERR_ARG, "live intervals not sorted, disjoint and merged");
+    prev_end = iv.end;
+    total += iv.end - iv.begin;
+  }
+  if (prev_end > s->next_pos) return fail(TU_ERR_ARG, "live position at or beyond the cursor");
+  if (total != s->len) return fail(TU_ERR_ARG, "live intervals cover %lld positions, len is %lld",
+                                   (long long)total, (long long)s->len);
+  return TU_OK;
+}
+
+// Result of range verification for one context.
+struct RangeCheck {
+  int64_t removed = 0;
+  int64_t first_row = 0;                  // cache row of the first removed position
+  std::vector<tu_interval> live_after;    // intervals after the removal
+};
+
+int check_ranges(const tu_seq* s, const int64_t* ranges, int n, RangeCheck* out) {
+  if (n < 0) return fail(TU_ERR_ARG, "negative range count");
+  if (n > 0 && !ranges) return fail(TU_ERR_ARG, "null ranges");
+  if (n > TU_MAX_RANGES) return fail(TU_ERR_ARG, "more than %d ranges in one call", TU_MAX_RANGES);
+  out->removed = 0;
+  out->first_row = s->len;
+  int64_t prev_end = INT64_MIN;
+  // prefix of live rows before each interval
+  std::vector<int64_t> before(s->n_live + 1, 0);
+  for (int i = 0; i < s->n_live; ++i) before[i + 1] = before[i] + (s->live[i].end - s->live[i].begin);
+  for (int q = 0; q < n; ++q) {
+    const int64_t a = ranges[2 * q], b = ranges[2 * q + 1];
+    if (b <= a) return fail(TU_ERR_RANGE, "range %d [%lld,%lld) is empty", q, (long long)a, (long long)b);
+    if (a < prev_end) return fail(TU_ERR_RANGE, "ranges are not sorted and disjoint (range %d)", q);
+    if (a < 0 || b > s->next_pos)
+      return fail(TU_ERR_RANGE, "range %d [%lld,%lld) reaches past the cursor %lld", q, (long long)a,
+                  (long long)b, (long long)s->next_pos);
+    // the interval that holds position a
+    int lo = 0, hi = s->n_live - 1, at = -1;
+    while (lo <= hi) {
+      const int mid = (lo + hi) / 2;
+      if (s->live[mid].end <= a) lo = mid + 1;
+      else if (s->live[mid].begin > a) hi = mid - 1;
+      else { at = mid; break; }
+    }
+    if (at < 0 || b > s->live[at].end)
+      return fail(TU_ERR_RANGE, "range %d [%lld,%lld) is not live", q, (long long)a, (long long)b);
+    if (q == 0) out->first_row = before[at] + (a - s->live[at].begin);
+    out->removed += b - a;
+    prev_end = b;
+  }
+  // intervals after removal
+  out->live_after.clear();
+  int q = 0;
+  for (int i = 0; i < s->n_live; ++i) {
+    int64_t cur = s->live[i].begin;
+    const int64_t end = s->live[i].end;
+    while (q < n && ranges[2 * q] < end) {
+      if (ranges[2 * q] > cur) out->live_after.push_back({cur, ranges[2 * q]});
+      cur = std::max(cur, ranges[2 * q + 1]);
+      ++q;
+    }
+    if (cur < end) out->live_after.push_back({cur, end});
+  }
+  return TU_OK;
+}
+
+int check_attn(const tu_attn_params* p) {
+  if (!p) return fail(TU_ERR_ARG, "null attention parameters");
+  if (p->n_kv_heads <= 0 || p->n_q_heads <= 0 || p->n_q_heads % p->n_kv_heads)
+    return fail(TU_ERR_ARG, "n_q_heads must be a positive multiple of n_kv_heads");
+  if (p->head_dim != 64 && p->head_dim != 256) return fail(TU_ERR_ARG, "head_dim must be 64 or 256");
+  if (p->rotary_dim < 0 || p->rotary_dim > p->head_dim || (p->rotary_dim & 1))
+    return fail(TU_ERR_ARG, "rotary_dim must be even and within [0, head_dim]");
+  if (!(p->rope_theta > 0.0) || !std::isfinite(p->rope_theta)) return fail(TU_ERR_ARG, "rope_theta must be positive");
+  if (!(p->softmax_scale > 0.f) || !std::isfinite(p->softmax_scale)) return fail(TU_ERR_ARG, "softmax_scale must be positive");
+  if (p->kv_splits < 0 || p->kv_splits > 64) return fail(TU_ERR_ARG, "kv_splits must be in [0, 64]");
+  if ((long)p->n_kv_heads * p->head_dim * 2 > kGatherStripeBytes) return fail(TU_ERR_ARG, "cache row too wide");
+  return TU_OK;
+}
+
+int check_delta(const tu_delta_params* p) {
+  if (!p) return fail(TU_ERR_ARG, "null delta parameters");
+  if (p->n_k_heads <= 0 || p->n_v_heads <= 0 || p->n_v_heads % p->n_k_heads)
+    return fail(TU_ERR_ARG, "n_v_heads must be a positive multiple of n_k_heads");
+  if (p->d_k != p->d_v || (p->d_k != 64 && p->d_k != 128)) return fail(TU_ERR_ARG, "d_k = d_v must be 64 or 128");
+  if (p->chunk != 16 && p->chunk != 32 && p->chunk != 64) return fail(TU_ERR_ARG, "chunk must be 16, 32 or 64");
+  if (!std::isfinite(p->scale)) return fail(TU_ERR_ARG, "scale must be finite");
+  return TU_OK;
+}
+
+int hip_check(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(TU_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return TU_OK;
+}
+
+// ------------------------------------------------------------------ kernel timing
+
+struct ProfRec {
+  const char* name;
+  hipEvent_t start;
+  hipEvent_t stop;
+};
+thread_local bool g_prof = false;
+thread_local std::vector<ProfRec> g_recs;
+
+// Runs `launch` (which enqueues one kernel on `st`), bracketed by events when profiling.
+template <class F>
+hipError_t timed(const char* name, hipStream_t st, F&& launch) {
+  if (!g_prof) return launch();
+  ProfRec r{name, nullptr, nullptr};
+  if (hipEventCreate(&r.start) != hipSuccess) return launch();
+  if (hipEventCreate(&r.stop) != hipSuccess) {
+    (void)hipEventDestroy(r.start);
+    return launch();
+  }
+  (void)hipEventRecord(r.start, st);
+  const hipError_t e = launch();
+  (void)hipEventRecord(r.stop, st);
+  g_recs.push_back(r);
+  return e;
+}
+
+// ------------------------------------------------------------------ compaction plan
+
+struct CompactItem {
+  tu_seq* seq;
+  const int64_t* ranges;
+  int n_ranges;
+  RangeCheck rc;
+  int32_t* src_index;        // device, caller's or workspace
+  bool user_index = false;   // the caller asked for src_index
+  std::vector<void*> bufs;   // K and V of every attention layer
+};
+
+struct CompactPlan {
+  std::vector<ScanArgs> scans;
+  std::vector<GatherArgs> gathers;
+  std::vector<int> gather_blocks;
+  size_t ws_bytes = 0;
+};
+
+// Builds the launches for a set of contexts. With ws == nullptr only sizes are computed.
+int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, CompactPlan* plan) {
+  Arena ar(ws);
+  const int R = kGatherStripeBytes / row_bytes;
+  // src_index storage
+  for (auto& it : items) {
+    void* p = ar.take(sizeof(int32_t) * std::max<int64_t>(1, it.seq->len));
+    it.user_index = it.src_index != nullptr && it.src_index != p;
+    if (!it.user_index) it.src_index = static_cast<int32_t*>(p);
+  }
+  // gather launches: (context, buffer chunk) entries
+  struct Entry { int item; int buf0; int nbuf; };
+  std::vector<std::vector<Entry>> groups;
+  {
+    std::vector<Entry> cur;
+    int cur_bufs = 0;
+    for (int i = 0; i < (int)items.size(); ++i) {
+      const auto& it = items[i];
+      if (it.rc.removed == 0 || it.seq->len - it.rc.removed <= it.rc.first_row) continue;
+      for (int b0 = 0; b0 < (int)it.bufs.size(); b0 += kMaxBufPerLaunch) {
+        const int nb = std::min<int>(kMaxBufPerLaunch, (int)it.bufs.size() - b0);
+        if ((int)cur.size() == kMaxSeqPerLaunch || cur_bufs + nb > kMaxBufPerLaunch) {
+          groups.push_back(cur);
+          cur.clear();
+          cur_bufs = 0;
+        }
+        cur.push_back({i, b0, nb});
+        cur_bufs += nb;
+      }
+    }
+    if (!cur.empty()) groups.push_back(cur);
+  }
+  // counters: per launch one ticket + one error word, then stripe counters
+  const size_t counters_at = ar.used;
+  std::vector<size_t> flag_words;
+  size_t words = 0;
+  for (auto& g : groups) {
+    size_t w = 2;
+    for (auto& e : g) {
+      const auto& it = items[e.item];
+      const int64_t n_keep = it.seq->len - it.rc.removed;
+      const int64_t align_rows = std::max(1, 128 / row_bytes);
+      const int64_t rb = (it.rc.first_row / align_rows) * align_rows;
+      w += (n_keep - rb + R - 1) / R;
+    }
+    flag_words.push_back(w);
+    words += w;
+  }
+  int32_t* counters = static_cast<int32_t*>(ar.take(sizeof(int32_t) * std::max<size_t>(1, words)));
+  (void)counters_at;
+  plan->ws_bytes = ar.used;
+  if (!ws) return TU_OK;
+
+  // scan launches
+  plan->scans.clear();
+  {
+    ScanArgs a{};
+    int nr = 0;
+    auto flush = [&]() {
+      if (a.n_seq == 0) return;
+      plan->scans.push_back(a);
+      a = ScanArgs{};
+      nr = 0;
+    };
+    for (auto& it : items) {
+      if (it.seq->len == 0 || (it.rc.removed == 0 && !it.user_index)) continue;
+      if (a.n_seq == kMaxSeqPerLaunch || nr + it.n_ranges > kMaxRangesPerLaunch) flush();
+      ScanSeq& s = a.seq[a.n_seq++];
+      s.pos = it.seq->d_pos;
+      s.src_index = it.src_index;
+      s.L_old = (int32_t)it.seq->len;
+      s.range_begin = nr;
+      s.n_ranges = it.n_ranges;
+      for (int q = 0; q < it.n_ranges; ++q) {
+        a.ranges[nr + q][0] = (int32_t)it.ranges[2 * q];
+        a.ranges[nr + q][1] = (int32_t)it.ranges[2 * q + 1];
+      }
+      nr += it.n_ranges;
+    }
+    flush();
+    if (!plan->scans.empty()) {
+      plan->scans[0].zero_ptr = counters;
+      plan->scans[0].zero_count = (int32_t)words;
+    }
+  }
+  // gather launches
+  plan->gathers.clear();
+  plan->gather_blocks.clear();
+  size_t woff = 0;
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    GatherArgs a{};
+    int32_t* base = counters + woff;
+    a.ticket = base;
+    a.err = base + 1;
+    a.flags = base + 2;
+    a.rows_per_stripe = R;
+    a.row_bytes = row_bytes;
+    int items_total = 0, flag_off = 0, nbufs = 0;
+    for (auto& e : groups[gi]) {
+      const auto& it = items[e.item];
+      GatherSeq& s = a.seq[a.n_seq++];
+      const int64_t n_keep = it.seq->len - it.rc.removed;
+      const int64_t align_rows = std::max(1, 128 / row_bytes);
+      const int64_t rb = (it.rc.first_row / align_rows) * align_rows;
+      s.src_index = it.src_index;
+      s.row_begin = (int32_t)rb;
+      s.n_keep = (int32_t)n_keep;
+      s.n_stripes = (int32_t)((n_keep - rb + R - 1) / R);
+      s.item_begin = items_total;
+      s.buf_begin = nbufs;
+      s.n_buf = e.nbuf;
+      s.flag_begin = flag_off;
+      s.window = (int32_t)((it.rc.removed + R - 1 + R - 1) / R);
+      for (int b = 0; b < e.nbuf; ++b) a.bufs[nbufs++] = it.bufs[e.buf0 + b];
+      items_total += s.n_stripes * s.n_buf;
+      flag_off += s.n_stripes;
+    }
+    a.total_items = items_total;
+    plan->gathers.push_back(a);
+    plan->gather_blocks.push_back(items_total);
+    woff += flag_words[gi];
+  }
+  return TU_OK;
+}
+
+int run_compaction(const CompactPlan& plan, hipStream_t st) {
+  for (const auto& a : plan.scans)
+    if (int e = hip_check(timed("keep_scan", st, [&] { return launch_keep_scan(a, st); }), "keep-scan launch")) return e;
+  for (size_t i = 0; i < plan.gathers.size(); ++i)
+    if (int e = hip_check(timed("gather", st, [&] { return launch_gather(plan.gathers[i], plan.gather_blocks[i], st); }), "gather launch")) return e;
+  return TU_OK;
+}
+
+// ------------------------------------------------------------------ attention plan
+
+struct AttnItem {
+  const tu_seq* seq;
+  int64_t L_keep;           // surviving rows (new rows are appended at L_keep)
+  int64_t T;
+  int64_t cursor;
+  void* k_cache;
+  void* v_cache;
+  const bf16_t* q;
+  const bf16_t* k;
+  const bf16_t* v;
+  float* out;
+  bf16_t* q_hat;            // caller's or null (workspace)
+};
+
+struct AttnLaunch {
+  RopeArgs rope;
+  int rope_tokens;
+  AttnArgs attn;
+  MergeArgs merge;
+  int merge_rows;
+};
+
+int choose_splits(const tu_attn_params* p, int64_t L_keep, int64_t T, int64_t base_items_total) {
+  if (p->kv_splits > 0) return p->kv_splits;
+  const int G = p->n_q_heads / p->n_kv_heads;
+  (void)G;
+  const int64_t n_kt = (L_keep + T + 63) / 64;
+  int want = (int)std::max<int64_t>(1, (256 + base_items_total - 1) / std::max<int64_t>(1, base_items_total));
+  const int max_by_len = (int)std::max<int64_t>(1, n_kt / 4);  // at least 4 key tiles per split
+  return std::max(1, std::min({want, max_by_len, 64}));
+}
+
+int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* ws, std::vector<AttnLaunch>* out,
+                   size_t* ws_bytes) {
+  const int Hq = p->n_q_heads, Hkv = p->n_kv_heads, D = p->head_dim, G = Hq / Hkv;
+  size_t max_used = 0;
+  out->clear();
+  for (size_t g0 = 0; g0 < items.size(); g0 += kMaxSeqPerLaunch) {
+    const size_t g1 = std::min(items.size(), g0 + kMaxSeqPerLaunch);
+    Arena ar(ws);
+    int64_t base_items = 0;
+    for (size_t i = g0; i < g1; ++i) base_items += (int64_t)Hkv * ((items[i].T * G + 127) / 128);
+    AttnLaunch L{};
+    L.rope.n_q_heads = Hq;
+    L.rope.n_kv_heads = Hkv;
+    L.rope.head_dim = D;
+    L.rope.rotary_dim = p->rotary_dim;
+    L.rope.theta = p->rope_theta;
+    L.attn.n_q_heads = Hq;
+    L.attn.n_kv_heads = Hkv;
+    L.attn.scale_log2 = p->softmax_scale * 1.4426950408889634f;
+    L.merge.n_q_heads = Hq;
+    int tok = 0, item_total = 0, mrows = 0;
+    for (size_t i = g0; i < g1; ++i) {
+      const AttnItem& it = items[i];
+      if (it.T <= 0) continue;
+      bf16_t* qh = it.q_hat;
+      void* qh_ws = ar.take(sizeof(bf16_t) * it.T * Hq * D);
+      if (!qh) qh = static_cast<bf16_t*>(qh_ws);
+      const int tiles = (int)((it.T * G + 127) / 128);
+      const int splits = choose_splits(p, it.L_keep, it.T, base_items);
+      float* po = nullptr;
+      float* pml = nullptr;
+      if (splits > 1) {
+        po = static_cast<float*>(ar.take(sizeof(float) * splits * it.T * Hq * D));
+        pml = static_cast<float*>(ar.take(sizeof(float) * 2 * splits * it.T * Hq));
+      }
+      RopeSeq& r = L.rope.seq[L.rope.n_seq++];
+      r.q = it.q;
+      r.k = it.k;
+      r.v = it.v;
+      r.q_hat = qh;
+      r.k_cache = static_cast<bf16_t*>(it.k_cache);
+      r.v_cache = static_cast<bf16_t*>(it.v_cache);
+      r.pos = it.seq->d_pos;
+      r.cursor = it.cursor;
+      r.L_keep = (int32_t)it.L_keep;
+      r.T = (int32_t)it.T;
+      r.tok_begin = tok;
+      tok += (int)it.T;
+      AttnSeq& s = L.attn.seq[L.attn.n_seq++];
+      s.q_hat = qh;
+      s.k_cache = static_cast<const bf16_t*>(it.k_cache);
+      s.v_cache = static_cast<const bf16_t*>(it.v_cache);
+      s.out = it.out;
+      s.part_o = po;
+      s.part_ml = pml;
+      s.L_keep = (int32_t)it.L_keep;
+      s.T = (int32_t)it.T;
+      s.n_tiles = tiles;
+      s.n_splits = splits;
+      s.item_begin = item_total;
+      item_total += Hkv * splits * tiles;
+      if (splits > 1) {
+        L.merge.row_begin[L.merge.n_seq] = mrows;
+        L.merge.seq[L.merge.n_seq++] = s;
+        mrows += (int)(it.T * Hq);
+      }
+    }
+    L.merge.row_begin[L.merge.n_seq] = mrows;
+    L.rope_tokens = tok;
+    L.attn.total_items = item_total;
+    L.merge_rows = mrows;
+    max_used = std::max(max_used, ar.used);
+    if (L.rope.n_seq > 0) out->push_back(L);
+  }
+  *ws_bytes = max_used;
+  return TU_OK;
+}
+
+int run_attention(const std::vector<AttnLaunch>& ls, int D, hipStream_t st) {
+  for (const auto& L : ls) {
+    if (int e = hip_check(timed("rope_append", st, [&] { return launch_rope_append(L.rope, L.rope_tokens, st); }), "rope-append launch")) return e;
+    if (int e = hip_check(timed("attention", st, [&] { return launch_attention(L.attn, D, st); }), "attention launch")) return e;
+    if (L.merge_rows > 0)
+      if (int e = hip_check(timed("attention_merge", st, [&] { return launch_attention_merge(L.merge, L.merge_rows, D, st); }), "merge launch")) return e;
+  }
+  return TU_OK;
+}
+
+// ------------------------------------------------------------------ delta plan
+
+struct DeltaItem {
+  float* state;
+  const bf16_t* q;
+  const bf16_t* k;
+  const bf16_t* v;
+  const float* beta;
+  const float* g;
+  float* out;
+  int64_t T;
+};
+
+int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, void* ws, std::vector<DeltaArgs>* out,
+               size_t* ws_bytes) {
+  const int C = p->chunk, Hv = p->n_v_heads, DK = p->d_k;
+  size_t max_used = 0;
+  out->clear();
+  int n_active = 0;
+  for (const auto& it : items) n_active += it.T > 0;
+  // slice d_v so that the chain has enough workgroups
+  const int wg64 = n_active * Hv * (DK / 64);
+  const int dvs = (wg64 >= 256) ? 64 : 32;
+  for (size_t g0 = 0; g0 < items.size(); g0 += kMaxSeqPerLaunch) {
+    const size_t g1 = std::min(items.size(), g0 + kMaxSeqPerLaunch);
+    DeltaArgs a{};
+    a.n_k_heads = p->n_k_heads;
+    a.n_v_heads = Hv;
+    a.scale = p->scale;
+    a.n_slices = DK / dvs;
+    int chunks = 0;
+    for (size_t i = g0; i < g1; ++i) {
+      const auto& it = items[i];
+      if (it.T <= 0) continue;
+      DeltaSeq& s = a.seq[a.n_seq++];
+      s.q = it.q;
+      s.k = it.k;
+      s.v = it.v;
+      s.beta = it.beta;
+      s.g = it.g;
+      s.state = it.state;
+      s.out = it.out;
+      s.T = (int32_t)it.T;
+      s.n_chunks = (int32_t)((it.T + C - 1) / C);
+      s.chunk_begin = chunks;
+      chunks += s.n_chunks;
+    }
+    a.total_chunks = chunks;
+    Arena ar(ws);
+    a.ws_w = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * DK));
+    a.ws_u = static_cast<float*>(ar.take(sizeof(float) * (size_t)chunks * Hv * C * DK));
+    a.ws_p = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * C));
+    a.ws_lg = static_cast<float*>(ar.take(sizeof(float) * (size_t)chunks * Hv * C));
+    max_used = std::max(max_used, ar.used);
+    if (a.n_seq > 0) out->push_back(a);
+  }
+  *ws_bytes = max_used;
+  return TU_OK;
+}
+
+int run_delta(const std::vector<DeltaArgs>& ls, const tu_delta_params* p, hipStream_t st) {
+  for (const auto& a : ls) {
+    if (int e = hip_check(timed("delta_prep", st, [&] { return launch_delta_prep(a, p->d_k, p->chunk, st); }), "delta-prep launch")) return e;
+    if (int e = hip_check(timed("delta_chain", st, [&] { return launch_delta_chain(a, p->d_k, p->chunk, st); }), "delta-chain launch")) return e;
+  }
+  return TU_OK;
+}
+
+void append_tail(std::vector<tu_interval>& iv, int64_t begin, int64_t T) {
+  if (T <= 0) return;
+  if (!iv.empty() && iv.back().end == begin) iv.back().end = begin + T;
+  else iv.push_back({begin, begin + T});
+}
+
+int commit_intervals(tu_seq* s, const std::vector<tu_interval>& iv) {
+  if ((int64_t)iv.size() > s->live_cap) return fail(TU_ERR_CAPACITY, "live-interval list full (%d)", s->live_cap);
+  for (size_t i = 0; i < iv.size(); ++i) s->live[i] = iv[i];
+  s->n_live = (int32_t)iv.size();
+  return TU_OK;
+}
+
+// ------------------------------------------------------------------ stack update
+
+struct StackPlan {
+  std::vector<RangeCheck> rc;
+  std::vector<std::vector<tu_interval>> final_iv;
+  std::vector<int64_t> tail_begin;   // row offset of each context in the packed tail inputs
+  int n_attn = 0, n_delta = 0;
+};
+
+int validate_stack(const tu_update* u, StackPlan* sp) {
+  if (!u) return fail(TU_ERR_ARG, "null update");
+  if (u->n_seq < 0 || (u->n_seq > 0 && !u->seqs)) return fail(TU_ERR_ARG, "bad context list");
+  if (u->n_layers < 0 || (u->n_layers > 0 && !u->layers)) return fail(TU_ERR_ARG, "bad layer list");
+  sp->rc.assign(u->n_seq, RangeCheck{});
+  sp->final_iv.assign(u->n_seq, {});
+  sp->tail_begin.assign(u->n_seq + 1, 0);
+  for (int l = 0; l < u->n_layers; ++l) {
+    const int kind = u->layers[l].kind;
+    if (kind == TU_LAYER_ATTN) ++sp->n_attn;
+    else if (kind == TU_LAYER_DELTA) ++sp->n_delta;
+    else return fail(TU_ERR_ARG, "layer %d: unknown kind %d", l, kind);
+  }
+  if (sp->n_attn) if (int e = check_attn(&u->attn)) return e;
+  if (sp->n_delta) if (int e = check_delta(&u->delta)) return e;
+  for (int s = 0; s < u->n_seq; ++s) {
+    const tu_seq_update& su = u->seqs[s];
+    if (int e = check_seq(su.seq)) return e;
+    for (int t = 0; t < s; ++t)
+      if (u->seqs[t].seq == su.seq) return fail(TU_ERR_ARG, "context %d appears twice", s);
+    if (su.T < 0) return fail(TU_ERR_ARG, "context %d: negative T", s);
+    if (int e = check_ranges(su.seq, su.ranges, su.n_ranges, &sp->rc[s])) return e;
+    const int64_t L_keep = su.seq->len - sp->rc[s].removed;
+    if (L_keep + su.T > su.seq->capacity)
+      return fail(TU_ERR_CAPACITY, "context %d: %lld surviving + %lld tail rows exceed capacity %lld", s,
+                  (long long)L_keep, (long long)su.T, (long long)su.seq->capacity);
+    if (su.seq->next_pos + su.T > INT32_MAX) return fail(TU_ERR_ARG, "context %d: positions overflow int32", s);
+    if (L_keep + su.T > INT32_MAX / 2) return fail(TU_ERR_ARG, "context %d: too many rows", s);
+    sp->final_iv[s] = sp->rc[s].live_after;
+    append_tail(sp->final_iv[s], su.seq->next_pos, su.T);
+    if ((int64_t)sp->final_iv[s].size() > su.seq->live_cap)
+      return fail(TU_ERR_CAPACITY, "context %d: live-interval list would exceed %d", s, su.seq->live_cap);
+    sp->tail_begin[s + 1] = sp->tail_begin[s] + su.T;
+  }
+  const int64_t total_T = sp->tail_begin[u->n_seq];
+  for (int l = 0; l < u->n_layers; ++l) {
+    const tu_layer_io& L = u->layers[l];
+    if (total_T > 0) {
+      if (!L.q || !L.k || !L.v || !L.out) return fail(TU_ERR_ARG, "layer %d: null tail tensor", l);
+      if (!aligned16(L.q) || !aligned16(L.k) || !aligned16(L.v) || !aligned16(L.out))
+        return fail(TU_ERR_ARG, "layer %d: tail tensors must be 16-byte aligned", l);
+    }
+    if (L.kind == TU_LAYER_ATTN) {
+      if (u->n_seq > 0 && (!L.k_cache || !L.v_cache)) return fail(TU_ERR_ARG, "layer %d: null cache list", l);
+      for (int s = 0; s < u->n_seq; ++s) {
+        if (u->seqs[s].seq->capacity == 0) continue;
+        if (!L.k_cache[s] || !L.v_cache[s]) return fail(TU_ERR_ARG, "layer %d context %d: null cache", l, s);
+        if (!aligned16(L.k_cache[s]) || !aligned16(L.v_cache[s]))
+          return fail(TU_ERR_ARG, "layer %d context %d: caches must be 16-byte aligned", l, s);
+      }
+    } else {
+      if (total_T > 0 && (!L.beta || !L.g)) return fail(TU_ERR_ARG, "layer %d: null beta/g", l);
+      if (u->n_seq > 0 && !L.state) return fail(TU_ERR_ARG, "layer %d: null state list", l);
+      for (int s = 0; s < u->n_seq; ++s) {
+        if (!L.state[s]) return fail(TU_ERR_ARG, "layer %d context %d: null state", l, s);
+        if (!aligned16(L.state[s])) return fail(TU_ERR_ARG, "layer %d context %d: state must be 16-byte aligned", l, s);
+      }
+    }
+  }
+  return TU_OK;
+}
+
+std::vector<CompactItem> stack_compact_items(const tu_update* u, const StackPlan& sp) {
+  std::vector<CompactItem> items;
+  for (int s = 0; s < u->n_seq; ++s) {
+    const tu_seq_update& su = u->seqs[s];
+    CompactItem it;
+    it.seq = su.seq;
+    it.ranges = su.ranges;
+    it.n_ranges = su.n_ranges;
+    it.rc = sp.rc[s];
+    it.src_index = su.src_index;
+    for (int l = 0; l < u->n_layers; ++l)
+      if (u->layers[l].kind == TU_LAYER_ATTN) {
+        it.bufs.push_back(u->layers[l].k_cache[s]);
+        it.bufs.push_back(u->layers[l].v_cache[s]);
+      }
+    items.push_back(std::move(it));
+  }
+  return items;
+}
+
+std::vector<AttnItem> stack_attn_items(const tu_update* u, const StackPlan& sp, const tu_layer_io& L) {
+  std::vector<AttnItem> items;
+  const int64_t qrow = (int64_t)u->attn.n_q_heads * u->attn.head_dim;
+  const int64_t krow = (int64_t)u->attn.n_kv_heads * u->attn.head_dim;
+  for (int s = 0; s < u->n_seq; ++s) {
+    const tu_seq_update& su = u->seqs[s];
+    AttnItem it;
+    it.seq = su.seq;
+    it.L_keep = su.seq->len - sp.rc[s].removed;
+    it.T = su.T;
+    it.cursor = su.seq->next_pos;
+    it.k_cache = L.k_cache ? L.k_cache[s] : nullptr;
+    it.v_cache = L.v_cache ? L.v_cache[s] : nullptr;
+    const int64_t r0 = sp.tail_begin[s];
+    it.q = static_cast<const bf16_t*>(L.q) + r0 * qrow;
+    it.k = static_cast<const bf16_t*>(L.k) + r0 * krow;
+    it.v = static_cast<const bf16_t*>(L.v) + r0 * krow;
+    it.out = L.out + r0 * qrow;
+    it.q_hat = nullptr;
+    items.push_back(it);
+  }
+  return items;
+}
+
+std::vector<DeltaItem> stack_delta_items(const tu_update* u, const StackPlan& sp, const tu_layer_io& L) {
+  std::vector<DeltaItem> items;
+  const int64_t krow = (int64_t)u->delta.n_k_heads * u->delta.d_k;
+  const int64_t vrow = (int64_t)u->delta.n_v_heads * u->delta.d_v;
+  for (int s = 0; s < u->n_seq; ++s) {
+    const int64_t r0 = sp.tail_begin[s];
+    DeltaItem it;
+    it.state = L.state[s];
+    it.q = static_cast<const bf16_t*>(L.q) + r0 * krow;
+    it.k = static_cast<const bf16_t*>(L.k) + r0 * krow;
+    it.v = static_cast<const bf16_t*>(L.v) + r0 * vrow;
+    it.beta = L.beta + r0 * u->delta.n_v_heads;
+    it.g = L.g + r0 * u->delta.n_v_heads;
+    it.out = L.out + r0 * vrow;
+    it.T = u->seqs[s].T;
+    items.push_back(it);
+  }
+  return items;
+}
+
+}  // namespace
+}  // namespace tu
+
+using namespace tu;
+
+extern "C" {
+
+int tu_abi_version(void) { return TU_ABI_VERSION; }
+
+const char* tu_last_error(void) { return g_err.c_str(); }
+
+int tu_validate_ranges(const tu_seq* seq, const int64_t* ranges, int32_t n_ranges, int64_t* n_removed) {
+  if (int e = check_seq(seq)) return e;
+  RangeCheck rc;
+  if (int e = check_ranges(seq, ranges, n_ranges, &rc)) return e;
+  if (n_removed) *n_removed = rc.removed;
+  return ok();
+}
+
+size_t compact_kv_workspace_size(int64_t len, int32_t n_layers, int32_t n_kv_heads, int32_t head_dim) {
+  if (len < 0 || n_layers < 0 || n_kv_heads <= 0 || head_dim <= 0) return 0;
+  const int row_bytes = n_kv_heads * head_dim * 2;
+  if (row_bytes > kGatherStripeBytes) return 0;
+  // the worst case: every row behind the first one moves
+  tu_seq fake{};
+  fake.len = len;
+  std::vector<CompactItem> items(1);
+  items[0].seq = &fake;
+  items[0].n_ranges = 1;
+  items[0].rc.removed = 1;
+  items[0].rc.first_row = 0;
+  items[0].src_index = nullptr;
+  items[0].bufs.assign(2 * (size_t)n_layers, nullptr);
+  fake.len = len + 1;
+  CompactPlan plan;
+  plan_compaction(items, row_bytes, nullptr, &plan);
+  return plan.ws_bytes;
+}
+
+int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_t n_layers, int32_t n_kv_heads,
+               int32_t head_dim, const int64_t* ranges, int32_t n_ranges, int32_t* src_index, void* workspace,
+               size_t workspace_bytes, void* stream) {
+  if (int e = check_seq(seq)) return e;
+  if (n_layers < 0 || (n_layers > 0 && (!k_layers || !v_layers))) return fail(TU_ERR_ARG, "bad layer arrays");
+  if (n_kv_heads <= 0 || head_dim <= 0 || ((long)n_kv_heads * head_dim * 2) % 16)
+    return fail(TU_ERR_ARG, "cache rows must be a positive multiple of 16 bytes");
+  const int row_bytes = n_kv_heads * head_dim * 2;
+  if (row_bytes > kGatherStripeBytes || (row_bytes < 128 && 128 % row_bytes) || (row_bytes > 128 && row_bytes % 128))
+    return fail(TU_ERR_ARG, "unsupported cache row size %d bytes", row_bytes);
+  for (int l = 0; l < n_layers; ++l) {
+    if (!k_layers[l] || !v_layers[l]) return fail(TU_ERR_ARG, "null cache of layer %d", l);
+    if (!aligned16(k_layers[l]) || !aligned16(v_layers[l])) return fail(TU_ERR_ARG, "caches must be 16-byte aligned");
+  }
+  std::vector<CompactItem> items(1);
+  items[0].seq = seq;
+  items[0].ranges = ranges;
+  items[0].n_ranges = n_ranges;
+  items[0].src_index = src_index;
+  if (int e = check_ranges(seq, ranges, n_ranges, &items[0].rc)) return e;
+  if ((int64_t)items[0].rc.live_after.size() > seq->live_cap)
+    return fail(TU_ERR_CAPACITY, "live-interval list would exceed %d", seq->live_cap);
+  for (int l = 0; l < n_layers; ++l) {
+    items[0].bufs.push_back(k_layers[l]);
+    items[0].bufs.push_back(v_layers[l]);
+  }
+  CompactPlan plan;
+  plan_compaction(items, row_bytes, nullptr, &plan);
+  if (!workspace || workspace_bytes < plan.ws_bytes)
+    return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.ws_bytes);
+  if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  items[0].src_index = src_index;
+  plan_compaction(items, row_bytes, workspace, &plan);
+  if (int e = run_compaction(plan, static_cast<hipStream_t>(stream))) return e;
+  const int64_t removed = items[0].rc.removed;
+  commit_intervals(seq, items[0].rc.live_after);
+  seq->len -= removed;
+  return ok();
+}
+
+size_t tail_prefill_attention_workspace_size(const tu_attn_params* p, int64_t T, int64_t len) {
+  if (check_attn(p) || T < 0 || len < 0) return 0;
+  tu_seq fake{};
+  std::vector<AttnItem> items(1);
+  items[0] = AttnItem{&fake, len, T, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  std::vector<AttnLaunch> ls;
+  size_t bytes = 0;
+  plan_attention(p, items, nullptr, &ls, &bytes);
+  return std::max<size_t>(bytes, kAlign);
+}
+
+int tail_prefill_attention(const tu_seq* seq, void* k_cache, void* v_cache, const tu_attn_params* p, const void* q,
+                           const void* k, const void* v, int64_t T, float* out, void* q_hat, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  if (int e = check_seq(seq)) return e;
+  if (int e = check_attn(p)) return e;
+  if (T < 0) return fail(TU_ERR_ARG, "negative T");
+  if (seq->len + T > seq->capacity)
+    return fail(TU_ERR_CAPACITY, "%lld rows + %lld tail rows exceed capacity %lld", (long long)seq->len, (long long)T,
+                (long long)seq->capacity);
+  if (seq->next_pos + T > INT32_MAX) return fail(TU_ERR_ARG, "positions overflow int32");
+  if (T == 0) return ok();
+  if (!k_cache || !v_cache || !q || !k || !v || !out) return fail(TU_ERR_ARG, "null tensor");
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(q) || !aligned16(k) || !aligned16(v) ||
+      !aligned16(out) || (q_hat && !aligned16(q_hat)))
+    return fail(TU_ERR_ARG, "tensors must be 16-byte aligned");
+  std::vector<AttnItem> items(1);
+  items[0] = AttnItem{seq, seq->len, T, seq->next_pos, k_cache, v_cache, static_cast<const bf16_t*>(q),
+                      static_cast<const bf16_t*>(k), static_cast<const bf16_t*>(v), out,
+                      static_cast<bf16_t*>(q_hat)};
+  std::vector<AttnLaunch> ls;
+  size_t need = 0;
+  plan_attention(p, items, nullptr, &ls, &need);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  if (workspace && !aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  plan_attention(p, items, workspace, &ls, &need);
+  if (int e = run_attention(ls, p->head_dim, static_cast<hipStream_t>(stream))) return e;
+  return ok();
+}
+
+int commit_tail(tu_seq* seq, int64_t T) {
+  if (int e = check_seq(seq)) return e;
+  if (T < 0) return fail(TU_ERR_ARG, "negative T");
+  if (seq->len + T > seq->capacity) return fail(TU_ERR_CAPACITY, "commit exceeds capacity");
+  if (seq->next_pos + T > INT32_MAX) return fail(TU_ERR_ARG, "positions overflow int32");
+  std::vector<tu_interval> iv(seq->live, seq->live + seq->n_live);
+  append_tail(iv, seq->next_pos, T);
+  if ((int64_t)iv.size() > seq->live_cap) return fail(TU_ERR_CAPACITY, "live-interval list full");
+  commit_intervals(seq, iv);
+  seq->len += T;
+  seq->next_pos += T;
+  return ok();
+}
+
+size_t delta_rule_continue_workspace_size(const tu_delta_params* p, int64_t T) {
+  if (check_delta(p) || T < 0) return 0;
+  std::vector<DeltaItem> items(1);
+  items[0] = DeltaItem{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, T};
+  std::vector<DeltaArgs> ls;
+  size_t bytes = 0;
+  plan_delta(p, items, nullptr, &ls, &bytes);
+  return std::max<size_t>(bytes, kAlign);
+}
+
+int delta_rule_continue(float* state, const void* q, const void* k, const void* v, const float* beta, const float* g,
+                        int64_t T, const tu_delta_params* p, float* out, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  if (int e = check_delta(p)) return e;
+  if (T < 0) return fail(TU_ERR_ARG, "negative T");
+  if (T == 0) return ok();
+  if (T > INT32_MAX / 2) return fail(TU_ERR_ARG, "T too large");
+  if (!state || !q || !k || !v || !beta || !g || !out) return fail(TU_ERR_ARG, "null tensor");
+  if (!aligned16(state) || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(TU_ERR_ARG, "tensors must be 16-byte aligned");
+  std::vector<DeltaItem> items(1);
+  items[0] = DeltaItem{state, static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
+                       static_cast<const bf16_t*>(v), beta, g, out, T};
+  std::vector<DeltaArgs> ls;
+  size_t need = 0;
+  plan_delta(p, items, nullptr, &ls, &need);
+  if (!workspace || workspace_bytes < need)
+    return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  plan_delta(p, items, workspace, &ls, &need);
+  if (int e = run_delta(ls, p, static_cast<hipStream_t>(stream))) return e;
+  return ok();
+}
+
+size_t update_layer_stack_workspace_size(const tu_update* u) {
+  StackPlan sp;
+  if (validate_stack(u, &sp)) return 0;
+  size_t need = kAlign;
+  if (sp.n_attn) {
+    auto items = stack_compact_items(u, sp);
+    CompactPlan cp;
+    plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, nullptr, &cp);
+    need = std::max(need, cp.ws_bytes);
+  }
+  for (int l = 0; l < u->n_layers; ++l) {
+    size_t b = 0;
+    if (u->layers[l].kind == TU_LAYER_ATTN) {
+      auto items = stack_attn_items(u, sp, u->layers[l]);
+      std::vector<AttnLaunch> ls;
+      plan_attention(&u->attn, items, nullptr, &ls, &b);
+    } else {
+      auto items = stack_delta_items(u, sp, u->layers[l]);
+      std::vector<DeltaArgs> ls;
+      plan_delta(&u->delta, items, nullptr, &ls, &b);
+    }
+    need = std::max(need, b);
+  }
+  return need;
+}
+
+int tu_validate_update(const tu_update* u) {
+  StackPlan sp;
+  if (int e = validate_stack(u, &sp)) return e;
+  return ok();
+}
+
+int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_bytes, void* stream) {
+  StackPlan sp;
+  if (int e = validate_stack(u, &sp)) return e;
+  const size_t need = update_layer_stack_workspace_size(u);
+  if (!workspace || workspace_bytes < need)
+    return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // a2-a3: one keep-scan and one gather over every attention layer of every context
+  if (sp.n_attn) {
+    auto items = stack_compact_items(u, sp);
+    CompactPlan cp;
+    plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, workspace, &cp);
+    if (int e = run_compaction(cp, st)) return e;
+  }
+  // a4-a7 in layer order
+  for (int l = 0; l < u->n_layers; ++l) {
+    const tu_layer_io& L = u->layers[l];
+    size_t b = 0;
+    if (L.kind == TU_LAYER_ATTN) {
+      auto items = stack_attn_items(u, sp, L);
+      std::vector<AttnLaunch> ls;
+      plan_attention(&u->attn, items, workspace, &ls, &b);
+      if (int e = run_attention(ls, u->attn.head_dim, st)) return e;
+    } else {
+      auto items = stack_delta_items(u, sp, L);
+      std::vector<DeltaArgs> ls;
+      plan_delta(&u->delta, items, workspace, &ls, &b);
+      if (int e = run_delta(ls, &u->delta, st)) return e;
+    }
+  }
+  // a8: commit metadata
+  for (int s = 0; s < u->n_seq; ++s) {
+    tu_seq* seq = u->seqs[s].seq;
+    commit_intervals(seq, sp.final_iv[s]);
+    seq->len = seq->len - sp.rc[s].removed + u->seqs[s].T;
+    seq->next_pos += u->seqs[s].T;
+  }
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,200 @@
+// Shared device types and helpers of the tail-update library (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tu {
+
+typedef uint16_t bf16_t;  // bfloat16 storage
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+
+constexpr int kMaxSeqPerLaunch = 16;
+constexpr int kMaxRangesPerLaunch = 128;
+constexpr int kMaxBufPerLaunch = 64;
+constexpr int kGatherStripeBytes = 256 * 8 * 16;  // threads x vectors x 16 B
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// float -> bf16, round to nearest even (inputs are finite).
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// double -> bf16, round to nearest even from the exact value. The double is first
+// rounded to float with round-to-odd (truncate, then force the last bit to 1 when
+// inexact); float carries 16 more significand bits than bf16, so the second
+// rounding to bf16 is then correctly rounded (no double-rounding error).
+__device__ __forceinline__ uint32_t f64_to_bf16_rne(double x) {
+  float f = (float)x;                       // round to nearest
+  uint32_t u = __float_as_uint(f);
+  double back = (double)f;
+  if (back != x) {
+    // step toward zero if the nearest float overshot |x|
+    if (fabs(back) > fabs(x)) u -= 1u;
+    u |= 1u;                                // sticky bit: round-to-odd
+  }
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// XCD-aware remap: blocks are dispatched round-robin over the 8 XCDs (block b runs
+// on XCD b % 8). Returns the work item for block b so that consecutive work items
+// land on the same XCD and share its L2.
+__device__ __forceinline__ int xcd_remap(int b, int n_blocks) {
+  const int per = (n_blocks + 7) >> 3;
+  const int xcd = b & 7;
+  const int slot = b >> 3;
+  return xcd * per + slot;
+}
+
+// ------------------------------------------------------------------ launch records
+
+struct ScanSeq {
+  int32_t* pos;        // [capacity] compacted in place
+  int32_t* src_index;  // [L_old] out
+  int32_t L_old;
+  int32_t range_begin; // index into ScanArgs::ranges
+  int32_t n_ranges;
+  int32_t pad;
+};
+
+struct ScanArgs {
+  ScanSeq seq[kMaxSeqPerLaunch];
+  int32_t ranges[kMaxRangesPerLaunch][2];
+  int32_t n_seq;
+  int32_t zero_count;   // int32 words of gather flags/tickets to clear
+  int32_t* zero_ptr;
+};
+
+struct GatherSeq {
+  const int32_t* src_index;
+  int32_t row_begin;    // first destination row handled (aligned, <= first moved row)
+  int32_t n_keep;       // destination rows end
+  int32_t n_stripes;
+  int32_t item_begin;   // first ticket of this context
+  int32_t buf_begin;    // index of its first buffer in GatherArgs::bufs
+  int32_t n_buf;
+  int32_t flag_begin;   // its stripe read-counters
+  int32_t window;       // stripes before s whose sources may overlap stripe s's rows
+};
+
+struct GatherArgs {
+  GatherSeq seq[kMaxSeqPerLaunch];
+  void* bufs[kMaxBufPerLaunch];
+  int32_t n_seq;
+  int32_t total_items;
+  int32_t rows_per_stripe;
+  int32_t row_bytes;
+  int32_t* ticket;
+  int32_t* flags;
+  int32_t* err;
+};
+
+struct RopeSeq {
+  const bf16_t* q;
+  const bf16_t* k;
+  const bf16_t* v;
+  bf16_t* q_hat;
+  bf16_t* k_cache;
+  bf16_t* v_cache;
+  int32_t* pos;
+  int64_t cursor;
+  int32_t L_keep;
+  int32_t T;
+  int32_t tok_begin;
+  int32_t pad;
+};
+
+struct RopeArgs {
+  RopeSeq seq[kMaxSeqPerLaunch];
+  int32_t n_seq;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t rotary_dim;
+  int32_t pad;
+  double theta;
+};
+
+struct AttnSeq {
+  const bf16_t* q_hat;   // [T][Hq][D]
+  const bf16_t* k_cache; // [cap][Hkv][D]
+  const bf16_t* v_cache;
+  float* out;            // [T][Hq][D]
+  float* part_o;         // [splits][T*Hq][D] (unused when splits == 1)
+  float* part_ml;        // [splits][T*Hq][2]
+  int32_t L_keep;
+  int32_t T;
+  int32_t n_tiles;       // ceil(T*G / 128)
+  int32_t n_splits;
+  int32_t item_begin;
+  int32_t pad;
+};
+
+struct AttnArgs {
+  AttnSeq seq[kMaxSeqPerLaunch];
+  int32_t n_seq;
+  int32_t total_items;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  float scale_log2;      // softmax_scale * log2(e)
+  int32_t pad;
+};
+
+struct MergeArgs {
+  AttnSeq seq[kMaxSeqPerLaunch];
+  int32_t n_seq;
+  int32_t n_q_heads;
+  int32_t row_begin[kMaxSeqPerLaunch + 1];  // prefix of T*Hq over contexts
+};
+
+struct DeltaSeq {
+  const bf16_t* q;       // [T][Hk][dk]
+  const bf16_t* k;
+  const bf16_t* v;       // [T][Hv][dv]
+  const float* beta;     // [T][Hv]
+  const float* g;
+  float* state;          // [Hv][dv][dk]
+  float* out;            // [T][Hv][dv]
+  int32_t T;
+  int32_t n_chunks;
+  int32_t chunk_begin;   // first global chunk index (workspace slot)
+  int32_t pad;
+};
+
+struct DeltaArgs {
+  DeltaSeq seq[kMaxSeqPerLaunch];
+  int32_t n_seq;
+  int32_t n_k_heads;
+  int32_t n_v_heads;
+  int32_t total_chunks;
+  float scale;
+  int32_t n_slices;      // d_v slices per value head in the chain kernel
+  _Float16* ws_w;        // [chunks][Hv][C][dk]
+  float* ws_u;           // [chunks][Hv][C][dv]
+  _Float16* ws_p;        // [chunks][Hv][C][C]
+  float* ws_lg;          // [chunks][Hv][C]
+};
+
+// ------------------------------------------------------------------ launchers
+// (defined in the kernel translation units; return a hipError_t)
+hipError_t launch_keep_scan(const ScanArgs& a, hipStream_t s);
+hipError_t launch_gather(const GatherArgs& a, int n_blocks, hipStream_t s);
+hipError_t launch_rope_append(const RopeArgs& a, int total_tokens, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_attention_merge(const MergeArgs& a, int total_rows, int head_dim, hipStream_t s);
+hipError_t launch_delta_prep(const DeltaArgs& a, int d, int chunk, hipStream_t s);
+hipError_t launch_delta_chain(const DeltaArgs& a, int d, int chunk, hipStream_t s);
+
+}  // namespace tu

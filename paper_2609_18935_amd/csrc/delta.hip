@@ -1,0 +1,505 @@
+// Gated delta-rule continuation (paper Section 4.1, Eq. 3: the recurrent state
+// continues from its previous value over the replacement tokens; the layers are
+// Gated DeltaNet layers, Yang et al. 2025). Per value head the state S (d_v x d_k)
+// follows
+//     S_t = g_t S_{t-1} (I - beta_t k_t k_t^T) + beta_t v_t k_t^T,   o_t = scale S_t q_t.
+//
+// The tail is cut into chunks of C tokens starting at its first token. Inside a
+// chunk (rows r, i), with lg_r = sum_{s<=r} log2 g_s and G[r][i] = 2^(lg_r - lg_i):
+//     M = strictly-lower(diag(beta) (G .* K K^T)),   T = (I + M)^-1
+//     W = T diag(beta 2^lg) K,   U~ = T diag(beta) V                     (k_delta_prep)
+//     U = U~ - W S^T
+//     O = scale (diag(2^lg) Q S^T + lower(G .* Q K^T) U)
+//     S <- 2^lg_last S + U^T diag(2^(lg_last - lg)) K                      (k_delta_chain)
+// Only decay ratios <= 1 are formed. A ragged last chunk is padded with k = q = v = 0,
+// beta = 0, g = 1, which leaves the recurrence unchanged.
+//
+// k_delta_prep: one workgroup per (chunk, value head), all chunks in parallel.
+//   K K^T and Q K^T on v_mfma_f32_16x16x32_bf16 (exact bf16 products, fp32 sums);
+//   T by blocked forward substitution in fp32 (16x16 diagonal blocks by one lane per
+//   column, then off-diagonal blocks level by level); W and U~ on
+//   v_mfma_f32_16x16x32_f16 with T and the scaled K, V rounded to f16. Writes W (f16),
+//   U~ (fp32), P = scale * lower(G .* Q K^T) (f16) and lg (fp32) to the workspace.
+// k_delta_chain: one workgroup per (context, value head, slice of DVS rows of S). Rows
+//   of S evolve independently (row i only needs U[:, i]), so slicing d_v spreads a
+//   head over several workgroups. The fp32 state slice lives in MFMA accumulators
+//   for the whole tail, is read from HBM once and written once; each chunk it is
+//   rounded to f16 into LDS to serve as the MFMA operand of W S^T and Q S^T.
+//   f16 (10 stored mantissa bits) keeps the operands of these fp32-intermediate
+//   products accurate enough for the error bound where bf16 would not.
+#include "common.h"
+
+namespace tu {
+
+namespace {
+
+typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2;
+
+__device__ __forceinline__ f16x8 ld_f16x8(const _Float16* p) { return __builtin_bit_cast(f16x8, *(const u32x4*)p); }
+__device__ __forceinline__ bf16x8 ld_bf16x8(const bf16_t* p) { return __builtin_bit_cast(bf16x8, *(const u32x4*)p); }
+__device__ __forceinline__ f16x8 zero_f16x8() { return __builtin_bit_cast(f16x8, u32x4{0, 0, 0, 0}); }
+
+__device__ __forceinline__ f32x4 mfma_f16(f16x8 a, f16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// 8 bf16 -> 8 f16 (values are well inside the f16 range)
+__device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 w) {
+  f16x8 h;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const uint32_t bits = (e & 1) ? (w[e >> 1] & 0xFFFF0000u) : (w[e >> 1] << 16);
+    h[e] = (_Float16)__uint_as_float(bits);
+  }
+  return __builtin_bit_cast(u32x4, h);
+}
+
+__device__ __forceinline__ int find_seq_by_chunk(const DeltaArgs& a, int c) {
+  int si = 0;
+  while (si + 1 < a.n_seq && a.seq[si + 1].chunk_begin <= c) ++si;
+  return si;
+}
+
+// ------------------------------------------------------------------ prep
+template <int DK, int C>
+__global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
+  constexpr int DV = DK;
+  constexpr int NB = C / 16;     // 16-row blocks of the chunk
+  constexpr int KP = DK + 8;     // pitch of [C][DK] bf16 tiles
+  constexpr int CP = C + 4;      // pitch of [C][C] fp32 tiles
+  constexpr int CH = C + 8;      // pitch of [*][C] f16 tiles
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[C][KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Qs[C][KP];
+  __shared__ __attribute__((aligned(16))) float Mf[C][CP];
+  __shared__ __attribute__((aligned(16))) float Tf[C][CP];
+  __shared__ __attribute__((aligned(16))) float Xs[3][16][20];
+  __shared__ __attribute__((aligned(16))) _Float16 Th[C][CH];
+  __shared__ __attribute__((aligned(16))) _Float16 Bt[DK][CH];
+  __shared__ __attribute__((aligned(16))) _Float16 Vt[DV][CH];
+  __shared__ float lg[C];
+  __shared__ float bt[C];
+
+  const int Hk = a.n_k_heads, Hv = a.n_v_heads;
+  const int c = blockIdx.x / Hv;          // global chunk
+  const int h = blockIdx.x - c * Hv;      // value head
+  const int si = find_seq_by_chunk(a, c);
+  const DeltaSeq S = a.seq[si];
+  const int t0 = (c - S.chunk_begin) * C;
+  const int Cr = min(C, S.T - t0);
+  const int kh = h / (Hv / Hk);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g4 = lane >> 4;
+
+  // ---- phase 0: stage K, Q (bf16), beta, log2 g
+  for (int e = tid; e < C * (DK / 8); e += 256) {
+    const int r = e / (DK / 8), cc = e - r * (DK / 8);
+    u32x4 kw = {0, 0, 0, 0}, qw = {0, 0, 0, 0};
+    if (r < Cr) {
+      const long off = ((long)(t0 + r) * Hk + kh) * DK + cc * 8;
+      kw = *(const u32x4*)(S.k + off);
+      qw = *(const u32x4*)(S.q + off);
+    }
+    *(u32x4*)&Ks[r][cc * 8] = kw;
+    *(u32x4*)&Qs[r][cc * 8] = qw;
+  }
+  if (tid < C) {
+    const bool ok = tid < Cr;
+    bt[tid] = ok ? S.beta[(long)(t0 + tid) * Hv + h] : 0.f;
+    lg[tid] = ok ? __log2f(S.g[(long)(t0 + tid) * Hv + h]) : 0.f;
+  }
+  __syncthreads();
+
+  // ---- phase 1: cumulative log-decay (wave 0) and K K^T, Q K^T lower blocks (MFMA)
+  if (wave == 0) {
+    float x = lane < C ? lg[lane] : 0.f;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const float y = __shfl_up(x, d, 64);
+      if (lane >= d) x += y;
+    }
+    if (lane < C) lg[lane] = x;
+  }
+  constexpr int NLB = NB * (NB + 1) / 2;   // lower blocks incl. diagonal
+  constexpr int NPW = (2 * NLB + 3) / 4;   // blocks per wave (KK and QK together)
+  f32x4 acc[NPW];
+  int blk_of[NPW];
+#pragma unroll
+  for (int j = 0; j < NPW; ++j) {
+    const int idx = wave + 4 * j;
+    blk_of[j] = idx;
+    acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (idx < 2 * NLB) {
+      const int li = idx % NLB;
+      const bool is_q = idx >= NLB;
+      int bi = 0;
+      while ((bi + 1) * (bi + 2) / 2 <= li) ++bi;
+      const int bj = li - bi * (bi + 1) / 2;
+#pragma unroll
+      for (int kk = 0; kk < DK / 32; ++kk) {
+        const bf16x8 av = is_q ? ld_bf16x8(&Qs[16 * bi + l16][32 * kk + 8 * g4])
+                               : ld_bf16x8(&Ks[16 * bi + l16][32 * kk + 8 * g4]);
+        const bf16x8 bv = ld_bf16x8(&Ks[16 * bj + l16][32 * kk + 8 * g4]);
+        acc[j] = mfma_bf16(av, bv, acc[j]);
+      }
+    }
+  }
+  __syncthreads();   // lg ready
+
+  // ---- phase 2: M (fp32, LDS) and P (f16, workspace) from the MFMA results
+  const long slot = (long)c * Hv + h;
+  _Float16* Pg = a.ws_p + slot * C * C;
+#pragma unroll
+  for (int j = 0; j < NPW; ++j) {
+    const int idx = blk_of[j];
+    if (idx >= 2 * NLB) continue;
+    const int li = idx % NLB;
+    const bool is_q = idx >= NLB;
+    int bi = 0;
+    while ((bi + 1) * (bi + 2) / 2 <= li) ++bi;
+    const int bj = li - bi * (bi + 1) / 2;
+    const int i = 16 * bj + l16;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * bi + 4 * g4 + e;
+      const float gam = __builtin_amdgcn_exp2f(fminf(lg[r] - lg[i], 0.f));
+      if (is_q)
+        Pg[r * C + i] = (_Float16)(i <= r ? a.scale * gam * acc[j][e] : 0.f);
+      else
+        Mf[r][i] = i < r ? bt[r] * gam * acc[j][e] : 0.f;
+    }
+  }
+  // zero the upper blocks of P
+  for (int e = tid; e < C * C; e += 256) {
+    const int r = e / C, i = e - r * C;
+    if ((i >> 4) > (r >> 4)) Pg[r * C + i] = (_Float16)0.f;
+  }
+  if (tid < C) a.ws_lg[slot * C + tid] = lg[tid];
+  __syncthreads();
+
+  // ---- phase 3: diagonal 16x16 blocks of T = (I + M)^-1, one lane per column
+  if (wave == 0 && g4 < NB) {
+    const int b = g4, cc = l16;
+    float x[16];
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) {
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < rr; ++i) s += Mf[16 * b + rr][16 * b + i] * x[i];
+      x[rr] = rr < cc ? 0.f : (rr == cc ? 1.f : -s);
+    }
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) Tf[16 * b + rr][16 * b + cc] = x[rr];
+  }
+  __syncthreads();
+
+  // ---- phase 4: off-diagonal blocks, level by level: T_ij = -T_ii sum_{m=j}^{i-1} M_im T_mj
+#pragma unroll
+  for (int lev = 1; lev < NB; ++lev) {
+    const int nblk = NB - lev;
+    const int q = tid >> 6;            // block of this thread (64 threads per block)
+    const int rr = (tid >> 2) & 15;
+    const int c4 = (tid & 3) * 4;
+    if (q < nblk) {
+      const int j = q, i = q + lev;
+      f32x4 x = {0.f, 0.f, 0.f, 0.f};
+      for (int m = j; m < i; ++m)
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+          x += Mf[16 * i + rr][16 * m + k] * *(const f32x4*)&Tf[16 * m + k][16 * j + c4];
+      *(f32x4*)&Xs[q][rr][c4] = x;
+    }
+    __syncthreads();
+    if (q < nblk) {
+      const int j = q, i = q + lev;
+      f32x4 y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < 16; ++k) y += Tf[16 * i + rr][16 * i + k] * *(const f32x4*)&Xs[q][k][c4];
+      *(f32x4*)&Tf[16 * i + rr][16 * j + c4] = -y;
+    }
+    __syncthreads();
+  }
+
+  // ---- phase 5: f16 copies: T (lower, zero upper), (beta 2^lg K)^T and (beta V)^T
+  for (int e = tid; e < C * C; e += 256) {
+    const int r = e / C, i = e - r * C;
+    Th[r][i] = (_Float16)((i >> 4) <= (r >> 4) ? Tf[r][i] : 0.f);
+  }
+  for (int e = tid; e < (C / 4) * (DK / 8); e += 256) {
+    const int s4 = (e % (C / 4)) * 4, d0 = (e / (C / 4)) * 8;
+    float wk[4], wv[4];
+    u32x4 kw[4], vw[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int s = s4 + j;
+      wv[j] = bt[s];
+      wk[j] = bt[s] * __builtin_amdgcn_exp2f(lg[s]);
+      kw[j] = *(const u32x4*)&Ks[s][d0];
+      vw[j] = (s < Cr) ? *(const u32x4*)(S.v + ((long)(t0 + s) * Hv + h) * DV + d0) : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      f16x4 hk, hv;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t kb = (d & 1) ? (kw[j][d >> 1] & 0xFFFF0000u) : (kw[j][d >> 1] << 16);
+        const uint32_t vb = (d & 1) ? (vw[j][d >> 1] & 0xFFFF0000u) : (vw[j][d >> 1] << 16);
+        hk[j] = (_Float16)(wk[j] * __uint_as_float(kb));
+        hv[j] = (_Float16)(wv[j] * __uint_as_float(vb));
+      }
+      *(f16x4*)&Bt[d0 + d][s4] = hk;
+      *(f16x4*)&Vt[d0 + d][s4] = hv;
+    }
+  }
+  __syncthreads();
+
+  // ---- phase 6: W = T (beta 2^lg K), U~ = T (beta V) on MFMA; write to workspace
+  _Float16* Wg = a.ws_w + slot * C * DK;
+  float* Ug = a.ws_u + slot * C * DV;
+  constexpr int NOB = NB * (DK / 16);   // output blocks per matrix
+  for (int idx = wave; idx < 2 * NOB; idx += 4) {
+    const bool is_u = idx >= NOB;
+    const int b = idx % NOB;
+    const int rb = b / (DK / 16), db = b % (DK / 16);
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < (C + 31) / 32; ++kk) {
+      f16x8 av = zero_f16x8(), bv = zero_f16x8();
+      if (C >= 32 || g4 < 2) {
+        av = ld_f16x8(&Th[16 * rb + l16][32 * kk + 8 * g4]);
+        bv = is_u ? ld_f16x8(&Vt[16 * db + l16][32 * kk + 8 * g4]) : ld_f16x8(&Bt[16 * db + l16][32 * kk + 8 * g4]);
+      }
+      o = mfma_f16(av, bv, o);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * rb + 4 * g4 + e, d = 16 * db + l16;
+      if (is_u)
+        Ug[r * DV + d] = o[e];
+      else
+        Wg[r * DK + d] = (_Float16)o[e];
+    }
+  }
+}
+
+// ------------------------------------------------------------------ chain
+template <int DK, int C, int DVS>
+__global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
+  constexpr int DV = DK;
+  constexpr int KP = DK + 8;
+  constexpr int CH = C + 8;
+  constexpr int NCB = DVS / 16;                 // column blocks of the slice
+  constexpr int NXB = (C / 16) * NCB;           // blocks of W S^T / Q S^T / O
+  constexpr int NXW = (NXB + 3) / 4;            // per wave
+  constexpr int NSB = (DK / 16) * NCB;          // blocks of S^T
+  constexpr int NSW = NSB / 4;                  // per wave
+  static_assert(NSB % 4 == 0, "state blocks must split over 4 waves");
+  __shared__ __attribute__((aligned(16))) _Float16 Ws[C][KP];
+  __shared__ __attribute__((aligned(16))) _Float16 Qs[C][KP];
+  __shared__ __attribute__((aligned(16))) _Float16 Kdt[DK][CH];
+  __shared__ __attribute__((aligned(16))) _Float16 Ph[C][CH];
+  __shared__ __attribute__((aligned(16))) _Float16 Ut[DVS][CH];
+  __shared__ __attribute__((aligned(16))) _Float16 Sh[DVS][KP];
+  __shared__ float lg[C];
+
+  const int Hk = a.n_k_heads, Hv = a.n_v_heads;
+  const int per_seq = Hv * a.n_slices;
+  const int si = blockIdx.x / per_seq;
+  const int rem = blockIdx.x - si * per_seq;
+  const int h = rem / a.n_slices;
+  const int i0 = (rem - h * a.n_slices) * DVS;
+  const DeltaSeq S = a.seq[si];
+  const int kh = h / (Hv / Hk);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g4 = lane >> 4;
+  const bool kpart = (C >= 32) || (g4 < 2);     // lanes that carry chunk-dim K elements
+
+  // ---- load the state slice: S^T blocks (d rows, i cols) in accumulators, f16 copy in LDS
+  float* Sg = S.state + (long)h * DV * DK;
+  f32x4 st[NSW];
+#pragma unroll
+  for (int j = 0; j < NSW; ++j) {
+    const int b = wave + 4 * j;
+    const int db = b / NCB, cb = b % NCB;
+    const int i = 16 * cb + l16, d = 16 * db + 4 * g4;
+    st[j] = *(const f32x4*)(Sg + (long)(i0 + i) * DK + d);
+    f16x4 hv = {(_Float16)st[j][0], (_Float16)st[j][1], (_Float16)st[j][2], (_Float16)st[j][3]};
+    *(f16x4*)&Sh[i][d] = hv;
+  }
+
+  for (int lc = 0; lc < S.n_chunks; ++lc) {
+    const int c = S.chunk_begin + lc;
+    const long slot = (long)c * Hv + h;
+    const int t0 = lc * C;
+    const int Cr = min(C, S.T - t0);
+    // ---- stage W, Q (as f16), P and lg
+    {
+      const _Float16* Wg = a.ws_w + slot * C * DK;
+      for (int e = tid; e < C * (DK / 8); e += 256) {
+        const int r = e / (DK / 8), cc = e - r * (DK / 8);
+        *(u32x4*)&Ws[r][cc * 8] = *(const u32x4*)(Wg + r * DK + cc * 8);
+        u32x4 qw = {0, 0, 0, 0};
+        if (r < Cr) qw = bf16x8_to_f16x8(*(const u32x4*)(S.q + ((long)(t0 + r) * Hk + kh) * DK + cc * 8));
+        *(u32x4*)&Qs[r][cc * 8] = qw;
+      }
+      const _Float16* Pg = a.ws_p + slot * C * C;
+      for (int e = tid; e < C * (C / 8); e += 256) {
+        const int r = e / (C / 8), cc = e - r * (C / 8);
+        *(u32x4*)&Ph[r][cc * 8] = *(const u32x4*)(Pg + r * C + cc * 8);
+      }
+      if (tid < C) lg[tid] = a.ws_lg[slot * C + tid];
+    }
+    __syncthreads();
+    const float lg_last = lg[C - 1];
+    const float g_last = __builtin_amdgcn_exp2f(lg_last);
+    // K^T scaled by the decay to the chunk end, as f16
+    for (int e = tid; e < (C / 4) * (DK / 8); e += 256) {
+      const int s4 = (e % (C / 4)) * 4, d0 = (e / (C / 4)) * 8;
+      u32x4 kw[4];
+      float w[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int s = s4 + j;
+        w[j] = __builtin_amdgcn_exp2f(lg_last - lg[s]);
+        kw[j] = (s < Cr) ? *(const u32x4*)(S.k + ((long)(t0 + s) * Hk + kh) * DK + d0) : u32x4{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        f16x4 hk;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t kb = (d & 1) ? (kw[j][d >> 1] & 0xFFFF0000u) : (kw[j][d >> 1] << 16);
+          hk[j] = (_Float16)(w[j] * __uint_as_float(kb));
+        }
+        *(f16x4*)&Kdt[d0 + d][s4] = hk;
+      }
+    }
+
+    // ---- X = W S^T -> U = U~ - X (to LDS as U^T);  Y = Q S^T -> O accumulator
+    f32x4 oacc[NXW];
+#pragma unroll
+    for (int j = 0; j < NXW; ++j) {
+      const int b = wave + 4 * j;
+      oacc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (b >= NXB) continue;
+      const int rb = b / NCB, cb = b % NCB;
+      f32x4 x = {0.f, 0.f, 0.f, 0.f}, y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < DK / 32; ++kk) {
+        const f16x8 sv = ld_f16x8(&Sh[16 * cb + l16][32 * kk + 8 * g4]);
+        x = mfma_f16(ld_f16x8(&Ws[16 * rb + l16][32 * kk + 8 * g4]), sv, x);
+        y = mfma_f16(ld_f16x8(&Qs[16 * rb + l16][32 * kk + 8 * g4]), sv, y);
+      }
+      const float* Ug = a.ws_u + slot * C * DV + i0 + 16 * cb + l16;
+      f16x4 uh;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 16 * rb + 4 * g4 + e;
+        uh[e] = (_Float16)(Ug[(long)r * DV] - x[e]);
+        oacc[j][e] = y[e] * a.scale * __builtin_amdgcn_exp2f(lg[r]);
+      }
+      *(f16x4*)&Ut[16 * cb + l16][16 * rb + 4 * g4] = uh;
+    }
+    __syncthreads();
+
+    // ---- O += P U, written out; S^T <- 2^lg_last S^T + Kd^T U
+#pragma unroll
+    for (int j = 0; j < NXW; ++j) {
+      const int b = wave + 4 * j;
+      if (b >= NXB) continue;
+      const int rb = b / NCB, cb = b % NCB;
+      f32x4 o = oacc[j];
+#pragma unroll
+      for (int kk = 0; kk < (C + 31) / 32; ++kk) {
+        f16x8 av = zero_f16x8(), bv = zero_f16x8();
+        if (kpart) {
+          av = ld_f16x8(&Ph[16 * rb + l16][32 * kk + 8 * g4]);
+          bv = ld_f16x8(&Ut[16 * cb + l16][32 * kk + 8 * g4]);
+        }
+        o = mfma_f16(av, bv, o);
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 16 * rb + 4 * g4 + e;
+        if (r < Cr) S.out[((long)(t0 + r) * Hv + h) * DV + i0 + 16 * cb + l16] = o[e];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NSW; ++j) {
+      const int b = wave + 4 * j;
+      const int db = b / NCB, cb = b % NCB;
+      f32x4 s = st[j] * g_last;
+#pragma unroll
+      for (int kk = 0; kk < (C + 31) / 32; ++kk) {
+        f16x8 av = zero_f16x8(), bv = zero_f16x8();
+        if (kpart) {
+          av = ld_f16x8(&Kdt[16 * db + l16][32 * kk + 8 * g4]);
+          bv = ld_f16x8(&Ut[16 * cb + l16][32 * kk + 8 * g4]);
+        }
+        s = mfma_f16(av, bv, s);
+      }
+      st[j] = s;
+    }
+    __syncthreads();   // all reads of Sh / Ut / staged tiles done
+#pragma unroll
+    for (int j = 0; j < NSW; ++j) {
+      const int b = wave + 4 * j;
+      const int db = b / NCB, cb = b % NCB;
+      f16x4 hv = {(_Float16)st[j][0], (_Float16)st[j][1], (_Float16)st[j][2], (_Float16)st[j][3]};
+      *(f16x4*)&Sh[16 * cb + l16][16 * db + 4 * g4] = hv;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NSW; ++j) {
+    const int b = wave + 4 * j;
+    const int db = b / NCB, cb = b % NCB;
+    *(f32x4*)(Sg + (long)(i0 + 16 * cb + l16) * DK + 16 * db + 4 * g4) = st[j];
+  }
+}
+
+template <int DK, int C>
+hipError_t prep_for(const DeltaArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((k_delta_prep<DK, C>), dim3(a.total_chunks * a.n_v_heads), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int DK, int C>
+hipError_t chain_for(const DeltaArgs& a, hipStream_t s) {
+  const int blocks = a.n_seq * a.n_v_heads * a.n_slices;
+  const int dvs = DK / a.n_slices;
+  if (dvs == 32)
+    hipLaunchKernelGGL((k_delta_chain<DK, C, 32>), dim3(blocks), dim3(256), 0, s, a);
+  else if (dvs == 64)
+    hipLaunchKernelGGL((k_delta_chain<DK, C, 64>), dim3(blocks), dim3(256), 0, s, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_delta_prep(const DeltaArgs& a, int d, int chunk, hipStream_t s) {
+  if (a.total_chunks <= 0) return hipSuccess;
+  if (d == 128 && chunk == 64) return prep_for<128, 64>(a, s);
+  if (d == 128 && chunk == 32) return prep_for<128, 32>(a, s);
+  if (d == 128 && chunk == 16) return prep_for<128, 16>(a, s);
+  if (d == 64 && chunk == 64) return prep_for<64, 64>(a, s);
+  if (d == 64 && chunk == 32) return prep_for<64, 32>(a, s);
+  if (d == 64 && chunk == 16) return prep_for<64, 16>(a, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_delta_chain(const DeltaArgs& a, int d, int chunk, hipStream_t s) {
+  if (a.total_chunks <= 0) return hipSuccess;
+  if (d == 128 && chunk == 64) return chain_for<128, 64>(a, s);
+  if (d == 128 && chunk == 32) return chain_for<128, 32>(a, s);
+  if (d == 128 && chunk == 16) return chain_for<128, 16>(a, s);
+  if (d == 64 && chunk == 64) return chain_for<64, 64>(a, s);
+  if (d == 64 && chunk == 32) return chain_for<64, 32>(a, s);
+  if (d == 64 && chunk == 16) return chain_for<64, 16>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace tu

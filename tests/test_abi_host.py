@@ -1,0 +1,177 @@
+"""C-ABI tests that need no GPU: the library loads, exports every function the
+header declares, and its host-side verification (Section 4.2: deletion ranges
+are checked against the live spans before anything is removed) accepts and
+rejects exactly what it should, leaving the metadata unchanged on error.
+
+Device pointers below are host addresses that the host-only checks never
+dereference.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_18935_amd as tu
+from paper_2609_18935_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tailupdate.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(B.LIB_PATH):
+        B_build = __import__("paper_2609_18935_amd.build", fromlist=["build"])
+        B_build.build()
+    return B.lib()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?(?:int|size_t|char\s*\*|const char\s*\*)\s*\*?\s*(\w+)\s*\(", text, re.M)
+    return sorted(set(names))
+
+
+def test_header_functions_are_exported(L):
+    names = _declared_functions()
+    assert {"compact_kv", "tail_prefill_attention", "delta_rule_continue", "update_layer_stack"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in tailupdate.h but not exported"
+    assert set(names) == set(B._SIGNATURES), "binding signatures out of sync with the header"
+    assert L.tu_abi_version() == 1
+
+
+def _ctx(intervals, cursor, capacity=None, live_cap=64):
+    n = sum(b - a for a, b in intervals)
+    ctx = tu.Context(capacity if capacity is not None else n + 64, device="cpu", live_cap=live_cap)
+    ctx.set_metadata(intervals, cursor)
+    return ctx
+
+
+def test_validate_ranges_matches_oracle(L):
+    rng = np.random.default_rng(5)
+    for trial in range(300):
+        # random live set with holes, random candidate ranges (valid or not)
+        cursor = int(rng.integers(10, 200))
+        live = np.sort(rng.choice(cursor, size=int(rng.integers(1, cursor)), replace=False))
+        ivs = []
+        for p in live.tolist():
+            if ivs and ivs[-1][1] == p:
+                ivs[-1] = (ivs[-1][0], p + 1)
+            else:
+                ivs.append((p, p + 1))
+        ctx = _ctx(ivs, cursor)
+        n = int(rng.integers(0, 4))
+        starts = np.sort(rng.integers(-2, cursor + 2, size=n))
+        ranges = [(int(a), int(a + rng.integers(0, 6))) for a in starts]
+        try:
+            oracle.validate_ranges(ranges, live, cursor)
+            expect_ok = True
+        except oracle.RangeError:
+            expect_ok = False
+        before = (ctx.intervals(), ctx.len, ctx.next_pos)
+        if expect_ok:
+            assert ctx.validate_ranges(ranges) == sum(b - a for a, b in ranges)
+        else:
+            with pytest.raises(tu.TailUpdateError) as ei:
+                ctx.validate_ranges(ranges)
+            assert ei.value.code == B.TU_ERR_RANGE
+        assert (ctx.intervals(), ctx.len, ctx.next_pos) == before
+
+
+def _stack(ctx_list, ranges, tails, kinds, cap_ok=True):
+    attn = tu.attn_params(16, 2, 256)
+    delta = tu.delta_params(16, 32, 128, 128, 64)
+    fake = torch.zeros(64, dtype=torch.float32)   # 16-byte aligned host buffer, never read
+    layers = []
+    for kind in kinds:
+        if kind == "attn":
+            layers.append(tu.LayerIO(B.TU_LAYER_ATTN, fake, fake, fake, fake,
+                                     k_cache=[fake] * len(ctx_list), v_cache=[fake] * len(ctx_list)))
+        else:
+            layers.append(tu.LayerIO(B.TU_LAYER_DELTA, fake, fake, fake, fake, state=[fake] * len(ctx_list),
+                                     beta=fake, g=fake))
+    return tu.StackUpdate(ctx_list, ranges, tails, layers, attn, delta)
+
+
+def test_validate_update_accepts_and_sizes(L):
+    a = _ctx([(0, 1000)], 1000, capacity=2000)
+    b = _ctx([(0, 10), (20, 500)], 600, capacity=1000)
+    up = _stack([a, b], [[(100, 228)], [(30, 40), (300, 310)]], [512, 256], ["attn", "delta"])
+    up.validate()
+    assert up.workspace_size() > 0
+
+
+@pytest.mark.parametrize("case,code", [
+    ("capacity", B.TU_ERR_CAPACITY),
+    ("range_not_live", B.TU_ERR_RANGE),
+    ("range_past_cursor", B.TU_ERR_RANGE),
+    ("duplicate_context", B.TU_ERR_ARG),
+    ("bad_heads", B.TU_ERR_ARG),
+    ("interval_list_full", B.TU_ERR_CAPACITY),
+])
+def test_validate_update_rejects(L, case, code):
+    a = _ctx([(0, 1000)], 1000, capacity=1600)
+    ctxs, ranges, tails, kinds = [a], [[(100, 228)]], [512], ["attn", "delta"]
+    if case == "capacity":
+        tails = [800]
+    elif case == "range_not_live":
+        a.set_metadata([(0, 100), (200, 1100)], 1100)
+        ranges = [[(90, 110)]]
+    elif case == "range_past_cursor":
+        ranges = [[(990, 1010)]]
+    elif case == "duplicate_context":
+        ctxs, ranges, tails = [a, a], [[], []], [1, 1]
+    elif case == "interval_list_full":
+        a = _ctx([(0, 1000)], 1000, capacity=1600, live_cap=2)
+        ctxs = [a]
+        ranges = [[(100, 110), (200, 210)]]
+    up = _stack(ctxs, ranges, tails, kinds)
+    if case == "bad_heads":
+        up.u.attn.n_q_heads = 15
+    before = (a.intervals(), a.len, a.next_pos)
+    with pytest.raises(tu.TailUpdateError) as ei:
+        up.validate()
+    assert ei.value.code == code
+    assert (a.intervals(), a.len, a.next_pos) == before
+    assert L.update_layer_stack_workspace_size(ctypes.byref(up.u)) == 0
+
+
+def test_entry_points_reject_before_touching_device(L):
+    # invalid calls must fail in the host checks; no device memory is involved
+    a = _ctx([(0, 100)], 100, capacity=120)
+    fake = torch.zeros(64).view(-1, 1, 64)
+    before = (a.intervals(), a.len)
+    with pytest.raises(tu.TailUpdateError) as ei:   # range crosses the cursor
+        tu.compact_kv(a, [fake], [fake], [(90, 101)], workspace=torch.zeros(1 << 16, dtype=torch.uint8))
+    assert ei.value.code == B.TU_ERR_RANGE
+    with pytest.raises(tu.TailUpdateError) as ei:   # too small a workspace
+        tu.compact_kv(a, [fake], [fake], [(10, 20)],
+                      workspace=torch.zeros(16, dtype=torch.uint8))
+    assert ei.value.code == B.TU_ERR_WORKSPACE
+    assert (a.intervals(), a.len) == before
+    p = tu.attn_params(16, 2, 256)
+    with pytest.raises(tu.TailUpdateError) as ei:   # capacity
+        tu.tail_prefill_attention(a, fake, fake, p, torch.zeros(30, 16, 256, dtype=torch.bfloat16),
+                                  fake, fake, fake, workspace=torch.zeros(256, dtype=torch.uint8))
+    assert ei.value.code == B.TU_ERR_CAPACITY
+    d = tu.delta_params(16, 32, 128, 128, 48)
+    with pytest.raises(tu.TailUpdateError) as ei:   # unsupported chunk
+        tu.delta_rule_continue(fake, torch.zeros(4, 16, 128, dtype=torch.bfloat16), fake, fake, fake, fake, d, fake,
+                               workspace=torch.zeros(256, dtype=torch.uint8))
+    assert ei.value.code == B.TU_ERR_ARG
+
+
+def test_commit_tail_advances_cursor_and_intervals(L):
+    a = _ctx([(0, 10), (20, 30)], 40, capacity=100)
+    tu.commit_tail(a, 5)
+    assert a.intervals() == [(0, 10), (20, 30), (40, 45)] and a.len == 25 and a.next_pos == 45
+    tu.commit_tail(a, 3)
+    assert a.intervals() == [(0, 10), (20, 30), (40, 48)] and a.next_pos == 48
+    with pytest.raises(tu.TailUpdateError):
+        tu.commit_tail(a, 1000)

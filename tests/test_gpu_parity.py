@@ -1,0 +1,263 @@
+"""GPU parity of the HIP path against the float64 oracle (MI355X only).
+
+Every call goes through the C ABI (libtailupdate.so) via the ctypes binding.
+Inputs are the seeded synthetic workloads of `synth`; each test prints the case
+it runs before the GPU work so a failure names it.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import paper_2609_18935_amd as tu
+from gpu_cases import (AttnCase, DeltaCase, DEV, assert_bf16_close_bits, assert_close, bits_of, errors,
+                       to_dev_bf16)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    tu.lib()
+
+
+def _say(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def _ctx_for(case: AttnCase):
+    ctx = tu.Context(case.capacity, device=DEV)
+    ctx.pos[: case.L_old] = torch.from_numpy(case.positions.astype(np.int32)).to(DEV)
+    iv = []
+    for p in case.positions.tolist():
+        if iv and iv[-1][1] == p:
+            iv[-1] = (iv[-1][0], p + 1)
+        else:
+            iv.append((p, p + 1))
+    ctx.set_metadata(iv, int(case.positions[-1]) + 1 if case.L_old else 0)
+    return ctx
+
+
+# ----------------------------------------------------------------------------- compaction
+
+@pytest.mark.parametrize("cfg", [0, 1, 4])
+def test_compaction_bit_exact(cfg):
+    sc = synth.make_scenario(cfg, seed=0)
+    r = sc.chars[0].rounds[0]
+    shape = sc.cfg.attn
+    n_layers = 3 if cfg == 4 else 1
+    _say(f"compaction cfg{cfg} L_old={r.L_old} ranges={r.ranges.tolist()} layers={n_layers}")
+    cases = [AttnCase(shape, 0, cfg, 4 * l + 3, r.L_old, 0, capacity=r.L_old) for l in range(n_layers)]
+    ctx = _ctx_for(cases[0])
+    src = torch.full((r.L_old,), -1, dtype=torch.int32, device=DEV)
+    tu.compact_kv(ctx, [c.k_cache for c in cases], [c.v_cache for c in cases], r.ranges, src_index=src)
+    torch.cuda.synchronize()
+    want_src, want_pos = oracle.compact(np.arange(r.L_old), r.ranges)
+    n = len(want_src)
+    assert ctx.len == n and ctx.next_pos == r.cursor
+    assert np.array_equal(src[:n].cpu().numpy(), want_src)
+    assert np.array_equal(ctx.pos[:n].cpu().numpy(), want_pos)
+    for c in cases:
+        assert np.array_equal(bits_of(c.k_cache[:n]), c.k_bits[want_src])
+        assert np.array_equal(bits_of(c.v_cache[:n]), c.v_bits[want_src])
+    assert ctx.intervals() == synth.subtract_ranges(r.intervals, r.ranges)
+
+
+@pytest.mark.parametrize("name,L,ranges", [
+    ("front", 3000, [(0, 700)]),
+    ("back", 3000, [(2900, 3000)]),
+    ("adjacent", 3000, [(100, 200), (200, 300), (2999, 3000)]),
+    ("everything", 500, [(0, 500)]),
+    ("many_small", 20000, [(i * 150 + 7, i * 150 + 9) for i in range(128)]),
+    ("none", 1000, []),
+])
+def test_compaction_edge_cases(name, L, ranges):
+    shape = synth.AttnShape(2, 1, 64)      # 128-byte rows: many rows per stripe
+    _say(f"compaction edge {name} L={L} n_ranges={len(ranges)}")
+    case = AttnCase(shape, 1, 0, 1, L, 0, capacity=L)
+    ctx = _ctx_for(case)
+    src = torch.full((L,), -1, dtype=torch.int32, device=DEV)
+    tu.compact_kv(ctx, [case.k_cache], [case.v_cache], np.asarray(ranges, dtype=np.int64).reshape(-1, 2),
+                  src_index=src)
+    torch.cuda.synchronize()
+    want_src, want_pos = oracle.compact(np.arange(L), ranges)
+    n = len(want_src)
+    assert ctx.len == n
+    assert np.array_equal(src[:n].cpu().numpy(), want_src)
+    assert np.array_equal(ctx.pos[:n].cpu().numpy(), want_pos)
+    assert np.array_equal(bits_of(case.k_cache[:n]), case.k_bits[want_src])
+    assert np.array_equal(bits_of(case.v_cache[:n]), case.v_bits[want_src])
+
+
+# ----------------------------------------------------------------------------- attention
+
+def _attn_update(case, ctx, ranges, params, src=None):
+    tu.compact_kv(ctx, [case.k_cache], [case.v_cache], ranges, src_index=src)
+    tu.tail_prefill_attention(ctx, case.k_cache, case.v_cache, params, case.q, case.k, case.v, case.out,
+                              q_hat=case.q_hat)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_attention_update_parity(cfg):
+    sc = synth.make_scenario(cfg, seed=0)
+    r = sc.chars[0].rounds[0]
+    s = sc.cfg.attn
+    _say(f"attention cfg{cfg} L_old={r.L_old} L_keep={r.L_keep} T={r.T}")
+    case = AttnCase(s, 0, cfg, 0, r.L_old, r.T)
+    ctx = _ctx_for(case)
+    p = tu.attn_params(s.n_q_heads, s.n_kv_heads, s.head_dim, s.rdim, s.rope_theta, s.softmax_scale)
+    _attn_update(case, ctx, r.ranges, p)
+    ref = case.oracle(r.ranges, r.cursor)
+    assert_bf16_close_bits(bits_of(case.q_hat), ref["q_hat"], f"cfg{cfg} rotated q")
+    N = r.L_keep + r.T
+    assert_bf16_close_bits(bits_of(case.k_cache[:N]), ref["k_cache"], f"cfg{cfg} K cache")
+    assert np.array_equal(bits_of(case.v_cache[:N]), ref["v_cache"])
+    assert np.array_equal(ctx.pos[:N].cpu().numpy(), ref["pos"])
+    assert_close(case.out.cpu().numpy(), ref["out"], f"cfg{cfg} attention out")
+
+
+@pytest.mark.parametrize("L_keep,T,splits", [(0, 1, 0), (0, 77, 0), (5, 1, 0), (300, 17, 1), (1000, 200, 3),
+                                             (4000, 64, 0), (2000, 511, 7)])
+def test_attention_shapes(L_keep, T, splits):
+    s = synth.CONFIGS[1].attn
+    _say(f"attention shape L_keep={L_keep} T={T} splits={splits}")
+    case = AttnCase(s, 3, 1, 0, L_keep, T)
+    ctx = _ctx_for(case)
+    p = tu.attn_params(s.n_q_heads, s.n_kv_heads, s.head_dim, s.rdim, s.rope_theta, s.softmax_scale, kv_splits=splits)
+    _attn_update(case, ctx, np.zeros((0, 2), np.int64), p)
+    ref = case.oracle(np.zeros((0, 2), np.int64), L_keep)
+    assert_close(case.out.cpu().numpy(), ref["out"], f"L_keep={L_keep} T={T} splits={splits}")
+
+
+def test_attention_splits_agree():
+    s = synth.CONFIGS[1].attn
+    _say("attention split counts 1 vs 4 vs auto on cfg1 shapes")
+    outs = []
+    for splits in (1, 4, 0):
+        case = AttnCase(s, 0, 1, 0, 8192, 512)
+        ctx = _ctx_for(case)
+        p = tu.attn_params(s.n_q_heads, s.n_kv_heads, s.head_dim, kv_splits=splits)
+        _attn_update(case, ctx, np.zeros((0, 2), np.int64), p)
+        outs.append(case.out.cpu().numpy())
+    assert_close(outs[1], outs[0], "splits 4 vs 1")
+    assert_close(outs[2], outs[0], "splits auto vs 1")
+
+
+def test_attention_large_positions():
+    # true-tail cursor of the paper's placement case (Section 6.3): 479,547
+    s = synth.CONFIGS[1].attn
+    pos = np.concatenate([np.arange(0, 2000), np.arange(470000, 477547)])
+    _say("attention at cursor 479547")
+    case = AttnCase(s, 4, 1, 0, len(pos), 300, positions=pos)
+    ctx = _ctx_for(case)
+    ctx.set_metadata([(0, 2000), (470000, 477547)], 479547)
+    p = tu.attn_params(s.n_q_heads, s.n_kv_heads, s.head_dim, s.rdim, s.rope_theta, s.softmax_scale)
+    ranges = np.array([[100, 228], [471000, 471300]])
+    _attn_update(case, ctx, ranges, p)
+    ref = case.oracle(ranges, 479547)
+    assert_bf16_close_bits(bits_of(case.q_hat), ref["q_hat"], "rotated q at 479547")
+    assert_close(case.out.cpu().numpy(), ref["out"], "attention at 479547")
+
+
+# ----------------------------------------------------------------------------- delta rule
+
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_delta_parity(cfg):
+    sc = synth.make_scenario(cfg, seed=0)
+    T = sc.chars[0].rounds[0].T
+    d = sc.cfg.delta
+    _say(f"delta cfg{cfg} T={T} chunk={d.chunk}")
+    case = DeltaCase(d, 0, cfg, 1, T)
+    p = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
+    tu.delta_rule_continue(case.state, case.q, case.k, case.v, case.beta_d, case.g_d, p, case.out)
+    torch.cuda.synchronize()
+    o_ref, S_ref = case.oracle()
+    assert_close(case.out.cpu().numpy(), o_ref, f"cfg{cfg} delta out")
+    assert_close(case.state.cpu().numpy(), S_ref, f"cfg{cfg} delta state")
+
+
+@pytest.mark.parametrize("d,chunk,T,hk,hv", [(128, 64, 100, 2, 4), (128, 64, 1, 2, 4), (128, 32, 70, 1, 2),
+                                             (128, 16, 33, 1, 1), (64, 64, 129, 2, 2), (64, 16, 50, 1, 2)])
+def test_delta_shapes(d, chunk, T, hk, hv):
+    shape = synth.DeltaShape(hk, hv, d, d, chunk)
+    _say(f"delta shape d={d} chunk={chunk} T={T} Hk={hk} Hv={hv}")
+    case = DeltaCase(shape, 5, 9, 0, T)
+    p = tu.delta_params(hk, hv, d, d, chunk, shape.scale)
+    tu.delta_rule_continue(case.state, case.q, case.k, case.v, case.beta_d, case.g_d, p, case.out)
+    torch.cuda.synchronize()
+    o_ref, S_ref = case.oracle()
+    assert_close(case.out.cpu().numpy(), o_ref, f"delta d={d} C={chunk} T={T} out")
+    assert_close(case.state.cpu().numpy(), S_ref, f"delta d={d} C={chunk} T={T} state")
+
+
+def test_delta_continuation_equals_one_pass():
+    d = synth.CONFIGS[1].delta
+    _say("delta 3 calls (200+57+255) vs oracle one pass")
+    case = DeltaCase(d, 6, 1, 1, 512)
+    p = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
+    for a, b in [(0, 200), (200, 257), (257, 512)]:
+        out = torch.empty((b - a, d.n_v_heads, d.d_v), dtype=torch.float32, device=DEV)
+        tu.delta_rule_continue(case.state, case.q[a:b], case.k[a:b], case.v[a:b], case.beta_d[a:b], case.g_d[a:b], p,
+                               out)
+        case.out[a:b] = out
+    torch.cuda.synchronize()
+    o_ref, S_ref = case.oracle()
+    assert_close(case.out.cpu().numpy(), o_ref, "split delta out")
+    assert_close(case.state.cpu().numpy(), S_ref, "split delta state")
+
+
+# ----------------------------------------------------------------------------- stack update
+
+def _stack_case(cfg, seed=0, char=0, rnd=0, plan_round=None, cases=None):
+    sc = synth.make_scenario(cfg, seed=seed)
+    r = plan_round if plan_round is not None else sc.chars[char].rounds[rnd]
+    return sc, r
+
+
+def test_stack_update_cfg1_matches_oracle_and_commits():
+    sc, r = _stack_case(1)
+    a, d = sc.cfg.attn, sc.cfg.delta
+    _say(f"stack cfg1 [attn, delta] L_old={r.L_old} T={r.T}")
+    ac = AttnCase(a, 0, 1, 0, r.L_old, r.T)
+    dc = DeltaCase(d, 0, 1, 1, r.T)
+    ctx = _ctx_for(ac)
+    layers = [tu.LayerIO(tu.TU_LAYER_ATTN, ac.q, ac.k, ac.v, ac.out, k_cache=[ac.k_cache], v_cache=[ac.v_cache]),
+              tu.LayerIO(tu.TU_LAYER_DELTA, dc.q, dc.k, dc.v, dc.out, state=[dc.state], beta=dc.beta_d, g=dc.g_d)]
+    src = torch.full((r.L_old,), -1, dtype=torch.int32, device=DEV)
+    tu.update_layer_stack([ctx], [r.ranges], [r.T], layers,
+                          tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta),
+                          tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk), src_index=[src])
+    torch.cuda.synchronize()
+    ref = ac.oracle(r.ranges, r.cursor)
+    assert np.array_equal(src[: r.L_keep].cpu().numpy(), ref["src_index"])
+    assert_close(ac.out.cpu().numpy(), ref["out"], "stack attention out")
+    o_ref, S_ref = dc.oracle()
+    assert_close(dc.out.cpu().numpy(), o_ref, "stack delta out")
+    assert_close(dc.state.cpu().numpy(), S_ref, "stack delta state")
+    assert ctx.len == r.L_keep + r.T and ctx.next_pos == r.cursor + r.T
+    assert ctx.intervals() == synth.append_interval(synth.subtract_ranges(r.intervals, r.ranges), r.cursor, r.T)
+
+
+def test_stack_is_deterministic():
+    sc, r = _stack_case(1)
+    a, d = sc.cfg.attn, sc.cfg.delta
+    _say("stack cfg1 run twice, bit-identical")
+    res = []
+    for _ in range(2):
+        ac = AttnCase(a, 0, 1, 0, r.L_old, r.T)
+        dc = DeltaCase(d, 0, 1, 1, r.T)
+        ctx = _ctx_for(ac)
+        layers = [tu.LayerIO(tu.TU_LAYER_ATTN, ac.q, ac.k, ac.v, ac.out, k_cache=[ac.k_cache], v_cache=[ac.v_cache]),
+                  tu.LayerIO(tu.TU_LAYER_DELTA, dc.q, dc.k, dc.v, dc.out, state=[dc.state], beta=dc.beta_d,
+                             g=dc.g_d)]
+        tu.update_layer_stack([ctx], [r.ranges], [r.T], layers, tu.attn_params(16, 2, 256),
+                              tu.delta_params(16, 32, 128, 128, 64))
+        torch.cuda.synchronize()
+        res.append((ac.out.cpu().numpy().copy(), dc.out.cpu().numpy().copy(), dc.state.cpu().numpy().copy(),
+                    bits_of(ac.k_cache)))
+    for x, y in zip(res[0], res[1]):
+        assert np.array_equal(x, y)
