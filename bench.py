@@ -1,0 +1,417 @@
+#!/usr/bin/env python3
+"""Benchmark of the true-tail update of a hybrid layer stack on one MI355X.
+
+A step is one whole update (paper Section 4.1, Eq. 1-3) of the workload's
+contexts: range verification, KV compaction of every attention layer, then in
+layer order tail attention (RoPE append + causal GQA over surviving + new KV)
+or gated delta-rule continuation from the carried state; metadata commit. Each
+step runs on its own pristine copy of the contexts (caches, states, positions),
+prepared before the timed region, so the K timed steps run back to back between
+two device synchronisations.
+
+Printed: one JSON line with tail tokens/s, the speedup over a full refill of the
+same final context through the same kernels, the roofline fraction of the
+dominant kernel (its duration measured with HIP events on its stream, in a
+second pass over the same steps) and the CPU oracle timed on this host.
+
+    python bench.py [--config 1] [--steps 20] [--warmup 3] [--gpus 1]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA16_PEAK_TFLOPS = 2500.0
+METRIC = "tail-update tokens/s (hybrid layer stack) + speedup vs full refill; % roofline"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=1, choices=[0, 1, 3, 4])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--refill-steps", type=int, default=5)
+    ap.add_argument("--no-refill", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--kv-splits", type=int, default=0)
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------------------- device inputs
+
+class DevRng:
+    """Seeded device-side draws with the workload's value distributions."""
+
+    def __init__(self, seed, device):
+        import torch
+        self.torch = torch
+        self.g = torch.Generator(device=device)
+        self.g.manual_seed(int(seed))
+        self.dev = device
+
+    def normal(self, shape, std=1.0, mean=0.0, dtype=None):
+        t = self.torch.randn(*shape, generator=self.g, device=self.dev, dtype=self.torch.float32)
+        if std != 1.0 or mean != 0.0:
+            t = t * std + mean
+        return t if dtype is None else t.to(dtype)
+
+    def bf16(self, shape):
+        return self.normal(shape).to(self.torch.bfloat16)
+
+    def unit_bf16(self, shape):
+        t = self.normal(shape)
+        return (t / t.norm(dim=-1, keepdim=True)).to(self.torch.bfloat16)
+
+    def beta(self, shape):
+        return self.torch.sigmoid(self.normal(shape))
+
+    def gate(self, shape):
+        return self.torch.exp(-self.torch.nn.functional.softplus(self.normal(shape, mean=-4.0)))
+
+
+def build_workload(cfg, seed, device):
+    """Per-context plans plus pristine device buffers and packed tail inputs."""
+    import torch
+    import synth
+    sc = synth.make_scenario(cfg.index, seed=seed)
+    rng = DevRng(seed * 1000 + cfg.index, device)
+    a, d = cfg.attn, cfg.delta
+    kinds = cfg.layer_kinds()
+    chars = []
+    for ch in sc.chars:
+        r = ch.rounds[0]
+        chars.append({"L_old": r.L_old, "L_keep": r.L_keep, "T": r.T, "ranges": r.ranges, "cursor": r.cursor,
+                      "intervals": r.intervals, "cap": max(r.L_old, r.L_keep + r.T)})
+    sumT = sum(c["T"] for c in chars)
+    layers = []
+    for kind in kinds:
+        if kind == "attn":
+            caches = [(rng.bf16((c["cap"], a.n_kv_heads, a.head_dim)), rng.bf16((c["cap"], a.n_kv_heads, a.head_dim)))
+                      for c in chars]
+            layers.append({"kind": "attn", "caches": caches,
+                           "q": rng.bf16((sumT, a.n_q_heads, a.head_dim)),
+                           "k": rng.bf16((sumT, a.n_kv_heads, a.head_dim)),
+                           "v": rng.bf16((sumT, a.n_kv_heads, a.head_dim)),
+                           "out": torch.empty((sumT, a.n_q_heads, a.head_dim), dtype=torch.float32, device=device)})
+        else:
+            layers.append({"kind": "delta",
+                           "states": [rng.normal((d.n_v_heads, d.d_v, d.d_k), std=0.1) for _ in chars],
+                           "q": rng.bf16((sumT, d.n_k_heads, d.d_k)),
+                           "k": rng.unit_bf16((sumT, d.n_k_heads, d.d_k)),
+                           "v": rng.bf16((sumT, d.n_v_heads, d.d_v)),
+                           "beta": rng.beta((sumT, d.n_v_heads)), "g": rng.gate((sumT, d.n_v_heads)),
+                           "out": torch.empty((sumT, d.n_v_heads, d.d_v), dtype=torch.float32, device=device)})
+    return sc, chars, layers, rng
+
+
+def make_copy(tu, chars, layers, device, pristine=True):
+    """A fresh set of contexts/caches/states equal to the pristine workload."""
+    import torch
+    ctxs = []
+    for c in chars:
+        ctx = tu.Context(c["cap"], device=device)
+        ctx.pos[: c["L_old"]] = torch.arange(c["L_old"], dtype=torch.int32, device=device)
+        ctx.set_metadata(c["intervals"], c["cursor"])
+        ctxs.append(ctx)
+    own = []
+    for L in layers:
+        if L["kind"] == "attn":
+            own.append({"caches": [(k.clone(), v.clone()) for (k, v) in L["caches"]]})
+        else:
+            own.append({"states": [s.clone() for s in L["states"]]})
+    return ctxs, own
+
+
+def stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p, tails=None, inputs=None, ranges=None):
+    ios = []
+    for L, O in zip(layers, own):
+        src = inputs[id(L)] if inputs is not None else L
+        if L["kind"] == "attn":
+            ios.append(tu.LayerIO(tu.TU_LAYER_ATTN, src["q"], src["k"], src["v"], src["out"],
+                                  k_cache=[k for (k, _) in O["caches"]], v_cache=[v for (_, v) in O["caches"]]))
+        else:
+            ios.append(tu.LayerIO(tu.TU_LAYER_DELTA, src["q"], src["k"], src["v"], src["out"], state=O["states"],
+                                  beta=src["beta"], g=src["g"]))
+    rr = ranges if ranges is not None else [c["ranges"] for c in chars]
+    tt = tails if tails is not None else [c["T"] for c in chars]
+    return tu.StackUpdate(ctxs, rr, tt, ios, attn_p, delta_p)
+
+
+# ----------------------------------------------------------------------------- algorithmic work
+
+def attention_flops(cfg, chars):
+    a = cfg.attn
+    return sum(4.0 * a.n_q_heads * a.head_dim * (c["T"] * c["L_keep"] + c["T"] * (c["T"] + 1) / 2.0)
+               for c in chars)
+
+
+def delta_bytes(cfg, chars):
+    d = cfg.delta
+    per_tok = d.n_k_heads * d.d_k * 2 * 2 + d.n_v_heads * d.d_v * 2 + d.n_v_heads * 8 + d.n_v_heads * d.d_v * 4
+    state = d.n_v_heads * d.d_v * d.d_k * 4 * 2
+    return sum(c["T"] * per_tok + state for c in chars)
+
+
+def gather_bytes(cfg, chars):
+    """Minimum: every surviving row behind the first hole is read and written once."""
+    a = cfg.attn
+    row = a.n_kv_heads * a.head_dim * 2
+    total = 0
+    for c in chars:
+        if len(c["ranges"]) == 0:
+            continue
+        first = int(c["ranges"][0][0])   # positions are 0..L_old-1 at round 0, so position == row
+        moved = c["L_keep"] - first
+        total += 2 * 2 * moved * row     # K and V, read + write
+    return total
+
+
+# ----------------------------------------------------------------------------- CPU oracle leg
+
+def cpu_baseline(cfg, seed, budget_s):
+    """The float64 oracle on this host: one full update of the workload's first context
+    (all tail rows of one attention layer, all tail tokens of one delta layer), repeated
+    while within the budget, scaled to the workload's layer counts."""
+    import numpy as np
+    import oracle
+    import synth
+    cores = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threadpool_limits(cores)
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [cores])
+    except Exception:
+        blas_threads = cores
+    sc = synth.make_scenario(cfg.index, seed=seed)
+    r = sc.chars[0].rounds[0]
+    a, d = cfg.attn, cfg.delta
+    kb, vb = synth.gen_attn_cache(seed, cfg.index, 0, r.L_old, a)
+    q, k, v = synth.gen_attn_tail(seed, cfg.index, 0, r.T, a)
+    S0 = synth.gen_delta_state(seed, cfg.index, 1, d).astype(np.float64)
+    dq, dk, dv, beta, g = synth.gen_delta_inputs(seed, cfg.index, 1, r.T, d)
+    # rows / tokens sampled so one repetition stays within the budget
+    rows = np.arange(r.T)
+    toks = r.T
+    est = (4.0 * a.n_q_heads * a.head_dim * r.T * (r.L_keep + r.T) / 2e10) + r.T * 4e-3
+    if est > budget_s:
+        frac = budget_s / est
+        rows = np.unique(np.linspace(0, r.T - 1, max(8, int(r.T * frac))).astype(np.int64))
+        toks = max(16, int(r.T * frac))
+    t_attn, t_delta, reps = [], [], 0
+    t_start = time.time()
+    while reps < 3 and (reps == 0 or time.time() - t_start < budget_s):
+        t0 = time.time()
+        oracle.attention_layer_update(np.arange(r.L_old), kb, vb, r.ranges, r.cursor, q, k, v, a.rdim, a.rope_theta,
+                                      a.softmax_scale, rows=rows)
+        t1 = time.time()
+        oracle.delta_layer_update(S0, dq[:toks], dk[:toks], dv[:toks], beta[:toks], g[:toks], d.scale)
+        t2 = time.time()
+        t_attn.append((t1 - t0) * r.T / len(rows))
+        t_delta.append((t2 - t1) * r.T / toks)
+        reps += 1
+    kinds = cfg.layer_kinds()
+    n_attn = kinds.count("attn")
+    n_delta = kinds.count("delta")
+    per_char = n_attn * min(t_attn) + n_delta * min(t_delta)
+    total_T = sum(c.rounds[0].T for c in sc.chars)
+    # other contexts scale with their attention work and tail length
+    scale = total_T / r.T if len(sc.chars) > 1 else 1.0
+    secs = per_char * scale
+    sample = (f"context 0 of the workload: attention layer rows {len(rows)}/{r.T}, delta tokens {toks}/{r.T}, "
+              f"{reps} repetitions (best), scaled to {n_attn} attention + {n_delta} delta layers"
+              + (f" and {len(sc.chars)} contexts by tail length" if len(sc.chars) > 1 else ""))
+    return {"value": total_T / secs, "unit": "tail tokens/s", "cores": int(blas_threads), "kind": "oracle",
+            "sample": sample, "seconds_per_update": secs}
+
+
+# ----------------------------------------------------------------------------- main
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the update of one context does not "
+                                   "span devices here (--gpus 1)"}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+    import synth
+    import paper_2609_18935_amd as tu
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    tu.lib()
+    cfg = synth.CONFIGS[args.config]
+    a, d = cfg.attn, cfg.delta
+    attn_p = tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta, a.softmax_scale,
+                            kv_splits=args.kv_splits)
+    delta_p = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
+    sc, chars, layers, rng = build_workload(cfg, args.seed, dev)
+    W, K = args.warmup, args.steps
+    print(f"[bench] config {cfg.index} ({cfg.name}): {len(chars)} context(s), {len(layers)} layers, "
+          f"sum T = {sum(c['T'] for c in chars)}", file=sys.stderr, flush=True)
+
+    # ---- update: one pristine copy per step
+    copies = [make_copy(tu, chars, layers, dev) for _ in range(W + K)]
+    ups = [stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p) for (ctxs, own) in copies]
+    ws = torch.empty(max(u.workspace_size() for u in ups), dtype=torch.uint8, device=dev)
+    for i in range(W):
+        ups[i].run(ws)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    h0 = time.perf_counter()
+    ev0.record()
+    for i in range(W, W + K):
+        ups[i].run(ws)
+    ev1.record()
+    torch.cuda.synchronize()
+    h1 = time.perf_counter()
+    upd_ms = ev0.elapsed_time(ev1) / K
+    print(f"[bench] update: {upd_ms:.4f} ms/step (host {1e3 * (h1 - h0) / K:.4f})", file=sys.stderr, flush=True)
+
+    # ---- profiled pass over the same steps (fresh copies), per-kernel HIP events
+    copies2 = [make_copy(tu, chars, layers, dev) for _ in range(K)]
+    ups2 = [stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p) for (ctxs, own) in copies2]
+    torch.cuda.synchronize()
+    tu.profile_enable(True)
+    for u in ups2:
+        u.run(ws)
+    prof = tu.profile_collect()
+    tu.profile_enable(False)
+    del copies2, ups2
+    kern = {n: {"launches_per_step": c / K, "avg_ms": t / c, "ms_per_step": t / K} for n, (c, t) in prof.items()}
+    print(f"[bench] kernels: {json.dumps(kern)}", file=sys.stderr, flush=True)
+
+    sumT = sum(c["T"] for c in chars)
+    kinds = cfg.layer_kinds()
+    # algorithmic work per step of each stage, and the kernels that carry it
+    work = {
+        "attention": (["attention"], "mfma", attention_flops(cfg, chars) * kinds.count("attn") / 1e12, "TFLOP/s",
+                      MFMA16_PEAK_TFLOPS),
+        "delta": (["delta_prep", "delta_chain"], "hbm", delta_bytes(cfg, chars) * kinds.count("delta") / 1e9, "GB/s",
+                  HBM_PEAK_GBS),
+        "compaction": (["keep_scan", "gather"], "hbm", gather_bytes(cfg, chars) / 1e9, "GB/s", HBM_PEAK_GBS),
+    }
+    stages = {}
+    for name, (ks, bound, units, unit, peak) in work.items():
+        ms = sum(kern[k]["ms_per_step"] for k in ks if k in kern)
+        if ms > 0 and units > 0:
+            ach = units / (ms / 1e3)
+            stages[name] = {"kernels": ks, "ms_per_step": round(ms, 5), "bound": bound, "achieved": round(ach, 3),
+                            "peak": peak, "unit": unit, "frac": round(ach / peak, 4)}
+    dom = max(kern, key=lambda n: kern[n]["ms_per_step"])
+    work = {"attention": work["attention"][1:]}
+    if dom in work:
+        bound, units, unit, peak = work[dom]
+        launches = kern[dom]["launches_per_step"]
+        ach = units / (kern[dom]["ms_per_step"] / 1e3)
+        roofline = {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
+                    "frac": round(ach / peak, 4), "traffic": None, "kernel": dom,
+                    "per_launch": round(units / launches, 6), "avg_launch_ms": round(kern[dom]["avg_ms"], 5)}
+    else:
+        roofline = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
+                    "kernel": dom}
+
+    # ---- full refill of the same final context through the same kernels
+    refill = None
+    if not args.no_refill and args.refill_steps > 0:
+        N = [c["L_keep"] + c["T"] for c in chars]
+        sumN = sum(N)
+        rin = {}
+        for L in layers:
+            if L["kind"] == "attn":
+                rin[id(L)] = {"q": rng.bf16((sumN, a.n_q_heads, a.head_dim)),
+                              "k": rng.bf16((sumN, a.n_kv_heads, a.head_dim)),
+                              "v": rng.bf16((sumN, a.n_kv_heads, a.head_dim)),
+                              "out": torch.empty((sumN, a.n_q_heads, a.head_dim), dtype=torch.float32, device=dev)}
+            else:
+                rin[id(L)] = {"q": rng.bf16((sumN, d.n_k_heads, d.d_k)), "k": rng.unit_bf16((sumN, d.n_k_heads, d.d_k)),
+                              "v": rng.bf16((sumN, d.n_v_heads, d.d_v)), "beta": rng.beta((sumN, d.n_v_heads)),
+                              "g": rng.gate((sumN, d.n_v_heads)),
+                              "out": torch.empty((sumN, d.n_v_heads, d.d_v), dtype=torch.float32, device=dev)}
+        rchars = [dict(c, L_old=0, intervals=[], cursor=0, cap=n) for c, n in zip(chars, N)]
+        # refill writes every cache row and starts from zero states: buffers are shared, states zeroed per step
+        own = []
+        for L in layers:
+            if L["kind"] == "attn":
+                own.append({"caches": [(torch.empty((n, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev),
+                                        torch.empty((n, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev))
+                                       for n in N]})
+            else:
+                own.append({"states": None})
+        R = args.refill_steps
+        rups = []
+        for i in range(R + 1):
+            ctxs = []
+            for c in rchars:
+                ctx = tu.Context(c["cap"], device=dev)
+                ctx.set_metadata([], 0)
+                ctxs.append(ctx)
+            own_i = []
+            for L, O in zip(layers, own):
+                if L["kind"] == "attn":
+                    own_i.append(O)
+                else:
+                    own_i.append({"states": [torch.zeros((d.n_v_heads, d.d_v, d.d_k), dtype=torch.float32, device=dev)
+                                             for _ in chars]})
+            rups.append(stack_update(tu, ctxs, own_i, rchars, layers, attn_p, delta_p, tails=N, inputs=rin,
+                                     ranges=[np.zeros((0, 2), np.int64)] * len(chars)))
+        rws = torch.empty(max(u.workspace_size() for u in rups), dtype=torch.uint8, device=dev)
+        rups[0].run(rws)
+        torch.cuda.synchronize()
+        ev0.record()
+        for u in rups[1:]:
+            u.run(rws)
+        ev1.record()
+        torch.cuda.synchronize()
+        refill_ms = ev0.elapsed_time(ev1) / R
+        refill = {"ms": refill_ms, "tokens": sumN, "speedup": refill_ms / upd_ms}
+        print(f"[bench] refill: {refill_ms:.4f} ms ({sumN} tokens), speedup {refill_ms / upd_ms:.2f}x",
+              file=sys.stderr, flush=True)
+        del rups, rin, own, rws
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] cpu oracle leg ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(cfg, args.seed, args.cpu_budget_s)
+
+    line = {
+        "metric": METRIC,
+        "value": round(sumT / (upd_ms / 1e3), 1),
+        "unit": "tail tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(upd_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"config {cfg.index}: {cfg.name}", "contexts": len(chars), "layers": len(layers),
+                   "attention_layers": kinds.count("attn"), "delta_layers": kinds.count("delta"),
+                   "tail_tokens": sumT, "surviving_rows": [c["L_keep"] for c in chars][:4],
+                   "removed_rows": sum(c["L_old"] - c["L_keep"] for c in chars),
+                   "attn": f"{a.n_q_heads}q/{a.n_kv_heads}kv x {a.head_dim}",
+                   "delta": f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}"},
+        "roofline": roofline,
+        "stages": stages,
+        "speedup_vs_refill":round(refill["speedup"], 3) if refill else None,
+        "refill_ms": round(refill["ms"], 5) if refill else None,
+        "kernels": {n: {k: (round(v, 6) if isinstance(v, float) else v) for k, v in kv.items()}
+                    for n, kv in kern.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

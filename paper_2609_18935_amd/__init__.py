@@ -17,6 +17,8 @@ from .binding import (  # noqa: F401
     delta_params,
     delta_rule_continue,
     lib,
+    profile_collect,
+    profile_enable,
     tail_prefill_attention,
     update_layer_stack,
     TU_LAYER_ATTN,

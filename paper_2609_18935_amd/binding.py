@@ -86,6 +86,9 @@ _SIGNATURES = {
     "update_layer_stack_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_update)]),
     "tu_validate_update": (_i32, [ctypes.POINTER(tu_update)]),
     "update_layer_stack": (_i32, [ctypes.POINTER(tu_update), _vp, ctypes.c_size_t, _vp]),
+    "tu_profile_enable": (_i32, [_i32]),
+    "tu_profile_collect": (_i32, [ctypes.c_char_p, _i32, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double),
+                                  _i32]),
 }
 
 _lib_handle = None
@@ -304,6 +307,28 @@ class StackUpdate:
 
     def run(self, workspace: torch.Tensor, stream=None):
         _check(lib().update_layer_stack(ctypes.byref(self.u), _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def profile_enable(on: bool = True):
+    """Bracket every library kernel launch of this thread with HIP events on its stream."""
+    _check(lib().tu_profile_enable(1 if on else 0))
+
+
+def profile_collect(max_entries: int = 32) -> dict:
+    """{kernel name: (launch count, summed milliseconds)} since the last collect."""
+    stride = 64
+    names = ctypes.create_string_buffer(stride * max_entries)
+    counts = (_i32 * max_entries)()
+    totals = (ctypes.c_double * max_entries)()
+    n = lib().tu_profile_collect(names, stride, counts, totals, max_entries)
+    if n < 0:
+        _check(n)
+    raw = names.raw
+    out = {}
+    for i in range(n):
+        name = raw[i * stride:(i + 1) * stride].split(b"\0", 1)[0].decode()
+        out[name] = (int(counts[i]), float(totals[i]))
+    return out
 
 
 def update_layer_stack(contexts, ranges, tails, layers, attn=None, delta=None, workspace=None, stream=None,

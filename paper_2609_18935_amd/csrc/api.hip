@@ -869,6 +869,46 @@ size_t update_layer_stack_workspace_size(const tu_update* u) {
   return need;
 }
 
+int tu_profile_enable(int on) {
+  g_prof = on != 0;
+  return ok();
+}
+
+int tu_profile_collect(char* names, int32_t name_stride, int32_t* counts, double* total_ms, int32_t max_entries) {
+  if (max_entries < 0 || (max_entries > 0 && (!names || !counts || !total_ms || name_stride < 2)))
+    return fail(TU_ERR_ARG, "bad output arrays");
+  std::vector<std::string> keys;
+  std::vector<int32_t> cnt;
+  std::vector<double> sum;
+  int status = TU_OK;
+  for (auto& r : g_recs) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.stop) != hipSuccess || hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess)
+      status = fail(TU_ERR_HIP, "event timing failed");
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+    size_t k = 0;
+    while (k < keys.size() && keys[k] != r.name) ++k;
+    if (k == keys.size()) {
+      keys.push_back(r.name);
+      cnt.push_back(0);
+      sum.push_back(0.0);
+    }
+    cnt[k] += 1;
+    sum[k] += ms;
+  }
+  g_recs.clear();
+  if (status != TU_OK) return status;
+  const int n = std::min<int>((int)keys.size(), max_entries);
+  for (int i = 0; i < n; ++i) {
+    snprintf(names + (size_t)i * name_stride, name_stride, "%s", keys[i].c_str());
+    counts[i] = cnt[i];
+    total_ms[i] = sum[i];
+  }
+  ok();
+  return n;
+}
+
 int tu_validate_update(const tu_update* u) {
   StackPlan sp;
   if (int e = validate_stack(u, &sp)) return e;

@@ -34,10 +34,24 @@ constexpr int kBM = 128;   // packed query rows per workgroup
 constexpr int kBN = 64;    // keys per tile
 constexpr int kKPad = 8;   // bf16 padding per K row in LDS
 constexpr int kVPad = 8;   // f16 padding per V^T row in LDS
+constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units): P < 2^8 fits f16
 
 __device__ __forceinline__ int key_slot(int k) {
   // swap bits 2 and 3 of the key index within its 16-key group
   return (k & ~0xC) | ((k & 4) << 1) | ((k & 8) >> 1);
+}
+
+// Scales an MFMA accumulator that lives in AGPRs. Going through explicit AGPR
+// reads/writes keeps the accumulator out of the VALU register class, so the
+// compiler does not shuttle it between AGPRs and VGPRs on every key tile.
+__device__ __forceinline__ void scale_acc(f32x16& acc, float s) {
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    float v;
+    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(acc[e]));
+    v *= s;
+    asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(acc[e]) : "v"(v));
+  }
 }
 
 __device__ __forceinline__ _Float16 bf16_lo_to_f16(uint32_t w) { return (_Float16)__uint_as_float(w << 16); }
@@ -100,48 +114,93 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[db][e] = 0.f;
+  // Online softmax in the log2 domain with a lazily moved reference max: the
+  // probabilities are 2^(s*c - m_run) with m_run raised (and O, l rescaled) only
+  // when a tile's max exceeds it by more than kTau, so P stays below 2^kTau.
   float m_run = -__builtin_inff();
   float l_run = 0.f;
+  const float c2 = a.scale_log2;
 
   const long rs = (long)Hkv * D;  // elements per cache row
   const bf16_t* kbase = S.k_cache + (long)hkv * D;
   const bf16_t* vbase = S.v_cache + (long)hkv * D;
 
-  for (int kt = kt_begin; kt < kt_end; ++kt) {
+  // staging: K rows are copied as 16-byte vectors, V as (4 keys x 8 dims) blocks
+  constexpr int KIT = kBN * D / 8 / 256;
+  constexpr int KROWS = 256 / (D / 8);
+  constexpr int VTASK = (kBN / 4) * (D / 8);
+  constexpr int VIT = (VTASK + 255) / 256;
+  const int k_kr = threadIdx.x / (D / 8);
+  const int k_kc = threadIdx.x % (D / 8);
+  u32x4 kreg[KIT];
+  u32x4 vreg[VIT][4];
+
+  // per-thread source addresses of the first tile; later tiles add a uniform offset
+  const bf16_t* kthr = kbase + (long)k_kr * rs + k_kc * 8;
+  const bf16_t* vthr[VIT];
+#pragma unroll
+  for (int it = 0; it < VIT; ++it) {
+    const int c = threadIdx.x + 256 * it;
+    vthr[it] = vbase + (long)((c % (kBN / 4)) * 4) * rs + (c / (kBN / 4)) * 8;
+  }
+  auto load_tile = [&](int kt) {
     const int key0 = kt * kBN;
-    // ---- stage K rows (bf16) and V^T (f16, permuted key order) in LDS
+    const long toff = (long)key0 * rs;
+    if (key0 + kBN <= n_keys) {
 #pragma unroll
-    for (int it = 0; it < kBN * D / 8 / 256; ++it) {
-      const int c = threadIdx.x + 256 * it;
-      const int kr = c / (D / 8);
-      const int kc = c - kr * (D / 8);
-      const int key = key0 + kr;
-      u32x4 w = key < n_keys ? *(const u32x4*)(kbase + key * rs + kc * 8) : u32x4{0, 0, 0, 0};
-      *(u32x4*)&Ks[kr][kc * 8] = w;
-    }
+      for (int it = 0; it < KIT; ++it) kreg[it] = *(const u32x4*)(kthr + toff + (long)(KROWS * it) * rs);
 #pragma unroll
-    for (int it = 0; it < ((kBN / 4) * (D / 8) + 255) / 256; ++it) {
-      const int c = threadIdx.x + 256 * it;
-      if (c >= (kBN / 4) * (D / 8)) break;
-      const int kq = c % (kBN / 4);
-      const int dc = c / (kBN / 4);
-      u32x4 w[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int key = key0 + kq * 4 + j;
-        w[j] = key < n_keys ? *(const u32x4*)(vbase + key * rs + dc * 8) : u32x4{0, 0, 0, 0};
-      }
-      const int slot = key_slot(kq * 4);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        f16x4 h4;
+      for (int it = 0; it < VIT; ++it)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          h4[j] = (e & 1) ? bf16_hi_to_f16(w[j][e >> 1]) : bf16_lo_to_f16(w[j][e >> 1]);
-        *(f16x4*)&Vt[dc * 8 + e][slot] = h4;
+          vreg[it][j] = (threadIdx.x + 256 * it < VTASK) ? *(const u32x4*)(vthr[it] + toff + j * rs)
+                                                          : u32x4{0, 0, 0, 0};
+    } else {
+#pragma unroll
+      for (int it = 0; it < KIT; ++it) {
+        const int key = key0 + k_kr + KROWS * it;
+        kreg[it] = key < n_keys ? *(const u32x4*)(kthr + toff + (long)(KROWS * it) * rs) : u32x4{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int it = 0; it < VIT; ++it) {
+        const int c = threadIdx.x + 256 * it;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int key = key0 + (c % (kBN / 4)) * 4 + j;
+          vreg[it][j] = (c < VTASK && key < n_keys) ? *(const u32x4*)(vthr[it] + toff + j * rs)
+                                                     : u32x4{0, 0, 0, 0};
+        }
       }
     }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int it = 0; it < KIT; ++it) *(u32x4*)&Ks[k_kr + KROWS * it][k_kc * 8] = kreg[it];
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int c = threadIdx.x + 256 * it;
+      if (c < VTASK) {
+        const int kq = c % (kBN / 4);
+        const int dc = c / (kBN / 4);
+        const int slot = key_slot(kq * 4);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          f16x4 h4;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            h4[j] = (e & 1) ? bf16_hi_to_f16(vreg[it][j][e >> 1]) : bf16_lo_to_f16(vreg[it][j][e >> 1]);
+          *(f16x4*)&Vt[dc * 8 + e][slot] = h4;
+        }
+      }
+    }
+  };
+
+  if (kt_begin < kt_end) load_tile(kt_begin);
+  for (int kt = kt_begin; kt < kt_end; ++kt) {
+    const int key0 = kt * kBN;
+    store_tile();
     __syncthreads();
+    if (kt + 1 < kt_end) load_tile(kt + 1);   // in flight while this tile is computed
 
     // ---- S^T = K Q^T for the 64 keys: two 32x32 blocks
     f32x16 sacc[2];
@@ -156,41 +215,42 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       }
     }
 
-    // ---- online softmax (log2 domain)
-    const bool need_mask = key0 + kBN - 1 > S.L_keep + t_lo;
+    // ---- causal mask (only on tiles that cross the tail diagonal) and tile max
+    if (key0 + kBN - 1 > S.L_keep + t_lo) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = key0 + kb * 32 + 8 * (e >> 2) + 4 * hl + (e & 3);
+          if (key > my_limit) sacc[kb][e] = -__builtin_inff();
+        }
+    }
     float mx = -__builtin_inff();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float v = sacc[kb][e] * a.scale_log2;
-        if (need_mask) {
-          const int key = key0 + kb * 32 + 8 * (e >> 2) + 4 * hl + (e & 3);
-          if (key > my_limit) v = -__builtin_inff();
-        }
-        sacc[kb][e] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -__builtin_inff()) ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[kb][e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+    if (__any(mx > m_run + kTau)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = (m_new == -__builtin_inff()) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) scale_acc(o[db], alpha);
+    }
+    const float m_use = (m_run == -__builtin_inff()) ? 0.f : m_run;
     float psum = 0.f;
     f16x8 pf[4];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float p = __builtin_amdgcn_exp2f(sacc[kb][e] - m_use);
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][e], c2, -m_use));
         psum += p;
         pf[kb * 2 + (e >> 3)][e & 7] = (_Float16)p;
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
+    l_run += psum;
 
     // ---- O^T += V^T P^T over 4 steps of 16 keys
 #pragma unroll
