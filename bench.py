@@ -298,7 +298,8 @@ def main():
                       MFMA16_PEAK_TFLOPS),
         "delta": (["delta_prep", "delta_chain"], "hbm", delta_bytes(cfg, chars) * kinds.count("delta") / 1e9, "GB/s",
                   HBM_PEAK_GBS),
-        "compaction": (["keep_scan", "gather"], "hbm", gather_bytes(cfg, chars) / 1e9, "GB/s", HBM_PEAK_GBS),
+        "compaction": (["compact"], "hbm", gather_bytes(cfg, chars) * kinds.count("attn") / 1e9, "GB/s",
+                       HBM_PEAK_GBS),
     }
     stages = {}
     for name, (ks, bound, units, unit, peak) in work.items():

@@ -79,6 +79,7 @@ int check_seq(const tu_seq* s) {
 struct RangeCheck {
   int64_t removed = 0;
   int64_t first_row = 0;                  // cache row of the first removed position
+  std::vector<int64_t> rows;              // cache row of the first position of each range
   std::vector<tu_interval> live_after;    // intervals after the removal
 };
 
@@ -88,6 +89,7 @@ int check_ranges(const tu_seq* s, const int64_t* ranges, int n, RangeCheck* out)
   if (n > TU_MAX_RANGES) return fail(TU_ERR_ARG, "more than %d ranges in one call", TU_MAX_RANGES);
   out->removed = 0;
   out->first_row = s->len;
+  out->rows.clear();
   int64_t prev_end = INT64_MIN;
   // prefix of live rows before each interval
   std::vector<int64_t> before(s->n_live + 1, 0);
@@ -109,7 +111,8 @@ int check_ranges(const tu_seq* s, const int64_t* ranges, int n, RangeCheck* out)
     }
     if (at < 0 || b > s->live[at].end)
       return fail(TU_ERR_RANGE, "range %d [%lld,%lld) is not live", q, (long long)a, (long long)b);
-    if (q == 0) out->first_row = before[at] + (a - s->live[at].begin);
+    out->rows.push_back(before[at] + (a - s->live[at].begin));
+    if (q == 0) out->first_row = out->rows[0];
     out->removed += b - a;
     prev_end = b;
   }
@@ -198,142 +201,139 @@ struct CompactItem {
 };
 
 struct CompactPlan {
-  std::vector<ScanArgs> scans;
-  std::vector<GatherArgs> gathers;
-  std::vector<int> gather_blocks;
+  std::vector<CompactArgs> launches;
+  std::vector<int> workers;
   size_t ws_bytes = 0;
 };
 
-// Builds the launches for a set of contexts. With ws == nullptr only sizes are computed.
+// Builds the compaction launches for a set of contexts. With ws == nullptr only the
+// workspace size is computed.
 int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, CompactPlan* plan) {
   Arena ar(ws);
   const int R = kGatherStripeBytes / row_bytes;
-  // src_index storage
-  for (auto& it : items) {
+  const int64_t align_rows = std::max(1, 128 / row_bytes);
+  for (auto& it : items) {   // src_index storage
     void* p = ar.take(sizeof(int32_t) * std::max<int64_t>(1, it.seq->len));
     it.user_index = it.src_index != nullptr && it.src_index != p;
     if (!it.user_index) it.src_index = static_cast<int32_t*>(p);
   }
-  // gather launches: (context, buffer chunk) entries
-  struct Entry { int item; int buf0; int nbuf; };
+  // launch groups of (context, buffer range, scan?, move?) entries
+  struct Entry {
+    int item, buf0, nbuf;
+    bool scan, move;
+  };
   std::vector<std::vector<Entry>> groups;
   {
     std::vector<Entry> cur;
-    int cur_bufs = 0;
+    int bufs = 0, nr = 0, ns = 0;
+    auto flush = [&] {
+      if (!cur.empty()) groups.push_back(cur);
+      cur.clear();
+      bufs = nr = ns = 0;
+    };
     for (int i = 0; i < (int)items.size(); ++i) {
       const auto& it = items[i];
-      if (it.rc.removed == 0 || it.seq->len - it.rc.removed <= it.rc.first_row) continue;
-      for (int b0 = 0; b0 < (int)it.bufs.size(); b0 += kMaxBufPerLaunch) {
-        const int nb = std::min<int>(kMaxBufPerLaunch, (int)it.bufs.size() - b0);
-        if ((int)cur.size() == kMaxSeqPerLaunch || cur_bufs + nb > kMaxBufPerLaunch) {
-          groups.push_back(cur);
-          cur.clear();
-          cur_bufs = 0;
-        }
-        cur.push_back({i, b0, nb});
-        cur_bufs += nb;
-      }
-    }
-    if (!cur.empty()) groups.push_back(cur);
-  }
-  // counters: per launch one ticket + one error word, then stripe counters
-  const size_t counters_at = ar.used;
-  std::vector<size_t> flag_words;
-  size_t words = 0;
-  for (auto& g : groups) {
-    size_t w = 2;
-    for (auto& e : g) {
-      const auto& it = items[e.item];
-      const int64_t n_keep = it.seq->len - it.rc.removed;
-      const int64_t align_rows = std::max(1, 128 / row_bytes);
-      const int64_t rb = (it.rc.first_row / align_rows) * align_rows;
-      w += (n_keep - rb + R - 1) / R;
-    }
-    flag_words.push_back(w);
-    words += w;
-  }
-  int32_t* counters = static_cast<int32_t*>(ar.take(sizeof(int32_t) * std::max<size_t>(1, words)));
-  (void)counters_at;
-  plan->ws_bytes = ar.used;
-  if (!ws) return TU_OK;
-
-  // scan launches
-  plan->scans.clear();
-  {
-    ScanArgs a{};
-    int nr = 0;
-    auto flush = [&]() {
-      if (a.n_seq == 0) return;
-      plan->scans.push_back(a);
-      a = ScanArgs{};
-      nr = 0;
-    };
-    for (auto& it : items) {
-      if (it.seq->len == 0 || (it.rc.removed == 0 && !it.user_index)) continue;
-      if (a.n_seq == kMaxSeqPerLaunch || nr + it.n_ranges > kMaxRangesPerLaunch) flush();
-      ScanSeq& s = a.seq[a.n_seq++];
-      s.pos = it.seq->d_pos;
-      s.src_index = it.src_index;
-      s.L_old = (int32_t)it.seq->len;
-      s.range_begin = nr;
-      s.n_ranges = it.n_ranges;
-      for (int q = 0; q < it.n_ranges; ++q) {
-        a.ranges[nr + q][0] = (int32_t)it.ranges[2 * q];
-        a.ranges[nr + q][1] = (int32_t)it.ranges[2 * q + 1];
-      }
-      nr += it.n_ranges;
+      const bool moves = it.rc.removed > 0 && it.seq->len - it.rc.removed > it.rc.first_row && !it.bufs.empty();
+      const bool scans = it.seq->len > 0 && (it.rc.removed > 0 || it.user_index);
+      if (!moves && !scans) continue;
+      int b0 = 0;
+      bool first = true;
+      do {
+        const int nb = moves ? std::min<int>(kMaxBufPerLaunch, (int)it.bufs.size() - b0) : 0;
+        const bool sc = scans && first;
+        if ((int)cur.size() == kMaxSeqPerCompact || bufs + nb > kMaxBufPerLaunch ||
+            (sc && nr + it.n_ranges > kMaxRangesPerLaunch) || (ns + it.n_ranges > kMaxRangesPerLaunch))
+          flush();
+        cur.push_back({i, b0, nb, sc, moves});
+        bufs += nb;
+        if (sc) nr += it.n_ranges;
+        ns += it.n_ranges;   // spans are referenced by both the scan and the move entries
+        b0 += nb;
+        first = false;
+      } while (moves && b0 < (int)it.bufs.size());
     }
     flush();
-    if (!plan->scans.empty()) {
-      plan->scans[0].zero_ptr = counters;
-      plan->scans[0].zero_count = (int32_t)words;
-    }
   }
-  // gather launches
-  plan->gathers.clear();
-  plan->gather_blocks.clear();
-  size_t woff = 0;
-  for (size_t gi = 0; gi < groups.size(); ++gi) {
-    GatherArgs a{};
-    int32_t* base = counters + woff;
-    a.ticket = base;
-    a.err = base + 1;
-    a.flags = base + 2;
+  plan->launches.clear();
+  plan->workers.clear();
+  const int max_blocks = ws ? compact_max_blocks() : 0;
+  for (auto& g : groups) {
+    CompactArgs a{};
     a.rows_per_stripe = R;
     a.row_bytes = row_bytes;
-    int items_total = 0, flag_off = 0, nbufs = 0;
-    for (auto& e : groups[gi]) {
+    int nr = 0, ns = 0, items_total = 0, flag_off = 0, nbufs = 0;
+    std::vector<int> span_at(items.size(), -1);   // where each context's spans sit in this launch
+    auto spans_of = [&](const CompactItem& it, int idx) {
+      if (span_at[idx] >= 0) return span_at[idx];
+      span_at[idx] = ns;
+      int64_t before = 0;
+      for (int q = 0; q < it.n_ranges; ++q) {
+        const int64_t len = it.ranges[2 * q + 1] - it.ranges[2 * q];
+        a.spans[ns + q][0] = (int32_t)(it.rc.rows[q] - before);
+        a.spans[ns + q][1] = (int32_t)len;
+        before += len;
+      }
+      ns += it.n_ranges;
+      return span_at[idx];
+    };
+    for (auto& e : g) {
       const auto& it = items[e.item];
-      GatherSeq& s = a.seq[a.n_seq++];
-      const int64_t n_keep = it.seq->len - it.rc.removed;
-      const int64_t align_rows = std::max(1, 128 / row_bytes);
-      const int64_t rb = (it.rc.first_row / align_rows) * align_rows;
-      s.src_index = it.src_index;
-      s.row_begin = (int32_t)rb;
-      s.n_keep = (int32_t)n_keep;
-      s.n_stripes = (int32_t)((n_keep - rb + R - 1) / R);
-      s.item_begin = items_total;
-      s.buf_begin = nbufs;
-      s.n_buf = e.nbuf;
-      s.flag_begin = flag_off;
-      s.window = (int32_t)((it.rc.removed + R - 1 + R - 1) / R);
-      for (int b = 0; b < e.nbuf; ++b) a.bufs[nbufs++] = it.bufs[e.buf0 + b];
-      items_total += s.n_stripes * s.n_buf;
-      flag_off += s.n_stripes;
+      if (e.scan) {
+        ScanSeq& c = a.scan[a.n_scan++];
+        c.pos = it.seq->d_pos;
+        c.src_index = it.src_index;
+        c.L_old = (int32_t)it.seq->len;
+        c.range_begin = nr;
+        c.n_ranges = it.n_ranges;
+        c.span_begin = spans_of(it, e.item);
+        c.n_spans = it.n_ranges;
+        c.block_begin = a.n_scan_blocks;
+        a.n_scan_blocks += (int32_t)((it.seq->len + kScanRows - 1) / kScanRows);
+        for (int q = 0; q < it.n_ranges; ++q) {
+          a.ranges[nr + q][0] = (int32_t)it.ranges[2 * q];
+          a.ranges[nr + q][1] = (int32_t)it.ranges[2 * q + 1];
+        }
+        nr += it.n_ranges;
+      }
+      if (e.move && e.nbuf > 0) {
+        GatherSeq& m = a.seq[a.n_seq++];
+        const int64_t n_keep = it.seq->len - it.rc.removed;
+        const int64_t rb = (it.rc.first_row / align_rows) * align_rows;
+        const bool with_pos = e.buf0 == 0;   // the context's first buffer group also moves positions
+        m.pos = with_pos ? it.seq->d_pos : nullptr;
+        m.row_begin = (int32_t)rb;
+        m.n_keep = (int32_t)n_keep;
+        m.n_stripes = (int32_t)((n_keep - rb + R - 1) / R);
+        m.item_begin = items_total;
+        m.buf_begin = nbufs;
+        m.n_buf = e.nbuf + (with_pos ? 1 : 0);
+        m.flag_begin = flag_off;
+        m.window = (int32_t)((it.rc.removed + R - 1 + R - 1) / R);
+        m.span_begin = spans_of(it, e.item);
+        m.n_spans = it.n_ranges;
+        for (int b = 0; b < e.nbuf; ++b) a.bufs[nbufs++] = it.bufs[e.buf0 + b];
+        items_total += m.n_stripes * m.n_buf;
+        flag_off += m.n_stripes;
+      }
     }
     a.total_items = items_total;
-    plan->gathers.push_back(a);
-    plan->gather_blocks.push_back(items_total);
-    woff += flag_words[gi];
+    a.n_flag_words = flag_off * kFlagStride;
+    int32_t* words = static_cast<int32_t*>(ar.take(sizeof(int32_t) * (1 + (size_t)a.n_flag_words)));
+    a.err = words;
+    a.flags = words ? words + 1 : nullptr;
+    plan->launches.push_back(a);
+    plan->workers.push_back(std::max(0, std::min(items_total, max_blocks - a.n_scan_blocks)));
   }
+  plan->ws_bytes = ar.used;
+  if (ws && max_blocks <= 8) return fail(TU_ERR_HIP, "cannot size the compaction grid");
   return TU_OK;
 }
 
 int run_compaction(const CompactPlan& plan, hipStream_t st) {
-  for (const auto& a : plan.scans)
-    if (int e = hip_check(timed("keep_scan", st, [&] { return launch_keep_scan(a, st); }), "keep-scan launch")) return e;
-  for (size_t i = 0; i < plan.gathers.size(); ++i)
-    if (int e = hip_check(timed("gather", st, [&] { return launch_gather(plan.gathers[i], plan.gather_blocks[i], st); }), "gather launch")) return e;
+  for (size_t i = 0; i < plan.launches.size(); ++i)
+    if (int e = hip_check(timed("compact", st, [&] { return launch_compact(plan.launches[i], plan.workers[i], st); }),
+                          "compaction launch"))
+      return e;
   return TU_OK;
 }
 
@@ -512,6 +512,8 @@ int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, vo
     a.ws_u = static_cast<float*>(ar.take(sizeof(float) * (size_t)chunks * Hv * C * DK));
     a.ws_p = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * C));
     a.ws_lg = static_cast<float*>(ar.take(sizeof(float) * (size_t)chunks * Hv * C));
+    a.ws_q = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * DK));
+    a.ws_kt = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * DK));
     max_used = std::max(max_used, ar.used);
     if (a.n_seq > 0) out->push_back(a);
   }
@@ -703,7 +705,7 @@ size_t compact_kv_workspace_size(int64_t len, int32_t n_layers, int32_t n_kv_hea
   fake.len = len;
   std::vector<CompactItem> items(1);
   items[0].seq = &fake;
-  items[0].n_ranges = 1;
+  items[0].n_ranges = 0;   // sizing only: spans are not read
   items[0].rc.removed = 1;
   items[0].rc.first_row = 0;
   items[0].src_index = nullptr;
@@ -746,7 +748,7 @@ int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_
     return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.ws_bytes);
   if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
   items[0].src_index = src_index;
-  plan_compaction(items, row_bytes, workspace, &plan);
+  if (int e = plan_compaction(items, row_bytes, workspace, &plan)) return e;
   if (int e = run_compaction(plan, static_cast<hipStream_t>(stream))) return e;
   const int64_t removed = items[0].rc.removed;
   commit_intervals(seq, items[0].rc.live_after);
@@ -923,11 +925,11 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
     return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
   if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  // a2-a3: one keep-scan and one gather over every attention layer of every context
+  // a2-a3: keep-scan and in-place row move over every attention layer of every context
   if (sp.n_attn) {
     auto items = stack_compact_items(u, sp);
     CompactPlan cp;
-    plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, workspace, &cp);
+    if (int e = plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, workspace, &cp)) return e;
     if (int e = run_compaction(cp, st)) return e;
   }
   // a4-a7 in layer order

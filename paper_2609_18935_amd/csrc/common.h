@@ -17,7 +17,10 @@ typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
 
 constexpr int kMaxSeqPerLaunch = 16;
 constexpr int kMaxRangesPerLaunch = 128;
-constexpr int kMaxBufPerLaunch = 64;
+constexpr int kMaxBufPerLaunch = 32;
+constexpr int kMaxSeqPerCompact = 8;
+constexpr int kScanRows = 4096;  // rows per keep-scan workgroup
+constexpr int kFlagStride = 32;   // compaction stripe counters sit one per 128-byte line
 constexpr int kGatherStripeBytes = 256 * 8 * 16;  // threads x vectors x 16 B
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
@@ -61,44 +64,47 @@ __device__ __forceinline__ int xcd_remap(int b, int n_blocks) {
 // ------------------------------------------------------------------ launch records
 
 struct ScanSeq {
-  int32_t* pos;        // [capacity] compacted in place
+  const int32_t* pos;  // [L_old] positions of the cache rows (read only)
   int32_t* src_index;  // [L_old] out
   int32_t L_old;
-  int32_t range_begin; // index into ScanArgs::ranges
+  int32_t range_begin; // index into CompactArgs::ranges
   int32_t n_ranges;
-  int32_t pad;
-};
-
-struct ScanArgs {
-  ScanSeq seq[kMaxSeqPerLaunch];
-  int32_t ranges[kMaxRangesPerLaunch][2];
-  int32_t n_seq;
-  int32_t zero_count;   // int32 words of gather flags/tickets to clear
-  int32_t* zero_ptr;
+  int32_t span_begin;  // index into CompactArgs::spans
+  int32_t n_spans;
+  int32_t block_begin; // first scan workgroup of this context
 };
 
 struct GatherSeq {
-  const int32_t* src_index;
+  int32_t* pos;         // d_pos of the context when this entry also moves positions, else null
   int32_t row_begin;    // first destination row handled (aligned, <= first moved row)
   int32_t n_keep;       // destination rows end
   int32_t n_stripes;
-  int32_t item_begin;   // first ticket of this context
-  int32_t buf_begin;    // index of its first buffer in GatherArgs::bufs
-  int32_t n_buf;
+  int32_t item_begin;   // first item of this context
+  int32_t buf_begin;    // index of its first buffer in CompactArgs::bufs
+  int32_t n_buf;        // items per stripe (K/V buffers, plus one for positions when pos != null)
   int32_t flag_begin;   // its stripe read-counters
-  int32_t window;       // stripes before s whose sources may overlap stripe s's rows
+  int32_t window;       // stripes before s whose sources may reach stripe s's rows
+  int32_t span_begin;   // index into CompactArgs::spans
+  int32_t n_spans;
 };
 
-struct GatherArgs {
-  GatherSeq seq[kMaxSeqPerLaunch];
+// One cooperative compaction launch: keep-scan for n_scan contexts and the row move
+// for n_seq (context, buffer-group) entries.
+struct CompactArgs {
+  ScanSeq scan[kMaxSeqPerCompact];
+  GatherSeq seq[kMaxSeqPerCompact];
   void* bufs[kMaxBufPerLaunch];
+  int32_t ranges[kMaxRangesPerLaunch][2];  // position ranges [a, b) of the scan contexts
+  int32_t spans[kMaxRangesPerLaunch][2];   // (kept rows before the span, span length) per removed span
+  int32_t n_scan;          // scan contexts
+  int32_t n_scan_blocks;   // scan workgroups (kScanRows rows each)
   int32_t n_seq;
   int32_t total_items;
   int32_t rows_per_stripe;
   int32_t row_bytes;
-  int32_t* ticket;
-  int32_t* flags;
-  int32_t* err;
+  int32_t n_flag_words;   // stripe counters x kFlagStride
+  int32_t* flags;   // [n_flag_words] stripe read counters, kFlagStride apart
+  int32_t* err;     // flags - 1: set when a bounded wait expired
 };
 
 struct RopeSeq {
@@ -185,12 +191,14 @@ struct DeltaArgs {
   float* ws_u;           // [chunks][Hv][C][dv]
   _Float16* ws_p;        // [chunks][Hv][C][C]
   float* ws_lg;          // [chunks][Hv][C]
+  _Float16* ws_q;        // [chunks][Hv][C][dk]  scale * 2^lg q
+  _Float16* ws_kt;       // [chunks][Hv][dk][C]  2^(lg_last - lg) k, transposed
 };
 
 // ------------------------------------------------------------------ launchers
 // (defined in the kernel translation units; return a hipError_t)
-hipError_t launch_keep_scan(const ScanArgs& a, hipStream_t s);
-hipError_t launch_gather(const GatherArgs& a, int n_blocks, hipStream_t s);
+int compact_max_blocks();   // co-resident workgroups of the compaction kernel
+hipError_t launch_compact(const CompactArgs& a, int n_workers, hipStream_t s);
 hipError_t launch_rope_append(const RopeArgs& a, int total_tokens, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention_merge(const MergeArgs& a, int total_rows, int head_dim, hipStream_t s);

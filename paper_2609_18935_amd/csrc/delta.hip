@@ -229,29 +229,45 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
   }
   for (int e = tid; e < (C / 4) * (DK / 8); e += 256) {
     const int s4 = (e % (C / 4)) * 4, d0 = (e / (C / 4)) * 8;
-    float wk[4], wv[4];
+    float wk[4], wv[4], wd[4];
     u32x4 kw[4], vw[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int s = s4 + j;
       wv[j] = bt[s];
       wk[j] = bt[s] * __builtin_amdgcn_exp2f(lg[s]);
+      wd[j] = __builtin_amdgcn_exp2f(lg[C - 1] - lg[s]);
       kw[j] = *(const u32x4*)&Ks[s][d0];
       vw[j] = (s < Cr) ? *(const u32x4*)(S.v + ((long)(t0 + s) * Hv + h) * DV + d0) : u32x4{0, 0, 0, 0};
     }
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
-      f16x4 hk, hv;
+      f16x4 hk, hv, hd;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint32_t kb = (d & 1) ? (kw[j][d >> 1] & 0xFFFF0000u) : (kw[j][d >> 1] << 16);
         const uint32_t vb = (d & 1) ? (vw[j][d >> 1] & 0xFFFF0000u) : (vw[j][d >> 1] << 16);
         hk[j] = (_Float16)(wk[j] * __uint_as_float(kb));
         hv[j] = (_Float16)(wv[j] * __uint_as_float(vb));
+        hd[j] = (_Float16)(wd[j] * __uint_as_float(kb));
       }
       *(f16x4*)&Bt[d0 + d][s4] = hk;
       *(f16x4*)&Vt[d0 + d][s4] = hv;
+      *(f16x4*)(a.ws_kt + slot * DK * C + (long)(d0 + d) * C + s4) = hd;
     }
+  }
+  // scale * 2^lg Q as f16 (the chain's Q S^T operand, row decay folded in)
+  for (int e = tid; e < C * (DK / 8); e += 256) {
+    const int r = e / (DK / 8), cc = e - r * (DK / 8);
+    const float w = a.scale * __builtin_amdgcn_exp2f(lg[r]);
+    const u32x4 qw = *(const u32x4*)&Qs[r][cc * 8];
+    f16x8 hq;
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      const uint32_t qb = (d & 1) ? (qw[d >> 1] & 0xFFFF0000u) : (qw[d >> 1] << 16);
+      hq[d] = (_Float16)(w * __uint_as_float(qb));
+    }
+    *(f16x8*)(a.ws_q + slot * C * DK + (long)r * DK + cc * 8) = hq;
   }
   __syncthreads();
 
@@ -296,22 +312,30 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
   constexpr int NSB = (DK / 16) * NCB;          // blocks of S^T
   constexpr int NSW = NSB / 4;                  // per wave
   static_assert(NSB % 4 == 0, "state blocks must split over 4 waves");
+  // per-chunk operands staged from the workspace (all f16 except U~)
+  constexpr int VQ = C * DK / 8;                // 16-byte vectors of W and of Qg
+  constexpr int VK = DK * C / 8;                // of Kd^T
+  constexpr int VP = C * C / 8;                 // of P
+  constexpr int VU = C * DVS / 4;               // 16-byte vectors of the U~ slice (fp32)
+  constexpr int RQ = (VQ + 255) / 256, RK = (VK + 255) / 256, RP = (VP + 255) / 256, RU = (VU + 255) / 256;
   __shared__ __attribute__((aligned(16))) _Float16 Ws[C][KP];
   __shared__ __attribute__((aligned(16))) _Float16 Qs[C][KP];
   __shared__ __attribute__((aligned(16))) _Float16 Kdt[DK][CH];
   __shared__ __attribute__((aligned(16))) _Float16 Ph[C][CH];
+  __shared__ __attribute__((aligned(16))) float Us[C][DVS + 4];
   __shared__ __attribute__((aligned(16))) _Float16 Ut[DVS][CH];
   __shared__ __attribute__((aligned(16))) _Float16 Sh[DVS][KP];
-  __shared__ float lg[C];
+  __shared__ float s_glast;
 
-  const int Hk = a.n_k_heads, Hv = a.n_v_heads;
+  const int Hv = a.n_v_heads;
   const int per_seq = Hv * a.n_slices;
-  const int si = blockIdx.x / per_seq;
-  const int rem = blockIdx.x - si * per_seq;
+  const int item = xcd_remap(blockIdx.x, gridDim.x);   // slices of one head share an XCD
+  if (item >= a.n_seq * per_seq) return;
+  const int si = item / per_seq;
+  const int rem = item - si * per_seq;
   const int h = rem / a.n_slices;
   const int i0 = (rem - h * a.n_slices) * DVS;
   const DeltaSeq S = a.seq[si];
-  const int kh = h / (Hv / Hk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g4 = lane >> 4;
   const bool kpart = (C >= 32) || (g4 < 2);     // lanes that carry chunk-dim K elements
@@ -329,55 +353,87 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     *(f16x4*)&Sh[i][d] = hv;
   }
 
+  // ---- next chunk's operands are fetched into registers while the current one is computed
+  u32x4 rw[RQ], rq[RQ], rk[RK], rp[RP], ru[RU];
+  float rg = 0.f;
+  auto prefetch = [&](int lc) {
+    const long slot = (long)(S.chunk_begin + lc) * Hv + h;
+    const u32x4* W4 = (const u32x4*)(a.ws_w + slot * C * DK);
+    const u32x4* Q4 = (const u32x4*)(a.ws_q + slot * C * DK);
+    const u32x4* K4 = (const u32x4*)(a.ws_kt + slot * DK * C);
+    const u32x4* P4 = (const u32x4*)(a.ws_p + slot * C * C);
+    const float* U = a.ws_u + slot * C * DV + i0;
+#pragma unroll
+    for (int j = 0; j < RQ; ++j) {
+      const int e = tid + 256 * j;
+      if (e < VQ) {
+        rw[j] = W4[e];
+        rq[j] = Q4[e];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RK; ++j)
+      if (tid + 256 * j < VK) rk[j] = K4[tid + 256 * j];
+#pragma unroll
+    for (int j = 0; j < RP; ++j)
+      if (tid + 256 * j < VP) rp[j] = P4[tid + 256 * j];
+#pragma unroll
+    for (int j = 0; j < RU; ++j) {
+      const int e = tid + 256 * j;
+      if (e < VU) {
+        const int r = e / (DVS / 4), c4 = e - r * (DVS / 4);
+        ru[j] = *(const u32x4*)(U + (long)r * DV + 4 * c4);
+      }
+    }
+    rg = a.ws_lg[slot * C + C - 1];
+  };
+  auto stage = [&]() {
+#pragma unroll
+    for (int j = 0; j < RQ; ++j) {
+      const int e = tid + 256 * j;
+      if (e < VQ) {
+        const int r = e / (DK / 8), c8 = e - r * (DK / 8);
+        *(u32x4*)&Ws[r][8 * c8] = rw[j];
+        *(u32x4*)&Qs[r][8 * c8] = rq[j];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RK; ++j) {
+      const int e = tid + 256 * j;
+      if (e < VK) {
+        const int d = e / (C / 8), c8 = e - d * (C / 8);
+        *(u32x4*)&Kdt[d][8 * c8] = rk[j];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RP; ++j) {
+      const int e = tid + 256 * j;
+      if (e < VP) {
+        const int r = e / (C / 8), c8 = e - r * (C / 8);
+        *(u32x4*)&Ph[r][8 * c8] = rp[j];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RU; ++j) {
+      const int e = tid + 256 * j;
+      if (e < VU) {
+        const int r = e / (DVS / 4), c4 = e - r * (DVS / 4);
+        *(u32x4*)&Us[r][4 * c4] = ru[j];
+      }
+    }
+    if (tid == 0) s_glast = __builtin_amdgcn_exp2f(rg);
+  };
+
+  prefetch(0);
   for (int lc = 0; lc < S.n_chunks; ++lc) {
-    const int c = S.chunk_begin + lc;
-    const long slot = (long)c * Hv + h;
     const int t0 = lc * C;
     const int Cr = min(C, S.T - t0);
-    // ---- stage W, Q (as f16), P and lg
-    {
-      const _Float16* Wg = a.ws_w + slot * C * DK;
-      for (int e = tid; e < C * (DK / 8); e += 256) {
-        const int r = e / (DK / 8), cc = e - r * (DK / 8);
-        *(u32x4*)&Ws[r][cc * 8] = *(const u32x4*)(Wg + r * DK + cc * 8);
-        u32x4 qw = {0, 0, 0, 0};
-        if (r < Cr) qw = bf16x8_to_f16x8(*(const u32x4*)(S.q + ((long)(t0 + r) * Hk + kh) * DK + cc * 8));
-        *(u32x4*)&Qs[r][cc * 8] = qw;
-      }
-      const _Float16* Pg = a.ws_p + slot * C * C;
-      for (int e = tid; e < C * (C / 8); e += 256) {
-        const int r = e / (C / 8), cc = e - r * (C / 8);
-        *(u32x4*)&Ph[r][cc * 8] = *(const u32x4*)(Pg + r * C + cc * 8);
-      }
-      if (tid < C) lg[tid] = a.ws_lg[slot * C + tid];
-    }
+    stage();
     __syncthreads();
-    const float lg_last = lg[C - 1];
-    const float g_last = __builtin_amdgcn_exp2f(lg_last);
-    // K^T scaled by the decay to the chunk end, as f16
-    for (int e = tid; e < (C / 4) * (DK / 8); e += 256) {
-      const int s4 = (e % (C / 4)) * 4, d0 = (e / (C / 4)) * 8;
-      u32x4 kw[4];
-      float w[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int s = s4 + j;
-        w[j] = __builtin_amdgcn_exp2f(lg_last - lg[s]);
-        kw[j] = (s < Cr) ? *(const u32x4*)(S.k + ((long)(t0 + s) * Hk + kh) * DK + d0) : u32x4{0, 0, 0, 0};
-      }
-#pragma unroll
-      for (int d = 0; d < 8; ++d) {
-        f16x4 hk;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t kb = (d & 1) ? (kw[j][d >> 1] & 0xFFFF0000u) : (kw[j][d >> 1] << 16);
-          hk[j] = (_Float16)(w[j] * __uint_as_float(kb));
-        }
-        *(f16x4*)&Kdt[d0 + d][s4] = hk;
-      }
-    }
+    if (lc + 1 < S.n_chunks) prefetch(lc + 1);
+    const float g_last = s_glast;
 
-    // ---- X = W S^T -> U = U~ - X (to LDS as U^T);  Y = Q S^T -> O accumulator
+    // ---- X = W S^T -> U = U~ - X (to LDS as U^T);  Y = Qg S^T starts O
     f32x4 oacc[NXW];
 #pragma unroll
     for (int j = 0; j < NXW; ++j) {
@@ -392,19 +448,15 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
         x = mfma_f16(ld_f16x8(&Ws[16 * rb + l16][32 * kk + 8 * g4]), sv, x);
         y = mfma_f16(ld_f16x8(&Qs[16 * rb + l16][32 * kk + 8 * g4]), sv, y);
       }
-      const float* Ug = a.ws_u + slot * C * DV + i0 + 16 * cb + l16;
       f16x4 uh;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = 16 * rb + 4 * g4 + e;
-        uh[e] = (_Float16)(Ug[(long)r * DV] - x[e]);
-        oacc[j][e] = y[e] * a.scale * __builtin_amdgcn_exp2f(lg[r]);
-      }
+      for (int e = 0; e < 4; ++e) uh[e] = (_Float16)(Us[16 * rb + 4 * g4 + e][16 * cb + l16] - x[e]);
       *(f16x4*)&Ut[16 * cb + l16][16 * rb + 4 * g4] = uh;
+      oacc[j] = y;
     }
     __syncthreads();
 
-    // ---- O += P U, written out; S^T <- 2^lg_last S^T + Kd^T U
+    // ---- O += P U, written out; S^T <- 2^lg_last S^T + Kd^T U; refresh the f16 copy of S
 #pragma unroll
     for (int j = 0; j < NXW; ++j) {
       const int b = wave + 4 * j;
@@ -430,7 +482,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     for (int j = 0; j < NSW; ++j) {
       const int b = wave + 4 * j;
       const int db = b / NCB, cb = b % NCB;
-      f32x4 s = st[j] * g_last;
+      f32x4 sacc = st[j] * g_last;
 #pragma unroll
       for (int kk = 0; kk < (C + 31) / 32; ++kk) {
         f16x8 av = zero_f16x8(), bv = zero_f16x8();
@@ -438,18 +490,14 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
           av = ld_f16x8(&Kdt[16 * db + l16][32 * kk + 8 * g4]);
           bv = ld_f16x8(&Ut[16 * cb + l16][32 * kk + 8 * g4]);
         }
-        s = mfma_f16(av, bv, s);
+        sacc = mfma_f16(av, bv, sacc);
       }
-      st[j] = s;
-    }
-    __syncthreads();   // all reads of Sh / Ut / staged tiles done
-#pragma unroll
-    for (int j = 0; j < NSW; ++j) {
-      const int b = wave + 4 * j;
-      const int db = b / NCB, cb = b % NCB;
-      f16x4 hv = {(_Float16)st[j][0], (_Float16)st[j][1], (_Float16)st[j][2], (_Float16)st[j][3]};
+      st[j] = sacc;
+      // every read of Sh for this chunk happened before the barrier above
+      f16x4 hv = {(_Float16)sacc[0], (_Float16)sacc[1], (_Float16)sacc[2], (_Float16)sacc[3]};
       *(f16x4*)&Sh[16 * cb + l16][16 * db + 4 * g4] = hv;
     }
+    __syncthreads();   // staged tiles, U^T and S are free for the next chunk
   }
 #pragma unroll
   for (int j = 0; j < NSW; ++j) {
@@ -467,7 +515,7 @@ hipError_t prep_for(const DeltaArgs& a, hipStream_t s) {
 
 template <int DK, int C>
 hipError_t chain_for(const DeltaArgs& a, hipStream_t s) {
-  const int blocks = a.n_seq * a.n_v_heads * a.n_slices;
+  const int blocks = (a.n_seq * a.n_v_heads * a.n_slices + 7) & ~7;   // XCD remap needs a multiple of 8
   const int dvs = DK / a.n_slices;
   if (dvs == 32)
     hipLaunchKernelGGL((k_delta_chain<DK, C, 32>), dim3(blocks), dim3(256), 0, s, a);
