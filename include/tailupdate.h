@@ -74,7 +74,7 @@ typedef struct tu_seq {
 
 /*
  * Attention-layer shape. Query head h reads KV head h / (n_q_heads / n_kv_heads).
- * head_dim must be 64 or 256; rotary_dim even, 0 <= rotary_dim <= head_dim
+ * head_dim must be 64, 128 or 256; rotary_dim even, 0 <= rotary_dim <= head_dim
  * (rotate-half pairs (j, j + rotary_dim/2), angle pos * rope_theta^(-2j/rotary_dim)).
  * kv_splits = 0 lets the library split the key range for occupancy; a positive
  * value forces that many splits (results are the same up to rounding).
@@ -233,7 +233,7 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
  * entry in `names`) the launch count and the summed duration in milliseconds,
  * for at most `max_entries` kernels; it returns the number of entries written
  * (or a negative status) and clears the records. Kernel names: compact,
- * rope_append, attention, attention_merge, delta_prep, delta_chain.
+ * rope_append, vt_pack, attention, attention_merge, delta_prep, delta_chain.
  */
 int tu_profile_enable(int on);
 int tu_profile_collect(char* names, int32_t name_stride, int32_t* counts, double* total_ms, int32_t max_entries);

@@ -136,7 +136,8 @@ int check_attn(const tu_attn_params* p) {
   if (!p) return fail(TU_ERR_ARG, "null attention parameters");
   if (p->n_kv_heads <= 0 || p->n_q_heads <= 0 || p->n_q_heads % p->n_kv_heads)
     return fail(TU_ERR_ARG, "n_q_heads must be a positive multiple of n_kv_heads");
-  if (p->head_dim != 64 && p->head_dim != 256) return fail(TU_ERR_ARG, "head_dim must be 64 or 256");
+  if (p->head_dim != 64 && p->head_dim != 128 && p->head_dim != 256)
+    return fail(TU_ERR_ARG, "head_dim must be 64, 128 or 256");
   if (p->rotary_dim < 0 || p->rotary_dim > p->head_dim || (p->rotary_dim & 1))
     return fail(TU_ERR_ARG, "rotary_dim must be even and within [0, head_dim]");
   if (!(p->rope_theta > 0.0) || !std::isfinite(p->rope_theta)) return fail(TU_ERR_ARG, "rope_theta must be positive");
@@ -365,7 +366,7 @@ int choose_splits(const tu_attn_params* p, int64_t L_keep, int64_t T, int64_t ba
   if (p->kv_splits > 0) return p->kv_splits;
   const int G = p->n_q_heads / p->n_kv_heads;
   (void)G;
-  const int64_t n_kt = (L_keep + T + 63) / 64;
+  const int64_t n_kt = (L_keep + T + kAttnKeys - 1) / kAttnKeys;
   int want = (int)std::max<int64_t>(1, (256 + base_items_total - 1) / std::max<int64_t>(1, base_items_total));
   const int max_by_len = (int)std::max<int64_t>(1, n_kt / 4);  // at least 4 key tiles per split
   return std::max(1, std::min({want, max_by_len, 64}));
@@ -380,7 +381,7 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
     const size_t g1 = std::min(items.size(), g0 + kMaxSeqPerLaunch);
     Arena ar(ws);
     int64_t base_items = 0;
-    for (size_t i = g0; i < g1; ++i) base_items += (int64_t)Hkv * ((items[i].T * G + 127) / 128);
+    for (size_t i = g0; i < g1; ++i) base_items += (int64_t)Hkv * ((items[i].T * G + kAttnRows - 1) / kAttnRows);
     AttnLaunch L{};
     L.rope.n_q_heads = Hq;
     L.rope.n_kv_heads = Hkv;
@@ -391,19 +392,21 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
     L.attn.n_kv_heads = Hkv;
     L.attn.scale_log2 = p->softmax_scale * 1.4426950408889634f;
     L.merge.n_q_heads = Hq;
-    int tok = 0, item_total = 0, mrows = 0;
+    int tok = 0, item_total = 0, pack_total = 0, mrows = 0;
     for (size_t i = g0; i < g1; ++i) {
       const AttnItem& it = items[i];
       if (it.T <= 0) continue;
       bf16_t* qh = it.q_hat;
       void* qh_ws = ar.take(sizeof(bf16_t) * it.T * Hq * D);
       if (!qh) qh = static_cast<bf16_t*>(qh_ws);
-      const int tiles = (int)((it.T * G + 127) / 128);
+      const int tiles = (int)((it.T * G + kAttnRows - 1) / kAttnRows);
       const int splits = choose_splits(p, it.L_keep, it.T, base_items);
-      float* po = nullptr;
+      const int vt_tiles = (int)((it.L_keep + it.T + kAttnKeys - 1) / kAttnKeys);
+      _Float16* vt = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)Hkv * vt_tiles * D * kVtRow));
+      _Float16* po = nullptr;
       float* pml = nullptr;
       if (splits > 1) {
-        po = static_cast<float*>(ar.take(sizeof(float) * splits * it.T * Hq * D));
+        po = static_cast<_Float16*>(ar.take(sizeof(_Float16) * splits * it.T * Hq * D));
         pml = static_cast<float*>(ar.take(sizeof(float) * 2 * splits * it.T * Hq));
       }
       RopeSeq& r = L.rope.seq[L.rope.n_seq++];
@@ -423,6 +426,7 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
       s.q_hat = qh;
       s.k_cache = static_cast<const bf16_t*>(it.k_cache);
       s.v_cache = static_cast<const bf16_t*>(it.v_cache);
+      s.vt = vt;
       s.out = it.out;
       s.part_o = po;
       s.part_ml = pml;
@@ -431,7 +435,10 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
       s.n_tiles = tiles;
       s.n_splits = splits;
       s.item_begin = item_total;
+      s.n_vt_tiles = vt_tiles;
+      s.pack_begin = pack_total;
       item_total += Hkv * splits * tiles;
+      pack_total += Hkv * vt_tiles;
       if (splits > 1) {
         L.merge.row_begin[L.merge.n_seq] = mrows;
         L.merge.seq[L.merge.n_seq++] = s;
@@ -441,6 +448,7 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
     L.merge.row_begin[L.merge.n_seq] = mrows;
     L.rope_tokens = tok;
     L.attn.total_items = item_total;
+    L.attn.pack_items = pack_total;
     L.merge_rows = mrows;
     max_used = std::max(max_used, ar.used);
     if (L.rope.n_seq > 0) out->push_back(L);
@@ -452,6 +460,7 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
 int run_attention(const std::vector<AttnLaunch>& ls, int D, hipStream_t st) {
   for (const auto& L : ls) {
     if (int e = hip_check(timed("rope_append", st, [&] { return launch_rope_append(L.rope, L.rope_tokens, st); }), "rope-append launch")) return e;
+    if (int e = hip_check(timed("vt_pack", st, [&] { return launch_vt_pack(L.attn, D, st); }), "V^T pack launch")) return e;
     if (int e = hip_check(timed("attention", st, [&] { return launch_attention(L.attn, D, st); }), "attention launch")) return e;
     if (L.merge_rows > 0)
       if (int e = hip_check(timed("attention_merge", st, [&] { return launch_attention_merge(L.merge, L.merge_rows, D, st); }), "merge launch")) return e;

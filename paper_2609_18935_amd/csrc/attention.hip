@@ -7,39 +7,99 @@
 // rows (token-major: packed row = t * G + (h mod G)), so one workgroup tile of
 // 128 packed rows reads each K/V tile once for all of them.
 //
-// Workgroup: 4 waves x 32 packed rows, key tiles of 64 rows staged in LDS.
-// The scores are formed transposed, S^T = K Q^T, on v_mfma_f32_32x32x16_bf16:
-// A = 32 keys x 16 dims of K (LDS), B = 16 dims x 32 queries of Q (registers).
-// A lane's accumulator then holds 16 keys of ONE query (lane % 32), so the
-// online-softmax state (running max, running sum) is per lane; the two lanes
-// sharing a query (l and l ^ 32) exchange their maxima once per tile. The output
-// is accumulated transposed too, O^T += V^T P^T, on v_mfma_f32_32x32x16_f16: V is
-// written into LDS transposed ([dim][key]) and converted to f16, and the
-// probabilities P (in [0, 1]) are rounded to f16, whose 10 stored mantissa bits
-// keep the result within the accuracy bound where bf16's 7 would not. Within each
-// 16-key group the LDS key order is permuted so that a lane's 8 keys of a B
-// fragment are contiguous (one 16-byte read).
+// Workgroup: 4 waves of 32 packed rows each (one wave per SIMD); key tiles of 64
+// rows in LDS, processed as two 32-key units. Scores are formed transposed,
+// S^T = K Q^T, on v_mfma_f32_32x32x16_bf16 (A = 32 keys x 16 dims of K from LDS,
+// B = 16 dims x 32 queries of Q held in registers), so a lane's accumulator holds
+// 16 keys of ONE query and the online-softmax state is per lane; the two lanes of a
+// query (l and l ^ 32) exchange their maxima once per unit. The output is accumulated
+// transposed too, O^T += V^T P^T, on v_mfma_f32_32x32x16_f16 with P in [0, 2^8) rounded to f16
+// (10 stored mantissa bits keep the result inside the accuracy bound; bf16's 7 do
+// not). V^T comes pre-packed per 64-key tile as f16 by k_vt_pack, in exactly the LDS
+// layout, so staging it is a plain copy.
 //
-// For occupancy the key range of a tile is split over `n_splits` workgroups; each
-// writes an unnormalised partial (O, running max, sum) and k_attn_merge combines
-// them. Workgroups are ordered (kv head, split, tile) and remapped so that the
-// tiles of one (head, split) key range share an XCD and its L2.
+// Tiles move HBM/L2 -> LDS with buffer_load_dwordx4 ... lds (no staging registers;
+// the buffer resource of a tile ends at the cache's data, so rows past it read as
+// zeros), double-buffered: the K half of tile k+2 is requested once every wave has formed
+// the scores of tile k, and the V half once every wave has used V of tile k. With one
+// wave per SIMD nothing else hides latency, so the loop is software-pipelined: the
+// softmax of one unit is issued together with the score MFMAs of the next (VALU work
+// in the shadow of the matrix core) and LDS fragment reads run several MFMAs ahead.
+//
+// For occupancy the key range is split over `n_splits` workgroups; each writes a
+// normalised f16 partial (O / l) with its reference max and sum, and k_attn_merge
+// combines them. Workgroups are ordered (kv head, split, tile) and remapped so that
+// the query tiles of one (head, split) key range share an XCD and its L2.
 #include "common.h"
 
 namespace tu {
 
 namespace {
 
-constexpr int kBM = 128;   // packed query rows per workgroup
-constexpr int kBN = 64;    // keys per tile
-constexpr int kKPad = 8;   // bf16 padding per K row in LDS
-constexpr int kVPad = 8;   // f16 padding per V^T row in LDS
+constexpr int kBM = kAttnRows;
+constexpr int kBN = kAttnKeys;
 constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units): P < 2^8 fits f16
 
-__device__ __forceinline__ int key_slot(int k) {
-  // swap bits 2 and 3 of the key index within its 16-key group
-  return (k & ~0xC) | ((k & 4) << 1) | ((k & 8) >> 1);
+typedef __attribute__((address_space(3))) void lds_void;
+
+// s_waitcnt immediate that waits on the vector-memory counter only
+constexpr int vm_wait(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
+// Fourth word of a raw buffer resource (32-bit data, no swizzle) on CDNA
+constexpr int kBufWord3 = 0x00020000;
+
+// Copies 16 bytes per lane from base + voff + soff to LDS (lane i writes lds + 16 i).
+// The resource covers `bytes` from base; lanes past it write zeros. base and bytes are
+// wave-uniform; reading them through readfirstlane lets the compiler see that, so the
+// resource stays in scalar registers (no per-lane loop around the load).
+__device__ __forceinline__ void dma16(const void* base, int bytes, uint32_t voff, uint32_t soff, void* lds) {
+  const uint64_t b = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  void* ub = (void*)(((uint64_t)hi << 32) | lo);
+  const __amdgpu_buffer_rsrc_t res =
+      __builtin_amdgcn_make_buffer_rsrc(ub, 0, __builtin_amdgcn_readfirstlane(bytes), kBufWord3);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(res, (lds_void*)lds, 16, voff, soff, 0, 0);
 }
+
+// s_waitcnt immediate that waits on the LDS counter only
+constexpr int kLgkmWait0 = 15 | (7 << 4) | (0 << 8) | (3 << 14);
+
+// Workgroup barrier without the memory fence of __syncthreads: the fence would also
+// wait for the tile prefetches still in flight. LDS hazards are covered by the
+// explicit vm waits plus this barrier; the wave's own LDS reads have returned before
+// it arrives, and the empty asm keeps the compiler from moving memory accesses
+// across it.
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(kLgkmWait0);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Two stages of K (bf16 [64 keys][D + 8]) and V^T (f16 [D][64 + 8], packed layout),
+// sized for D = 256. Every row carries one 16-byte pad so that 16 consecutive rows
+// read at the same column fall in 16 distinct bank groups while fragment addresses
+// stay affine (one base register plus immediates). A stage is rounded up to whole
+// rounds of 16-byte loads by the workgroup, so every wave issues the same number of
+// loads per tile. Separate arrays, so the compiler sees that a prefetch into one stage
+// does not alias reads of the other.
+constexpr int kThreads = 256;       // 4 waves x 32 packed rows
+constexpr int kVRow = kVtRow;       // f16 elements per V^T row
+template <int D>
+struct StageGeom {
+  static constexpr int RC = D / 8;                            // data chunks per K row
+  static constexpr int KRC = RC + 1;                          // chunks per K row in LDS
+  static constexpr int NLK = (kBN * KRC + kThreads - 1) / kThreads;  // K loads per thread
+  static constexpr int NLV = (D * (kVRow / 8) + kThreads - 1) / kThreads;
+  static constexpr int NCV = D * (kVRow / 8);                 // V^T data chunks
+};
+constexpr int kKStage = StageGeom<256>::NLK * kThreads * 8;   // bf16 per K stage
+constexpr int kVStage = StageGeom<256>::NLV * kThreads * 8;   // f16 per V^T stage
+__shared__ __attribute__((aligned(16))) bf16_t g_ks0[kKStage];
+__shared__ __attribute__((aligned(16))) bf16_t g_ks1[kKStage];
+__shared__ __attribute__((aligned(16))) _Float16 g_vt0[kVStage];
+__shared__ __attribute__((aligned(16))) _Float16 g_vt1[kVStage];
 
 // Scales an MFMA accumulator that lives in AGPRs. Going through explicit AGPR
 // reads/writes keeps the accumulator out of the VALU register class, so the
@@ -54,21 +114,22 @@ __device__ __forceinline__ void scale_acc(f32x16& acc, float s) {
   }
 }
 
-__device__ __forceinline__ _Float16 bf16_lo_to_f16(uint32_t w) { return (_Float16)__uint_as_float(w << 16); }
-__device__ __forceinline__ _Float16 bf16_hi_to_f16(uint32_t w) { return (_Float16)__uint_as_float(w & 0xFFFF0000u); }
+template <int B>
+struct IntC {
+  static constexpr int value = B;
+};
 
 template <int D>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
-  constexpr int NS = D / 16;   // 16-dim steps of Q K^T
-  constexpr int NDB = D / 32;  // 32-dim blocks of O^T
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[kBN][D + kKPad];
-  __shared__ __attribute__((aligned(16))) _Float16 Vt[D][kBN + kVPad];
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_attn(AttnArgs a) {
+  constexpr int NS = D / 16;                // 16-dim steps of S^T = K Q^T
+  constexpr int NDB = D / 32;               // 32-dim blocks of O^T
+  constexpr int RC = D / 8;                 // 16-byte chunks of data per K row
 
   const int item = xcd_remap(blockIdx.x, gridDim.x);
   if (item >= a.total_items) return;
   int si = 0;
   while (si + 1 < a.n_seq && a.seq[si + 1].item_begin <= item) ++si;
-  const AttnSeq S = a.seq[si];
+  const AttnSeq& S = a.seq[si];
   int local = item - S.item_begin;
   const int tile = local % S.n_tiles;
   local /= S.n_tiles;
@@ -78,25 +139,29 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int Hq = a.n_q_heads;
   const int Hkv = a.n_kv_heads;
   const int G = Hq / Hkv;
-  const int rows_total = S.T * G;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int T = S.T;
+  const int L_keep = S.L_keep;
+  const int rows_total = T * G;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hl = lane >> 5;     // half of the wave
   const int col = lane & 31;    // query column of this lane
 
   const int r = tile * kBM + wave * 32 + col;
   const bool row_ok = r < rows_total;
-  const int t = row_ok ? r / G : S.T - 1;
+  const int t = row_ok ? r / G : T - 1;
   const int qh = hkv * G + (row_ok ? r - (r / G) * G : 0);
+  const int my_limit = L_keep + t;  // last key this query may see
   const int r_last = min(rows_total, (tile + 1) * kBM) - 1;
   const int t_hi = r_last / G;
   const int t_lo = (tile * kBM) / G;
-  const int n_keys = S.L_keep + t_hi + 1;
+  const int n_keys = L_keep + t_hi + 1;
   const int n_kt = (n_keys + kBN - 1) / kBN;
   const int tps = (n_kt + S.n_splits - 1) / S.n_splits;
   const int kt_begin = split * tps;
   const int kt_end = min(n_kt, kt_begin + tps);
-  const int my_limit = S.L_keep + t;  // last key this query may see
+  const int n_valid = L_keep + T;   // cache rows holding data
 
   // Q fragments stay in registers for the whole key loop
   bf16x8 qf[NS];
@@ -116,120 +181,85 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     for (int e = 0; e < 16; ++e) o[db][e] = 0.f;
   // Online softmax in the log2 domain with a lazily moved reference max: the
   // probabilities are 2^(s*c - m_run) with m_run raised (and O, l rescaled) only
-  // when a tile's max exceeds it by more than kTau, so P stays below 2^kTau.
+  // when a unit's max exceeds it by more than kTau, so P stays below 2^kTau.
   float m_run = -__builtin_inff();
   float l_run = 0.f;
   const float c2 = a.scale_log2;
 
   const long rs = (long)Hkv * D;  // elements per cache row
   const bf16_t* kbase = S.k_cache + (long)hkv * D;
-  const bf16_t* vbase = S.v_cache + (long)hkv * D;
+  const _Float16* vtbase = S.vt + (long)hkv * S.n_vt_tiles * (D * kVRow);
 
-  // staging: K rows are copied as 16-byte vectors, V as (4 keys x 8 dims) blocks
-  constexpr int KIT = kBN * D / 8 / 256;
-  constexpr int KROWS = 256 / (D / 8);
-  constexpr int VTASK = (kBN / 4) * (D / 8);
-  constexpr int VIT = (VTASK + 255) / 256;
-  const int k_kr = threadIdx.x / (D / 8);
-  const int k_kc = threadIdx.x % (D / 8);
-  u32x4 kreg[KIT];
-  u32x4 vreg[VIT][4];
-
-  // per-thread source addresses of the first tile; later tiles add a uniform offset
-  const bf16_t* kthr = kbase + (long)k_kr * rs + k_kc * 8;
-  const bf16_t* vthr[VIT];
+  // ---- tile prefetch. A stage holds K as rows of RC + 1 chunks (16 B each; the last
+  // is padding) and V^T as D rows of 9 chunks. LDS chunk q = i * kThreads + tid is
+  // written by load i of thread tid (a wave's 64 lanes fill 64 consecutive chunks).
+  // Loads go through a buffer resource per tile whose size ends at the cache's data:
+  // lanes past it (the last tile's missing rows, the round-up tail of a stage) read
+  // zeros. Padding chunks receive a copy of their row's first chunk (never read). V^T
+  // tiles come from k_vt_pack in this exact layout and are copied chunk for chunk.
+  using GM = StageGeom<D>;
+  constexpr int KRC = GM::KRC;
+  constexpr int NLK = GM::NLK;
+  constexpr int NLV = GM::NLV;
+  // lane byte offsets of the K loads within a tile
+  uint32_t koff[NLK];
 #pragma unroll
-  for (int it = 0; it < VIT; ++it) {
-    const int c = threadIdx.x + 256 * it;
-    vthr[it] = vbase + (long)((c % (kBN / 4)) * 4) * rs + (c / (kBN / 4)) * 8;
+  for (int i = 0; i < NLK; ++i) {
+    const int q = i * kThreads + tid;
+    const int row = q / KRC;
+    const int c = q - row * KRC;
+    koff[i] = (uint32_t)(row * rs * 2 + (c < RC ? c : 0) * 16);
   }
-  auto load_tile = [&](int kt) {
+  auto load_k = [&](auto bc, int kt) __attribute__((always_inline)) {
+    constexpr int B = decltype(bc)::value;
+    bf16_t* dst = B ? g_ks1 : g_ks0;
     const int key0 = kt * kBN;
-    const long toff = (long)key0 * rs;
-    if (key0 + kBN <= n_keys) {
+    // bytes from this head's part of row key0 to the end of its part of the last data row
+    const long avail = (long)(n_valid - key0) * rs * 2 - (rs - D) * 2;
+    const int bytes = (int)min(avail, (long)2 * kBN * rs * 2);
+    const bf16_t* base = kbase + (long)key0 * rs;
 #pragma unroll
-      for (int it = 0; it < KIT; ++it) kreg[it] = *(const u32x4*)(kthr + toff + (long)(KROWS * it) * rs);
-#pragma unroll
-      for (int it = 0; it < VIT; ++it)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          vreg[it][j] = (threadIdx.x + 256 * it < VTASK) ? *(const u32x4*)(vthr[it] + toff + j * rs)
-                                                          : u32x4{0, 0, 0, 0};
-    } else {
-#pragma unroll
-      for (int it = 0; it < KIT; ++it) {
-        const int key = key0 + k_kr + KROWS * it;
-        kreg[it] = key < n_keys ? *(const u32x4*)(kthr + toff + (long)(KROWS * it) * rs) : u32x4{0, 0, 0, 0};
-      }
-#pragma unroll
-      for (int it = 0; it < VIT; ++it) {
-        const int c = threadIdx.x + 256 * it;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int key = key0 + (c % (kBN / 4)) * 4 + j;
-          vreg[it][j] = (c < VTASK && key < n_keys) ? *(const u32x4*)(vthr[it] + toff + j * rs)
-                                                     : u32x4{0, 0, 0, 0};
-        }
-      }
-    }
+    for (int i = 0; i < NLK; ++i) dma16(base, bytes, koff[i], 0, dst + (i * kThreads + wave * 64) * 8);
   };
-  auto store_tile = [&]() {
+  const uint32_t voff = (uint32_t)tid * 16;
+  auto load_v = [&](auto bc, int kt) __attribute__((always_inline)) {
+    constexpr int B = decltype(bc)::value;
+    _Float16* dst = B ? g_vt1 : g_vt0;
+    const _Float16* base = vtbase + (long)kt * (D * kVRow);
 #pragma unroll
-    for (int it = 0; it < KIT; ++it) *(u32x4*)&Ks[k_kr + KROWS * it][k_kc * 8] = kreg[it];
-#pragma unroll
-    for (int it = 0; it < VIT; ++it) {
-      const int c = threadIdx.x + 256 * it;
-      if (c < VTASK) {
-        const int kq = c % (kBN / 4);
-        const int dc = c / (kBN / 4);
-        const int slot = key_slot(kq * 4);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          f16x4 h4;
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            h4[j] = (e & 1) ? bf16_hi_to_f16(vreg[it][j][e >> 1]) : bf16_lo_to_f16(vreg[it][j][e >> 1]);
-          *(f16x4*)&Vt[dc * 8 + e][slot] = h4;
-        }
-      }
-    }
+    for (int i = 0; i < NLV; ++i) dma16(base, GM::NCV * 16, voff, i * kThreads * 16, dst + (i * kThreads + wave * 64) * 8);
   };
 
-  if (kt_begin < kt_end) load_tile(kt_begin);
-  for (int kt = kt_begin; kt < kt_end; ++kt) {
-    const int key0 = kt * kBN;
-    store_tile();
-    __syncthreads();
-    if (kt + 1 < kt_end) load_tile(kt + 1);   // in flight while this tile is computed
+  // ---- LDS fragment addresses: K row 32 * half + col, chunk 2s + hl; V^T row
+  // 32 db + col, chunk 2u + hl (16-key group u of the tile)
+  const uint32_t ka_base = (uint32_t)(col * KRC * 16 + hl * 16);
+  const uint32_t va_base = (uint32_t)(col * kVRow * 2 + hl * 16);
 
-    // ---- S^T = K Q^T for the 64 keys: two 32x32 blocks
-    f32x16 sacc[2];
+  // ---- S^T for the 32 keys of unit `half` of the tile in stage B
+  auto qk = [&](auto bc, int half, f32x16& sacc) __attribute__((always_inline)) {
+    constexpr int B = decltype(bc)::value;
+    const char* ks = (const char*)(B ? g_ks1 : g_ks0) + ka_base + half * 32 * KRC * 16;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int e = 0; e < 16; ++e) sacc[e] = 0.f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.f;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const bf16x8 ka = __builtin_bit_cast(bf16x8, *(const u32x4*)&Ks[kb * 32 + col][16 * s + 8 * hl]);
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[s], sacc[kb], 0, 0, 0);
-      }
+    for (int s = 0; s < NS; ++s) {
+      const bf16x8 ka = __builtin_bit_cast(bf16x8, *(const u32x4*)(ks + s * 32));
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[s], sacc, 0, 0, 0);
     }
-
-    // ---- causal mask (only on tiles that cross the tail diagonal) and tile max
-    if (key0 + kBN - 1 > S.L_keep + t_lo) {
+  };
+  // ---- causal mask (units crossing the tail diagonal) and lazy max update
+  auto smax = [&](int kb0, f32x16& sacc) __attribute__((always_inline)) {
+    if (kb0 + 31 > L_keep + t_lo) {
+      // element e holds key kb0 + 4 hl + 8 (e >> 2) + (e & 3); comparing its constant
+      // part against one per-unit difference keeps the offsets as immediates
+      const int room = my_limit - kb0 - 4 * hl;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = key0 + kb * 32 + 8 * (e >> 2) + 4 * hl + (e & 3);
-          if (key > my_limit) sacc[kb][e] = -__builtin_inff();
-        }
+      for (int e = 0; e < 16; ++e)
+        if (8 * (e >> 2) + (e & 3) > room) sacc[e] = -__builtin_inff();
     }
     float mx = -__builtin_inff();
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[kb][e]);
+    for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[e]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
     if (__any(mx > m_run + kTau)) {
       const float m_new = fmaxf(m_run, mx);
@@ -239,35 +269,107 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) scale_acc(o[db], alpha);
     }
+  };
+  // ---- probabilities, rounded to f16 in the key order of the P^T fragments
+  auto sexp = [&](const f32x16& sacc, f16x8 (&pf)[2]) __attribute__((always_inline)) {
     const float m_use = (m_run == -__builtin_inff()) ? 0.f : m_run;
     float psum = 0.f;
-    f16x8 pf[4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][e], c2, -m_use));
-        psum += p;
-        pf[kb * 2 + (e >> 3)][e & 7] = (_Float16)p;
-      }
+    for (int e = 0; e < 16; ++e) {
+      const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], c2, -m_use));
+      psum += p;
+      pf[e >> 3][e & 7] = (_Float16)p;
+    }
     l_run += psum;
-
-    // ---- O^T += V^T P^T over 4 steps of 16 keys
+  };
+  // ---- O^T += V^T P^T for the 32 keys of unit `half` of the tile in stage B
+  auto pv = [&](auto bc, int half, const f16x8 (&pf)[2]) __attribute__((always_inline)) {
+    constexpr int B = decltype(bc)::value;
+    const char* vt = (const char*)(B ? g_vt1 : g_vt0) + va_base;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks16 = 0; ks16 < 2; ++ks16) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const f16x8 va = __builtin_bit_cast(f16x8, *(const u32x4*)&Vt[db * 32 + col][ks * 16 + 8 * hl]);
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, pf[ks], o[db], 0, 0, 0);
+        const f16x8 va = __builtin_bit_cast(
+            f16x8, *(const u32x4*)(vt + db * 32 * kVRow * 2 + (half * 2 + ks16) * 32));
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, pf[ks16], o[db], 0, 0, 0);
       }
     }
-    __syncthreads();
+  };
+
+  // Instruction order of one phase (softmax of a unit, scores of the next, P.V of the
+  // first): LDS reads run a few fragments ahead of the MFMAs, and the softmax VALU work
+  // sits in the shadow of the score MFMAs.
+  auto phase_schedule = [&]() __attribute__((always_inline)) {
+    constexpr int kMfma = 0x008, kValu = 0x002, kDsRead = 0x100;
+    constexpr int kAhead = 6;
+    __builtin_amdgcn_sched_group_barrier(kDsRead, kAhead, 0);
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kValu, 5, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 2 * NDB - kAhead; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(kMfma, kAhead, 0);
+  };
+
+  f32x16 sa, sb;
+  f16x8 pf[2];
+  // One key tile kt in stage B. On entry sa holds the scores of the tile's first
+  // 32-key unit, on exit those of tile kt + 1's first unit. The softmax of each unit is
+  // issued together with the score MFMAs of the next, so that they share a basic block.
+  // On a split's last tile that next unit reads the idle stage and is discarded.
+  auto step = [&](auto bc, int kt) __attribute__((always_inline)) {
+    constexpr int B = decltype(bc)::value;
+    const bool more = kt + 1 < kt_end;
+    const bool more2 = kt + 2 < kt_end;
+    smax(kt * kBN, sa);
+    sexp(sa, pf);
+    qk(bc, 1, sb);
+    pv(bc, 0, pf);
+    phase_schedule();
+    if (more) __builtin_amdgcn_s_waitcnt(vm_wait(NLV));  // K of tile kt + 1 has landed
+    else __builtin_amdgcn_s_waitcnt(vm_wait(0));
+    wg_barrier();                       // every wave is done with K of stage B
+    if (more2) load_k(bc, kt + 2);
+    smax(kt * kBN + 32, sb);
+    sexp(sb, pf);
+    qk(IntC<B ^ 1>{}, 0, sa);
+    pv(bc, 1, pf);
+    phase_schedule();
+    if (more2) __builtin_amdgcn_s_waitcnt(vm_wait(NLK));  // V of tile kt + 1 has landed
+    else __builtin_amdgcn_s_waitcnt(vm_wait(0));
+    wg_barrier();                       // every wave is done with V of stage B
+    if (more2) load_v(bc, kt + 2);
+  };
+
+  if (kt_begin < kt_end) {
+    load_k(IntC<0>{}, kt_begin);
+    load_v(IntC<0>{}, kt_begin);
+    if (kt_begin + 1 < kt_end) {
+      load_k(IntC<1>{}, kt_begin + 1);
+      load_v(IntC<1>{}, kt_begin + 1);
+      __builtin_amdgcn_s_waitcnt(vm_wait(NLK + NLV));  // tile kt_begin has landed
+    } else {
+      __builtin_amdgcn_s_waitcnt(vm_wait(0));
+    }
+    wg_barrier();
+    qk(IntC<0>{}, 0, sa);
+    for (int kt = kt_begin; kt < kt_end; kt += 2) {
+      step(IntC<0>{}, kt);
+      if (kt + 1 < kt_end) step(IntC<1>{}, kt + 1);
+    }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (!row_ok) return;
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   if (S.n_splits == 1) {
-    const float inv = 1.f / l_tot;
     float* orow = S.out + ((long)t * Hq + qh) * D;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
@@ -277,60 +379,121 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         *(f32x4*)(orow + db * 32 + 8 * i + 4 * hl) = v;
       }
   } else {
-    const long prow = (long)split * S.T * Hq + (long)t * Hq + qh;
-    float* orow = S.part_o + prow * D;
+    const long prow = (long)split * T * Hq + (long)t * Hq + qh;
+    _Float16* orow = S.part_o + prow * D;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        f32x4 v = {o[db][4 * i], o[db][4 * i + 1], o[db][4 * i + 2], o[db][4 * i + 3]};
-        *(f32x4*)(orow + db * 32 + 8 * i + 4 * hl) = v;
+        f16x4 v = {(_Float16)(o[db][4 * i] * inv), (_Float16)(o[db][4 * i + 1] * inv),
+                   (_Float16)(o[db][4 * i + 2] * inv), (_Float16)(o[db][4 * i + 3] * inv)};
+        *(f16x4*)(orow + db * 32 + 8 * i + 4 * hl) = v;
       }
     if (hl == 0) {
-      S.part_ml[prow * 2] = m_run;
+      S.part_ml[prow * 2] = l_tot > 0.f ? m_run : -__builtin_inff();
       S.part_ml[prow * 2 + 1] = l_tot;
     }
   }
 }
 
-// One thread per 4 output dims of one (token, head) row.
+// One workgroup per (context, kv head, 64-key tile): V rows -> f16 V^T tile in the
+// attention kernel's LDS layout: D rows (dims) of kVtRow halves, each 64 keys in
+// key_slot order within 16-key groups followed by 8 halves of zero padding. Keys
+// past the cache's data are zero.
+template <int D>
+__global__ __launch_bounds__(256) void k_vt_pack(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t vs[kBN][D + 8];
+  const int item = blockIdx.x;
+  if (item >= a.pack_items) return;
+  int si = 0;
+  while (si + 1 < a.n_seq && a.seq[si + 1].pack_begin <= item) ++si;
+  const AttnSeq& S = a.seq[si];
+  const int local = item - S.pack_begin;
+  const int kt = local % S.n_vt_tiles;
+  const int hkv = local / S.n_vt_tiles;
+  const int n_valid = S.L_keep + S.T;
+  const int key0 = kt * kBN;
+  const long rs = (long)a.n_kv_heads * D;
+  const bf16_t* src = S.v_cache + (long)hkv * D;
+  constexpr int RC = D / 8;
+  for (int q = threadIdx.x; q < kBN * RC; q += 256) {
+    const int r = q / RC, c = q % RC;
+    const int key = key0 + r;
+    const u32x4 w = key < n_valid ? *(const u32x4*)(src + (long)key * rs + c * 8) : u32x4{0, 0, 0, 0};
+    *(u32x4*)&vs[r][c * 8] = w;
+  }
+  __syncthreads();
+  constexpr int CPR = kVtRow / 8;  // chunks per V^T row
+  _Float16* dst = S.vt + ((long)hkv * S.n_vt_tiles + kt) * (D * kVtRow);
+  for (int q = threadIdx.x; q < D * CPR; q += 256) {
+    const int d = q / CPR;
+    const int c = q - d * CPR;
+    f16x8 h;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[j] = c < kBN / 8 ? (_Float16)bf16_to_f32(vs[key_slot(8 * c + j)][d]) : (_Float16)0.f;
+    *(f16x8*)(dst + q * 8) = h;
+  }
+}
+
+// One thread per 8 output dims of one (token, head) row.
 template <int D>
 __global__ __launch_bounds__(256) void k_attn_merge(MergeArgs a) {
-  constexpr int TPR = D / 4;  // threads per row
+  constexpr int TPR = D / 8;  // threads per row
   const int g = blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
-  const int d4 = threadIdx.x % TPR;
+  const int d8 = threadIdx.x % TPR;
   if (g >= a.row_begin[a.n_seq]) return;
   int si = 0;
   while (si + 1 < a.n_seq && a.row_begin[si + 1] <= g) ++si;
-  const AttnSeq S = a.seq[si];
+  const AttnSeq& S = a.seq[si];
   const long row = g - a.row_begin[si];
   const long R = (long)S.T * a.n_q_heads;
   float M = -__builtin_inff();
   for (int s = 0; s < S.n_splits; ++s) M = fmaxf(M, S.part_ml[(s * R + row) * 2]);
   float L = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
   for (int s = 0; s < S.n_splits; ++s) {
     const float m = S.part_ml[(s * R + row) * 2];
     if (m == -__builtin_inff()) continue;
-    const float w = __builtin_amdgcn_exp2f(m - M);
-    L += w * S.part_ml[(s * R + row) * 2 + 1];
-    const f32x4 v = *(const f32x4*)(S.part_o + (s * R + row) * D + 4 * d4);
-    acc += w * v;
+    const float w = __builtin_amdgcn_exp2f(m - M) * S.part_ml[(s * R + row) * 2 + 1];
+    L += w;
+    const f16x8 v = *(const f16x8*)(S.part_o + (s * R + row) * D + 8 * d8);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc0[j] += w * (float)v[j];
+      acc1[j] += w * (float)v[4 + j];
+    }
   }
   const float inv = 1.f / L;
-  *(f32x4*)(S.out + row * D + 4 * d4) = acc * inv;
+  float* orow = S.out + row * D + 8 * d8;
+  *(f32x4*)orow = acc0 * inv;
+  *(f32x4*)(orow + 4) = acc1 * inv;
 }
 
 }  // namespace
+
+hipError_t launch_vt_pack(const AttnArgs& a, int head_dim, hipStream_t s) {
+  if (a.pack_items <= 0) return hipSuccess;
+  if (head_dim == 256)
+    hipLaunchKernelGGL(k_vt_pack<256>, dim3(a.pack_items), dim3(256), 0, s, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL(k_vt_pack<128>, dim3(a.pack_items), dim3(256), 0, s, a);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(k_vt_pack<64>, dim3(a.pack_items), dim3(256), 0, s, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s) {
   if (a.total_items <= 0) return hipSuccess;
   // round the grid up to a multiple of 8 so the XCD remap is a bijection
   const int blocks = (a.total_items + 7) & ~7;
   if (head_dim == 256)
-    hipLaunchKernelGGL(k_attn<256>, dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_attn<256>, dim3(blocks), dim3(kThreads), 0, s, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL(k_attn<128>, dim3(blocks), dim3(kThreads), 0, s, a);
   else if (head_dim == 64)
-    hipLaunchKernelGGL(k_attn<64>, dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_attn<64>, dim3(blocks), dim3(kThreads), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -338,10 +501,12 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s) {
 
 hipError_t launch_attention_merge(const MergeArgs& a, int total_rows, int head_dim, hipStream_t s) {
   if (total_rows <= 0) return hipSuccess;
-  const int rows_per_block = 256 / (head_dim / 4);
+  const int rows_per_block = 256 / (head_dim / 8);
   const int blocks = (total_rows + rows_per_block - 1) / rows_per_block;
   if (head_dim == 256)
     hipLaunchKernelGGL(k_attn_merge<256>, dim3(blocks), dim3(256), 0, s, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL(k_attn_merge<128>, dim3(blocks), dim3(256), 0, s, a);
   else if (head_dim == 64)
     hipLaunchKernelGGL(k_attn_merge<64>, dim3(blocks), dim3(256), 0, s, a);
   else

@@ -22,6 +22,9 @@ constexpr int kMaxSeqPerCompact = 8;
 constexpr int kScanRows = 4096;  // rows per keep-scan workgroup
 constexpr int kFlagStride = 32;   // compaction stripe counters sit one per 128-byte line
 constexpr int kGatherStripeBytes = 256 * 8 * 16;  // threads x vectors x 16 B
+constexpr int kAttnRows = 128;  // packed query rows per attention workgroup
+constexpr int kAttnKeys = 64;   // keys per attention K/V tile
+constexpr int kVtRow = kAttnKeys + 8;  // f16 per row of a packed V^T tile (64 keys + pad)
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
   return __uint_as_float(bits16 << 16);
@@ -59,6 +62,12 @@ __device__ __forceinline__ int xcd_remap(int b, int n_blocks) {
   const int xcd = b & 7;
   const int slot = b >> 3;
   return xcd * per + slot;
+}
+
+// Key order inside a 16-key group of a packed V^T tile: bits 2 and 3 swapped, so that
+// the 8 keys one lane feeds to a P.V product are one contiguous 16-byte chunk.
+__device__ __forceinline__ int key_slot(int k) {
+  return (k & ~0xC) | ((k & 4) << 1) | ((k & 8) >> 1);
 }
 
 // ------------------------------------------------------------------ launch records
@@ -137,25 +146,28 @@ struct AttnSeq {
   const bf16_t* q_hat;   // [T][Hq][D]
   const bf16_t* k_cache; // [cap][Hkv][D]
   const bf16_t* v_cache;
+  _Float16* vt;          // [Hkv][n_vt_tiles][D * kVtRow] packed f16 V^T tiles
   float* out;            // [T][Hq][D]
-  float* part_o;         // [splits][T*Hq][D] (unused when splits == 1)
-  float* part_ml;        // [splits][T*Hq][2]
+  _Float16* part_o;      // [splits][T*Hq][D] normalised split outputs (unused when splits == 1)
+  float* part_ml;        // [splits][T*Hq][2] (reference max in log2 units, sum)
   int32_t L_keep;
   int32_t T;
-  int32_t n_tiles;       // ceil(T*G / 128)
+  int32_t n_tiles;       // ceil(T*G / kAttnRows)
   int32_t n_splits;
-  int32_t item_begin;
+  int32_t item_begin;    // first attention workgroup of this context
+  int32_t n_vt_tiles;    // ceil((L_keep + T) / kAttnKeys)
+  int32_t pack_begin;    // first V^T packing workgroup of this context
   int32_t pad;
 };
 
 struct AttnArgs {
   AttnSeq seq[kMaxSeqPerLaunch];
   int32_t n_seq;
-  int32_t total_items;
+  int32_t total_items;   // attention workgroups
+  int32_t pack_items;    // V^T packing workgroups
   int32_t n_q_heads;
   int32_t n_kv_heads;
   float scale_log2;      // softmax_scale * log2(e)
-  int32_t pad;
 };
 
 struct MergeArgs {
@@ -200,6 +212,7 @@ struct DeltaArgs {
 int compact_max_blocks();   // co-resident workgroups of the compaction kernel
 hipError_t launch_compact(const CompactArgs& a, int n_workers, hipStream_t s);
 hipError_t launch_rope_append(const RopeArgs& a, int total_tokens, hipStream_t s);
+hipError_t launch_vt_pack(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention_merge(const MergeArgs& a, int total_rows, int head_dim, hipStream_t s);
 hipError_t launch_delta_prep(const DeltaArgs& a, int d, int chunk, hipStream_t s);
