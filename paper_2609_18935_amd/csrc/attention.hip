@@ -398,11 +398,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
 
 // One workgroup per (context, kv head, 64-key tile): V rows -> f16 V^T tile in the
 // attention kernel's LDS layout: D rows (dims) of kVtRow halves, each 64 keys in
-// key_slot order within 16-key groups followed by 8 halves of zero padding. Keys
-// past the cache's data are zero.
+// key_slot order within 16-key groups followed by 8 halves of padding (left
+// unwritten; the attention kernel never reads it). Keys past the cache's data are
+// zero. Thread (c, m) builds chunk c (8 keys) of the 8 rows 8m .. 8m + 7: it loads
+// those 8 keys' dims 8m .. 8m + 7 (16 bytes each, consecutive threads read
+// consecutive bytes of a row), transposes the 8 x 8 block in registers and writes 8
+// chunks.
 template <int D>
 __global__ __launch_bounds__(256) void k_vt_pack(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t vs[kBN][D + 8];
+  constexpr int M = D / 8;                 // 8-dim blocks per row
+  constexpr int CPR = kVtRow / 8;          // chunks per V^T row
   const int item = blockIdx.x;
   if (item >= a.pack_items) return;
   int si = 0;
@@ -415,23 +420,26 @@ __global__ __launch_bounds__(256) void k_vt_pack(AttnArgs a) {
   const int key0 = kt * kBN;
   const long rs = (long)a.n_kv_heads * D;
   const bf16_t* src = S.v_cache + (long)hkv * D;
-  constexpr int RC = D / 8;
-  for (int q = threadIdx.x; q < kBN * RC; q += 256) {
-    const int r = q / RC, c = q % RC;
-    const int key = key0 + r;
-    const u32x4 w = key < n_valid ? *(const u32x4*)(src + (long)key * rs + c * 8) : u32x4{0, 0, 0, 0};
-    *(u32x4*)&vs[r][c * 8] = w;
-  }
-  __syncthreads();
-  constexpr int CPR = kVtRow / 8;  // chunks per V^T row
   _Float16* dst = S.vt + ((long)hkv * S.n_vt_tiles + kt) * (D * kVtRow);
-  for (int q = threadIdx.x; q < D * CPR; q += 256) {
-    const int d = q / CPR;
-    const int c = q - d * CPR;
-    f16x8 h;
+  for (int w = threadIdx.x; w < 8 * M; w += 256) {
+    const int m = w % M;        // consecutive threads: consecutive dim blocks
+    const int c = w / M;        // key chunk 0..7
+    u32x4 rowv[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) h[j] = c < kBN / 8 ? (_Float16)bf16_to_f32(vs[key_slot(8 * c + j)][d]) : (_Float16)0.f;
-    *(f16x8*)(dst + q * 8) = h;
+    for (int j = 0; j < 8; ++j) {
+      const int key = key0 + key_slot(8 * c + j);
+      rowv[j] = key < n_valid ? *(const u32x4*)(src + (long)key * rs + 8 * m) : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      f16x8 h;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t word = rowv[j][d >> 1];
+        h[j] = (_Float16)bf16_to_f32((d & 1) ? (word >> 16) : (word & 0xFFFFu));
+      }
+      *(f16x8*)(dst + ((8 * m + d) * CPR + c) * 8) = h;
+    }
   }
 }
 
