@@ -219,6 +219,11 @@ typedef struct tu_update {
  * for delta layers, batched over the contexts; finally commit each context's
  * metadata (len = survivors + T, live intervals, cursor += T). A full refill is
  * the same call on empty contexts (len 0) with zero states.
+ * Delta layers read nothing the attention path writes, so they run concurrently
+ * with it on a side stream of the current device (one per calling thread, created on
+ * first use, default priority), forked after the work already queued on `stream`
+ * and joined back into `stream` before the call returns: all results are ordered on
+ * `stream`.
  * tu_validate_update performs only the host checks (no device access).
  */
 size_t update_layer_stack_workspace_size(const tu_update* u);

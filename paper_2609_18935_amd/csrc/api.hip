@@ -457,6 +457,30 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
   return TU_OK;
 }
 
+// Side stream of the current device for the calling thread (created on first use,
+// default priority, kept for the life of the thread) with the two events that fork
+// work onto it and join it back.
+struct SideStream {
+  hipStream_t stream = nullptr;
+  hipEvent_t fork = nullptr;
+  hipEvent_t join = nullptr;
+};
+
+int side_stream(SideStream** out) {
+  thread_local SideStream per_device[64];
+  int dev = 0;
+  if (int e = hip_check(hipGetDevice(&dev), "current device")) return e;
+  if (dev < 0 || dev >= 64) return fail(TU_ERR_HIP, "device index %d out of range", dev);
+  SideStream& s = per_device[dev];
+  if (!s.stream) {
+    if (int e = hip_check(hipStreamCreateWithFlags(&s.stream, hipStreamNonBlocking), "side stream")) return e;
+    if (int e = hip_check(hipEventCreateWithFlags(&s.fork, hipEventDisableTiming), "fork event")) return e;
+    if (int e = hip_check(hipEventCreateWithFlags(&s.join, hipEventDisableTiming), "join event")) return e;
+  }
+  *out = &s;
+  return TU_OK;
+}
+
 int run_attention(const std::vector<AttnLaunch>& ls, int D, hipStream_t st) {
   for (const auto& L : ls) {
     if (int e = hip_check(timed("rope_append", st, [&] { return launch_rope_append(L.rope, L.rope_tokens, st); }), "rope-append launch")) return e;
@@ -854,15 +878,23 @@ int delta_rule_continue(float* state, const void* q, const void* k, const void* 
   return ok();
 }
 
-size_t update_layer_stack_workspace_size(const tu_update* u) {
-  StackPlan sp;
-  if (validate_stack(u, &sp)) return 0;
-  size_t need = kAlign;
+// Workspace of a stack update: [compaction / attention region | delta region]. Delta
+// layers run on a second stream concurrently with the attention path, so the two
+// regions are disjoint; layers of one kind run in order and reuse their region.
+struct StackWorkspace {
+  size_t attn = 0;    // compaction and attention layers
+  size_t delta = 0;   // delta layers
+  size_t total() const { return align_up(attn) + align_up(delta); }
+};
+
+StackWorkspace stack_workspace(const tu_update* u, const StackPlan& sp) {
+  StackWorkspace w;
+  w.attn = kAlign;
   if (sp.n_attn) {
     auto items = stack_compact_items(u, sp);
     CompactPlan cp;
     plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, nullptr, &cp);
-    need = std::max(need, cp.ws_bytes);
+    w.attn = std::max(w.attn, cp.ws_bytes);
   }
   for (int l = 0; l < u->n_layers; ++l) {
     size_t b = 0;
@@ -870,14 +902,21 @@ size_t update_layer_stack_workspace_size(const tu_update* u) {
       auto items = stack_attn_items(u, sp, u->layers[l]);
       std::vector<AttnLaunch> ls;
       plan_attention(&u->attn, items, nullptr, &ls, &b);
+      w.attn = std::max(w.attn, b);
     } else {
       auto items = stack_delta_items(u, sp, u->layers[l]);
       std::vector<DeltaArgs> ls;
       plan_delta(&u->delta, items, nullptr, &ls, &b);
+      w.delta = std::max(w.delta, b);
     }
-    need = std::max(need, b);
   }
-  return need;
+  return w;
+}
+
+size_t update_layer_stack_workspace_size(const tu_update* u) {
+  StackPlan sp;
+  if (validate_stack(u, &sp)) return 0;
+  return stack_workspace(u, sp).total();
 }
 
 int tu_profile_enable(int on) {
@@ -929,33 +968,57 @@ int tu_validate_update(const tu_update* u) {
 int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_bytes, void* stream) {
   StackPlan sp;
   if (int e = validate_stack(u, &sp)) return e;
-  const size_t need = update_layer_stack_workspace_size(u);
+  const StackWorkspace ws = stack_workspace(u, sp);
+  const size_t need = ws.total();
   if (!workspace || workspace_bytes < need)
     return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
   if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
   hipStream_t st = static_cast<hipStream_t>(stream);
+  void* ws_attn = workspace;
+  void* ws_delta = static_cast<char*>(workspace) + align_up(ws.attn);
+
+  // Delta layers depend on nothing the attention path writes (the layers' inputs are
+  // given), so they run on a side stream of this device, forked after the work
+  // already queued on `st` and joined back before returning: every result is then
+  // ordered on `st` as if the layers had run in sequence.
+  int n_delta = 0;
+  for (int l = 0; l < u->n_layers; ++l) n_delta += u->layers[l].kind == TU_LAYER_DELTA;
+  SideStream* side = nullptr;
+  if (n_delta > 0 && (sp.n_attn > 0 || n_delta < u->n_layers)) {
+    if (int e = side_stream(&side)) return e;
+    if (int e = hip_check(hipEventRecord(side->fork, st), "fork event")) return e;
+    if (int e = hip_check(hipStreamWaitEvent(side->stream, side->fork, 0), "side stream wait")) return e;
+  }
+  hipStream_t sd = side ? side->stream : st;
+  for (int l = 0; l < u->n_layers; ++l) {
+    const tu_layer_io& L = u->layers[l];
+    if (L.kind != TU_LAYER_DELTA) continue;
+    size_t b = 0;
+    auto items = stack_delta_items(u, sp, L);
+    std::vector<DeltaArgs> ls;
+    plan_delta(&u->delta, items, ws_delta, &ls, &b);
+    if (int e = run_delta(ls, &u->delta, sd)) return e;
+  }
   // a2-a3: keep-scan and in-place row move over every attention layer of every context
   if (sp.n_attn) {
     auto items = stack_compact_items(u, sp);
     CompactPlan cp;
-    if (int e = plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, workspace, &cp)) return e;
+    if (int e = plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, ws_attn, &cp)) return e;
     if (int e = run_compaction(cp, st)) return e;
   }
-  // a4-a7 in layer order
+  // a4-a5 in layer order
   for (int l = 0; l < u->n_layers; ++l) {
     const tu_layer_io& L = u->layers[l];
+    if (L.kind != TU_LAYER_ATTN) continue;
     size_t b = 0;
-    if (L.kind == TU_LAYER_ATTN) {
-      auto items = stack_attn_items(u, sp, L);
-      std::vector<AttnLaunch> ls;
-      plan_attention(&u->attn, items, workspace, &ls, &b);
-      if (int e = run_attention(ls, u->attn.head_dim, st)) return e;
-    } else {
-      auto items = stack_delta_items(u, sp, L);
-      std::vector<DeltaArgs> ls;
-      plan_delta(&u->delta, items, workspace, &ls, &b);
-      if (int e = run_delta(ls, &u->delta, st)) return e;
-    }
+    auto items = stack_attn_items(u, sp, L);
+    std::vector<AttnLaunch> ls;
+    plan_attention(&u->attn, items, ws_attn, &ls, &b);
+    if (int e = run_attention(ls, u->attn.head_dim, st)) return e;
+  }
+  if (side) {
+    if (int e = hip_check(hipEventRecord(side->join, side->stream), "join event")) return e;
+    if (int e = hip_check(hipStreamWaitEvent(st, side->join, 0), "join wait")) return e;
   }
   // a8: commit metadata
   for (int s = 0; s < u->n_seq; ++s) {
