@@ -17,6 +17,7 @@ second pass over the same steps) and the CPU oracle timed on this host.
     python bench.py [--config 1] [--steps 20] [--warmup 3] [--gpus 1]
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -235,6 +236,28 @@ def cpu_baseline(cfg, seed, budget_s):
 
 # ----------------------------------------------------------------------------- main
 
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE and
+    WRITE_SIZE passes (profiles/traffic_config*.json), or None when there is no record
+    for this workload or the kernel's sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic_config1.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel") != kernel or rec.get("workload") != workload:
+        return None
+    h = hashlib.sha256()
+    for src in rec["sources"]:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec["sources_sha256"]:
+        return None
+    return {"bytes_per_launch": rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"],
+            "read": rec["fetch_bytes_per_launch"], "written": rec["write_bytes_per_launch"],
+            "source": rec["summary"]}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -320,6 +343,12 @@ def main():
     else:
         roofline = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
                     "kernel": dom}
+    # HBM bytes per launch of the dominant kernel, from the committed counter passes
+    traffic = measured_traffic(dom, f"config {cfg.index}: {cfg.name}")
+    if traffic is not None:
+        roofline["traffic"] = traffic["bytes_per_launch"]
+        roofline["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
+        roofline["traffic_detail"] = traffic
 
     # ---- full refill of the same final context through the same kernels
     refill = None
