@@ -510,13 +510,13 @@ int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, vo
   const int C = p->chunk, Hv = p->n_v_heads, DK = p->d_k;
   size_t max_used = 0;
   out->clear();
-  int n_active = 0;
-  for (const auto& it : items) n_active += it.T > 0;
-  // slice d_v so that the chain has enough workgroups
-  const int wg64 = n_active * Hv * (DK / 64);
-  const int dvs = (wg64 >= 256) ? 64 : 32;
   for (size_t g0 = 0; g0 < items.size(); g0 += kMaxSeqPerLaunch) {
     const size_t g1 = std::min(items.size(), g0 + kMaxSeqPerLaunch);
+    int n_active = 0;
+    for (size_t i = g0; i < g1; ++i) n_active += items[i].T > 0;
+    // slice d_v so that the chain has enough workgroups
+    const int wg64 = n_active * Hv * (DK / 64);
+    const int dvs = (wg64 >= 256) ? 64 : 32;
     DeltaArgs a{};
     a.n_k_heads = p->n_k_heads;
     a.n_v_heads = Hv;
@@ -690,8 +690,8 @@ std::vector<AttnItem> stack_attn_items(const tu_update* u, const StackPlan& sp, 
   return items;
 }
 
-std::vector<DeltaItem> stack_delta_items(const tu_update* u, const StackPlan& sp, const tu_layer_io& L) {
-  std::vector<DeltaItem> items;
+void append_delta_items(const tu_update* u, const StackPlan& sp, const tu_layer_io& L,
+                        std::vector<DeltaItem>* items) {
   const int64_t krow = (int64_t)u->delta.n_k_heads * u->delta.d_k;
   const int64_t vrow = (int64_t)u->delta.n_v_heads * u->delta.d_v;
   for (int s = 0; s < u->n_seq; ++s) {
@@ -705,7 +705,19 @@ std::vector<DeltaItem> stack_delta_items(const tu_update* u, const StackPlan& sp
     it.g = L.g + r0 * u->delta.n_v_heads;
     it.out = L.out + r0 * vrow;
     it.T = u->seqs[s].T;
-    items.push_back(it);
+    items->push_back(it);
+  }
+}
+
+// Items of every delta layer of the stack, layer by layer and context by context.
+// Each (layer, context) pair owns its state and its inputs, so all of them are
+// independent and share launches (up to kMaxSeqPerLaunch items each).
+std::vector<DeltaItem> stack_delta_items(const tu_update* u, const StackPlan& sp) {
+  std::vector<DeltaItem> items;
+  for (int l = 0; l < u->n_layers; ++l) {
+    const tu_layer_io& L = u->layers[l];
+    if (L.kind != TU_LAYER_DELTA) continue;
+    append_delta_items(u, sp, L, &items);
   }
   return items;
 }
@@ -880,7 +892,9 @@ int delta_rule_continue(float* state, const void* q, const void* k, const void* 
 
 // Workspace of a stack update: [compaction / attention region | delta region]. Delta
 // layers run on a second stream concurrently with the attention path, so the two
-// regions are disjoint; layers of one kind run in order and reuse their region.
+// regions are disjoint. Attention layers run in order and reuse their region; the
+// (layer, context) items of all delta layers are planned together into launches of
+// up to kMaxSeqPerLaunch items, which run in order and reuse the delta region.
 struct StackWorkspace {
   size_t attn = 0;    // compaction and attention layers
   size_t delta = 0;   // delta layers
@@ -903,12 +917,12 @@ StackWorkspace stack_workspace(const tu_update* u, const StackPlan& sp) {
       std::vector<AttnLaunch> ls;
       plan_attention(&u->attn, items, nullptr, &ls, &b);
       w.attn = std::max(w.attn, b);
-    } else {
-      auto items = stack_delta_items(u, sp, u->layers[l]);
-      std::vector<DeltaArgs> ls;
-      plan_delta(&u->delta, items, nullptr, &ls, &b);
-      w.delta = std::max(w.delta, b);
     }
+  }
+  auto items = stack_delta_items(u, sp);
+  if (!items.empty()) {
+    std::vector<DeltaArgs> ls;
+    plan_delta(&u->delta, items, nullptr, &ls, &w.delta);
   }
   return w;
 }
@@ -990,11 +1004,9 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
     if (int e = hip_check(hipStreamWaitEvent(side->stream, side->fork, 0), "side stream wait")) return e;
   }
   hipStream_t sd = side ? side->stream : st;
-  for (int l = 0; l < u->n_layers; ++l) {
-    const tu_layer_io& L = u->layers[l];
-    if (L.kind != TU_LAYER_DELTA) continue;
+  if (n_delta > 0) {
     size_t b = 0;
-    auto items = stack_delta_items(u, sp, L);
+    auto items = stack_delta_items(u, sp);
     std::vector<DeltaArgs> ls;
     plan_delta(&u->delta, items, ws_delta, &ls, &b);
     if (int e = run_delta(ls, &u->delta, sd)) return e;
