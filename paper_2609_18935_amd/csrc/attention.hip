@@ -20,11 +20,15 @@
 //
 // Tiles move HBM/L2 -> LDS with buffer_load_dwordx4 ... lds (no staging registers;
 // the buffer resource of a tile ends at the cache's data, so rows past it read as
-// zeros), double-buffered: the K half of tile k+2 is requested once every wave has formed
-// the scores of tile k, and the V half once every wave has used V of tile k. With one
-// wave per SIMD nothing else hides latency, so the loop is software-pipelined: the
-// softmax of one unit is issued together with the score MFMAs of the next (VALU work
-// in the shadow of the matrix core) and LDS fragment reads run several MFMAs ahead.
+// zeros), double-buffered: K of tile k+2 is requested once every wave has formed the
+// scores of tile k, V of tile k+1 once every wave has used V of tile k-1. With one wave
+// per SIMD nothing else hides latency, so every phase (softmax of one 32-key unit,
+// scores of the next, P.V of the first) keeps the matrix core fed: half of the next
+// unit's score MFMAs are issued around the max reduction, the uniform branch that
+// rarely moves the reference max follows, and the other half runs with the
+// exponentials, followed by P.V with the tile loads interleaved. Loads are issued on
+// every tile (zero bytes past the split's end), so the wait counts never change, and
+// the lane-pair exchanges use v_permlane32_swap instead of an LDS round trip.
 //
 // For occupancy the key range is split over `n_splits` workgroups; each writes a
 // normalised f16 partial (O / l) with its reference max and sum, and k_attn_merge
@@ -131,10 +135,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   while (si + 1 < a.n_seq && a.seq[si + 1].item_begin <= item) ++si;
   const AttnSeq& S = a.seq[si];
   int local = item - S.item_begin;
-  const int tile = local % S.n_tiles;
+  const int tile = __builtin_amdgcn_readfirstlane(local % S.n_tiles);
   local /= S.n_tiles;
-  const int split = local % S.n_splits;
-  const int hkv = local / S.n_splits;
+  const int split = __builtin_amdgcn_readfirstlane(local % S.n_splits);
+  const int hkv = __builtin_amdgcn_readfirstlane(local / S.n_splits);
 
   const int Hq = a.n_q_heads;
   const int Hkv = a.n_kv_heads;
@@ -155,12 +159,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   const int my_limit = L_keep + t;  // last key this query may see
   const int r_last = min(rows_total, (tile + 1) * kBM) - 1;
   const int t_hi = r_last / G;
-  const int t_lo = (tile * kBM) / G;
+  const int t_lo = __builtin_amdgcn_readfirstlane((tile * kBM) / G);
   const int n_keys = L_keep + t_hi + 1;
   const int n_kt = (n_keys + kBN - 1) / kBN;
   const int tps = (n_kt + S.n_splits - 1) / S.n_splits;
-  const int kt_begin = split * tps;
-  const int kt_end = min(n_kt, kt_begin + tps);
+  const int kt_begin = __builtin_amdgcn_readfirstlane(split * tps);
+  const int kt_end = __builtin_amdgcn_readfirstlane(min(n_kt, kt_begin + tps));
   const int n_valid = L_keep + T;   // cache rows holding data
 
   // Q fragments stay in registers for the whole key loop
@@ -214,9 +218,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     constexpr int B = decltype(bc)::value;
     bf16_t* dst = B ? g_ks1 : g_ks0;
     const int key0 = kt * kBN;
-    // bytes from this head's part of row key0 to the end of its part of the last data row
-    const long avail = (long)(n_valid - key0) * rs * 2 - (rs - D) * 2;
-    const int bytes = (int)min(avail, (long)2 * kBN * rs * 2);
+    // bytes from this head's part of row key0 to the end of its part of the last data
+    // row (zero past the split's last tile)
+    const int rows = min(n_valid - key0, 2 * kBN);
+    const int bytes = max(rows * (int)rs * 2 - ((int)rs - D) * 2, 0) * (int)(kt < kt_end);
     const bf16_t* base = kbase + (long)key0 * rs;
 #pragma unroll
     for (int i = 0; i < NLK; ++i) dma16(base, bytes, koff[i], 0, dst + (i * kThreads + wave * 64) * 8);
@@ -226,8 +231,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     constexpr int B = decltype(bc)::value;
     _Float16* dst = B ? g_vt1 : g_vt0;
     const _Float16* base = vtbase + (long)kt * (D * kVRow);
+    const int bytes = kt < kt_end ? GM::NCV * 16 : 0;
 #pragma unroll
-    for (int i = 0; i < NLV; ++i) dma16(base, GM::NCV * 16, voff, i * kThreads * 16, dst + (i * kThreads + wave * 64) * 8);
+    for (int i = 0; i < NLV; ++i) dma16(base, bytes, voff, i * kThreads * 16, dst + (i * kThreads + wave * 64) * 8);
   };
 
   // ---- LDS fragment addresses: K row 32 * half + col, chunk 2s + hl; V^T row
@@ -235,20 +241,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   const uint32_t ka_base = (uint32_t)(col * KRC * 16 + hl * 16);
   const uint32_t va_base = (uint32_t)(col * kVRow * 2 + hl * 16);
 
-  // ---- S^T for the 32 keys of unit `half` of the tile in stage B
-  auto qk = [&](auto bc, int half, f32x16& sacc) __attribute__((always_inline)) {
+  // ---- S^T for the 32 keys of unit `half` of the tile in stage B, dim steps [S0, S1)
+  auto qk_part = [&](auto bc, int half, f32x16& sacc, auto s0c, auto s1c) __attribute__((always_inline)) {
     constexpr int B = decltype(bc)::value;
+    constexpr int S0 = decltype(s0c)::value, S1 = decltype(s1c)::value;
     const char* ks = (const char*)(B ? g_ks1 : g_ks0) + ka_base + half * 32 * KRC * 16;
+    if constexpr (S0 == 0) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) sacc[e] = 0.f;
+      for (int e = 0; e < 16; ++e) sacc[e] = 0.f;
+    }
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
+    for (int s = S0; s < S1; ++s) {
       const bf16x8 ka = __builtin_bit_cast(bf16x8, *(const u32x4*)(ks + s * 32));
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[s], sacc, 0, 0, 0);
     }
   };
-  // ---- causal mask (units crossing the tail diagonal) and lazy max update
-  auto smax = [&](int kb0, f32x16& sacc) __attribute__((always_inline)) {
+  // ---- causal mask of a unit crossing the tail diagonal (a uniform branch)
+  auto mask = [&](int kb0, f32x16& sacc) __attribute__((always_inline)) {
     if (kb0 + 31 > L_keep + t_lo) {
       // element e holds key kb0 + 4 hl + 8 (e >> 2) + (e & 3); comparing its constant
       // part against one per-unit difference keeps the offsets as immediates
@@ -257,10 +266,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
       for (int e = 0; e < 16; ++e)
         if (8 * (e >> 2) + (e & 3) > room) sacc[e] = -__builtin_inff();
     }
+  };
+  // ---- the unit's max over the query's 32 keys (lanes l and l ^ 32 hold 16 each)
+  auto rowmax = [&](const f32x16& sacc) __attribute__((always_inline)) -> float {
     float mx = -__builtin_inff();
 #pragma unroll
     for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[e]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+    const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, mx),
+                                                     __builtin_bit_cast(uint32_t, mx), false, false);
+    return fmaxf(__builtin_bit_cast(float, (uint32_t)sw[0]), __builtin_bit_cast(float, (uint32_t)sw[1])) * c2;
+  };
+  // ---- lazy move of the reference max (rare: O and l rescaled)
+  auto rescale_if = [&](float mx) __attribute__((always_inline)) {
     if (__any(mx > m_run + kTau)) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = (m_new == -__builtin_inff()) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
@@ -273,14 +290,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   // ---- probabilities, rounded to f16 in the key order of the P^T fragments
   auto sexp = [&](const f32x16& sacc, f16x8 (&pf)[2]) __attribute__((always_inline)) {
     const float m_use = (m_run == -__builtin_inff()) ? 0.f : m_run;
-    float psum = 0.f;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], c2, -m_use));
-      psum += p;
+      ps[e & 3] += p;
       pf[e >> 3][e & 7] = (_Float16)p;
     }
-    l_run += psum;
+    l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
   };
   // ---- O^T += V^T P^T for the 32 keys of unit `half` of the tile in stage B
   auto pv = [&](auto bc, int half, const f16x8 (&pf)[2]) __attribute__((always_inline)) {
@@ -297,76 +314,89 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     }
   };
 
-  // Instruction order of one phase (softmax of a unit, scores of the next, P.V of the
-  // first): LDS reads run a few fragments ahead of the MFMAs, and the softmax VALU work
-  // sits in the shadow of the score MFMAs.
-  auto phase_schedule = [&]() __attribute__((always_inline)) {
-    constexpr int kMfma = 0x008, kValu = 0x002, kDsRead = 0x100;
-    constexpr int kAhead = 6;
+  constexpr int kMfma = 0x008, kValu = 0x002, kVmemRd = 0x020, kDsRead = 0x100;
+  // first part of a phase: half the score MFMAs of the next unit with the max reduction
+  auto sched_head = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
+#pragma unroll
+    for (int i = 0; i < NS / 2; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+      if (i < NS / 2 - 4) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kValu, 4, 0);
+    }
+  };
+  // second part: the other score MFMAs and P.V with the exponentials and the tile loads
+  auto sched_tail = [&](int nload) __attribute__((always_inline)) {
+    constexpr int kAhead = 4;
     __builtin_amdgcn_sched_group_barrier(kDsRead, kAhead, 0);
 #pragma unroll
-    for (int i = 0; i < NS; ++i) {
+    for (int i = 0; i < NS / 2; ++i) {
       __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
       __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
       __builtin_amdgcn_sched_group_barrier(kValu, 5, 0);
     }
 #pragma unroll
-    for (int i = 0; i < 2 * NDB - kAhead; ++i) {
+    for (int i = 0; i < 2 * NDB; ++i) {
       __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+      if (i < 2 * NDB - kAhead) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+      if (i < nload) __builtin_amdgcn_sched_group_barrier(kVmemRd, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kValu, 2, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(kMfma, kAhead, 0);
   };
 
   f32x16 sa, sb;
   f16x8 pf[2];
   // One key tile kt in stage B. On entry sa holds the scores of the tile's first
-  // 32-key unit, on exit those of tile kt + 1's first unit. The softmax of each unit is
-  // issued together with the score MFMAs of the next, so that they share a basic block.
-  // On a split's last tile that next unit reads the idle stage and is discarded.
+  // 32-key unit, on exit those of tile kt + 1's first unit. Tile loads are issued
+  // unconditionally (past the split's last tile they have zero bytes and only write
+  // zeros to a stage that is no longer read), so the wait counts are the same on every
+  // tile. On a split's last tile the scores of the next unit read the idle stage and
+  // are discarded.
   auto step = [&](auto bc, int kt) __attribute__((always_inline)) {
     constexpr int B = decltype(bc)::value;
-    const bool more = kt + 1 < kt_end;
-    const bool more2 = kt + 2 < kt_end;
-    smax(kt * kBN, sa);
+    mask(kt * kBN, sa);
+    qk_part(bc, 1, sb, IntC<0>{}, IntC<NS / 2>{});
+    float mx = rowmax(sa);
+    sched_head();
+    rescale_if(mx);
+    qk_part(bc, 1, sb, IntC<NS / 2>{}, IntC<NS>{});
     sexp(sa, pf);
-    qk(bc, 1, sb);
     pv(bc, 0, pf);
-    phase_schedule();
-    if (more) __builtin_amdgcn_s_waitcnt(vm_wait(NLV));  // K of tile kt + 1 has landed
-    else __builtin_amdgcn_s_waitcnt(vm_wait(0));
-    wg_barrier();                       // every wave is done with K of stage B
-    if (more2) load_k(bc, kt + 2);
-    smax(kt * kBN + 32, sb);
+    load_v(IntC<B ^ 1>{}, kt + 1);
+    sched_tail(NLV);
+    __builtin_amdgcn_s_waitcnt(vm_wait(NLV));  // K of tile kt + 1 has landed
+    wg_barrier();                               // every wave is done with K of stage B
+    mask(kt * kBN + 32, sb);
+    qk_part(IntC<B ^ 1>{}, 0, sa, IntC<0>{}, IntC<NS / 2>{});
+    mx = rowmax(sb);
+    sched_head();
+    rescale_if(mx);
+    qk_part(IntC<B ^ 1>{}, 0, sa, IntC<NS / 2>{}, IntC<NS>{});
     sexp(sb, pf);
-    qk(IntC<B ^ 1>{}, 0, sa);
     pv(bc, 1, pf);
-    phase_schedule();
-    if (more2) __builtin_amdgcn_s_waitcnt(vm_wait(NLK));  // V of tile kt + 1 has landed
-    else __builtin_amdgcn_s_waitcnt(vm_wait(0));
-    wg_barrier();                       // every wave is done with V of stage B
-    if (more2) load_v(bc, kt + 2);
+    load_k(bc, kt + 2);
+    sched_tail(NLK);
+    __builtin_amdgcn_s_waitcnt(vm_wait(NLK));  // V of tile kt + 1 has landed
+    wg_barrier();                               // every wave is done with V of stage B
   };
 
   if (kt_begin < kt_end) {
     load_k(IntC<0>{}, kt_begin);
     load_v(IntC<0>{}, kt_begin);
-    if (kt_begin + 1 < kt_end) {
-      load_k(IntC<1>{}, kt_begin + 1);
-      load_v(IntC<1>{}, kt_begin + 1);
-      __builtin_amdgcn_s_waitcnt(vm_wait(NLK + NLV));  // tile kt_begin has landed
-    } else {
-      __builtin_amdgcn_s_waitcnt(vm_wait(0));
-    }
+    load_k(IntC<1>{}, kt_begin + 1);
+    __builtin_amdgcn_s_waitcnt(vm_wait(NLK));  // tile kt_begin has landed
     wg_barrier();
-    qk(IntC<0>{}, 0, sa);
+    qk_part(IntC<0>{}, 0, sa, IntC<0>{}, IntC<NS>{});
     for (int kt = kt_begin; kt < kt_end; kt += 2) {
       step(IntC<0>{}, kt);
       if (kt + 1 < kt_end) step(IntC<1>{}, kt + 1);
     }
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));  // no tile write may outlive the workgroup
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const auto lsw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, l_run),
+                                                    __builtin_bit_cast(uint32_t, l_run), false, false);
+  const float l_tot = __builtin_bit_cast(float, (uint32_t)lsw[0]) + __builtin_bit_cast(float, (uint32_t)lsw[1]);
   if (!row_ok) return;
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   if (S.n_splits == 1) {

@@ -133,6 +133,21 @@ def test_attention_shapes(L_keep, T, splits):
     assert_close(case.out.cpu().numpy(), ref["out"], f"L_keep={L_keep} T={T} splits={splits}")
 
 
+@pytest.mark.parametrize("Hq,Hkv,D,rdim,L_keep,T,splits", [(8, 2, 128, 128, 700, 45, 0), (4, 4, 128, 64, 300, 130, 2),
+                                                        (16, 2, 64, 64, 1500, 33, 0), (6, 2, 256, 192, 900, 70, 3)])
+def test_attention_head_dims(Hq, Hkv, D, rdim, L_keep, T, splits):
+    # every compiled head size, group sizes 1..8 and a partial rotary dimension
+    s = synth.AttnShape(n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D, rotary_dim=rdim)
+    _say(f"attention Hq={Hq} Hkv={Hkv} D={D} rdim={rdim} L_keep={L_keep} T={T} splits={splits}")
+    case = AttnCase(s, 5, 1, 0, L_keep, T)
+    ctx = _ctx_for(case)
+    p = tu.attn_params(Hq, Hkv, D, rdim, s.rope_theta, s.softmax_scale, kv_splits=splits)
+    _attn_update(case, ctx, np.zeros((0, 2), np.int64), p)
+    ref = case.oracle(np.zeros((0, 2), np.int64), L_keep)
+    assert_bf16_close_bits(bits_of(case.q_hat), ref["q_hat"], f"D={D} rotated q")
+    assert_close(case.out.cpu().numpy(), ref["out"], f"Hq={Hq} Hkv={Hkv} D={D} rdim={rdim}")
+
+
 def test_attention_splits_agree():
     s = synth.CONFIGS[1].attn
     _say("attention split counts 1 vs 4 vs auto on cfg1 shapes")
