@@ -203,7 +203,6 @@ struct CompactItem {
 
 struct CompactPlan {
   std::vector<CompactArgs> launches;
-  std::vector<int> workers;
   size_t ws_bytes = 0;
 };
 
@@ -256,7 +255,6 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
     flush();
   }
   plan->launches.clear();
-  plan->workers.clear();
   const int max_blocks = ws ? compact_max_blocks() : 0;
   for (auto& g : groups) {
     CompactArgs a{};
@@ -307,7 +305,7 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
         m.n_stripes = (int32_t)((n_keep - rb + R - 1) / R);
         m.item_begin = items_total;
         m.buf_begin = nbufs;
-        m.n_buf = e.nbuf + (with_pos ? 1 : 0);
+        m.n_buf = e.nbuf;
         m.flag_begin = flag_off;
         m.window = (int32_t)((it.rc.removed + R - 1 + R - 1) / R);
         m.span_begin = spans_of(it, e.item);
@@ -319,11 +317,17 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
     }
     a.total_items = items_total;
     a.n_flag_words = flag_off * kFlagStride;
-    int32_t* words = static_cast<int32_t*>(ar.take(sizeof(int32_t) * (1 + (size_t)a.n_flag_words)));
-    a.err = words;
-    a.flags = words ? words + 1 : nullptr;
+    // gather workgroups claim items in order, so any count works; one grid's worth of
+    // resident workgroups suffices (the sizing pass, without a device, takes the cap)
+    a.n_workers = std::min({items_total, kMaxGatherWorkers, ws ? std::max(1, max_blocks) : kMaxGatherWorkers});
+    // [claim counter | stripe counters | status words]; counters one 128-byte line apart
+    a.n_counter_words = kFlagStride + a.n_flag_words;
+    int32_t* words = static_cast<int32_t*>(
+        ar.take(sizeof(int32_t) * ((size_t)a.n_counter_words + a.n_scan_blocks + a.n_workers)));
+    a.claim = words;
+    a.flags = words ? words + kFlagStride : nullptr;
+    a.status = words ? words + a.n_counter_words : nullptr;
     plan->launches.push_back(a);
-    plan->workers.push_back(std::max(0, std::min(items_total, max_blocks - a.n_scan_blocks)));
   }
   plan->ws_bytes = ar.used;
   if (ws && max_blocks <= 8) return fail(TU_ERR_HIP, "cannot size the compaction grid");
@@ -332,7 +336,7 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
 
 int run_compaction(const CompactPlan& plan, hipStream_t st) {
   for (size_t i = 0; i < plan.launches.size(); ++i)
-    if (int e = hip_check(timed("compact", st, [&] { return launch_compact(plan.launches[i], plan.workers[i], st); }),
+    if (int e = hip_check(timed("compact", st, [&] { return launch_compact(plan.launches[i], st); }),
                           "compaction launch"))
       return e;
   return TU_OK;

@@ -19,7 +19,7 @@ constexpr int kMaxSeqPerLaunch = 16;
 constexpr int kMaxRangesPerLaunch = 128;
 constexpr int kMaxBufPerLaunch = 32;
 constexpr int kMaxSeqPerCompact = 8;
-constexpr int kScanRows = 4096;  // rows per keep-scan workgroup
+constexpr int kScanRows = 1024;  // rows per keep-scan workgroup (a multiple of 256, at most 16K)
 constexpr int kFlagStride = 32;   // compaction stripe counters sit one per 128-byte line
 constexpr int kGatherStripeBytes = 256 * 8 * 16;  // threads x vectors x 16 B
 constexpr int kAttnRows = 128;  // packed query rows per attention workgroup
@@ -90,7 +90,7 @@ struct GatherSeq {
   int32_t n_stripes;
   int32_t item_begin;   // first item of this context
   int32_t buf_begin;    // index of its first buffer in CompactArgs::bufs
-  int32_t n_buf;        // items per stripe (K/V buffers, plus one for positions when pos != null)
+  int32_t n_buf;        // items per stripe: one per K/V buffer (the first also moves positions)
   int32_t flag_begin;   // its stripe read-counters
   int32_t window;       // stripes before s whose sources may reach stripe s's rows
   int32_t span_begin;   // index into CompactArgs::spans
@@ -112,8 +112,11 @@ struct CompactArgs {
   int32_t rows_per_stripe;
   int32_t row_bytes;
   int32_t n_flag_words;   // stripe counters x kFlagStride
+  int32_t n_counter_words; // kFlagStride + n_flag_words: cleared by the scan launch
+  int32_t n_workers;       // gather workgroups
+  int32_t* claim;   // next unclaimed gather item (its own 128-byte line), then the flags
   int32_t* flags;   // [n_flag_words] stripe read counters, kFlagStride apart
-  int32_t* err;     // flags - 1: set when a bounded wait expired
+  int32_t* status;  // [n_scan_blocks + n_workers]: 0 ok, 2 scan mismatch, 1 wait expired
 };
 
 struct RopeSeq {
@@ -209,8 +212,9 @@ struct DeltaArgs {
 
 // ------------------------------------------------------------------ launchers
 // (defined in the kernel translation units; return a hipError_t)
-int compact_max_blocks();   // co-resident workgroups of the compaction kernel
-hipError_t launch_compact(const CompactArgs& a, int n_workers, hipStream_t s);
+int compact_max_blocks();   // resident workgroups of the gather kernel over the device
+constexpr int kMaxGatherWorkers = 2048;
+hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 hipError_t launch_rope_append(const RopeArgs& a, int total_tokens, hipStream_t s);
 hipError_t launch_vt_pack(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
