@@ -317,7 +317,7 @@ def main():
     kinds = cfg.layer_kinds()
     # algorithmic work per step of each stage, and the kernels that carry it
     work = {
-        "attention": (["vt_pack", "attention", "attention_merge"], "mfma",
+        "attention": (["rope_vt_pack", "attention", "attention_merge"], "mfma",
                       attention_flops(cfg, chars) * kinds.count("attn") / 1e12, "TFLOP/s", MFMA16_PEAK_TFLOPS),
         "delta": (["delta_prep", "delta_chain"], "hbm", delta_bytes(cfg, chars) * kinds.count("delta") / 1e9, "GB/s",
                   HBM_PEAK_GBS),

@@ -237,8 +237,10 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
  * events, then reports per kernel name (NUL-terminated, `name_stride` bytes per
  * entry in `names`) the launch count and the summed duration in milliseconds,
  * for at most `max_entries` kernels; it returns the number of entries written
- * (or a negative status) and clears the records. Kernel names: compact,
- * rope_append, vt_pack, attention, attention_merge, delta_prep, delta_chain.
+ * (or a negative status) and clears the records. Names (one per launch or pair
+ * of launches): compact (keep-scan, then gather), rope_vt_pack (RoPE + append of
+ * the tail with the V^T packing of the key tiles), attention, attention_merge,
+ * delta_prep, delta_chain.
  */
 int tu_profile_enable(int on);
 int tu_profile_collect(char* names, int32_t name_stride, int32_t* counts, double* total_ms, int32_t max_entries);

@@ -430,6 +430,7 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
       s.q_hat = qh;
       s.k_cache = static_cast<const bf16_t*>(it.k_cache);
       s.v_cache = static_cast<const bf16_t*>(it.v_cache);
+      s.v_new = it.v;
       s.vt = vt;
       s.out = it.out;
       s.part_o = po;
@@ -487,8 +488,7 @@ int side_stream(SideStream** out) {
 
 int run_attention(const std::vector<AttnLaunch>& ls, int D, hipStream_t st) {
   for (const auto& L : ls) {
-    if (int e = hip_check(timed("rope_append", st, [&] { return launch_rope_append(L.rope, L.rope_tokens, st); }), "rope-append launch")) return e;
-    if (int e = hip_check(timed("vt_pack", st, [&] { return launch_vt_pack(L.attn, D, st); }), "V^T pack launch")) return e;
+    if (int e = hip_check(timed("rope_vt_pack", st, [&] { return launch_stage(L.rope, L.rope_tokens, L.attn, D, st); }), "RoPE/V^T pack launch")) return e;
     if (int e = hip_check(timed("attention", st, [&] { return launch_attention(L.attn, D, st); }), "attention launch")) return e;
     if (L.merge_rows > 0)
       if (int e = hip_check(timed("attention_merge", st, [&] { return launch_attention_merge(L.merge, L.merge_rows, D, st); }), "merge launch")) return e;

@@ -40,6 +40,8 @@ namespace tu {
 
 namespace {
 
+typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2;
+
 constexpr int kBM = kAttnRows;
 constexpr int kBN = kAttnKeys;
 constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units): P < 2^8 fits f16
@@ -426,53 +428,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   }
 }
 
-// One workgroup per (context, kv head, 64-key tile): V rows -> f16 V^T tile in the
-// attention kernel's LDS layout: D rows (dims) of kVtRow halves, each 64 keys in
-// key_slot order within 16-key groups followed by 8 halves of padding (left
-// unwritten; the attention kernel never reads it). Keys past the cache's data are
-// zero. Thread (c, m) builds chunk c (8 keys) of the 8 rows 8m .. 8m + 7: it loads
-// those 8 keys' dims 8m .. 8m + 7 (16 bytes each, consecutive threads read
-// consecutive bytes of a row), transposes the 8 x 8 block in registers and writes 8
-// chunks.
-template <int D>
-__global__ __launch_bounds__(256) void k_vt_pack(AttnArgs a) {
-  constexpr int M = D / 8;                 // 8-dim blocks per row
-  constexpr int CPR = kVtRow / 8;          // chunks per V^T row
-  const int item = blockIdx.x;
-  if (item >= a.pack_items) return;
-  int si = 0;
-  while (si + 1 < a.n_seq && a.seq[si + 1].pack_begin <= item) ++si;
-  const AttnSeq& S = a.seq[si];
-  const int local = item - S.pack_begin;
-  const int kt = local % S.n_vt_tiles;
-  const int hkv = local / S.n_vt_tiles;
-  const int n_valid = S.L_keep + S.T;
-  const int key0 = kt * kBN;
-  const long rs = (long)a.n_kv_heads * D;
-  const bf16_t* src = S.v_cache + (long)hkv * D;
-  _Float16* dst = S.vt + ((long)hkv * S.n_vt_tiles + kt) * (D * kVtRow);
-  for (int w = threadIdx.x; w < 8 * M; w += 256) {
-    const int m = w % M;        // consecutive threads: consecutive dim blocks
-    const int c = w / M;        // key chunk 0..7
-    u32x4 rowv[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int key = key0 + key_slot(8 * c + j);
-      rowv[j] = key < n_valid ? *(const u32x4*)(src + (long)key * rs + 8 * m) : u32x4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int d = 0; d < 8; ++d) {
-      f16x8 h;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t word = rowv[j][d >> 1];
-        h[j] = (_Float16)bf16_to_f32((d & 1) ? (word >> 16) : (word & 0xFFFFu));
-      }
-      *(f16x8*)(dst + ((8 * m + d) * CPR + c) * 8) = h;
-    }
-  }
-}
-
 // One thread per 8 output dims of one (token, head) row.
 template <int D>
 __global__ __launch_bounds__(256) void k_attn_merge(MergeArgs a) {
@@ -485,21 +440,44 @@ __global__ __launch_bounds__(256) void k_attn_merge(MergeArgs a) {
   const AttnSeq& S = a.seq[si];
   const long row = g - a.row_begin[si];
   const long R = (long)S.T * a.n_q_heads;
-  float M = -__builtin_inff();
-  for (int s = 0; s < S.n_splits; ++s) M = fmaxf(M, S.part_ml[(s * R + row) * 2]);
-  float L = 0.f;
+  // splits in batches of 8 whose loads are all in flight together; the running max
+  // and sums move between batches
+  float M = -__builtin_inff(), L = 0.f;
   f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < S.n_splits; ++s) {
-    const float m = S.part_ml[(s * R + row) * 2];
-    if (m == -__builtin_inff()) continue;
-    const float w = __builtin_amdgcn_exp2f(m - M) * S.part_ml[(s * R + row) * 2 + 1];
-    L += w;
-    const f16x8 v = *(const f16x8*)(S.part_o + (s * R + row) * D + 8 * d8);
+  for (int s0 = 0; s0 < S.n_splits; s0 += 8) {
+    f32x2 ml[8];
+    f16x8 v[8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      acc0[j] += w * (float)v[j];
-      acc1[j] += w * (float)v[4 + j];
+    for (int j = 0; j < 8; ++j) {
+      const long at = (long)(s0 + j) * R + row;
+      if (s0 + j < S.n_splits) {
+        ml[j] = *(const f32x2*)(S.part_ml + at * 2);
+        v[j] = *(const f16x8*)(S.part_o + at * D + 8 * d8);
+      } else {
+        ml[j] = f32x2{-__builtin_inff(), 0.f};
+        v[j] = f16x8{};
+      }
     }
+    float Mb = M;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) Mb = fmaxf(Mb, ml[j][0]);
+    if (Mb == -__builtin_inff()) continue;
+    const float c = M == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
+    L *= c;
+    acc0 *= c;
+    acc1 *= c;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (ml[j][0] == -__builtin_inff()) continue;
+      const float w = __builtin_amdgcn_exp2f(ml[j][0] - Mb) * ml[j][1];
+      L += w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc0[e] += w * (float)v[j][e];
+        acc1[e] += w * (float)v[j][4 + e];
+      }
+    }
+    M = Mb;
   }
   const float inv = 1.f / L;
   float* orow = S.out + row * D + 8 * d8;
@@ -508,19 +486,6 @@ __global__ __launch_bounds__(256) void k_attn_merge(MergeArgs a) {
 }
 
 }  // namespace
-
-hipError_t launch_vt_pack(const AttnArgs& a, int head_dim, hipStream_t s) {
-  if (a.pack_items <= 0) return hipSuccess;
-  if (head_dim == 256)
-    hipLaunchKernelGGL(k_vt_pack<256>, dim3(a.pack_items), dim3(256), 0, s, a);
-  else if (head_dim == 128)
-    hipLaunchKernelGGL(k_vt_pack<128>, dim3(a.pack_items), dim3(256), 0, s, a);
-  else if (head_dim == 64)
-    hipLaunchKernelGGL(k_vt_pack<64>, dim3(a.pack_items), dim3(256), 0, s, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
-}
 
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s) {
   if (a.total_items <= 0) return hipSuccess;

@@ -149,6 +149,7 @@ struct AttnSeq {
   const bf16_t* q_hat;   // [T][Hq][D]
   const bf16_t* k_cache; // [cap][Hkv][D]
   const bf16_t* v_cache;
+  const bf16_t* v_new;   // [T][Hkv][D] the tail's values (rows L_keep .. L_keep + T - 1 of the cache)
   _Float16* vt;          // [Hkv][n_vt_tiles][D * kVtRow] packed f16 V^T tiles
   float* out;            // [T][Hq][D]
   _Float16* part_o;      // [splits][T*Hq][D] normalised split outputs (unused when splits == 1)
@@ -215,8 +216,8 @@ struct DeltaArgs {
 int compact_max_blocks();   // resident workgroups of the gather kernel over the device
 constexpr int kMaxGatherWorkers = 2048;
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
-hipError_t launch_rope_append(const RopeArgs& a, int total_tokens, hipStream_t s);
-hipError_t launch_vt_pack(const AttnArgs& a, int head_dim, hipStream_t s);
+// RoPE + append of the tail tokens and the V^T packing of every key tile, one launch
+hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention_merge(const MergeArgs& a, int total_rows, int head_dim, hipStream_t s);
 hipError_t launch_delta_prep(const DeltaArgs& a, int d, int chunk, hipStream_t s);

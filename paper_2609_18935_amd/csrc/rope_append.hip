@@ -3,7 +3,12 @@
 // keys and values are appended after the surviving rows. Keys are never rotated
 // back and no placeholder rows are written.
 //
-// One workgroup per tail token (all contexts of a launch packed). The angles
+// The same launch also packs every 64-key V tile of the attention into the f16 V^T
+// layout the attention kernel stages (k_stage: the first workgroups rotate tokens, the
+// rest pack tiles). The pack reads the tail's values from the input rather than from
+// the rows this launch appends, so the two parts never wait on each other.
+//
+// RoPE: one workgroup per tail token (all contexts of a launch packed). The angles
 // (cursor + i) * theta^(-2j/r) and their sines and cosines are formed in float64,
 // once per rotary pair j, into LDS. Then each thread rotates 8 consecutive pairs of
 // one query or key head: two 16-byte loads (components j .. j+7 and j+r/2 ..
@@ -23,10 +28,9 @@ __device__ __forceinline__ uint32_t pack_bf16(double lo, double hi) {
   return f64_to_bf16_rne(lo) | (f64_to_bf16_rne(hi) << 16);
 }
 
-__global__ __launch_bounds__(kRopeThreads) void k_rope_append(RopeArgs a) {
+__device__ void rope_token(const RopeArgs& a, int tok) {
   __shared__ double s_cos[kMaxHalf];
   __shared__ double s_sin[kMaxHalf];
-  const int tok = blockIdx.x;
   int si = 0;
   while (si + 1 < a.n_seq && a.seq[si + 1].tok_begin <= tok) ++si;
   const RopeSeq& S = a.seq[si];
@@ -112,12 +116,79 @@ __global__ __launch_bounds__(kRopeThreads) void k_rope_append(RopeArgs a) {
   if (threadIdx.x == 0) S.pos[row] = (int32_t)p;
 }
 
+
+// V^T pack: one workgroup per (context, kv head, 64-key tile): V rows -> f16 V^T tile in
+// the attention kernel's LDS layout: D rows (dims) of kVtRow halves, each 64 keys in
+// key_slot order within 16-key groups followed by 8 halves of padding (left
+// unwritten; the attention kernel never reads it). Keys past the cache's data are
+// zero. Thread (c, m) builds chunk c (8 keys) of the 8 rows 8m .. 8m + 7: it loads
+// those 8 keys' dims 8m .. 8m + 7 (16 bytes each, consecutive threads read
+// consecutive bytes of a row), transposes the 8 x 8 block in registers and writes 8
+// chunks.
+template <int D>
+__device__ void vt_pack_tile(const AttnArgs& a, int item) {
+  constexpr int M = D / 8;                 // 8-dim blocks per row
+  constexpr int CPR = kVtRow / 8;          // chunks per V^T row
+  int si = 0;
+  while (si + 1 < a.n_seq && a.seq[si + 1].pack_begin <= item) ++si;
+  const AttnSeq& S = a.seq[si];
+  const int local = item - S.pack_begin;
+  const int kt = local % S.n_vt_tiles;
+  const int hkv = local / S.n_vt_tiles;
+  const int L_keep = S.L_keep;
+  const int n_valid = L_keep + S.T;
+  const int key0 = kt * kAttnKeys;
+  const long rs = (long)a.n_kv_heads * D;
+  const bf16_t* src = S.v_cache + (long)hkv * D;
+  const bf16_t* src_new = S.v_new + (long)hkv * D;   // tail row key - L_keep
+  _Float16* dst = S.vt + ((long)hkv * S.n_vt_tiles + kt) * (D * kVtRow);
+  for (int w = threadIdx.x; w < 8 * M; w += kRopeThreads) {
+    const int m = w % M;        // consecutive threads: consecutive dim blocks
+    const int c = w / M;        // key chunk 0..7
+    u32x4 rowv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int key = key0 + key_slot(8 * c + j);
+      const bf16_t* row = (key < L_keep ? src + (long)key * rs : src_new + (long)(key - L_keep) * rs) + 8 * m;
+      rowv[j] = key < n_valid ? *(const u32x4*)row : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      f16x8 h;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t word = rowv[j][d >> 1];
+        h[j] = (_Float16)bf16_to_f32((d & 1) ? (word >> 16) : (word & 0xFFFFu));
+      }
+      *(f16x8*)(dst + ((8 * m + d) * CPR + c) * 8) = h;
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kRopeThreads) void k_stage(RopeArgs r, AttnArgs a, int rope_tokens) {
+  const int b = blockIdx.x;
+  if (b < rope_tokens) {
+    rope_token(r, b);
+    return;
+  }
+  if (b - rope_tokens < a.pack_items) vt_pack_tile<D>(a, b - rope_tokens);
+}
+
 }  // namespace
 
-hipError_t launch_rope_append(const RopeArgs& a, int total_tokens, hipStream_t s) {
-  if (total_tokens <= 0) return hipSuccess;
-  if (a.rotary_dim > 2 * kMaxHalf) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_rope_append, dim3(total_tokens), dim3(kRopeThreads), 0, s, a);
+hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const AttnArgs& a, int head_dim, hipStream_t s) {
+  const int blocks = rope_tokens + a.pack_items;
+  if (blocks <= 0) return hipSuccess;
+  if (r.rotary_dim > 2 * kMaxHalf) return hipErrorInvalidValue;
+  if (head_dim == 256)
+    hipLaunchKernelGGL(k_stage<256>, dim3(blocks), dim3(kRopeThreads), 0, s, r, a, rope_tokens);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL(k_stage<128>, dim3(blocks), dim3(kRopeThreads), 0, s, r, a, rope_tokens);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(k_stage<64>, dim3(blocks), dim3(kRopeThreads), 0, s, r, a, rope_tokens);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
