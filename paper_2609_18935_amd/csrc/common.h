@@ -66,6 +66,17 @@ __device__ __forceinline__ int xcd_remap(int b, int n_blocks) {
 
 // Key order inside a 16-key group of a packed V^T tile: bits 2 and 3 swapped, so that
 // the 8 keys one lane feeds to a P.V product are one contiguous 16-byte chunk.
+// Workgroup barrier over LDS only: this wave's LDS accesses have completed when it
+// arrives, while its global stores may still be in flight. For kernels whose
+// workgroups never read back, within the kernel, what they stored to global memory
+// (__syncthreads would also wait for those stores).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 __device__ __forceinline__ int key_slot(int k) {
   return (k & ~0xC) | ((k & 4) << 1) | ((k & 8) >> 1);
 }

@@ -105,12 +105,23 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
     *(u32x4*)&Ks[r][cc * 8] = kw;
     *(u32x4*)&Qs[r][cc * 8] = qw;
   }
+  // the values this thread converts in phase 5, fetched now so their latency overlaps
+  // phases 1-4 ((C / 4) * (DK / 8) <= 256: one item per thread at most)
+  constexpr int NE5 = (C / 4) * (DK / 8);
+  static_assert(NE5 <= 256, "phase 5 maps one item per thread");
+  u32x4 vw[4];
+  if (tid < NE5) {
+    const int s4 = (tid % (C / 4)) * 4, d0 = (tid / (C / 4)) * 8;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      vw[j] = (s4 + j < Cr) ? *(const u32x4*)(S.v + ((long)(t0 + s4 + j) * Hv + h) * DV + d0) : u32x4{0, 0, 0, 0};
+  }
   if (tid < C) {
     const bool ok = tid < Cr;
     bt[tid] = ok ? S.beta[(long)(t0 + tid) * Hv + h] : 0.f;
     lg[tid] = ok ? __log2f(S.g[(long)(t0 + tid) * Hv + h]) : 0.f;
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- phase 1: cumulative log-decay (wave 0) and K K^T, Q K^T lower blocks (MFMA)
   if (wave == 0) {
@@ -146,7 +157,7 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
       }
     }
   }
-  __syncthreads();   // lg ready
+  lds_barrier();   // lg ready
 
   // ---- phase 2: M (fp32, LDS) and P (f16, workspace) from the MFMA results
   const long slot = (long)c * Hv + h;
@@ -177,7 +188,7 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
     if ((i >> 4) > (r >> 4)) Pg[r * C + i] = (_Float16)0.f;
   }
   if (tid < C) a.ws_lg[slot * C + tid] = lg[tid];
-  __syncthreads();
+  lds_barrier();
 
   // ---- phase 3: diagonal 16x16 blocks of T = (I + M)^-1, one lane per column
   if (wave == 0 && g4 < NB) {
@@ -193,7 +204,7 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) Tf[16 * b + rr][16 * b + cc] = x[rr];
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- phase 4: off-diagonal blocks, level by level: T_ij = -T_ii sum_{m=j}^{i-1} M_im T_mj
 #pragma unroll
@@ -211,7 +222,7 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
           x += Mf[16 * i + rr][16 * m + k] * *(const f32x4*)&Tf[16 * m + k][16 * j + c4];
       *(f32x4*)&Xs[q][rr][c4] = x;
     }
-    __syncthreads();
+    lds_barrier();
     if (q < nblk) {
       const int j = q, i = q + lev;
       f32x4 y = {0.f, 0.f, 0.f, 0.f};
@@ -219,7 +230,7 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
       for (int k = 0; k < 16; ++k) y += Tf[16 * i + rr][16 * i + k] * *(const f32x4*)&Xs[q][k][c4];
       *(f32x4*)&Tf[16 * i + rr][16 * j + c4] = -y;
     }
-    __syncthreads();
+    lds_barrier();
   }
 
   // ---- phase 5: f16 copies: T (lower, zero upper), (beta 2^lg K)^T and (beta V)^T
@@ -227,10 +238,10 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
     const int r = e / C, i = e - r * C;
     Th[r][i] = (_Float16)((i >> 4) <= (r >> 4) ? Tf[r][i] : 0.f);
   }
-  for (int e = tid; e < (C / 4) * (DK / 8); e += 256) {
-    const int s4 = (e % (C / 4)) * 4, d0 = (e / (C / 4)) * 8;
+  if (tid < NE5) {
+    const int s4 = (tid % (C / 4)) * 4, d0 = (tid / (C / 4)) * 8;
     float wk[4], wv[4], wd[4];
-    u32x4 kw[4], vw[4];
+    u32x4 kw[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int s = s4 + j;
@@ -238,7 +249,6 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
       wk[j] = bt[s] * __builtin_amdgcn_exp2f(lg[s]);
       wd[j] = __builtin_amdgcn_exp2f(lg[C - 1] - lg[s]);
       kw[j] = *(const u32x4*)&Ks[s][d0];
-      vw[j] = (s < Cr) ? *(const u32x4*)(S.v + ((long)(t0 + s) * Hv + h) * DV + d0) : u32x4{0, 0, 0, 0};
     }
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
@@ -269,7 +279,7 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
     }
     *(f16x8*)(a.ws_q + slot * C * DK + (long)r * DK + cc * 8) = hq;
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- phase 6: W = T (beta 2^lg K), U~ = T (beta V) on MFMA; write to workspace
   _Float16* Wg = a.ws_w + slot * C * DK;
@@ -429,7 +439,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     const int t0 = lc * C;
     const int Cr = min(C, S.T - t0);
     stage();
-    __syncthreads();
+    lds_barrier();
     if (lc + 1 < S.n_chunks) prefetch(lc + 1);
     const float g_last = s_glast;
 
@@ -454,7 +464,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
       *(f16x4*)&Ut[16 * cb + l16][16 * rb + 4 * g4] = uh;
       oacc[j] = y;
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- O += P U, written out; S^T <- 2^lg_last S^T + Kd^T U; refresh the f16 copy of S
 #pragma unroll
@@ -497,7 +507,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
       f16x4 hv = {(_Float16)sacc[0], (_Float16)sacc[1], (_Float16)sacc[2], (_Float16)sacc[3]};
       *(f16x4*)&Sh[16 * cb + l16][16 * db + 4 * g4] = hv;
     }
-    __syncthreads();   // staged tiles, U^T and S are free for the next chunk
+    lds_barrier();   // staged tiles, U^T and S are free for the next chunk
   }
 #pragma unroll
   for (int j = 0; j < NSW; ++j) {
