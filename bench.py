@@ -44,6 +44,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--kv-splits", type=int, default=0)
+    ap.add_argument("--no-peaks", action="store_true", help="skip the copy and GEMM rate measurements")
     return ap.parse_args()
 
 
@@ -236,6 +237,46 @@ def cpu_baseline(cfg, seed, budget_s):
 
 # ----------------------------------------------------------------------------- main
 
+def measured_peaks(dev):
+    """Rates this GPU sustains in this run, as a second reference beside the datasheet peaks:
+    a plain 1 GiB device copy (bytes read + written per second) and an 8192^3 bf16 GEMM
+    (torch.matmul, contiguous operands), each timed over repeated back-to-back launches."""
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    a.fill_(1)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    reps = 10
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2.0 * n * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del a, b
+    m = 8192
+    x = torch.randn((m, m), device=dev, dtype=torch.float32).to(torch.bfloat16)
+    y = torch.randn((m, m), device=dev, dtype=torch.float32).to(torch.bfloat16)
+    for _ in range(5):
+        z = torch.matmul(x, y)
+    torch.cuda.synchronize()
+    reps = 50
+    e0.record()
+    for _ in range(reps):
+        z = torch.matmul(x, y)
+    e1.record()
+    torch.cuda.synchronize()
+    gemm_tflops = 2.0 * m ** 3 * reps / (e0.elapsed_time(e1) / 1e3) / 1e12
+    del x, y, z
+    torch.cuda.empty_cache()
+    return {"copy_gbs": round(copy_gbs, 1), "copy_bytes": 2 * n, "bf16_gemm_tflops": round(gemm_tflops, 1),
+            "gemm_shape": [m, m, m], "gemm_launches": reps}
+
+
 def measured_traffic(kernel, workload):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE and
     WRITE_SIZE passes (profiles/traffic_config*.json), or None when there is no record
@@ -408,6 +449,15 @@ def main():
               file=sys.stderr, flush=True)
         del rups, rin, own, rws
 
+    # ---- measured peaks of this part in this run: device copy bandwidth and a bf16 GEMM
+    peaks = None if args.no_peaks else measured_peaks(dev)
+    if peaks is not None:
+        meas = peaks["bf16_gemm_tflops"] if roofline.get("bound") == "mfma" else peaks["copy_gbs"]
+        if roofline.get("achieved") is not None and meas:
+            roofline["measured_peak"] = meas
+            roofline["frac_of_measured"] = round(roofline["achieved"] / meas, 4)
+        print(f"[bench] measured peaks: {json.dumps(peaks)}", file=sys.stderr, flush=True)
+
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] cpu oracle leg ...", file=sys.stderr, flush=True)
@@ -433,6 +483,7 @@ def main():
                    "attn": f"{a.n_q_heads}q/{a.n_kv_heads}kv x {a.head_dim}",
                    "delta": f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}"},
         "roofline": roofline,
+        "measured_peaks": peaks,
         "stages": stages,
         "speedup_vs_refill":round(refill["speedup"], 3) if refill else None,
         "refill_ms": round(refill["ms"], 5) if refill else None,
