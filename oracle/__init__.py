@@ -13,6 +13,8 @@ What it computes (paper: Section 4.1, Eq. 2 and Eq. 3; Section 4.2):
   * causal grouped-query softmax attention of the tail over surviving + new KV;
   * the gated delta-rule recurrence continuing from the carried state, token by
     token, plus a chunked form used only to check the invariant that both agree;
+  * the short causal convolution of the recurrent layers continuing from its
+    carried state (Section 4.1, Fig. 2: convolution state continues);
   * dense refill and fresh gapped prefill of the final context (Section 5.2).
 
 Functions with no independent pin are marked "parity unpinned" in their
@@ -23,6 +25,7 @@ from .compaction import RangeError, validate_ranges, live_positions, compact  # 
 from .rope import rope_frequencies, rope_rotate  # noqa: F401
 from .attention import causal_gqa_attention  # noqa: F401
 from .delta import gated_delta_tokens, gated_delta_chunked  # noqa: F401
+from .short_conv import silu, short_conv_continue  # noqa: F401
 from .update import (  # noqa: F401
     attention_layer_update,
     delta_layer_update,
