@@ -237,6 +237,36 @@ def cpu_baseline(cfg, seed, budget_s):
 
 # ----------------------------------------------------------------------------- main
 
+def short_conv_row(tu, synth, cfg, T, dev, reps):
+    """Short causal convolution continued from its carried state over the tail of one
+    delta layer: the q, k and v projections (channels Hk*d_k, Hk*d_k, Hv*d_v), width 4,
+    SiLU. Algorithmic bytes: x and y once, the carried rows read and written, weights."""
+    import numpy as np
+    import torch
+    d = cfg.delta
+    W = 4
+    chans = [d.n_k_heads * d.d_k, d.n_k_heads * d.d_k, d.n_v_heads * d.d_v]
+    bufs = []
+    for i, C in enumerate(chans):
+        st, x, w = synth.gen_conv_inputs(0, T, C, W, layer=i)
+        dv = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+        bufs.append((dv(st), dv(x), dv(w), torch.empty((T, C), dtype=torch.bfloat16, device=dev)))
+    tu.short_conv_continue_batch(bufs)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        tu.short_conv_continue_batch(bufs)   # one launch for the three tensors
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = sum(2 * T * C * 2 + 2 * (W - 1) * C * 2 + C * W * 2 for C in chans)
+    ach = nbytes / (ms / 1e3) / 1e9
+    return {"tokens": T, "channels": chans, "width": W, "launches": 1, "ms": round(ms, 5),
+            "bytes": nbytes, "bound": "hbm", "achieved": round(ach, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
+            "frac": round(ach / HBM_PEAK_GBS, 4)}
+
+
 def measured_peaks(dev):
     """Rates this GPU sustains in this run, as a second reference beside the datasheet peaks:
     a plain 1 GiB device copy (bytes read + written per second) and an 8192^3 bf16 GEMM
@@ -449,6 +479,12 @@ def main():
               file=sys.stderr, flush=True)
         del rups, rin, own, rws
 
+    # ---- the short-convolution continuation of one delta layer's q, k, v (width 4, SiLU)
+    extra = {}
+    if kinds.count("delta"):
+        extra["short_conv"] = short_conv_row(tu, synth, cfg, sumT, dev, K)
+        print(f"[bench] short conv: {json.dumps(extra['short_conv'])}", file=sys.stderr, flush=True)
+
     # ---- measured peaks of this part in this run: device copy bandwidth and a bf16 GEMM
     peaks = None if args.no_peaks else measured_peaks(dev)
     if peaks is not None:
@@ -456,6 +492,8 @@ def main():
         if roofline.get("achieved") is not None and meas:
             roofline["measured_peak"] = meas
             roofline["frac_of_measured"] = round(roofline["achieved"] / meas, 4)
+        for row in extra.values():
+            row["frac_of_measured_copy"] = round(row["achieved"] / peaks["copy_gbs"], 4)
         print(f"[bench] measured peaks: {json.dumps(peaks)}", file=sys.stderr, flush=True)
 
     cpu = None
@@ -484,6 +522,7 @@ def main():
                    "delta": f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}"},
         "roofline": roofline,
         "measured_peaks": peaks,
+        "extra_rows": extra,
         "stages": stages,
         "speedup_vs_refill":round(refill["speedup"], 3) if refill else None,
         "refill_ms": round(refill["ms"], 5) if refill else None,

@@ -172,6 +172,46 @@ int delta_rule_continue(float* state, const void* q, const void* k, const void* 
                         const float* g, int64_t T, const tu_delta_params* p, float* out,
                         void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Convolution-state continuation (Section 4.1 and Fig. 2: the recurrent layers'
+ * convolution state continues over the replacement tokens without rollback),
+ * read as the short depthwise causal convolution of Gated DeltaNet layers. For
+ * each tail token t and channel c of one projected tensor
+ *   y_t[c] = act( sum_{j<width} w[c][j] * xt[t + j][c] ),
+ * where xt is the width-1 carried rows followed by the T new rows; act is SiLU
+ * (x * sigmoid(x), TU_CONV_SILU) or the identity (TU_CONV_IDENTITY). Products
+ * are summed in fp32 in tap order and rounded to bf16 (nearest even).
+ *  state:  device bf16 [width-1][channels], the last width-1 input rows of the
+ *          context; replaced in place by the last width-1 rows of xt (may be NULL
+ *          when width == 1).
+ *  x:      device bf16 [T][channels] new rows (before the convolution).
+ *  weight: device bf16 [channels][width], tap width-1 multiplies the newest row.
+ *  out:    device bf16 [T][channels]; must not overlap x or state.
+ * channels: a positive multiple of 8; width 1 .. 8. T == 0 leaves state unchanged.
+ * Needs no workspace. Errors: TU_ERR_ARG (sizes, activation, null or misaligned
+ * pointers), TU_ERR_HIP (launch failure).
+ */
+#define TU_CONV_IDENTITY 0
+#define TU_CONV_SILU 1
+int short_conv_continue(void* state, const void* x, const void* weight, int64_t T, int32_t channels, int32_t width,
+                        int32_t activation, void* out, void* stream);
+
+/* Several independent tensors (e.g. the q, k and v projections of a layer, or the
+ * layers and contexts of a stack) in as few launches as possible: up to 16 tensors
+ * share one launch. Every field has the meaning it has in short_conv_continue;
+ * width and activation are common. All tensors are checked before any launch. */
+typedef struct tu_conv_tensor {
+  void* state;          /* device bf16 [width-1][channels], in place */
+  const void* x;        /* device bf16 [T][channels] */
+  const void* weight;   /* device bf16 [channels][width] */
+  void* out;            /* device bf16 [T][channels] */
+  int64_t T;
+  int32_t channels;
+  int32_t reserved;     /* 0 */
+} tu_conv_tensor;
+int short_conv_continue_batch(const tu_conv_tensor* tensors, int32_t n, int32_t width, int32_t activation,
+                              void* stream);
+
 /* One context's part of a stack update. */
 typedef struct tu_seq_update {
   tu_seq* seq;
@@ -240,7 +280,7 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
  * (or a negative status) and clears the records. Names (one per launch or pair
  * of launches): compact (keep-scan, then gather), rope_vt_pack (RoPE + append of
  * the tail with the V^T packing of the key tiles), attention, attention_merge,
- * delta_prep, delta_chain.
+ * delta_prep, delta_chain, short_conv.
  */
 int tu_profile_enable(int on);
 int tu_profile_collect(char* names, int32_t name_stride, int32_t* counts, double* total_ms, int32_t max_entries);

@@ -63,6 +63,11 @@ class tu_layer_io(ctypes.Structure):
                 ("out", _vp)]
 
 
+class tu_conv_tensor(ctypes.Structure):
+    _fields_ = [("state", _vp), ("x", _vp), ("weight", _vp), ("out", _vp), ("T", _i64), ("channels", _i32),
+                ("reserved", _i32)]
+
+
 class tu_update(ctypes.Structure):
     _fields_ = [("n_seq", _i32), ("seqs", ctypes.POINTER(tu_seq_update)), ("n_layers", _i32),
                 ("layers", ctypes.POINTER(tu_layer_io)), ("attn", tu_attn_params), ("delta", tu_delta_params)]
@@ -83,6 +88,8 @@ _SIGNATURES = {
     "delta_rule_continue_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_delta_params), _i64]),
     "delta_rule_continue": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i64, ctypes.POINTER(tu_delta_params), _vp, _vp,
                                    ctypes.c_size_t, _vp]),
+    "short_conv_continue": (_i32, [_vp, _vp, _vp, _i64, _i32, _i32, _i32, _vp, _vp]),
+    "short_conv_continue_batch": (_i32, [ctypes.POINTER(tu_conv_tensor), _i32, _i32, _i32, _vp]),
     "update_layer_stack_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_update)]),
     "tu_validate_update": (_i32, [ctypes.POINTER(tu_update)]),
     "update_layer_stack": (_i32, [ctypes.POINTER(tu_update), _vp, ctypes.c_size_t, _vp]),
@@ -255,6 +262,34 @@ def delta_rule_continue(state: torch.Tensor, q, k, v, beta, g, params: tu_delta_
     ws = _workspace(nbytes, state.device, workspace)
     _check(lib().delta_rule_continue(_ptr(state), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(g), T,
                                      ctypes.byref(params), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+TU_CONV_IDENTITY = 0
+TU_CONV_SILU = 1
+
+
+def short_conv_continue(state: Optional[torch.Tensor], x: torch.Tensor, weight: torch.Tensor, out: torch.Tensor,
+                        activation: str = "silu", stream=None):
+    """Short causal convolution of x [T][C] continued from state [W-1][C] (updated in
+    place); weight [C][W]; out [T][C]; all bf16 on the device."""
+    T, C = int(x.shape[0]), int(x.shape[1])
+    W = int(weight.shape[1])
+    act = {"silu": TU_CONV_SILU, "none": TU_CONV_IDENTITY}[activation]
+    _check(lib().short_conv_continue(_ptr(state), _ptr(x), _ptr(weight), T, C, W, act, _ptr(out), _stream(stream)))
+
+
+def short_conv_continue_batch(items, activation: str = "silu", stream=None):
+    """items: sequence of (state, x, weight, out) tensors sharing one width (see
+    short_conv_continue); all are continued in as few launches as possible."""
+    arr = (tu_conv_tensor * max(1, len(items)))()
+    W = None
+    for i, (st, x, w, out) in enumerate(items):
+        if W is not None and int(w.shape[1]) != W:
+            raise ValueError("all tensors of a batch share one width")
+        W = int(w.shape[1])
+        arr[i] = tu_conv_tensor(_ptr(st), _ptr(x), _ptr(w), _ptr(out), int(x.shape[0]), int(x.shape[1]), 0)
+    act = {"silu": TU_CONV_SILU, "none": TU_CONV_IDENTITY}[activation]
+    _check(lib().short_conv_continue_batch(arr, len(items), W or 1, act, _stream(stream)))
 
 
 class LayerIO:

@@ -894,6 +894,58 @@ int delta_rule_continue(float* state, const void* q, const void* k, const void* 
   return ok();
 }
 
+int short_conv_continue_batch(const tu_conv_tensor* tensors, int32_t n, int32_t width, int32_t activation,
+                              void* stream) {
+  if (n < 0 || (n > 0 && !tensors)) return fail(TU_ERR_ARG, "bad tensor array");
+  if (width < 1 || width > 8) return fail(TU_ERR_ARG, "width must be 1 .. 8");
+  if (activation != TU_CONV_IDENTITY && activation != TU_CONV_SILU) return fail(TU_ERR_ARG, "unknown activation");
+  for (int i = 0; i < n; ++i) {
+    const tu_conv_tensor& t = tensors[i];
+    if (t.T < 0) return fail(TU_ERR_ARG, "tensor %d: negative T", i);
+    if (t.T > INT32_MAX / 2) return fail(TU_ERR_ARG, "tensor %d: T too large", i);
+    if (t.channels <= 0 || t.channels % 8) return fail(TU_ERR_ARG, "tensor %d: channels must be a positive multiple of 8", i);
+    if (t.T == 0) continue;
+    if (!t.x || !t.weight || !t.out || (width > 1 && !t.state)) return fail(TU_ERR_ARG, "tensor %d: null pointer", i);
+    if (!aligned16(t.x) || !aligned16(t.weight) || !aligned16(t.out) || (t.state && !aligned16(t.state)))
+      return fail(TU_ERR_ARG, "tensor %d: pointers must be 16-byte aligned", i);
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  ConvArgs a{};
+  int blocks = 0;
+  auto flush = [&]() -> int {
+    if (a.n_jobs == 0) return TU_OK;
+    if (int e = hip_check(timed("short_conv", st, [&] { return launch_short_conv(a, blocks, width, st); }),
+                          "short-conv launch"))
+      return e;
+    a = ConvArgs{};
+    blocks = 0;
+    return TU_OK;
+  };
+  for (int i = 0; i < n; ++i) {
+    const tu_conv_tensor& t = tensors[i];
+    if (t.T == 0) continue;
+    ConvJob& j = a.job[a.n_jobs++];
+    j.state = static_cast<bf16_t*>(t.state);
+    j.x = static_cast<const bf16_t*>(t.x);
+    j.w = static_cast<const bf16_t*>(t.weight);
+    j.out = static_cast<bf16_t*>(t.out);
+    j.T = (int32_t)t.T;
+    j.C = t.channels;
+    j.act = activation == TU_CONV_SILU;
+    blocks += conv_blocks(j, blocks);
+    if (a.n_jobs == kMaxConvJobs)
+      if (int e = flush()) return e;
+  }
+  if (int e = flush()) return e;
+  return ok();
+}
+
+int short_conv_continue(void* state, const void* x, const void* weight, int64_t T, int32_t channels, int32_t width,
+                        int32_t activation, void* out, void* stream) {
+  const tu_conv_tensor t{state, x, weight, out, T, channels, 0};
+  return short_conv_continue_batch(&t, 1, width, activation, stream);
+}
+
 // Workspace of a stack update: [compaction / attention region | delta region]. Delta
 // layers run on a second stream concurrently with the attention path, so the two
 // regions are disjoint. Attention layers run in order and reuse their region; the

@@ -222,6 +222,27 @@ struct DeltaArgs {
   _Float16* ws_kt;       // [chunks][Hv][dk][C]  2^(lg_last - lg) k, transposed
 };
 
+// One tensor of a short-convolution launch: x [T][C] bf16, weights [C][W] bf16, state
+// [W-1][C] bf16 (in place), out [T][C] bf16.
+struct ConvJob {
+  bf16_t* state;
+  const bf16_t* x;
+  const bf16_t* w;
+  bf16_t* out;
+  int32_t T;
+  int32_t C;            // a multiple of 8
+  int32_t act;          // 1: SiLU, 0: identity
+  int32_t block_begin;  // first workgroup of this job
+  int32_t n_cblocks;    // workgroups across the channels
+  int32_t pad;
+};
+
+constexpr int kMaxConvJobs = 16;
+struct ConvArgs {
+  ConvJob job[kMaxConvJobs];
+  int32_t n_jobs;
+};
+
 // ------------------------------------------------------------------ launchers
 // (defined in the kernel translation units; return a hipError_t)
 int compact_max_blocks();   // resident workgroups of the gather kernel over the device
@@ -230,6 +251,8 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 // RoPE + append of the tail tokens and the V^T packing of every key tile, one launch
 hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
+int conv_blocks(ConvJob& j, int block_begin);   // sets block_begin / n_cblocks, returns the job's workgroups
+hipError_t launch_short_conv(const ConvArgs& a, int blocks, int width, hipStream_t s);
 hipError_t launch_attention_merge(const MergeArgs& a, int total_rows, int head_dim, hipStream_t s);
 hipError_t launch_delta_prep(const DeltaArgs& a, int d, int chunk, hipStream_t s);
 hipError_t launch_delta_chain(const DeltaArgs& a, int d, int chunk, hipStream_t s);

@@ -18,6 +18,7 @@ from .workloads import (  # noqa: F401
     gen_attn_tail,
     gen_delta_state,
     gen_delta_inputs,
+    gen_conv_inputs,
     draw_records,
     subtract_ranges,
     append_interval,

@@ -35,7 +35,7 @@ import numpy as np
 import torch
 
 # tensor ids for sub-seeding
-T_KCACHE, T_VCACHE, T_Q, T_K, T_V, T_BETA, T_G, T_STATE, T_PLAN = range(9)
+T_KCACHE, T_VCACHE, T_Q, T_K, T_V, T_BETA, T_G, T_STATE, T_PLAN, T_CONV_X, T_CONV_STATE, T_CONV_W = range(12)
 
 
 @dataclass(frozen=True)
@@ -185,6 +185,17 @@ def gen_delta_inputs(seed: int, cfg: int, layer: int, T: int, shape: DeltaShape,
 
 
 # ----------------------------------------------------------------------------- records
+
+def gen_conv_inputs(seed: int, T: int, channels: int, width: int, layer: int = 0, rnd: int = 0, char: int = 0):
+    """Short-convolution inputs of one projected tensor (bf16 bits):
+    x [T][channels] ~ N(0, 1) (pre-convolution projections), the carried rows
+    [width-1][channels] ~ N(0, 1) (earlier inputs of the same tensor), weights
+    [channels][width] ~ N(0, 1/width)."""
+    x = to_bf16_bits(_normal(sub_rng(seed, 0, layer, T_CONV_X, rnd, char), (T, channels)))
+    st = to_bf16_bits(_normal(sub_rng(seed, 0, layer, T_CONV_STATE, 0, char), (width - 1, channels)))
+    w = to_bf16_bits(_normal(sub_rng(seed, 0, layer, T_CONV_W, 0, char), (channels, width), std=width ** -0.5))
+    return st, x, w
+
 
 def initial_intervals(L_old: int) -> List[Tuple[int, int]]:
     return [(0, int(L_old))] if L_old > 0 else []

@@ -165,6 +165,18 @@ def test_entry_points_reject_before_touching_device(L):
         tu.delta_rule_continue(fake, torch.zeros(4, 16, 128, dtype=torch.bfloat16), fake, fake, fake, fake, d, fake,
                                workspace=torch.zeros(256, dtype=torch.uint8))
     assert ei.value.code == B.TU_ERR_ARG
+    st = torch.zeros(3, 24, dtype=torch.bfloat16)
+    xs = torch.zeros(5, 24, dtype=torch.bfloat16)
+    x20 = torch.zeros(5, 20, dtype=torch.bfloat16)
+    for args, what in [((st, x20, torch.zeros(20, 4, dtype=torch.bfloat16), x20), "channels % 8"),
+                       ((torch.zeros(9, 24, dtype=torch.bfloat16), xs, torch.zeros(24, 10, dtype=torch.bfloat16), xs),
+                        "width > 8"),
+                       ((None, xs, torch.zeros(24, 4, dtype=torch.bfloat16), xs), "state missing")]:
+        with pytest.raises(tu.TailUpdateError) as ei:
+            tu.short_conv_continue(*args)
+        assert ei.value.code == B.TU_ERR_ARG, what
+    assert L.short_conv_continue(None, None, None, 4, 16, 4, 7, None, None) == B.TU_ERR_ARG   # unknown activation
+    assert L.short_conv_continue(None, None, None, 0, 16, 4, 1, None, None) == 0   # T == 0: nothing to do
 
 
 def test_commit_tail_advances_cursor_and_intervals(L):

@@ -276,3 +276,61 @@ def test_stack_is_deterministic():
                     bits_of(ac.k_cache)))
     for x, y in zip(res[0], res[1]):
         assert np.array_equal(x, y)
+
+
+# ----------------------------------------------------------------------------- short convolution
+
+def _conv_run(st_bits, x_bits, w_bits, act):
+    st = to_dev_bf16(st_bits) if st_bits.shape[0] else None
+    x = to_dev_bf16(x_bits)
+    w = to_dev_bf16(w_bits)
+    out = torch.full(x.shape, float("nan"), dtype=torch.bfloat16, device=DEV)
+    tu.short_conv_continue(st, x, w, out, activation=act)
+    torch.cuda.synchronize()
+    return bits_of(out), (bits_of(st) if st is not None else st_bits)
+
+
+@pytest.mark.parametrize("W,C,T,act", [(4, 2048, 512, "silu"), (4, 4096, 2048, "silu"), (4, 4096, 37, "silu"),
+                                       (3, 8, 1, "none"), (4, 64, 2, "silu"), (1, 32, 19, "silu"),
+                                       (8, 264, 100, "none"), (2, 16, 300, "silu"), (4, 8192, 17, "none")])
+def test_short_conv_parity(W, C, T, act):
+    _say(f"short conv W={W} C={C} T={T} act={act}")
+    st, x, w = synth.gen_conv_inputs(11, T, C, W)
+    ref_y, _, ref_state = oracle.short_conv_continue(st, x, w, activation=act)
+    y, state = _conv_run(st, x, w, act)
+    assert_bf16_close_bits(y, ref_y, f"conv W={W} C={C} T={T} out")
+    assert np.array_equal(state, ref_state), "carried state must be the last input rows, bit for bit"
+
+
+def test_short_conv_continuation_is_split_invariant():
+    W, C, T = 4, 1024, 200
+    _say("short conv split into calls of 0, 1, 2, 61 and 136 tokens vs one call")
+    st, x, w = synth.gen_conv_inputs(12, T, C, W)
+    y_all, s_all = _conv_run(st, x, w, "silu")
+    parts, s = [], st
+    for a, b in [(0, 0), (0, 1), (1, 3), (3, 64), (64, 200)]:
+        y, s = _conv_run(s, x[a:b], w, "silu")
+        parts.append(y)
+    assert np.array_equal(np.concatenate(parts), y_all)
+    assert np.array_equal(s, s_all)
+    ref_y, _, ref_s = oracle.short_conv_continue(st, x, w)
+    assert_bf16_close_bits(y_all, ref_y, "conv one call vs oracle")
+    assert np.array_equal(s_all, ref_s)
+
+
+def test_short_conv_batch_matches_single_calls():
+    # q, k, v of two contexts with ragged tails (one empty) in one call
+    _say("short conv batch of 6 tensors (C 2048/2048/4096, T 300 and 0 and 5)")
+    W = 4
+    specs = [(2048, 300), (2048, 300), (4096, 300), (2048, 0), (2048, 5), (4096, 5)]
+    items, refs = [], []
+    for i, (C, T) in enumerate(specs):
+        st, x, w = synth.gen_conv_inputs(13, T, C, W, layer=i)
+        refs.append(oracle.short_conv_continue(st, x, w))
+        items.append((to_dev_bf16(st), to_dev_bf16(x), to_dev_bf16(w),
+                      torch.full((T, C), float("nan"), dtype=torch.bfloat16, device=DEV)))
+    tu.short_conv_continue_batch(items)
+    torch.cuda.synchronize()
+    for (st, x, w, out), (ref_y, _, ref_s), (C, T) in zip(items, refs, specs):
+        assert_bf16_close_bits(bits_of(out), ref_y, f"batch conv C={C} T={T}")
+        assert np.array_equal(bits_of(st), ref_s)
