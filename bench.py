@@ -133,7 +133,7 @@ def make_copy(tu, chars, layers, device, pristine=True):
     return ctxs, own
 
 
-def stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p, tails=None, inputs=None, ranges=None):
+def stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p, tails=None, inputs=None, ranges=None, post=None):
     ios = []
     for L, O in zip(layers, own):
         src = inputs[id(L)] if inputs is not None else L
@@ -145,7 +145,7 @@ def stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p, tails=None, inpu
                                   beta=src["beta"], g=src["g"]))
     rr = ranges if ranges is not None else [c["ranges"] for c in chars]
     tt = tails if tails is not None else [c["T"] for c in chars]
-    return tu.StackUpdate(ctxs, rr, tt, ios, attn_p, delta_p)
+    return tu.StackUpdate(ctxs, rr, tt, ios, attn_p, delta_p, post_ranges=post)
 
 
 # ----------------------------------------------------------------------------- algorithmic work
@@ -479,8 +479,34 @@ def main():
               file=sys.stderr, flush=True)
         del rups, rin, own, rws
 
-    # ---- the short-convolution continuation of one delta layer's q, k, v (width 4, SiLU)
+    # ---- the same update with an 11-token opening and a 3-token closing maintenance
+    # delimiter in every tail, removed from the caches once the tail is prefilled
     extra = {}
+    if kinds.count("attn") and all(c["T"] >= 14 for c in chars):
+        post = [np.array([[c["cursor"], c["cursor"] + 11], [c["cursor"] + c["T"] - 3, c["cursor"] + c["T"]]])
+                for c in chars]
+        copies3 = [make_copy(tu, chars, layers, dev) for _ in range(W + K)]
+        ups3 = [stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p, post=post) for (ctxs, own) in copies3]
+        ws3 = torch.empty(max(u.workspace_size() for u in ups3), dtype=torch.uint8, device=dev)
+        for i in range(W):
+            ups3[i].run(ws3)
+        torch.cuda.synchronize()
+        ev0.record()
+        for i in range(W, W + K):
+            ups3[i].run(ws3)
+        ev1.record()
+        torch.cuda.synchronize()
+        post_ms = ev0.elapsed_time(ev1) / K
+        row_b = a.n_kv_heads * a.head_dim * 2
+        moved = sum(c["T"] - 11 - 3 for c in chars)   # tail rows behind the first delimiter that survive
+        extra["delimiter_removal"] = {
+            "removed_rows_per_context": 14, "update_ms_with": round(post_ms, 5), "update_ms_without": round(upd_ms, 5),
+            "extra_ms": round(post_ms - upd_ms, 5),
+            "bytes": 2 * 2 * moved * row_b * kinds.count("attn"), "bound": "hbm"}
+        print(f"[bench] delimiter removal: {json.dumps(extra['delimiter_removal'])}", file=sys.stderr, flush=True)
+        del copies3, ups3, ws3
+
+    # ---- the short-convolution continuation of one delta layer's q, k, v (width 4, SiLU)
     if kinds.count("delta"):
         extra["short_conv"] = short_conv_row(tu, synth, cfg, sumT, dev, K)
         print(f"[bench] short conv: {json.dumps(extra['short_conv'])}", file=sys.stderr, flush=True)
@@ -493,7 +519,8 @@ def main():
             roofline["measured_peak"] = meas
             roofline["frac_of_measured"] = round(roofline["achieved"] / meas, 4)
         for row in extra.values():
-            row["frac_of_measured_copy"] = round(row["achieved"] / peaks["copy_gbs"], 4)
+            if "achieved" in row:
+                row["frac_of_measured_copy"] = round(row["achieved"] / peaks["copy_gbs"], 4)
         print(f"[bench] measured peaks: {json.dumps(peaks)}", file=sys.stderr, flush=True)
 
     cpu = None

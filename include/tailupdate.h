@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define TU_ABI_VERSION 1
+#define TU_ABI_VERSION 2
 
 #define TU_OK 0
 #define TU_ERR_ARG (-1)       /* null pointer, unsupported or inconsistent shape */
@@ -219,6 +219,13 @@ typedef struct tu_seq_update {
   int32_t n_ranges;
   int64_t T;              /* tail tokens */
   int32_t* src_index;     /* optional device int32 [>= seq->len] (see compact_kv) */
+  /* Rows removed once the tail is prefilled (Section 4.1: temporary maintenance
+   * delimiters whose direct KV are subsequently removed; Section 4.2): host int64
+   * [n_post_ranges][2] half-open position ranges inside this call's tail
+   * [seq->next_pos, seq->next_pos + T), sorted, disjoint, non-empty. May be NULL
+   * when n_post_ranges == 0. */
+  const int64_t* post_ranges;
+  int32_t n_post_ranges;
 } tu_seq_update;
 
 /*
@@ -256,9 +263,12 @@ typedef struct tu_update {
  * context's ranges and capacity; compact every attention layer's cache once per
  * context (one index list per context, reused by all attention layers); then, in
  * layer order, tail attention for attention layers and recurrence continuation
- * for delta layers, batched over the contexts; finally commit each context's
- * metadata (len = survivors + T, live intervals, cursor += T). A full refill is
- * the same call on empty contexts (len 0) with zero states.
+ * for delta layers, batched over the contexts; then remove each context's
+ * post-prefill rows (post_ranges) from every attention layer; finally commit each
+ * context's metadata (len = survivors + T - post-removed rows, live intervals,
+ * cursor += T: the positions of post-removed rows become holes, and the recurrent
+ * state keeps their influence). A full refill is the same call on empty contexts
+ * (len 0) with zero states.
  * Delta layers read nothing the attention path writes, so they run concurrently
  * with it on a side stream of the current device (one per calling thread, created on
  * first use, default priority), forked after the work already queued on `stream`

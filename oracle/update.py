@@ -27,13 +27,19 @@ from .rope import rope_rotate
 
 def attention_layer_update(pos, k_cache, v_cache, ranges, cursor: int, q, k, v, rotary_dim: int,
                            theta: float, scale: float, live: Optional[Sequence[int]] = None,
-                           rows: Optional[Sequence[int]] = None):
+                           rows: Optional[Sequence[int]] = None, post_ranges=None):
     """One attention layer of one character: Eq. 2 then the attention part of Eq. 3.
 
     pos: int [L_old] position of every cache row; k_cache, v_cache: bf16 bits
     [L_old, Hkv, D]; ranges: [n, 2] half-open position ranges to remove;
     q: bf16 bits [T, Hq, D]; k, v: bf16 bits [T, Hkv, D] (k before rotation).
     `live`, when given, is checked against the ranges first (Section 4.2).
+
+    post_ranges: [m, 2] position ranges inside the tail [cursor, cursor + T) whose
+    rows are removed after the tail is processed (Section 4.1: temporary maintenance
+    delimiters, processed and then dropped from the retained KV). Every tail row is
+    still computed and attended to first; only the returned cache, positions and
+    cursor reflect the removal (the cursor still advances by T).
     """
     if live is not None:
         validate_ranges(ranges, live, cursor)
@@ -47,10 +53,20 @@ def attention_layer_update(pos, k_cache, v_cache, ranges, cursor: int, q, k, v, 
     v_all = np.concatenate([np.asarray(v_cache)[src_index], np.asarray(v, dtype=np.uint16)], axis=0)
     out = causal_gqa_attention(bf16_to_f64(q_hat), bf16_to_f64(k_all), bf16_to_f64(v_all), L_keep,
                                scale, rows=rows)
+    final_pos = np.concatenate([kept_pos, tail_pos])
+    post_index = np.arange(len(final_pos))
+    if post_ranges is not None and len(post_ranges):
+        post = np.asarray(post_ranges, dtype=np.int64).reshape(-1, 2)
+        if np.any(post[:, 0] < cursor) or np.any(post[:, 1] > cursor + T):
+            raise ValueError("post-prefill ranges must lie inside the tail")
+        validate_ranges([tuple(r) for r in post], final_pos.tolist(), cursor + T)
+        post_index, final_pos = compact(final_pos, [tuple(r) for r in post])
+        k_all, v_all = k_all[post_index], v_all[post_index]
     return {
         "src_index": src_index,
         "L_keep": L_keep,
-        "pos": np.concatenate([kept_pos, tail_pos]),
+        "pos": np.asarray(final_pos),
+        "post_index": np.asarray(post_index),
         "k_cache": k_all,
         "v_cache": v_all,
         "q_hat": q_hat,

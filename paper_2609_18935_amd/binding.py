@@ -54,7 +54,7 @@ class tu_delta_params(ctypes.Structure):
 
 class tu_seq_update(ctypes.Structure):
     _fields_ = [("seq", ctypes.POINTER(tu_seq)), ("ranges", ctypes.POINTER(_i64)), ("n_ranges", _i32),
-                ("T", _i64), ("src_index", _vp)]
+                ("T", _i64), ("src_index", _vp), ("post_ranges", ctypes.POINTER(_i64)), ("n_post_ranges", _i32)]
 
 
 class tu_layer_io(ctypes.Structure):
@@ -99,6 +99,7 @@ _SIGNATURES = {
 }
 
 _lib_handle = None
+ABI_VERSION = 2   # TU_ABI_VERSION of include/tailupdate.h that these structures follow
 
 
 def lib():
@@ -112,6 +113,9 @@ def lib():
             fn = getattr(h, name)
             fn.restype = res
             fn.argtypes = args
+        if h.tu_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI version {h.tu_abi_version()}, this binding expects {ABI_VERSION}:"
+                               " rebuild it")
         _lib_handle = h
     return _lib_handle
 
@@ -307,7 +311,9 @@ class StackUpdate:
 
     def __init__(self, contexts: Sequence[Context], ranges: Sequence, tails: Sequence[int], layers: Sequence[LayerIO],
                  attn: Optional[tu_attn_params] = None, delta: Optional[tu_delta_params] = None,
-                 src_index: Optional[Sequence[Optional[torch.Tensor]]] = None):
+                 src_index: Optional[Sequence[Optional[torch.Tensor]]] = None, post_ranges: Optional[Sequence] = None):
+        """post_ranges[s]: position ranges inside context s's tail whose rows are removed
+        once the tail is prefilled (maintenance delimiters), or None."""
         n = len(contexts)
         self.contexts = list(contexts)
         self._keep = []
@@ -316,7 +322,10 @@ class StackUpdate:
             arr, nr = _ranges_array(ranges[s])
             self._keep.append(arr)
             si = None if src_index is None else src_index[s]
-            self._seq_arr[s] = tu_seq_update(ctypes.pointer(ctx.c), arr, nr, int(tails[s]), _ptr(si))
+            pr = None if post_ranges is None or post_ranges[s] is None else post_ranges[s]
+            parr, npr = _ranges_array(pr if pr is not None else [])
+            self._keep.append(parr)
+            self._seq_arr[s] = tu_seq_update(ctypes.pointer(ctx.c), arr, nr, int(tails[s]), _ptr(si), parr, npr)
         self._layer_arr = (tu_layer_io * max(1, len(layers)))()
         for l, L in enumerate(layers):
             def plist(ts):
@@ -367,8 +376,8 @@ def profile_collect(max_entries: int = 32) -> dict:
 
 
 def update_layer_stack(contexts, ranges, tails, layers, attn=None, delta=None, workspace=None, stream=None,
-                       src_index=None):
-    up = StackUpdate(contexts, ranges, tails, layers, attn, delta, src_index)
+                       src_index=None, post_ranges=None):
+    up = StackUpdate(contexts, ranges, tails, layers, attn, delta, src_index, post_ranges)
     nbytes = up.workspace_size()
     dev = contexts[0].pos.device if contexts else "cuda"
     ws = _workspace(nbytes, dev, workspace)

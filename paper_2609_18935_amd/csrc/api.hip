@@ -198,6 +198,7 @@ struct CompactItem {
   RangeCheck rc;
   int32_t* src_index;        // device, caller's or workspace
   bool user_index = false;   // the caller asked for src_index
+  bool scan = true;          // run the keep-scan (src_index, position check)
   std::vector<void*> bufs;   // K and V of every attention layer
 };
 
@@ -234,7 +235,7 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
     for (int i = 0; i < (int)items.size(); ++i) {
       const auto& it = items[i];
       const bool moves = it.rc.removed > 0 && it.seq->len - it.rc.removed > it.rc.first_row && !it.bufs.empty();
-      const bool scans = it.seq->len > 0 && (it.rc.removed > 0 || it.user_index);
+      const bool scans = it.scan && it.seq->len > 0 && (it.rc.removed > 0 || it.user_index);
       if (!moves && !scans) continue;
       int b0 = 0;
       bool first = true;
@@ -583,8 +584,12 @@ int commit_intervals(tu_seq* s, const std::vector<tu_interval>& iv) {
 
 struct StackPlan {
   std::vector<RangeCheck> rc;
-  std::vector<std::vector<tu_interval>> final_iv;
+  std::vector<std::vector<tu_interval>> final_iv;   // after the tail is appended
   std::vector<int64_t> tail_begin;   // row offset of each context in the packed tail inputs
+  // removal of rows inside the tail once it is prefilled (maintenance delimiters)
+  std::vector<RangeCheck> post_rc;
+  std::vector<tu_seq> post_seq;      // each context as it stands after the append
+  bool any_post = false;
   int n_attn = 0, n_delta = 0;
 };
 
@@ -595,6 +600,9 @@ int validate_stack(const tu_update* u, StackPlan* sp) {
   sp->rc.assign(u->n_seq, RangeCheck{});
   sp->final_iv.assign(u->n_seq, {});
   sp->tail_begin.assign(u->n_seq + 1, 0);
+  sp->post_rc.assign(u->n_seq, RangeCheck{});
+  sp->post_seq.assign(u->n_seq, tu_seq{});
+  sp->any_post = false;
   for (int l = 0; l < u->n_layers; ++l) {
     const int kind = u->layers[l].kind;
     if (kind == TU_LAYER_ATTN) ++sp->n_attn;
@@ -620,6 +628,23 @@ int validate_stack(const tu_update* u, StackPlan* sp) {
     append_tail(sp->final_iv[s], su.seq->next_pos, su.T);
     if ((int64_t)sp->final_iv[s].size() > su.seq->live_cap)
       return fail(TU_ERR_CAPACITY, "context %d: live-interval list would exceed %d", s, su.seq->live_cap);
+    // ranges removed after the prefill must lie inside this call's tail
+    tu_seq& ps = sp->post_seq[s];
+    ps = *su.seq;
+    ps.len = L_keep + su.T;
+    ps.next_pos = su.seq->next_pos + su.T;
+    ps.live = sp->final_iv[s].data();
+    ps.n_live = (int32_t)sp->final_iv[s].size();
+    if (su.n_post_ranges < 0 || (su.n_post_ranges > 0 && !su.post_ranges))
+      return fail(TU_ERR_ARG, "context %d: bad post-prefill ranges", s);
+    for (int q = 0; q < su.n_post_ranges; ++q)
+      if (su.post_ranges[2 * q] < su.seq->next_pos || su.post_ranges[2 * q + 1] > ps.next_pos)
+        return fail(TU_ERR_RANGE, "context %d: post-prefill range %d lies outside the tail [%lld, %lld)", s, q,
+                    (long long)su.seq->next_pos, (long long)ps.next_pos);
+    if (int e = check_ranges(&ps, su.post_ranges, su.n_post_ranges, &sp->post_rc[s])) return e;
+    if ((int64_t)sp->post_rc[s].live_after.size() > su.seq->live_cap)
+      return fail(TU_ERR_CAPACITY, "context %d: live-interval list would exceed %d", s, su.seq->live_cap);
+    sp->any_post = sp->any_post || sp->post_rc[s].removed > 0;
     sp->tail_begin[s + 1] = sp->tail_begin[s] + su.T;
   }
   const int64_t total_T = sp->tail_begin[u->n_seq];
@@ -648,6 +673,31 @@ int validate_stack(const tu_update* u, StackPlan* sp) {
     }
   }
   return TU_OK;
+}
+
+// Rows of the tail removed once it is prefilled: a second compaction of every
+// attention layer, against each context as it stands after the append (no keep-scan:
+// nothing reads its index list, and the tail positions were just written).
+std::vector<CompactItem> stack_post_items(const tu_update* u, StackPlan& sp) {
+  std::vector<CompactItem> items;
+  for (int s = 0; s < u->n_seq; ++s) {
+    const tu_seq_update& su = u->seqs[s];
+    if (sp.post_rc[s].removed == 0) continue;
+    CompactItem it;
+    it.seq = &sp.post_seq[s];
+    it.ranges = su.post_ranges;
+    it.n_ranges = su.n_post_ranges;
+    it.rc = sp.post_rc[s];
+    it.src_index = nullptr;
+    it.scan = false;
+    for (int l = 0; l < u->n_layers; ++l)
+      if (u->layers[l].kind == TU_LAYER_ATTN) {
+        it.bufs.push_back(u->layers[l].k_cache[s]);
+        it.bufs.push_back(u->layers[l].v_cache[s]);
+      }
+    items.push_back(it);
+  }
+  return items;
 }
 
 std::vector<CompactItem> stack_compact_items(const tu_update* u, const StackPlan& sp) {
@@ -957,7 +1007,7 @@ struct StackWorkspace {
   size_t total() const { return align_up(attn) + align_up(delta); }
 };
 
-StackWorkspace stack_workspace(const tu_update* u, const StackPlan& sp) {
+StackWorkspace stack_workspace(const tu_update* u, StackPlan& sp) {
   StackWorkspace w;
   w.attn = kAlign;
   if (sp.n_attn) {
@@ -965,6 +1015,11 @@ StackWorkspace stack_workspace(const tu_update* u, const StackPlan& sp) {
     CompactPlan cp;
     plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, nullptr, &cp);
     w.attn = std::max(w.attn, cp.ws_bytes);
+    if (sp.any_post) {
+      auto post = stack_post_items(u, sp);
+      plan_compaction(post, u->attn.n_kv_heads * u->attn.head_dim * 2, nullptr, &cp);
+      w.attn = std::max(w.attn, cp.ws_bytes);
+    }
   }
   for (int l = 0; l < u->n_layers; ++l) {
     size_t b = 0;
@@ -1084,6 +1139,14 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
     plan_attention(&u->attn, items, ws_attn, &ls, &b);
     if (int e = run_attention(ls, u->attn.head_dim, st)) return e;
   }
+  // rows of the tail removed once it is prefilled (maintenance delimiters): their
+  // direct KV goes, their effect on the recurrent state and on later rows stays
+  if (sp.n_attn && sp.any_post) {
+    auto items = stack_post_items(u, sp);
+    CompactPlan cp;
+    if (int e = plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, ws_attn, &cp)) return e;
+    if (int e = run_compaction(cp, st)) return e;
+  }
   if (side) {
     if (int e = hip_check(hipEventRecord(side->join, side->stream), "join event")) return e;
     if (int e = hip_check(hipStreamWaitEvent(st, side->join, 0), "join wait")) return e;
@@ -1091,8 +1154,9 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
   // a8: commit metadata
   for (int s = 0; s < u->n_seq; ++s) {
     tu_seq* seq = u->seqs[s].seq;
-    commit_intervals(seq, sp.final_iv[s]);
-    seq->len = seq->len - sp.rc[s].removed + u->seqs[s].T;
+    const bool post = sp.n_attn && sp.post_rc[s].removed > 0;
+    commit_intervals(seq, post ? sp.post_rc[s].live_after : sp.final_iv[s]);
+    seq->len = seq->len - sp.rc[s].removed + u->seqs[s].T - (post ? sp.post_rc[s].removed : 0);
     seq->next_pos += u->seqs[s].T;
   }
   return ok();

@@ -72,10 +72,11 @@ class AttnCase:
         self.out = torch.full((T, shape.n_q_heads, D), float("nan"), dtype=torch.float32, device=DEV)
         self.q_hat = torch.zeros((T, shape.n_q_heads, D), dtype=torch.bfloat16, device=DEV)
 
-    def oracle(self, ranges, cursor, rows=None):
+    def oracle(self, ranges, cursor, rows=None, post_ranges=None):
         s = self.shape
         return oracle.attention_layer_update(self.positions, self.k_bits, self.v_bits, ranges, cursor, self.q_t,
-                                             self.k_t, self.v_t, s.rdim, s.rope_theta, s.softmax_scale, rows=rows)
+                                             self.k_t, self.v_t, s.rdim, s.rope_theta, s.softmax_scale, rows=rows,
+                                             post_ranges=post_ranges)
 
 
 class DeltaCase:

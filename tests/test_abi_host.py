@@ -43,7 +43,10 @@ def test_header_functions_are_exported(L):
     for n in names:
         assert hasattr(L, n), f"{n} declared in tailupdate.h but not exported"
     assert set(names) == set(B._SIGNATURES), "binding signatures out of sync with the header"
-    assert L.tu_abi_version() == 1
+    import re
+    hdr = open(os.path.join(os.path.dirname(__file__), "..", "include", "tailupdate.h")).read()
+    declared = int(re.search(r"#define TU_ABI_VERSION (\d+)", hdr).group(1))
+    assert L.tu_abi_version() == declared == B.ABI_VERSION
 
 
 def _ctx(intervals, cursor, capacity=None, live_cap=64):
@@ -84,7 +87,7 @@ def test_validate_ranges_matches_oracle(L):
         assert (ctx.intervals(), ctx.len, ctx.next_pos) == before
 
 
-def _stack(ctx_list, ranges, tails, kinds, cap_ok=True):
+def _stack(ctx_list, ranges, tails, kinds, cap_ok=True, post=None):
     attn = tu.attn_params(16, 2, 256)
     delta = tu.delta_params(16, 32, 128, 128, 64)
     fake = torch.zeros(64, dtype=torch.float32)   # 16-byte aligned host buffer, never read
@@ -96,7 +99,7 @@ def _stack(ctx_list, ranges, tails, kinds, cap_ok=True):
         else:
             layers.append(tu.LayerIO(B.TU_LAYER_DELTA, fake, fake, fake, fake, state=[fake] * len(ctx_list),
                                      beta=fake, g=fake))
-    return tu.StackUpdate(ctx_list, ranges, tails, layers, attn, delta)
+    return tu.StackUpdate(ctx_list, ranges, tails, layers, attn, delta, post_ranges=post)
 
 
 def test_validate_update_accepts_and_sizes(L):
@@ -105,6 +108,11 @@ def test_validate_update_accepts_and_sizes(L):
     up = _stack([a, b], [[(100, 228)], [(30, 40), (300, 310)]], [512, 256], ["attn", "delta"])
     up.validate()
     assert up.workspace_size() > 0
+    # an opening and a closing maintenance delimiter inside each tail
+    up2 = _stack([a, b], [[(100, 228)], [(30, 40), (300, 310)]], [512, 256], ["attn", "delta"],
+                 post=[[(1000, 1011), (1509, 1512)], [(600, 611)]])
+    up2.validate()
+    assert up2.workspace_size() >= up.workspace_size()
 
 
 @pytest.mark.parametrize("case,code", [
@@ -114,6 +122,10 @@ def test_validate_update_accepts_and_sizes(L):
     ("duplicate_context", B.TU_ERR_ARG),
     ("bad_heads", B.TU_ERR_ARG),
     ("interval_list_full", B.TU_ERR_CAPACITY),
+    ("post_before_tail", B.TU_ERR_RANGE),
+    ("post_past_tail", B.TU_ERR_RANGE),
+    ("post_unsorted", B.TU_ERR_RANGE),
+    ("post_empty_range", B.TU_ERR_RANGE),
 ])
 def test_validate_update_rejects(L, case, code):
     a = _ctx([(0, 1000)], 1000, capacity=1600)
@@ -131,7 +143,16 @@ def test_validate_update_rejects(L, case, code):
         a = _ctx([(0, 1000)], 1000, capacity=1600, live_cap=2)
         ctxs = [a]
         ranges = [[(100, 110), (200, 210)]]
-    up = _stack(ctxs, ranges, tails, kinds)
+    post = None
+    if case == "post_before_tail":
+        post = [[(990, 1005)]]          # starts before the cursor
+    elif case == "post_past_tail":
+        post = [[(1500, 1513)]]         # the tail is [1000, 1512)
+    elif case == "post_unsorted":
+        post = [[(1100, 1110), (1000, 1011)]]
+    elif case == "post_empty_range":
+        post = [[(1000, 1000)]]
+    up = _stack(ctxs, ranges, tails, kinds, post=post)
     if case == "bad_heads":
         up.u.attn.n_q_heads = 15
     before = (a.intervals(), a.len, a.next_pos)

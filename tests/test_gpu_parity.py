@@ -257,6 +257,35 @@ def test_stack_update_cfg1_matches_oracle_and_commits():
     assert ctx.intervals() == synth.append_interval(synth.subtract_ranges(r.intervals, r.ranges), r.cursor, r.T)
 
 
+def test_stack_update_removes_delimiters_after_prefill():
+    # Section 4.1: an 11-token opening wrapper and a 3-token closing one are prefilled
+    # with the replacement, then their rows leave every attention cache
+    sc, r = _stack_case(1)
+    a, d = sc.cfg.attn, sc.cfg.delta
+    post = np.array([[r.cursor, r.cursor + 11], [r.cursor + r.T - 3, r.cursor + r.T]])
+    _say(f"stack cfg1 with post-prefill removal of {post.tolist()}")
+    ac = AttnCase(a, 0, 1, 0, r.L_old, r.T)
+    dc = DeltaCase(d, 0, 1, 1, r.T)
+    ctx = _ctx_for(ac)
+    layers = [tu.LayerIO(tu.TU_LAYER_ATTN, ac.q, ac.k, ac.v, ac.out, k_cache=[ac.k_cache], v_cache=[ac.v_cache]),
+              tu.LayerIO(tu.TU_LAYER_DELTA, dc.q, dc.k, dc.v, dc.out, state=[dc.state], beta=dc.beta_d, g=dc.g_d)]
+    tu.update_layer_stack([ctx], [r.ranges], [r.T], layers,
+                          tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta),
+                          tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk), post_ranges=[post])
+    torch.cuda.synchronize()
+    ref = ac.oracle(r.ranges, r.cursor, post_ranges=post)
+    n = r.L_keep + r.T - 14
+    assert ctx.len == n and ctx.next_pos == r.cursor + r.T
+    assert_close(ac.out.cpu().numpy(), ref["out"], "attention out of every tail row")
+    assert np.array_equal(ctx.pos[:n].cpu().numpy(), ref["pos"])
+    assert np.array_equal(bits_of(ac.v_cache[:n]), ref["v_cache"])
+    assert_bf16_close_bits(bits_of(ac.k_cache[:n]), ref["k_cache"], "retained K cache")
+    o_ref, S_ref = dc.oracle()
+    assert_close(dc.state.cpu().numpy(), S_ref, "delta state keeps the delimiters' influence")
+    iv = synth.append_interval(synth.subtract_ranges(r.intervals, r.ranges), r.cursor, r.T)
+    assert ctx.intervals() == synth.subtract_ranges(iv, post)
+
+
 def test_stack_is_deterministic():
     sc, r = _stack_case(1)
     a, d = sc.cfg.attn, sc.cfg.delta

@@ -132,3 +132,40 @@ def test_tail_rows_equal_gapped_refill():
     np.testing.assert_allclose(upd["out"], g_out[-T:], rtol=1e-12, atol=1e-13)
     assert np.array_equal(upd["k_cache"], g_khat)
     assert np.array_equal(upd["pos"], final_pos)
+
+
+def test_post_prefill_delimiter_removal():
+    # Section 4.1: maintenance delimiters are processed with the tail, then their direct
+    # KV is removed. The retained cache must be the surviving rows plus the rotated keys
+    # and values of the non-delimiter tail tokens at their own tail positions, built
+    # here without the compaction routine; outputs are those of the full tail.
+    rng = np.random.default_rng(15)
+    L, T, Hq, Hkv, D, theta = 30, 12, 4, 2, 16, 1.0e7
+    scale = D ** -0.5
+    q, k, v = _raw_context(rng, L, Hq, Hkv, D)
+    pos = np.arange(L)
+    cache_k = oracle.f64_to_bf16(oracle.rope_rotate(oracle.bf16_to_f64(k), pos, D, theta))
+    tq, tk, tv = _raw_context(rng, T, Hq, Hkv, D)
+    ranges = np.array([[3, 7]])
+    cursor = L
+    post = np.array([[cursor, cursor + 2], [cursor + 9, cursor + 12]])   # an opening and a closing wrapper
+    plain = oracle.attention_layer_update(pos, cache_k, v, ranges, cursor, tq, tk, tv, D, theta, scale)
+    upd = oracle.attention_layer_update(pos, cache_k, v, ranges, cursor, tq, tk, tv, D, theta, scale,
+                                        post_ranges=post)
+    assert np.array_equal(upd["out"], plain["out"])
+    keep_tail = np.ones(T, bool)
+    keep_tail[0:2] = False
+    keep_tail[9:12] = False
+    tail_pos = cursor + np.arange(T)
+    kh = oracle.f64_to_bf16(oracle.rope_rotate(oracle.bf16_to_f64(tk[keep_tail]), tail_pos[keep_tail], D, theta))
+    survivors = np.concatenate([np.arange(0, 3), np.arange(7, L)])
+    assert np.array_equal(upd["k_cache"], np.concatenate([cache_k[survivors], kh]))
+    assert np.array_equal(upd["v_cache"], np.concatenate([v[survivors], tv[keep_tail]]))
+    assert np.array_equal(upd["pos"], np.concatenate([survivors, tail_pos[keep_tail]]))
+    assert upd["cursor"] == cursor + T                       # delimiter positions become holes
+    empty = oracle.attention_layer_update(pos, cache_k, v, ranges, cursor, tq, tk, tv, D, theta, scale,
+                                          post_ranges=np.zeros((0, 2), np.int64))
+    assert np.array_equal(empty["k_cache"], plain["k_cache"]) and np.array_equal(empty["pos"], plain["pos"])
+    with pytest.raises(ValueError):
+        oracle.attention_layer_update(pos, cache_k, v, ranges, cursor, tq, tk, tv, D, theta, scale,
+                                      post_ranges=np.array([[cursor - 1, cursor + 1]]))
