@@ -37,7 +37,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=1, choices=[0, 1, 3, 4])
+    ap.add_argument("--config", type=int, default=1, choices=[0, 1, 2, 3, 4])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--refill-steps", type=int, default=5)
     ap.add_argument("--no-refill", action="store_true")
@@ -81,7 +81,11 @@ class DevRng:
 
 
 def build_workload(cfg, seed, device):
-    """Per-context plans plus pristine device buffers and packed tail inputs."""
+    """Per-context plans plus pristine device buffers and packed tail inputs of every round.
+
+    chars[c]: the context's initial state (L_old, intervals, cursor) and capacity;
+    rounds[r]: per context the removal ranges, tail length and surviving rows of round
+    r, and per layer that round's packed tail inputs."""
     import torch
     import synth
     sc = synth.make_scenario(cfg.index, seed=seed)
@@ -90,29 +94,40 @@ def build_workload(cfg, seed, device):
     kinds = cfg.layer_kinds()
     chars = []
     for ch in sc.chars:
-        r = ch.rounds[0]
-        chars.append({"L_old": r.L_old, "L_keep": r.L_keep, "T": r.T, "ranges": r.ranges, "cursor": r.cursor,
-                      "intervals": r.intervals, "cap": max(r.L_old, r.L_keep + r.T)})
-    sumT = sum(c["T"] for c in chars)
+        r0 = ch.rounds[0]
+        cap = max([r0.L_old] + [r.L_keep + r.T for r in ch.rounds])
+        chars.append({"L_old": r0.L_old, "cursor": r0.cursor, "intervals": r0.intervals, "cap": cap})
+    rounds = []
+    for ri in range(len(sc.chars[0].rounds)):
+        rr = [ch.rounds[ri] for ch in sc.chars]
+        sumT = sum(r.T for r in rr)
+        inputs = []
+        for kind in kinds:
+            if kind == "attn":
+                inputs.append({"q": rng.bf16((sumT, a.n_q_heads, a.head_dim)),
+                               "k": rng.bf16((sumT, a.n_kv_heads, a.head_dim)),
+                               "v": rng.bf16((sumT, a.n_kv_heads, a.head_dim)),
+                               "out": torch.empty((sumT, a.n_q_heads, a.head_dim), dtype=torch.float32,
+                                                  device=device)})
+            else:
+                inputs.append({"q": rng.bf16((sumT, d.n_k_heads, d.d_k)),
+                               "k": rng.unit_bf16((sumT, d.n_k_heads, d.d_k)),
+                               "v": rng.bf16((sumT, d.n_v_heads, d.d_v)),
+                               "beta": rng.beta((sumT, d.n_v_heads)), "g": rng.gate((sumT, d.n_v_heads)),
+                               "out": torch.empty((sumT, d.n_v_heads, d.d_v), dtype=torch.float32, device=device)})
+        rounds.append({"ranges": [r.ranges for r in rr], "T": [r.T for r in rr], "L_keep": [r.L_keep for r in rr],
+                       "L_old": [r.L_old for r in rr], "cursor": [r.cursor for r in rr],
+                       "intervals": [r.intervals for r in rr], "inputs": inputs})
     layers = []
     for kind in kinds:
         if kind == "attn":
-            caches = [(rng.bf16((c["cap"], a.n_kv_heads, a.head_dim)), rng.bf16((c["cap"], a.n_kv_heads, a.head_dim)))
-                      for c in chars]
-            layers.append({"kind": "attn", "caches": caches,
-                           "q": rng.bf16((sumT, a.n_q_heads, a.head_dim)),
-                           "k": rng.bf16((sumT, a.n_kv_heads, a.head_dim)),
-                           "v": rng.bf16((sumT, a.n_kv_heads, a.head_dim)),
-                           "out": torch.empty((sumT, a.n_q_heads, a.head_dim), dtype=torch.float32, device=device)})
+            layers.append({"kind": "attn",
+                           "caches": [(rng.bf16((c["cap"], a.n_kv_heads, a.head_dim)),
+                                       rng.bf16((c["cap"], a.n_kv_heads, a.head_dim))) for c in chars]})
         else:
             layers.append({"kind": "delta",
-                           "states": [rng.normal((d.n_v_heads, d.d_v, d.d_k), std=0.1) for _ in chars],
-                           "q": rng.bf16((sumT, d.n_k_heads, d.d_k)),
-                           "k": rng.unit_bf16((sumT, d.n_k_heads, d.d_k)),
-                           "v": rng.bf16((sumT, d.n_v_heads, d.d_v)),
-                           "beta": rng.beta((sumT, d.n_v_heads)), "g": rng.gate((sumT, d.n_v_heads)),
-                           "out": torch.empty((sumT, d.n_v_heads, d.d_v), dtype=torch.float32, device=device)})
-    return sc, chars, layers, rng
+                           "states": [rng.normal((d.n_v_heads, d.d_v, d.d_k), std=0.1) for _ in chars]})
+    return sc, chars, rounds, layers, rng
 
 
 def make_copy(tu, chars, layers, device, pristine=True):
@@ -133,47 +148,51 @@ def make_copy(tu, chars, layers, device, pristine=True):
     return ctxs, own
 
 
-def stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p, tails=None, inputs=None, ranges=None, post=None):
+def stack_update(tu, ctxs, own, layers, inputs, ranges, tails, attn_p, delta_p, post=None):
     ios = []
-    for L, O in zip(layers, own):
-        src = inputs[id(L)] if inputs is not None else L
+    for L, O, src in zip(layers, own, inputs):
         if L["kind"] == "attn":
             ios.append(tu.LayerIO(tu.TU_LAYER_ATTN, src["q"], src["k"], src["v"], src["out"],
                                   k_cache=[k for (k, _) in O["caches"]], v_cache=[v for (_, v) in O["caches"]]))
         else:
             ios.append(tu.LayerIO(tu.TU_LAYER_DELTA, src["q"], src["k"], src["v"], src["out"], state=O["states"],
                                   beta=src["beta"], g=src["g"]))
-    rr = ranges if ranges is not None else [c["ranges"] for c in chars]
-    tt = tails if tails is not None else [c["T"] for c in chars]
-    return tu.StackUpdate(ctxs, rr, tt, ios, attn_p, delta_p, post_ranges=post)
+    return tu.StackUpdate(ctxs, ranges, tails, ios, attn_p, delta_p, post_ranges=post)
+
+
+def round_updates(tu, ctxs, own, layers, rounds, attn_p, delta_p, post=None):
+    """The prepared calls of one step: every round of the workload, in order, on one copy."""
+    return [stack_update(tu, ctxs, own, layers, R["inputs"], R["ranges"], R["T"], attn_p, delta_p,
+                         post=None if post is None else post(R)) for R in rounds]
 
 
 # ----------------------------------------------------------------------------- algorithmic work
 
-def attention_flops(cfg, chars):
+def attention_flops(cfg, rounds):
     a = cfg.attn
-    return sum(4.0 * a.n_q_heads * a.head_dim * (c["T"] * c["L_keep"] + c["T"] * (c["T"] + 1) / 2.0)
-               for c in chars)
+    return sum(4.0 * a.n_q_heads * a.head_dim * (T * Lk + T * (T + 1) / 2.0)
+               for R in rounds for T, Lk in zip(R["T"], R["L_keep"]))
 
 
-def delta_bytes(cfg, chars):
+def delta_bytes(cfg, rounds):
     d = cfg.delta
     per_tok = d.n_k_heads * d.d_k * 2 * 2 + d.n_v_heads * d.d_v * 2 + d.n_v_heads * 8 + d.n_v_heads * d.d_v * 4
     state = d.n_v_heads * d.d_v * d.d_k * 4 * 2
-    return sum(c["T"] * per_tok + state for c in chars)
+    return sum(T * per_tok + state for R in rounds for T in R["T"])
 
 
-def gather_bytes(cfg, chars):
+def gather_bytes(cfg, rounds):
     """Minimum: every surviving row behind the first hole is read and written once."""
     a = cfg.attn
     row = a.n_kv_heads * a.head_dim * 2
     total = 0
-    for c in chars:
-        if len(c["ranges"]) == 0:
-            continue
-        first = int(c["ranges"][0][0])   # positions are 0..L_old-1 at round 0, so position == row
-        moved = c["L_keep"] - first
-        total += 2 * 2 * moved * row     # K and V, read + write
+    for R in rounds:
+        for rng_, Lk, iv in zip(R["ranges"], R["L_keep"], R["intervals"]):
+            if len(rng_) == 0:
+                continue
+            p = int(rng_[0][0])
+            first = sum(max(0, min(e, p) - s) for (s, e) in iv)   # live rows below the first removed position
+            total += 2 * 2 * (Lk - first) * row                    # K and V, read + write
     return total
 
 
@@ -224,13 +243,15 @@ def cpu_baseline(cfg, seed, budget_s):
     n_attn = kinds.count("attn")
     n_delta = kinds.count("delta")
     per_char = n_attn * min(t_attn) + n_delta * min(t_delta)
-    total_T = sum(c.rounds[0].T for c in sc.chars)
-    # other contexts scale with their attention work and tail length
-    scale = total_T / r.T if len(sc.chars) > 1 else 1.0
+    total_T = sum(rd.T for c in sc.chars for rd in c.rounds)
+    # other contexts and later rounds scale with their tail length
+    scale = total_T / r.T
     secs = per_char * scale
-    sample = (f"context 0 of the workload: attention layer rows {len(rows)}/{r.T}, delta tokens {toks}/{r.T}, "
-              f"{reps} repetitions (best), scaled to {n_attn} attention + {n_delta} delta layers"
-              + (f" and {len(sc.chars)} contexts by tail length" if len(sc.chars) > 1 else ""))
+    n_rounds = len(sc.chars[0].rounds)
+    sample = (f"round 0 of context 0 of the workload: attention layer rows {len(rows)}/{r.T}, delta tokens "
+              f"{toks}/{r.T}, {reps} repetitions (best), scaled to {n_attn} attention + {n_delta} delta layers"
+              + (f" and {len(sc.chars)} contexts by tail length" if len(sc.chars) > 1 else "")
+              + (f" and {n_rounds} rounds by tail length" if n_rounds > 1 else ""))
     return {"value": total_T / secs, "unit": "tail tokens/s", "cores": int(blas_threads), "kind": "oracle",
             "sample": sample, "seconds_per_update": secs}
 
@@ -348,51 +369,85 @@ def main():
     attn_p = tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta, a.softmax_scale,
                             kv_splits=args.kv_splits)
     delta_p = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
-    sc, chars, layers, rng = build_workload(cfg, args.seed, dev)
+    sc, chars, rounds, layers, rng = build_workload(cfg, args.seed, dev)
     W, K = args.warmup, args.steps
+    n_rounds = len(rounds)
+    sumT = sum(sum(R["T"]) for R in rounds)
     print(f"[bench] config {cfg.index} ({cfg.name}): {len(chars)} context(s), {len(layers)} layers, "
-          f"sum T = {sum(c['T'] for c in chars)}", file=sys.stderr, flush=True)
+          f"{n_rounds} round(s), sum T = {sumT}", file=sys.stderr, flush=True)
 
-    # ---- update: one pristine copy per step
+    def workspace_for(ctxs, ups):
+        """Largest workspace any round of a step needs (each round sized on its own metadata)."""
+        n = 0
+        for R, u in zip(rounds, ups):
+            for c, ctx in enumerate(ctxs):
+                ctx.set_metadata(R["intervals"][c], R["cursor"][c])
+            n = max(n, u.workspace_size())
+        for c, ctx in enumerate(ctxs):
+            ctx.set_metadata(chars[c]["intervals"], chars[c]["cursor"])
+        return n
+
+    def run_step(ups, ws, per_round=None):
+        for i, u in enumerate(ups):
+            u.run(ws)
+            if per_round is not None:
+                per_round[i].record()
+
+    # ---- update: one pristine copy per step; a step is every round of the workload
     copies = [make_copy(tu, chars, layers, dev) for _ in range(W + K)]
-    ups = [stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p) for (ctxs, own) in copies]
-    ws = torch.empty(max(u.workspace_size() for u in ups), dtype=torch.uint8, device=dev)
+    ups = [round_updates(tu, ctxs, own, layers, rounds, attn_p, delta_p) for (ctxs, own) in copies]
+    ws = torch.empty(workspace_for(copies[0][0], ups[0]), dtype=torch.uint8, device=dev)
     for i in range(W):
-        ups[i].run(ws)
+        run_step(ups[i], ws)
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     h0 = time.perf_counter()
     ev0.record()
     for i in range(W, W + K):
-        ups[i].run(ws)
+        run_step(ups[i], ws)
     ev1.record()
     torch.cuda.synchronize()
     h1 = time.perf_counter()
     upd_ms = ev0.elapsed_time(ev1) / K
     print(f"[bench] update: {upd_ms:.4f} ms/step (host {1e3 * (h1 - h0) / K:.4f})", file=sys.stderr, flush=True)
+    del copies, ups
+    round_ms = None
+    if n_rounds > 1:
+        # per-round durations, from events between the rounds of the same steps
+        copies = [make_copy(tu, chars, layers, dev) for _ in range(K)]
+        ups = [round_updates(tu, ctxs, own, layers, rounds, attn_p, delta_p) for (ctxs, own) in copies]
+        torch.cuda.synchronize()
+        marks = [[torch.cuda.Event(enable_timing=True) for _ in rounds] for _ in range(K)]
+        starts = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+        for i in range(K):
+            starts[i].record()
+            run_step(ups[i], ws, marks[i])
+        torch.cuda.synchronize()
+        round_ms = [sorted(((marks[i][r - 1] if r else starts[i]).elapsed_time(marks[i][r]) for i in range(K)))[K // 2]
+                    for r in range(n_rounds)]
+        del copies, ups
 
     # ---- profiled pass over the same steps (fresh copies), per-kernel HIP events
     copies2 = [make_copy(tu, chars, layers, dev) for _ in range(K)]
-    ups2 = [stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p) for (ctxs, own) in copies2]
+    ups2 = [round_updates(tu, ctxs, own, layers, rounds, attn_p, delta_p) for (ctxs, own) in copies2]
     torch.cuda.synchronize()
     tu.profile_enable(True)
     for u in ups2:
-        u.run(ws)
+        run_step(u, ws)
     prof = tu.profile_collect()
     tu.profile_enable(False)
     del copies2, ups2
     kern = {n: {"launches_per_step": c / K, "avg_ms": t / c, "ms_per_step": t / K} for n, (c, t) in prof.items()}
     print(f"[bench] kernels: {json.dumps(kern)}", file=sys.stderr, flush=True)
 
-    sumT = sum(c["T"] for c in chars)
     kinds = cfg.layer_kinds()
     # algorithmic work per step of each stage, and the kernels that carry it
     work = {
         "attention": (["rope_vt_pack", "attention", "attention_merge"], "mfma",
-                      attention_flops(cfg, chars) * kinds.count("attn") / 1e12, "TFLOP/s", MFMA16_PEAK_TFLOPS),
-        "delta": (["delta_prep", "delta_chain"], "hbm", delta_bytes(cfg, chars) * kinds.count("delta") / 1e9, "GB/s",
-                  HBM_PEAK_GBS),
-        "compaction": (["compact"], "hbm", gather_bytes(cfg, chars) * kinds.count("attn") / 1e9, "GB/s",
+                      attention_flops(cfg, rounds) * kinds.count("attn") / 1e12, "TFLOP/s", MFMA16_PEAK_TFLOPS),
+        "delta": (["delta_prep", "delta_chain"], "hbm", delta_bytes(cfg, rounds) * kinds.count("delta") / 1e9,
+                  "GB/s", HBM_PEAK_GBS),
+        "compaction": (["compact"], "hbm", gather_bytes(cfg, rounds) * kinds.count("attn") / 1e9, "GB/s",
                        HBM_PEAK_GBS),
     }
     stages = {}
@@ -421,87 +476,95 @@ def main():
         roofline["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
         roofline["traffic_detail"] = traffic
 
-    # ---- full refill of the same final context through the same kernels
+    # ---- full refill, through the same kernels, of the live context after every round
+    # (zero recurrent state, contiguous positions from 0, fresh caches); the speedup is
+    # the summed refill time over the summed update time
     refill = None
     if not args.no_refill and args.refill_steps > 0:
-        N = [c["L_keep"] + c["T"] for c in chars]
-        sumN = sum(N)
-        rin = {}
-        for L in layers:
-            if L["kind"] == "attn":
-                rin[id(L)] = {"q": rng.bf16((sumN, a.n_q_heads, a.head_dim)),
-                              "k": rng.bf16((sumN, a.n_kv_heads, a.head_dim)),
-                              "v": rng.bf16((sumN, a.n_kv_heads, a.head_dim)),
-                              "out": torch.empty((sumN, a.n_q_heads, a.head_dim), dtype=torch.float32, device=dev)}
-            else:
-                rin[id(L)] = {"q": rng.bf16((sumN, d.n_k_heads, d.d_k)), "k": rng.unit_bf16((sumN, d.n_k_heads, d.d_k)),
-                              "v": rng.bf16((sumN, d.n_v_heads, d.d_v)), "beta": rng.beta((sumN, d.n_v_heads)),
-                              "g": rng.gate((sumN, d.n_v_heads)),
-                              "out": torch.empty((sumN, d.n_v_heads, d.d_v), dtype=torch.float32, device=dev)}
-        rchars = [dict(c, L_old=0, intervals=[], cursor=0, cap=n) for c, n in zip(chars, N)]
-        # refill writes every cache row and starts from zero states: buffers are shared, states zeroed per step
-        own = []
-        for L in layers:
-            if L["kind"] == "attn":
-                own.append({"caches": [(torch.empty((n, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev),
-                                        torch.empty((n, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev))
-                                       for n in N]})
-            else:
-                own.append({"states": None})
-        R = args.refill_steps
-        rups = []
-        for i in range(R + 1):
-            ctxs = []
-            for c in rchars:
-                ctx = tu.Context(c["cap"], device=dev)
-                ctx.set_metadata([], 0)
-                ctxs.append(ctx)
-            own_i = []
-            for L, O in zip(layers, own):
+        R_ = args.refill_steps
+        refill_rounds = []
+        for ri, R in enumerate(rounds):
+            N = [Lk + T for Lk, T in zip(R["L_keep"], R["T"])]
+            sumN = sum(N)
+            rin = []
+            for L in layers:
                 if L["kind"] == "attn":
-                    own_i.append(O)
+                    rin.append({"q": rng.bf16((sumN, a.n_q_heads, a.head_dim)),
+                                "k": rng.bf16((sumN, a.n_kv_heads, a.head_dim)),
+                                "v": rng.bf16((sumN, a.n_kv_heads, a.head_dim)),
+                                "out": torch.empty((sumN, a.n_q_heads, a.head_dim), dtype=torch.float32, device=dev)})
                 else:
-                    own_i.append({"states": [torch.zeros((d.n_v_heads, d.d_v, d.d_k), dtype=torch.float32, device=dev)
-                                             for _ in chars]})
-            rups.append(stack_update(tu, ctxs, own_i, rchars, layers, attn_p, delta_p, tails=N, inputs=rin,
-                                     ranges=[np.zeros((0, 2), np.int64)] * len(chars)))
-        rws = torch.empty(max(u.workspace_size() for u in rups), dtype=torch.uint8, device=dev)
-        rups[0].run(rws)
-        torch.cuda.synchronize()
-        ev0.record()
-        for u in rups[1:]:
-            u.run(rws)
-        ev1.record()
-        torch.cuda.synchronize()
-        refill_ms = ev0.elapsed_time(ev1) / R
-        refill = {"ms": refill_ms, "tokens": sumN, "speedup": refill_ms / upd_ms}
-        print(f"[bench] refill: {refill_ms:.4f} ms ({sumN} tokens), speedup {refill_ms / upd_ms:.2f}x",
-              file=sys.stderr, flush=True)
-        del rups, rin, own, rws
+                    rin.append({"q": rng.bf16((sumN, d.n_k_heads, d.d_k)),
+                                "k": rng.unit_bf16((sumN, d.n_k_heads, d.d_k)),
+                                "v": rng.bf16((sumN, d.n_v_heads, d.d_v)), "beta": rng.beta((sumN, d.n_v_heads)),
+                                "g": rng.gate((sumN, d.n_v_heads)),
+                                "out": torch.empty((sumN, d.n_v_heads, d.d_v), dtype=torch.float32, device=dev)})
+            # refill writes every cache row and starts from zero states: caches are shared
+            # by the repetitions, states are zeroed per repetition
+            caches = [[(torch.empty((n, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev),
+                        torch.empty((n, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev)) for n in N]
+                      if L["kind"] == "attn" else None for L in layers]
+            rups = []
+            for i in range(R_ + 1):
+                ctxs = []
+                for n in N:
+                    ctx = tu.Context(n, device=dev)
+                    ctx.set_metadata([], 0)
+                    ctxs.append(ctx)
+                own_i = [{"caches": C} if L["kind"] == "attn" else
+                         {"states": [torch.zeros((d.n_v_heads, d.d_v, d.d_k), dtype=torch.float32, device=dev)
+                                     for _ in N]} for L, C in zip(layers, caches)]
+                rups.append(stack_update(tu, ctxs, own_i, layers, rin, [np.zeros((0, 2), np.int64)] * len(N), N,
+                                         attn_p, delta_p))
+            rws = torch.empty(max(u.workspace_size() for u in rups), dtype=torch.uint8, device=dev)
+            rups[0].run(rws)
+            torch.cuda.synchronize()
+            ev0.record()
+            for u in rups[1:]:
+                u.run(rws)
+            ev1.record()
+            torch.cuda.synchronize()
+            refill_rounds.append({"tokens": sumN, "ms": ev0.elapsed_time(ev1) / R_})
+            del rups, rin, caches, rws
+        refill_ms = sum(x["ms"] for x in refill_rounds)
+        refill = {"ms": refill_ms, "tokens": sum(x["tokens"] for x in refill_rounds), "speedup": refill_ms / upd_ms}
+        if n_rounds > 1:
+            refill["rounds"] = [{"tail": sum(R["T"]), "live_after": x["tokens"], "update_ms": round(um, 5),
+                                 "refill_ms": round(x["ms"], 5), "speedup": round(x["ms"] / um, 3)}
+                                for R, x, um in zip(rounds, refill_rounds, round_ms)]
+        print(f"[bench] refill: {refill_ms:.4f} ms ({refill['tokens']} tokens over {n_rounds} round(s)), "
+              f"speedup {refill_ms / upd_ms:.2f}x", file=sys.stderr, flush=True)
 
     # ---- the same update with an 11-token opening and a 3-token closing maintenance
     # delimiter in every tail, removed from the caches once the tail is prefilled
     extra = {}
-    if kinds.count("attn") and all(c["T"] >= 14 for c in chars):
-        post = [np.array([[c["cursor"], c["cursor"] + 11], [c["cursor"] + c["T"] - 3, c["cursor"] + c["T"]]])
-                for c in chars]
+    if kinds.count("attn") and all(T >= 14 for R in rounds for T in R["T"]):
+        def post(R):
+            return [np.array([[c0, c0 + 11], [c0 + T - 3, c0 + T]]) for c0, T in zip(R["cursor"], R["T"])]
+        # later rounds' removal ranges were drawn without delimiter holes; only the first
+        # round of each context is run with delimiters
+        rd = rounds[:1]
         copies3 = [make_copy(tu, chars, layers, dev) for _ in range(W + K)]
-        ups3 = [stack_update(tu, ctxs, own, chars, layers, attn_p, delta_p, post=post) for (ctxs, own) in copies3]
-        ws3 = torch.empty(max(u.workspace_size() for u in ups3), dtype=torch.uint8, device=dev)
+        ups3 = [round_updates(tu, ctxs, own, layers, rd, attn_p, delta_p, post=post) for (ctxs, own) in copies3]
+        plain = [round_updates(tu, ctxs, own, layers, rd, attn_p, delta_p) for (ctxs, own) in copies3]
+        ws3 = torch.empty(max(ups3[0][0].workspace_size(), plain[0][0].workspace_size()), dtype=torch.uint8,
+                          device=dev)
+        del plain
         for i in range(W):
-            ups3[i].run(ws3)
+            run_step(ups3[i], ws3)
         torch.cuda.synchronize()
         ev0.record()
         for i in range(W, W + K):
-            ups3[i].run(ws3)
+            run_step(ups3[i], ws3)
         ev1.record()
         torch.cuda.synchronize()
         post_ms = ev0.elapsed_time(ev1) / K
+        first_ms = round_ms[0] if round_ms else upd_ms
         row_b = a.n_kv_heads * a.head_dim * 2
-        moved = sum(c["T"] - 11 - 3 for c in chars)   # tail rows behind the first delimiter that survive
+        moved = sum(T - 11 - 3 for T in rd[0]["T"])   # tail rows behind the first delimiter that survive
         extra["delimiter_removal"] = {
-            "removed_rows_per_context": 14, "update_ms_with": round(post_ms, 5), "update_ms_without": round(upd_ms, 5),
-            "extra_ms": round(post_ms - upd_ms, 5),
+            "removed_rows_per_context": 14, "rounds": 1, "update_ms_with": round(post_ms, 5),
+            "update_ms_without": round(first_ms, 5), "extra_ms": round(post_ms - first_ms, 5),
             "bytes": 2 * 2 * moved * row_b * kinds.count("attn"), "bound": "hbm"}
         print(f"[bench] delimiter removal: {json.dumps(extra['delimiter_removal'])}", file=sys.stderr, flush=True)
         del copies3, ups3, ws3
@@ -543,8 +606,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"config {cfg.index}: {cfg.name}", "contexts": len(chars), "layers": len(layers),
                    "attention_layers": kinds.count("attn"), "delta_layers": kinds.count("delta"),
-                   "tail_tokens": sumT, "surviving_rows": [c["L_keep"] for c in chars][:4],
-                   "removed_rows": sum(c["L_old"] - c["L_keep"] for c in chars),
+                   "rounds": n_rounds, "tail_tokens": sumT, "surviving_rows": rounds[0]["L_keep"][:4],
+                   "removed_rows": sum(o - k for R in rounds for o, k in zip(R["L_old"], R["L_keep"])),
                    "attn": f"{a.n_q_heads}q/{a.n_kv_heads}kv x {a.head_dim}",
                    "delta": f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}"},
         "roofline": roofline,
@@ -553,6 +616,7 @@ def main():
         "stages": stages,
         "speedup_vs_refill":round(refill["speedup"], 3) if refill else None,
         "refill_ms": round(refill["ms"], 5) if refill else None,
+        "refill_rounds": refill.get("rounds") if refill else None,
         "kernels": {n: {k: (round(v, 6) if isinstance(v, float) else v) for k, v in kv.items()}
                     for n, kv in kern.items()},
         "cpu_baseline": cpu,

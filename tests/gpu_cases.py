@@ -96,3 +96,28 @@ class DeltaCase:
     def oracle(self):
         return oracle.delta_layer_update(self.S0.astype(np.float64), self.q_b, self.k_b, self.v_b, self.beta,
                                          self.g, self.shape.scale)
+
+
+def delta_oracle_heads(S0, q_b, k_b, v_b, beta, g, scale, key_heads):
+    """The per-token oracle restricted to some key heads and the value heads that read
+    them (heads are independent, so this is the full oracle on a sub-shape).
+
+    Returns (value head indices, o [T, n, d_v], S [n, d_v, d_k])."""
+    Hk = q_b.shape[1]
+    Hv = v_b.shape[1]
+    G = Hv // Hk
+    kh = np.asarray(key_heads, dtype=np.int64)
+    vh = (kh[:, None] * G + np.arange(G)[None, :]).reshape(-1)
+    o, S = oracle.delta_layer_update(np.asarray(S0, np.float64)[vh], q_b[:, kh], k_b[:, kh], v_b[:, vh],
+                                     beta[:, vh], g[:, vh], scale)
+    return vh, o, S
+
+
+def sample_rows(T, n, seed):
+    """Tail rows checked at full sizes: both ends, the middle and a seeded sample."""
+    if T <= 0:
+        return np.zeros(0, np.int64)
+    fixed = [0, 1, T // 2, T - 2, T - 1]
+    rng = np.random.default_rng(seed)
+    extra = rng.integers(0, T, size=max(0, n - len(fixed)))
+    return np.unique(np.clip(np.concatenate([fixed, extra]), 0, T - 1)).astype(np.int64)
