@@ -22,12 +22,14 @@ from .attention import causal_gqa_attention
 from .bf16 import bf16_to_f64, f64_to_bf16
 from .compaction import compact, validate_ranges
 from .delta import gated_delta_tokens
+from .placement import check_new_positions, relocate_keys
 from .rope import rope_rotate
 
 
 def attention_layer_update(pos, k_cache, v_cache, ranges, cursor: int, q, k, v, rotary_dim: int,
                            theta: float, scale: float, live: Optional[Sequence[int]] = None,
-                           rows: Optional[Sequence[int]] = None, post_ranges=None):
+                           rows: Optional[Sequence[int]] = None, post_ranges=None, placement: str = "tail",
+                           tail_positions=None):
     """One attention layer of one character: Eq. 2 then the attention part of Eq. 3.
 
     pos: int [L_old] position of every cache row; k_cache, v_cache: bf16 bits
@@ -40,26 +42,57 @@ def attention_layer_update(pos, k_cache, v_cache, ranges, cursor: int, q, k, v, 
     delimiters, processed and then dropped from the retained KV). Every tail row is
     still computed and attended to first; only the returned cache, positions and
     cursor reflect the removal (the cursor still advances by T).
+
+    placement (Section 5.2; the variants compared in Section 6.3):
+      "tail"      the replacement is rotated and kept at cursor + i (the method);
+      "slot"      it is rotated at tail_positions[i] (inside the original slot) while
+                  it is still computed after every surviving row (the causal work
+                  tail), and its rows keep those positions; the cursor becomes
+                  max(cursor, max(tail_positions) + 1);
+      "relocate"  it is computed exactly as "tail", then its stored keys are rotated
+                  from cursor + i to tail_positions[i] (relocate_keys) and its rows
+                  relabelled; values are untouched and the cursor advances by T.
+    post_ranges are given in the tail's final positions.
     """
     if live is not None:
         validate_ranges(ranges, live, cursor)
     src_index, kept_pos = compact(pos, ranges)
     T = int(np.asarray(q).shape[0])
     L_keep = len(src_index)
-    tail_pos = cursor + np.arange(T, dtype=np.int64)
-    q_hat = f64_to_bf16(rope_rotate(bf16_to_f64(q), tail_pos, rotary_dim, theta))
-    k_hat = f64_to_bf16(rope_rotate(bf16_to_f64(k), tail_pos, rotary_dim, theta))
+    true_tail = cursor + np.arange(T, dtype=np.int64)
+    if placement == "tail":
+        rot_pos, tail_pos, cursor_after = true_tail, true_tail, cursor + T
+    elif placement in ("slot", "relocate"):
+        tail_pos = np.asarray(tail_positions, dtype=np.int64).reshape(-1)
+        if tail_pos.shape != (T,):
+            raise ValueError("one position per tail token")
+        check_new_positions(tail_pos, kept_pos)
+        if placement == "slot":
+            rot_pos = tail_pos
+            cursor_after = max(cursor, int(tail_pos.max()) + 1) if T else cursor
+        else:
+            rot_pos = true_tail
+            cursor_after = max(cursor + T, int(tail_pos.max()) + 1) if T else cursor
+    else:
+        raise ValueError(f"unknown placement {placement!r}")
+    q_hat = f64_to_bf16(rope_rotate(bf16_to_f64(q), rot_pos, rotary_dim, theta))
+    k_hat = f64_to_bf16(rope_rotate(bf16_to_f64(k), rot_pos, rotary_dim, theta))
     k_all = np.concatenate([np.asarray(k_cache)[src_index], k_hat], axis=0)
     v_all = np.concatenate([np.asarray(v_cache)[src_index], np.asarray(v, dtype=np.uint16)], axis=0)
     out = causal_gqa_attention(bf16_to_f64(q_hat), bf16_to_f64(k_all), bf16_to_f64(v_all), L_keep,
                                scale, rows=rows)
+    if placement == "relocate" and T:
+        # the stored keys move from their computed positions to the slot, one token at a time
+        moves = np.stack([true_tail, true_tail + 1, tail_pos], axis=1)
+        _, k_all = relocate_keys(np.concatenate([kept_pos, true_tail]), k_all, moves, rotary_dim, theta)
     final_pos = np.concatenate([kept_pos, tail_pos])
     post_index = np.arange(len(final_pos))
     if post_ranges is not None and len(post_ranges):
         post = np.asarray(post_ranges, dtype=np.int64).reshape(-1, 2)
-        if np.any(post[:, 0] < cursor) or np.any(post[:, 1] > cursor + T):
+        in_tail = [np.all(np.isin(np.arange(a, b), tail_pos)) for (a, b) in post]
+        if not all(in_tail):
             raise ValueError("post-prefill ranges must lie inside the tail")
-        validate_ranges([tuple(r) for r in post], final_pos.tolist(), cursor + T)
+        validate_ranges([tuple(r) for r in post], final_pos.tolist(), cursor_after)
         post_index, final_pos = compact(final_pos, [tuple(r) for r in post])
         k_all, v_all = k_all[post_index], v_all[post_index]
     return {
@@ -72,7 +105,7 @@ def attention_layer_update(pos, k_cache, v_cache, ranges, cursor: int, q, k, v, 
         "q_hat": q_hat,
         "k_hat": k_hat,
         "out": out,
-        "cursor": cursor + T,
+        "cursor": cursor_after,
     }
 
 
