@@ -148,7 +148,8 @@ def make_copy(tu, chars, layers, device, pristine=True):
     return ctxs, own
 
 
-def stack_update(tu, ctxs, own, layers, inputs, ranges, tails, attn_p, delta_p, post=None):
+def stack_update(tu, ctxs, own, layers, inputs, ranges, tails, attn_p, delta_p, post=None, placement=None,
+                 place_runs=None):
     ios = []
     for L, O, src in zip(layers, own, inputs):
         if L["kind"] == "attn":
@@ -157,13 +158,33 @@ def stack_update(tu, ctxs, own, layers, inputs, ranges, tails, attn_p, delta_p, 
         else:
             ios.append(tu.LayerIO(tu.TU_LAYER_DELTA, src["q"], src["k"], src["v"], src["out"], state=O["states"],
                                   beta=src["beta"], g=src["g"]))
-    return tu.StackUpdate(ctxs, ranges, tails, ios, attn_p, delta_p, post_ranges=post)
+    return tu.StackUpdate(ctxs, ranges, tails, ios, attn_p, delta_p, post_ranges=post, placement=placement,
+                          place_runs=place_runs)
 
 
-def round_updates(tu, ctxs, own, layers, rounds, attn_p, delta_p, post=None):
+def round_updates(tu, ctxs, own, layers, rounds, attn_p, delta_p, post=None, arm=None, place=None):
     """The prepared calls of one step: every round of the workload, in order, on one copy."""
     return [stack_update(tu, ctxs, own, layers, R["inputs"], R["ranges"], R["T"], attn_p, delta_p,
-                         post=None if post is None else post(R)) for R in rounds]
+                         post=None if post is None else post(R),
+                         placement=None if arm is None else [arm] * len(R["T"]),
+                         place_runs=None if place is None else place(R)) for R in rounds]
+
+
+def slot_runs(R):
+    """Positions of a slot-placed tail: the removed records' slots in order, then a free
+    range 10,000 positions past the cursor for the tokens that do not fit."""
+    out = []
+    for rr, T, c0 in zip(R["ranges"], R["T"], R["cursor"]):
+        runs, left = [], T
+        for (a0, b0) in [tuple(x) for x in rr]:
+            n = min(left, int(b0) - int(a0))
+            if n > 0:
+                runs.append((int(a0), int(a0) + n))
+                left -= n
+        if left > 0:
+            runs.append((c0 + 10000, c0 + 10000 + left))
+        out.append(runs)
+    return out
 
 
 # ----------------------------------------------------------------------------- algorithmic work
@@ -568,6 +589,46 @@ def main():
             "bytes": 2 * 2 * moved * row_b * kinds.count("attn"), "bound": "hbm"}
         print(f"[bench] delimiter removal: {json.dumps(extra['delimiter_removal'])}", file=sys.stderr, flush=True)
         del copies3, ups3, ws3
+
+    # ---- the placement arms the paper compares (Section 5.2): slot-preserving (rotated at
+    # the removed records' slots) and tail-and-relocate (computed at the true tail, stored
+    # keys then rotated to the slots), on the first round
+    if kinds.count("attn"):
+        rd = rounds[:1]
+        first_ms = round_ms[0] if round_ms else upd_ms
+        place_row = {"update_ms_true_tail": round(first_ms, 5)}
+        for arm in ("slot", "relocate"):
+            copies4 = [make_copy(tu, chars, layers, dev) for _ in range(W + 2 * K)]
+            ups4 = [round_updates(tu, ctxs, own, layers, rd, attn_p, delta_p, arm=arm, place=slot_runs)
+                    for (ctxs, own) in copies4]
+            ws4 = torch.empty(ups4[0][0].workspace_size(), dtype=torch.uint8, device=dev)
+            for i in range(W):
+                run_step(ups4[i], ws4)
+            torch.cuda.synchronize()
+            ev0.record()
+            for i in range(W, W + K):
+                run_step(ups4[i], ws4)
+            ev1.record()
+            torch.cuda.synchronize()
+            place_row[f"update_ms_{arm}"] = round(ev0.elapsed_time(ev1) / K, 5)
+            if arm == "relocate":
+                tu.profile_enable(True)
+                for i in range(W + K, W + 2 * K):
+                    run_step(ups4[i], ws4)
+                rp = tu.profile_collect()
+                tu.profile_enable(False)
+                if "relocate" in rp:
+                    c_, t_ = rp["relocate"]
+                    rows = sum(rd[0]["T"]) * kinds.count("attn")
+                    nbytes = rows * (2 * a.n_kv_heads * a.head_dim * 2 + 8)   # key rows read + written, labels
+                    kms = t_ / c_
+                    place_row["relocate_kernel"] = {
+                        "launches_per_step": c_ / K, "avg_ms": round(kms, 5), "rows": rows, "bytes": nbytes,
+                        "bound": "hbm", "achieved": round(nbytes / (t_ / K / 1e3) / 1e9, 1), "unit": "GB/s",
+                        "peak": HBM_PEAK_GBS}
+            del copies4, ups4, ws4
+        extra["placement"] = place_row
+        print(f"[bench] placements: {json.dumps(place_row)}", file=sys.stderr, flush=True)
 
     # ---- the short-convolution continuation of one delta layer's q, k, v (width 4, SiLU)
     if kinds.count("delta"):

@@ -10,7 +10,9 @@
  * the carried state (Eq. 3). Section 4.2 fixes the bookkeeping: deletion ranges
  * are verified against the live spans first, removed positions become holes
  * (no placeholder rows), keys are never rotated back, and the cursor keeps
- * growing independently of the live length.
+ * growing independently of the live length. The other placements the paper
+ * compares (Section 5.2, Section 6.3) are available as variants of the stack
+ * update (slot-preserving, tail-and-relocate) and as relocate_keys.
  *
  * Conventions for every call below
  *  - Device buffers are caller-owned; the library never allocates or frees
@@ -36,7 +38,7 @@
 extern "C" {
 #endif
 
-#define TU_ABI_VERSION 2
+#define TU_ABI_VERSION 3
 
 #define TU_OK 0
 #define TU_ERR_ARG (-1)       /* null pointer, unsupported or inconsistent shape */
@@ -45,7 +47,8 @@ extern "C" {
 #define TU_ERR_WORKSPACE (-4) /* workspace missing or smaller than required */
 #define TU_ERR_HIP (-5)       /* a HIP launch failed */
 
-#define TU_MAX_RANGES 128     /* deletion ranges per context per call */
+#define TU_MAX_RANGES 128     /* deletion ranges per context per call (and row spans they map to) */
+#define TU_MAX_PLACE_RUNS 32  /* position runs of a slot-preserving or relocated tail */
 
 #define TU_LAYER_ATTN 0
 #define TU_LAYER_DELTA 1
@@ -59,8 +62,13 @@ typedef struct tu_interval {
 /*
  * One character context (Section 4.1 state; D3/D4 bookkeeping of Section 4.2).
  * Host-side metadata plus the device position array. Cache rows [0, len) hold
- * the live tokens in increasing position order; `live` lists their positions
- * as sorted, disjoint, non-adjacent intervals whose total length is `len`.
+ * the live tokens in the order they were computed (work order); d_pos labels each
+ * row with its position. `live` lists the positions as runs in row order: run i
+ * covers positions [begin, end) held by consecutive rows, runs are pairwise
+ * disjoint, two consecutive runs are never position-contiguous (they would be one
+ * run), and the lengths sum to `len`. With true-tail updates only, rows are in
+ * increasing position order and the runs are sorted; slot-preserving and relocated
+ * rows keep their work-order row but carry earlier positions.
  */
 typedef struct tu_seq {
   int64_t len;        /* live rows */
@@ -212,6 +220,28 @@ typedef struct tu_conv_tensor {
 int short_conv_continue_batch(const tu_conv_tensor* tensors, int32_t n, int32_t width, int32_t activation,
                               void* stream);
 
+/*
+ * Placement of a context's replacement tokens (Section 5.2; compared in Section 6.3):
+ *  TU_PLACE_TAIL      the method: rotated and kept at the next positions
+ *                     next_pos, next_pos + 1, ...; the cursor advances by T.
+ *  TU_PLACE_SLOT      slot-preserving maintenance: computed at the causal work tail
+ *                     (after every surviving row) but rotated at the positions of
+ *                     `place_runs`, which the rows then keep; the cursor becomes
+ *                     max(next_pos, last placed position + 1).
+ *  TU_PLACE_RELOCATE  tail-and-relocate: computed exactly as TU_PLACE_TAIL, then the
+ *                     stored keys are rotated from their tail positions to those of
+ *                     `place_runs` and the rows relabelled (values and recurrent state
+ *                     untouched); the cursor advances by T (or past the last placed
+ *                     position if that is further).
+ * place_runs: host int64 [n_place_runs][2] half-open position ranges, in tail order:
+ * the T tail tokens take their positions one run after the other (the lengths sum to
+ * T); the runs are disjoint, free of live positions after this call's removals, and
+ * below 2^31 - 1. At most TU_MAX_PLACE_RUNS runs.
+ */
+#define TU_PLACE_TAIL 0
+#define TU_PLACE_SLOT 1
+#define TU_PLACE_RELOCATE 2
+
 /* One context's part of a stack update. */
 typedef struct tu_seq_update {
   tu_seq* seq;
@@ -221,11 +251,15 @@ typedef struct tu_seq_update {
   int32_t* src_index;     /* optional device int32 [>= seq->len] (see compact_kv) */
   /* Rows removed once the tail is prefilled (Section 4.1: temporary maintenance
    * delimiters whose direct KV are subsequently removed; Section 4.2): host int64
-   * [n_post_ranges][2] half-open position ranges inside this call's tail
-   * [seq->next_pos, seq->next_pos + T), sorted, disjoint, non-empty. May be NULL
-   * when n_post_ranges == 0. */
+   * [n_post_ranges][2] half-open position ranges made of this call's tail positions
+   * (their final positions: [next_pos, next_pos + T) for TU_PLACE_TAIL, the placed
+   * positions otherwise), sorted, disjoint, non-empty. May be NULL when
+   * n_post_ranges == 0. */
   const int64_t* post_ranges;
   int32_t n_post_ranges;
+  int32_t placement;            /* TU_PLACE_TAIL (0), TU_PLACE_SLOT or TU_PLACE_RELOCATE */
+  const int64_t* place_runs;    /* host [n_place_runs][2]; NULL for TU_PLACE_TAIL */
+  int32_t n_place_runs;
 } tu_seq_update;
 
 /*
@@ -260,15 +294,16 @@ typedef struct tu_update {
 
 /*
  * Whole update of a hybrid layer stack for n_seq contexts (Eq. 1-3): verify every
- * context's ranges and capacity; compact every attention layer's cache once per
- * context (one index list per context, reused by all attention layers); then, in
- * layer order, tail attention for attention layers and recurrence continuation
- * for delta layers, batched over the contexts; then remove each context's
- * post-prefill rows (post_ranges) from every attention layer; finally commit each
- * context's metadata (len = survivors + T - post-removed rows, live intervals,
- * cursor += T: the positions of post-removed rows become holes, and the recurrent
- * state keeps their influence). A full refill is the same call on empty contexts
- * (len 0) with zero states.
+ * context's ranges, placement and capacity; compact every attention layer's cache
+ * once per context (one index list per context, reused by all attention layers);
+ * then, in layer order, tail attention for attention layers and recurrence
+ * continuation for delta layers, batched over the contexts; then relocate the keys
+ * of TU_PLACE_RELOCATE contexts; then remove each context's post-prefill rows
+ * (post_ranges) from every attention layer; finally commit each context's metadata
+ * (len = survivors + T - post-removed rows, live runs, cursor as the placement
+ * says: the positions of post-removed rows become holes, and the recurrent state
+ * keeps their influence). A full refill is the same call on empty contexts (len 0)
+ * with zero states.
  * Delta layers read nothing the attention path writes, so they run concurrently
  * with it on a side stream of the current device (one per calling thread, created on
  * first use, default priority), forked after the work already queued on `stream`
@@ -281,6 +316,25 @@ int tu_validate_update(const tu_update* u);
 int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Key relocation (Section 5.2, tail-and-relocate: stored keys rotated to other
+ * positions; values, row order and recurrent state unchanged). For every move
+ * (src_begin, src_end, dst_begin) the rows holding positions [src_begin, src_end)
+ * get their keys rotated by delta = dst_begin - src_begin, pair (j, j + r/2) by the
+ * angle delta * theta^(-2j/r) (float64 angle and rotation of the stored bf16 value,
+ * rounded to bf16 nearest even), and are relabelled with positions + delta.
+ *  k_layers: host array [n_layers] of device bf16 [capacity][n_kv_heads][head_dim]
+ *            key caches (the attention layers of the context; n_layers may be 0 to
+ *            relabel positions only). p: head shape, rotary_dim and rope_theta.
+ *  moves:    host int64 [n_moves][3]; sources sorted, disjoint and live;
+ *            destinations disjoint and not held by rows that stay; below 2^31 - 1.
+ * On success seq->live is relabelled and seq->next_pos becomes
+ * max(next_pos, last destination + 1). Needs no workspace. At most TU_MAX_RANGES
+ * moves (and row spans they map to). Errors: TU_ERR_ARG, TU_ERR_RANGE, TU_ERR_HIP.
+ */
+int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu_attn_params* p,
+                  const int64_t* moves, int32_t n_moves, void* stream);
+
+/*
  * Kernel timing (diagnostics, not part of the update). While enabled for the
  * calling thread, every kernel the library launches is bracketed by two HIP
  * events recorded on the launch's stream. tu_profile_collect waits for those
@@ -290,7 +344,7 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
  * (or a negative status) and clears the records. Names (one per launch or pair
  * of launches): compact (keep-scan, then gather), rope_vt_pack (RoPE + append of
  * the tail with the V^T packing of the key tiles), attention, attention_merge,
- * delta_prep, delta_chain, short_conv.
+ * delta_prep, delta_chain, short_conv, relocate.
  */
 int tu_profile_enable(int on);
 int tu_profile_collect(char* names, int32_t name_stride, int32_t* counts, double* total_ms, int32_t max_entries);

@@ -4,7 +4,9 @@ The HIP library libtailupdate.so (built from csrc/ by `build.py`) implements the
 update of a hybrid recurrent-attention context (paper Section 4.1, Eq. 2-3): KV
 compaction, rotary append at the true tail, causal GQA attention over surviving
 + new KV, and the gated delta-rule continuation from the carried state.
-It also continues the recurrent layers' short convolution from its carried state.
+It also continues the recurrent layers' short convolution from its carried state,
+and provides the slot-preserving and tail-and-relocate placements the paper compares
+(Section 5.2) together with the relocation of stored keys.
 `binding` is the ctypes layer over its C ABI (include/tailupdate.h).
 """
 from .binding import (  # noqa: F401
@@ -20,10 +22,14 @@ from .binding import (  # noqa: F401
     lib,
     profile_collect,
     profile_enable,
+    relocate_keys,
     short_conv_continue,
     short_conv_continue_batch,
     tail_prefill_attention,
     update_layer_stack,
     TU_LAYER_ATTN,
     TU_LAYER_DELTA,
+    TU_PLACE_RELOCATE,
+    TU_PLACE_SLOT,
+    TU_PLACE_TAIL,
 )

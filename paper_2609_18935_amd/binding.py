@@ -28,6 +28,11 @@ TU_ERR_HIP = -5
 TU_LAYER_ATTN = 0
 TU_LAYER_DELTA = 1
 TU_MAX_RANGES = 128
+TU_MAX_PLACE_RUNS = 32
+TU_PLACE_TAIL = 0
+TU_PLACE_SLOT = 1
+TU_PLACE_RELOCATE = 2
+_PLACEMENTS = {"tail": TU_PLACE_TAIL, "slot": TU_PLACE_SLOT, "relocate": TU_PLACE_RELOCATE}
 
 _i32, _i64, _f32, _f64, _vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
 
@@ -54,7 +59,8 @@ class tu_delta_params(ctypes.Structure):
 
 class tu_seq_update(ctypes.Structure):
     _fields_ = [("seq", ctypes.POINTER(tu_seq)), ("ranges", ctypes.POINTER(_i64)), ("n_ranges", _i32),
-                ("T", _i64), ("src_index", _vp), ("post_ranges", ctypes.POINTER(_i64)), ("n_post_ranges", _i32)]
+                ("T", _i64), ("src_index", _vp), ("post_ranges", ctypes.POINTER(_i64)), ("n_post_ranges", _i32),
+                ("placement", _i32), ("place_runs", ctypes.POINTER(_i64)), ("n_place_runs", _i32)]
 
 
 class tu_layer_io(ctypes.Structure):
@@ -93,13 +99,15 @@ _SIGNATURES = {
     "update_layer_stack_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_update)]),
     "tu_validate_update": (_i32, [ctypes.POINTER(tu_update)]),
     "update_layer_stack": (_i32, [ctypes.POINTER(tu_update), _vp, ctypes.c_size_t, _vp]),
+    "relocate_keys": (_i32, [ctypes.POINTER(tu_seq), ctypes.POINTER(_vp), _i32, ctypes.POINTER(tu_attn_params),
+                             ctypes.POINTER(_i64), _i32, _vp]),
     "tu_profile_enable": (_i32, [_i32]),
     "tu_profile_collect": (_i32, [ctypes.c_char_p, _i32, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double),
                                   _i32]),
 }
 
 _lib_handle = None
-ABI_VERSION = 2   # TU_ABI_VERSION of include/tailupdate.h that these structures follow
+ABI_VERSION = 3   # TU_ABI_VERSION of include/tailupdate.h that these structures follow
 
 
 def lib():
@@ -152,9 +160,9 @@ def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]) -> torch.
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
 
 
-def _ranges_array(ranges) -> tuple:
+def _ranges_array(ranges, width: int = 2) -> tuple:
     import numpy as np
-    r = np.ascontiguousarray(np.asarray(ranges, dtype=np.int64).reshape(-1, 2))
+    r = np.ascontiguousarray(np.asarray(ranges, dtype=np.int64).reshape(-1, width))
     arr = (_i64 * max(1, r.size))(*r.reshape(-1).tolist())
     return arr, int(r.shape[0])
 
@@ -268,6 +276,17 @@ def delta_rule_continue(state: torch.Tensor, q, k, v, beta, g, params: tu_delta_
                                      ctypes.byref(params), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
 
 
+def relocate_keys(ctx: Context, k_layers: Sequence[torch.Tensor], params: Optional[tu_attn_params], moves,
+                  stream=None):
+    """Rotate the stored keys of the rows holding each move's source positions
+    [src_begin, src_end) to dst_begin + offset and relabel them; moves: [n][3]."""
+    n = len(k_layers)
+    ks = (_vp * max(1, n))(*[_ptr(t) for t in k_layers])
+    arr, nm = _ranges_array(moves, 3)
+    p = params if params is not None else tu_attn_params()
+    _check(lib().relocate_keys(ctypes.byref(ctx.c), ks, n, ctypes.byref(p), arr, nm, _stream(stream)))
+
+
 TU_CONV_IDENTITY = 0
 TU_CONV_SILU = 1
 
@@ -311,9 +330,12 @@ class StackUpdate:
 
     def __init__(self, contexts: Sequence[Context], ranges: Sequence, tails: Sequence[int], layers: Sequence[LayerIO],
                  attn: Optional[tu_attn_params] = None, delta: Optional[tu_delta_params] = None,
-                 src_index: Optional[Sequence[Optional[torch.Tensor]]] = None, post_ranges: Optional[Sequence] = None):
-        """post_ranges[s]: position ranges inside context s's tail whose rows are removed
-        once the tail is prefilled (maintenance delimiters), or None."""
+                 src_index: Optional[Sequence[Optional[torch.Tensor]]] = None, post_ranges: Optional[Sequence] = None,
+                 placement: Optional[Sequence[str]] = None, place_runs: Optional[Sequence] = None):
+        """post_ranges[s]: position ranges made of context s's tail positions whose rows
+        are removed once the tail is prefilled (maintenance delimiters), or None.
+        placement[s]: "tail" (default), "slot" or "relocate"; place_runs[s]: the [n][2]
+        position runs the tail takes for "slot" and "relocate"."""
         n = len(contexts)
         self.contexts = list(contexts)
         self._keep = []
@@ -325,7 +347,12 @@ class StackUpdate:
             pr = None if post_ranges is None or post_ranges[s] is None else post_ranges[s]
             parr, npr = _ranges_array(pr if pr is not None else [])
             self._keep.append(parr)
-            self._seq_arr[s] = tu_seq_update(ctypes.pointer(ctx.c), arr, nr, int(tails[s]), _ptr(si), parr, npr)
+            pl = "tail" if placement is None or placement[s] is None else placement[s]
+            runs = None if place_runs is None or place_runs[s] is None else place_runs[s]
+            rarr, nrr = _ranges_array(runs if runs is not None else [])
+            self._keep.append(rarr)
+            self._seq_arr[s] = tu_seq_update(ctypes.pointer(ctx.c), arr, nr, int(tails[s]), _ptr(si), parr, npr,
+                                             _PLACEMENTS[pl], rarr, nrr)
         self._layer_arr = (tu_layer_io * max(1, len(layers)))()
         for l, L in enumerate(layers):
             def plist(ts):
@@ -376,8 +403,8 @@ def profile_collect(max_entries: int = 32) -> dict:
 
 
 def update_layer_stack(contexts, ranges, tails, layers, attn=None, delta=None, workspace=None, stream=None,
-                       src_index=None, post_ranges=None):
-    up = StackUpdate(contexts, ranges, tails, layers, attn, delta, src_index, post_ranges)
+                       src_index=None, post_ranges=None, placement=None, place_runs=None):
+    up = StackUpdate(contexts, ranges, tails, layers, attn, delta, src_index, post_ranges, placement, place_runs)
     nbytes = up.workspace_size()
     dev = contexts[0].pos.device if contexts else "cuda"
     ws = _workspace(nbytes, dev, workspace)

@@ -61,27 +61,104 @@ int check_seq(const tu_seq* s) {
   if (s->n_live > 0 && !s->live) return fail(TU_ERR_ARG, "null live-interval array");
   if (s->capacity > 0 && !s->d_pos) return fail(TU_ERR_ARG, "null d_pos");
   if (s->next_pos < 0 || s->next_pos > INT32_MAX) return fail(TU_ERR_ARG, "cursor outside the int32 position range");
-  int64_t total = 0, prev_end = -1;
+  int64_t total = 0, max_end = -1;
   for (int i = 0; i < s->n_live; ++i) {
     const tu_interval& iv = s->live[i];
-    if (iv.end <= iv.begin) return fail(TU_ERR_ARG, "empty live interval");
-    if (iv.begin <= prev_end) return fail(TU_ERR_ARG, "live intervals not sorted, disjoint and merged");
-    prev_end = iv.end;
+    if (iv.end <= iv.begin || iv.begin < 0) return fail(TU_ERR_ARG, "empty or negative live run");
+    if (i > 0 && iv.begin == s->live[i - 1].end)
+      return fail(TU_ERR_ARG, "consecutive live runs %d and %d are position-contiguous (not merged)", i - 1, i);
+    max_end = std::max(max_end, iv.end);
     total += iv.end - iv.begin;
   }
-  if (prev_end > s->next_pos) return fail(TU_ERR_ARG, "live position at or beyond the cursor");
-  if (total != s->len) return fail(TU_ERR_ARG, "live intervals cover %lld positions, len is %lld",
+  if (max_end > s->next_pos) return fail(TU_ERR_ARG, "live position at or beyond the cursor");
+  if (total != s->len) return fail(TU_ERR_ARG, "live runs cover %lld positions, len is %lld",
                                    (long long)total, (long long)s->len);
+  std::vector<tu_interval> sorted(s->live, s->live + s->n_live);
+  std::sort(sorted.begin(), sorted.end(), [](const tu_interval& x, const tu_interval& y) { return x.begin < y.begin; });
+  for (size_t i = 1; i < sorted.size(); ++i)
+    if (sorted[i].begin < sorted[i - 1].end) return fail(TU_ERR_ARG, "live runs overlap");
   return TU_OK;
+}
+
+// The live runs sorted by position, each with the cache row of its first position.
+struct RunIndex {
+  std::vector<tu_interval> run;   // sorted by begin
+  std::vector<int64_t> row;       // first row of run[i]
+  explicit RunIndex(const tu_interval* live, int n) {
+    std::vector<int64_t> row0(n + 1, 0);
+    for (int i = 0; i < n; ++i) row0[i + 1] = row0[i] + (live[i].end - live[i].begin);
+    std::vector<int> order(n);
+    for (int i = 0; i < n; ++i) order[i] = i;
+    std::sort(order.begin(), order.end(), [&](int x, int y) { return live[x].begin < live[y].begin; });
+    for (int i : order) {
+      run.push_back(live[i]);
+      row.push_back(row0[i]);
+    }
+  }
+  // index of the run holding position p, or -1
+  int find(int64_t p) const {
+    int lo = 0, hi = (int)run.size() - 1;
+    while (lo <= hi) {
+      const int mid = (lo + hi) / 2;
+      if (run[mid].end <= p) lo = mid + 1;
+      else if (run[mid].begin > p) hi = mid - 1;
+      else return mid;
+    }
+    return -1;
+  }
+};
+
+// Appends a run in row order, merging it into the previous run when contiguous.
+void push_run(std::vector<tu_interval>& iv, int64_t begin, int64_t end) {
+  if (end <= begin) return;
+  if (!iv.empty() && iv.back().end == begin) iv.back().end = end;
+  else iv.push_back({begin, end});
 }
 
 // Result of range verification for one context.
 struct RangeCheck {
   int64_t removed = 0;
-  int64_t first_row = 0;                  // cache row of the first removed position
-  std::vector<int64_t> rows;              // cache row of the first position of each range
-  std::vector<tu_interval> live_after;    // intervals after the removal
+  int64_t first_row = 0;                  // first removed cache row
+  // removed rows as (first row, length) spans, sorted by row; a range whose positions
+  // sit in several runs maps to several spans
+  std::vector<std::pair<int64_t, int64_t>> spans;
+  std::vector<tu_interval> live_after;    // runs after the removal, in row order
 };
+
+// Positions [a, b) as cache-row spans, appended to `spans`; false if a position is not live.
+bool range_rows(const RunIndex& ri, int64_t a, int64_t b, std::vector<std::pair<int64_t, int64_t>>* spans) {
+  int at = ri.find(a);
+  while (a < b) {
+    if (at < 0 || at >= (int)ri.run.size() || ri.run[at].begin > a) return false;
+    const int64_t e = std::min(b, ri.run[at].end);
+    spans->push_back({ri.row[at] + (a - ri.run[at].begin), e - a});
+    a = e;
+    ++at;   // the next run by position must start where this one ends
+  }
+  return true;
+}
+
+// The runs of `live` (row order) minus position ranges (sorted, disjoint), in row order.
+std::vector<tu_interval> subtract_runs(const tu_interval* live, int n_live, const int64_t* ranges, int n) {
+  std::vector<tu_interval> out;
+  for (int i = 0; i < n_live; ++i) {
+    int64_t cur = live[i].begin;
+    const int64_t end = live[i].end;
+    // first range ending after this run's start
+    int lo = 0, hi = n;
+    while (lo < hi) {
+      const int mid = (lo + hi) / 2;
+      if (ranges[2 * mid + 1] <= cur) lo = mid + 1;
+      else hi = mid;
+    }
+    for (int q = lo; q < n && ranges[2 * q] < end; ++q) {
+      push_run(out, cur, std::max(cur, ranges[2 * q]));
+      cur = std::max(cur, ranges[2 * q + 1]);
+    }
+    push_run(out, cur, end);
+  }
+  return out;
+}
 
 int check_ranges(const tu_seq* s, const int64_t* ranges, int n, RangeCheck* out) {
   if (n < 0) return fail(TU_ERR_ARG, "negative range count");
@@ -89,11 +166,9 @@ int check_ranges(const tu_seq* s, const int64_t* ranges, int n, RangeCheck* out)
   if (n > TU_MAX_RANGES) return fail(TU_ERR_ARG, "more than %d ranges in one call", TU_MAX_RANGES);
   out->removed = 0;
   out->first_row = s->len;
-  out->rows.clear();
+  out->spans.clear();
   int64_t prev_end = INT64_MIN;
-  // prefix of live rows before each interval
-  std::vector<int64_t> before(s->n_live + 1, 0);
-  for (int i = 0; i < s->n_live; ++i) before[i + 1] = before[i] + (s->live[i].end - s->live[i].begin);
+  const RunIndex ri(s->live, s->n_live);
   for (int q = 0; q < n; ++q) {
     const int64_t a = ranges[2 * q], b = ranges[2 * q + 1];
     if (b <= a) return fail(TU_ERR_RANGE, "range %d [%lld,%lld) is empty", q, (long long)a, (long long)b);
@@ -101,34 +176,47 @@ int check_ranges(const tu_seq* s, const int64_t* ranges, int n, RangeCheck* out)
     if (a < 0 || b > s->next_pos)
       return fail(TU_ERR_RANGE, "range %d [%lld,%lld) reaches past the cursor %lld", q, (long long)a,
                   (long long)b, (long long)s->next_pos);
-    // the interval that holds position a
-    int lo = 0, hi = s->n_live - 1, at = -1;
-    while (lo <= hi) {
-      const int mid = (lo + hi) / 2;
-      if (s->live[mid].end <= a) lo = mid + 1;
-      else if (s->live[mid].begin > a) hi = mid - 1;
-      else { at = mid; break; }
-    }
-    if (at < 0 || b > s->live[at].end)
+    if (!range_rows(ri, a, b, &out->spans))
       return fail(TU_ERR_RANGE, "range %d [%lld,%lld) is not live", q, (long long)a, (long long)b);
-    out->rows.push_back(before[at] + (a - s->live[at].begin));
-    if (q == 0) out->first_row = out->rows[0];
     out->removed += b - a;
     prev_end = b;
   }
-  // intervals after removal
-  out->live_after.clear();
-  int q = 0;
-  for (int i = 0; i < s->n_live; ++i) {
-    int64_t cur = s->live[i].begin;
-    const int64_t end = s->live[i].end;
-    while (q < n && ranges[2 * q] < end) {
-      if (ranges[2 * q] > cur) out->live_after.push_back({cur, ranges[2 * q]});
-      cur = std::max(cur, ranges[2 * q + 1]);
-      ++q;
-    }
-    if (cur < end) out->live_after.push_back({cur, end});
+  if ((int)out->spans.size() > TU_MAX_RANGES)
+    return fail(TU_ERR_RANGE, "the ranges map to %d row spans, more than %d", (int)out->spans.size(), TU_MAX_RANGES);
+  std::sort(out->spans.begin(), out->spans.end());
+  // merge row-adjacent spans (positions of two runs removed back to back)
+  std::vector<std::pair<int64_t, int64_t>> merged;
+  for (auto& sp : out->spans) {
+    if (!merged.empty() && merged.back().first + merged.back().second == sp.first) merged.back().second += sp.second;
+    else merged.push_back(sp);
   }
+  out->spans.swap(merged);
+  if (!out->spans.empty()) out->first_row = out->spans[0].first;
+  out->live_after = subtract_runs(s->live, s->n_live, ranges, n);
+  return TU_OK;
+}
+
+// Position runs (host [n][2]) that a placement gives the T tail tokens: non-empty,
+// disjoint, free of `live` positions, below 2^31 - 1, lengths summing to T.
+int check_place_runs(const int64_t* runs, int n, int64_t T, const std::vector<tu_interval>& live, int s) {
+  if (n < 0 || n > TU_MAX_PLACE_RUNS) return fail(TU_ERR_ARG, "context %d: 0 .. %d placement runs", s, TU_MAX_PLACE_RUNS);
+  if (n > 0 && !runs) return fail(TU_ERR_ARG, "context %d: null placement runs", s);
+  int64_t total = 0;
+  std::vector<tu_interval> all(live);
+  for (int q = 0; q < n; ++q) {
+    const int64_t a = runs[2 * q], b = runs[2 * q + 1];
+    if (b <= a || a < 0 || b > INT32_MAX)
+      return fail(TU_ERR_RANGE, "context %d: placement run %d [%lld,%lld) empty or outside [0, 2^31 - 1)", s, q,
+                  (long long)a, (long long)b);
+    total += b - a;
+    all.push_back({a, b});
+  }
+  if (total != T) return fail(TU_ERR_ARG, "context %d: placement runs hold %lld positions, T is %lld", s,
+                              (long long)total, (long long)T);
+  std::sort(all.begin(), all.end(), [](const tu_interval& x, const tu_interval& y) { return x.begin < y.begin; });
+  for (size_t i = 1; i < all.size(); ++i)
+    if (all[i].begin < all[i - 1].end)
+      return fail(TU_ERR_RANGE, "context %d: placement positions overlap each other or live positions", s);
   return TU_OK;
 }
 
@@ -243,12 +331,12 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
         const int nb = moves ? std::min<int>(kMaxBufPerLaunch, (int)it.bufs.size() - b0) : 0;
         const bool sc = scans && first;
         if ((int)cur.size() == kMaxSeqPerCompact || bufs + nb > kMaxBufPerLaunch ||
-            (sc && nr + it.n_ranges > kMaxRangesPerLaunch) || (ns + it.n_ranges > kMaxRangesPerLaunch))
+            (sc && nr + it.n_ranges > kMaxRangesPerLaunch) || (ns + (int)it.rc.spans.size() > kMaxRangesPerLaunch))
           flush();
         cur.push_back({i, b0, nb, sc, moves});
         bufs += nb;
         if (sc) nr += it.n_ranges;
-        ns += it.n_ranges;   // spans are referenced by both the scan and the move entries
+        ns += (int)it.rc.spans.size();   // spans are referenced by both the scan and the move entries
         b0 += nb;
         first = false;
       } while (moves && b0 < (int)it.bufs.size());
@@ -267,13 +355,13 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
       if (span_at[idx] >= 0) return span_at[idx];
       span_at[idx] = ns;
       int64_t before = 0;
-      for (int q = 0; q < it.n_ranges; ++q) {
-        const int64_t len = it.ranges[2 * q + 1] - it.ranges[2 * q];
-        a.spans[ns + q][0] = (int32_t)(it.rc.rows[q] - before);
-        a.spans[ns + q][1] = (int32_t)len;
-        before += len;
+      const int n_sp = (int)it.rc.spans.size();
+      for (int q = 0; q < n_sp; ++q) {
+        a.spans[ns + q][0] = (int32_t)(it.rc.spans[q].first - before);
+        a.spans[ns + q][1] = (int32_t)it.rc.spans[q].second;
+        before += it.rc.spans[q].second;
       }
-      ns += it.n_ranges;
+      ns += n_sp;
       return span_at[idx];
     };
     for (auto& e : g) {
@@ -286,7 +374,7 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
         c.range_begin = nr;
         c.n_ranges = it.n_ranges;
         c.span_begin = spans_of(it, e.item);
-        c.n_spans = it.n_ranges;
+        c.n_spans = (int32_t)it.rc.spans.size();
         c.block_begin = a.n_scan_blocks;
         a.n_scan_blocks += (int32_t)((it.seq->len + kScanRows - 1) / kScanRows);
         for (int q = 0; q < it.n_ranges; ++q) {
@@ -310,7 +398,7 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
         m.flag_begin = flag_off;
         m.window = (int32_t)((it.rc.removed + R - 1 + R - 1) / R);
         m.span_begin = spans_of(it, e.item);
-        m.n_spans = it.n_ranges;
+        m.n_spans = (int32_t)it.rc.spans.size();
         for (int b = 0; b < e.nbuf; ++b) a.bufs[nbufs++] = it.bufs[e.buf0 + b];
         items_total += m.n_stripes * m.n_buf;
         flag_off += m.n_stripes;
@@ -357,6 +445,8 @@ struct AttnItem {
   const bf16_t* v;
   float* out;
   bf16_t* q_hat;            // caller's or null (workspace)
+  const int64_t* place_runs = nullptr;   // slot placement: host [n][2] position runs of the tail
+  int n_place_runs = 0;
 };
 
 struct AttnLaunch {
@@ -382,8 +472,12 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
   const int Hq = p->n_q_heads, Hkv = p->n_kv_heads, D = p->head_dim, G = Hq / Hkv;
   size_t max_used = 0;
   out->clear();
-  for (size_t g0 = 0; g0 < items.size(); g0 += kMaxSeqPerLaunch) {
-    const size_t g1 = std::min(items.size(), g0 + kMaxSeqPerLaunch);
+  for (size_t g0 = 0, g1 = 0; g0 < items.size(); g0 = g1) {
+    // up to kMaxSeqPerLaunch contexts and kMaxPlaceRunsPerLaunch placement runs per launch
+    int runs = 0;
+    while (g1 < items.size() && g1 - g0 < (size_t)kMaxSeqPerLaunch &&
+           runs + items[g1].n_place_runs <= kMaxPlaceRunsPerLaunch)
+      runs += items[g1++].n_place_runs;
     Arena ar(ws);
     int64_t base_items = 0;
     for (size_t i = g0; i < g1; ++i) base_items += (int64_t)Hkv * ((items[i].T * G + kAttnRows - 1) / kAttnRows);
@@ -397,7 +491,7 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
     L.attn.n_kv_heads = Hkv;
     L.attn.scale_log2 = p->softmax_scale * 1.4426950408889634f;
     L.merge.n_q_heads = Hq;
-    int tok = 0, item_total = 0, pack_total = 0, mrows = 0;
+    int tok = 0, item_total = 0, pack_total = 0, mrows = 0, n_runs = 0;
     for (size_t i = g0; i < g1; ++i) {
       const AttnItem& it = items[i];
       if (it.T <= 0) continue;
@@ -426,6 +520,14 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
       r.L_keep = (int32_t)it.L_keep;
       r.T = (int32_t)it.T;
       r.tok_begin = tok;
+      r.run_begin = n_runs;
+      r.n_runs = it.n_place_runs;
+      for (int q = 0, t0 = 0; q < it.n_place_runs; ++q) {
+        L.rope.runs[n_runs][0] = (int32_t)it.place_runs[2 * q];
+        L.rope.runs[n_runs][1] = t0;
+        t0 += (int)(it.place_runs[2 * q + 1] - it.place_runs[2 * q]);
+        ++n_runs;
+      }
       tok += (int)it.T;
       AttnSeq& s = L.attn.seq[L.attn.n_seq++];
       s.q_hat = qh;
@@ -567,11 +669,6 @@ int run_delta(const std::vector<DeltaArgs>& ls, const tu_delta_params* p, hipStr
   return TU_OK;
 }
 
-void append_tail(std::vector<tu_interval>& iv, int64_t begin, int64_t T) {
-  if (T <= 0) return;
-  if (!iv.empty() && iv.back().end == begin) iv.back().end = begin + T;
-  else iv.push_back({begin, begin + T});
-}
 
 int commit_intervals(tu_seq* s, const std::vector<tu_interval>& iv) {
   if ((int64_t)iv.size() > s->live_cap) return fail(TU_ERR_CAPACITY, "live-interval list full (%d)", s->live_cap);
@@ -580,11 +677,79 @@ int commit_intervals(tu_seq* s, const std::vector<tu_interval>& iv) {
   return TU_OK;
 }
 
+// ------------------------------------------------------------------ key relocation
+
+struct RelocSpan {
+  int64_t row, len, delta;
+};
+
+// Rotates the keys of the rows in `spans` by their shifts in every buffer of `kbufs`
+// and relabels d_pos: launches of up to kMaxRelocSpans spans x kMaxBufPerLaunch
+// buffers (positions move with the first buffer group only).
+int run_relocation(const std::vector<RelocSpan>& spans, const std::vector<void*>& kbufs, int32_t* d_pos,
+                   const tu_attn_params* p, hipStream_t st) {
+  for (size_t s0 = 0; s0 < spans.size(); s0 += kMaxRelocSpans) {
+    const size_t s1 = std::min(spans.size(), s0 + kMaxRelocSpans);
+    size_t b0 = 0;
+    do {
+      RelocArgs a{};
+      a.pos = b0 == 0 ? d_pos : nullptr;
+      a.n_bufs = (int32_t)std::min<size_t>(kMaxBufPerLaunch, kbufs.size() - b0);
+      for (int b = 0; b < a.n_bufs; ++b) a.bufs[b] = static_cast<bf16_t*>(kbufs[b0 + b]);
+      if (a.n_bufs > 0) {
+        a.n_kv_heads = p->n_kv_heads;
+        a.head_dim = p->head_dim;
+        a.rotary_dim = p->rotary_dim;
+        a.theta = p->rope_theta;
+      }
+      a.block_begin[0] = 0;
+      for (size_t i = s0; i < s1; ++i) {
+        const int k = (int)(i - s0);
+        a.row[k] = (int32_t)spans[i].row;
+        a.delta[k] = (int32_t)spans[i].delta;
+        a.block_begin[k + 1] = a.block_begin[k] + (int32_t)spans[i].len;
+      }
+      a.n_spans = (int32_t)(s1 - s0);
+      if (a.pos || a.n_bufs > 0)
+        if (int e = hip_check(timed("relocate", st, [&] { return launch_relocate(a, st); }), "relocation launch"))
+          return e;
+      b0 += kMaxBufPerLaunch;
+    } while (b0 < kbufs.size());
+  }
+  return TU_OK;
+}
+
+// The runs of `live` (row order) with the positions of each move's source range
+// shifted to its destination (rows keep their place), in row order.
+std::vector<tu_interval> relabel_runs(const tu_interval* live, int n_live, const int64_t* moves, int n) {
+  std::vector<tu_interval> out;
+  for (int i = 0; i < n_live; ++i) {
+    int64_t cur = live[i].begin;
+    const int64_t end = live[i].end;
+    int lo = 0, hi = n;   // first move whose source ends after cur
+    while (lo < hi) {
+      const int mid = (lo + hi) / 2;
+      if (moves[3 * mid + 1] <= cur) lo = mid + 1;
+      else hi = mid;
+    }
+    for (int q = lo; q < n && moves[3 * q] < end; ++q) {
+      const int64_t a = std::max(cur, moves[3 * q]), b = std::min(end, moves[3 * q + 1]);
+      const int64_t d = moves[3 * q + 2] - moves[3 * q];
+      push_run(out, cur, a);
+      push_run(out, a + d, b + d);
+      cur = b;
+    }
+    push_run(out, cur, end);
+  }
+  return out;
+}
+
 // ------------------------------------------------------------------ stack update
 
 struct StackPlan {
   std::vector<RangeCheck> rc;
   std::vector<std::vector<tu_interval>> final_iv;   // after the tail is appended
+  std::vector<int64_t> cursor_after;                // cursor once the update commits
   std::vector<int64_t> tail_begin;   // row offset of each context in the packed tail inputs
   // removal of rows inside the tail once it is prefilled (maintenance delimiters)
   std::vector<RangeCheck> post_rc;
@@ -599,6 +764,7 @@ int validate_stack(const tu_update* u, StackPlan* sp) {
   if (u->n_layers < 0 || (u->n_layers > 0 && !u->layers)) return fail(TU_ERR_ARG, "bad layer list");
   sp->rc.assign(u->n_seq, RangeCheck{});
   sp->final_iv.assign(u->n_seq, {});
+  sp->cursor_after.assign(u->n_seq, 0);
   sp->tail_begin.assign(u->n_seq + 1, 0);
   sp->post_rc.assign(u->n_seq, RangeCheck{});
   sp->post_seq.assign(u->n_seq, tu_seq{});
@@ -622,26 +788,42 @@ int validate_stack(const tu_update* u, StackPlan* sp) {
     if (L_keep + su.T > su.seq->capacity)
       return fail(TU_ERR_CAPACITY, "context %d: %lld surviving + %lld tail rows exceed capacity %lld", s,
                   (long long)L_keep, (long long)su.T, (long long)su.seq->capacity);
-    if (su.seq->next_pos + su.T > INT32_MAX) return fail(TU_ERR_ARG, "context %d: positions overflow int32", s);
     if (L_keep + su.T > INT32_MAX / 2) return fail(TU_ERR_ARG, "context %d: too many rows", s);
+    const int pl = su.placement;
+    if (pl != TU_PLACE_TAIL && pl != TU_PLACE_SLOT && pl != TU_PLACE_RELOCATE)
+      return fail(TU_ERR_ARG, "context %d: unknown placement %d", s, pl);
+    // the tail is computed at next_pos + i unless it is slot-placed
+    if (pl != TU_PLACE_SLOT && su.seq->next_pos + su.T > INT32_MAX)
+      return fail(TU_ERR_ARG, "context %d: positions overflow int32", s);
     sp->final_iv[s] = sp->rc[s].live_after;
-    append_tail(sp->final_iv[s], su.seq->next_pos, su.T);
+    if (pl == TU_PLACE_TAIL) {
+      if (su.n_place_runs != 0) return fail(TU_ERR_ARG, "context %d: placement runs given for a true-tail update", s);
+      push_run(sp->final_iv[s], su.seq->next_pos, su.seq->next_pos + su.T);
+      sp->cursor_after[s] = su.seq->next_pos + su.T;
+    } else {
+      if (int e = check_place_runs(su.place_runs, su.n_place_runs, su.T, sp->rc[s].live_after, s)) return e;
+      int64_t last = 0;
+      for (int q = 0; q < su.n_place_runs; ++q) {
+        push_run(sp->final_iv[s], su.place_runs[2 * q], su.place_runs[2 * q + 1]);
+        last = std::max(last, su.place_runs[2 * q + 1]);
+      }
+      sp->cursor_after[s] = std::max(pl == TU_PLACE_SLOT ? su.seq->next_pos : su.seq->next_pos + su.T, last);
+    }
     if ((int64_t)sp->final_iv[s].size() > su.seq->live_cap)
       return fail(TU_ERR_CAPACITY, "context %d: live-interval list would exceed %d", s, su.seq->live_cap);
-    // ranges removed after the prefill must lie inside this call's tail
+    // ranges removed after the prefill must be made of this call's tail positions
     tu_seq& ps = sp->post_seq[s];
     ps = *su.seq;
     ps.len = L_keep + su.T;
-    ps.next_pos = su.seq->next_pos + su.T;
+    ps.next_pos = sp->cursor_after[s];
     ps.live = sp->final_iv[s].data();
     ps.n_live = (int32_t)sp->final_iv[s].size();
     if (su.n_post_ranges < 0 || (su.n_post_ranges > 0 && !su.post_ranges))
       return fail(TU_ERR_ARG, "context %d: bad post-prefill ranges", s);
-    for (int q = 0; q < su.n_post_ranges; ++q)
-      if (su.post_ranges[2 * q] < su.seq->next_pos || su.post_ranges[2 * q + 1] > ps.next_pos)
-        return fail(TU_ERR_RANGE, "context %d: post-prefill range %d lies outside the tail [%lld, %lld)", s, q,
-                    (long long)su.seq->next_pos, (long long)ps.next_pos);
     if (int e = check_ranges(&ps, su.post_ranges, su.n_post_ranges, &sp->post_rc[s])) return e;
+    for (const auto& span : sp->post_rc[s].spans)
+      if (span.first < L_keep)
+        return fail(TU_ERR_RANGE, "context %d: a post-prefill range holds positions outside this call's tail", s);
     if ((int64_t)sp->post_rc[s].live_after.size() > su.seq->live_cap)
       return fail(TU_ERR_CAPACITY, "context %d: live-interval list would exceed %d", s, su.seq->live_cap);
     sp->any_post = sp->any_post || sp->post_rc[s].removed > 0;
@@ -739,6 +921,10 @@ std::vector<AttnItem> stack_attn_items(const tu_update* u, const StackPlan& sp, 
     it.v = static_cast<const bf16_t*>(L.v) + r0 * krow;
     it.out = L.out + r0 * qrow;
     it.q_hat = nullptr;
+    if (su.placement == TU_PLACE_SLOT) {
+      it.place_runs = su.place_runs;
+      it.n_place_runs = su.n_place_runs;
+    }
     items.push_back(it);
   }
   return items;
@@ -902,7 +1088,7 @@ int commit_tail(tu_seq* seq, int64_t T) {
   if (seq->len + T > seq->capacity) return fail(TU_ERR_CAPACITY, "commit exceeds capacity");
   if (seq->next_pos + T > INT32_MAX) return fail(TU_ERR_ARG, "positions overflow int32");
   std::vector<tu_interval> iv(seq->live, seq->live + seq->n_live);
-  append_tail(iv, seq->next_pos, T);
+  push_run(iv, seq->next_pos, seq->next_pos + T);
   if ((int64_t)iv.size() > seq->live_cap) return fail(TU_ERR_CAPACITY, "live-interval list full");
   commit_intervals(seq, iv);
   seq->len += T;
@@ -1044,6 +1230,54 @@ size_t update_layer_stack_workspace_size(const tu_update* u) {
   return stack_workspace(u, sp).total();
 }
 
+int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu_attn_params* p,
+                  const int64_t* moves, int32_t n_moves, void* stream) {
+  if (int e = check_seq(seq)) return e;
+  if (n_layers < 0 || (n_layers > 0 && !k_layers)) return fail(TU_ERR_ARG, "bad layer array");
+  if (n_layers > 0) {
+    if (int e = check_attn(p)) return e;
+    for (int l = 0; l < n_layers; ++l)
+      if (!k_layers[l] || !aligned16(k_layers[l])) return fail(TU_ERR_ARG, "key cache %d null or misaligned", l);
+  }
+  if (n_moves < 0 || n_moves > TU_MAX_RANGES || (n_moves > 0 && !moves))
+    return fail(TU_ERR_ARG, "0 .. %d moves", TU_MAX_RANGES);
+  const RunIndex ri(seq->live, seq->n_live);
+  std::vector<int64_t> src(2 * (size_t)std::max(1, (int)n_moves));
+  std::vector<RelocSpan> spans;
+  std::vector<tu_interval> dst;
+  int64_t prev_end = INT64_MIN, last = seq->next_pos;
+  for (int q = 0; q < n_moves; ++q) {
+    const int64_t s = moves[3 * q], e = moves[3 * q + 1], d = moves[3 * q + 2];
+    if (e <= s || s < prev_end || s < 0)
+      return fail(TU_ERR_RANGE, "move %d: sources must be non-empty, sorted and disjoint", q);
+    if (d < 0 || d + (e - s) > INT32_MAX) return fail(TU_ERR_RANGE, "move %d: destination outside [0, 2^31 - 1)", q);
+    std::vector<std::pair<int64_t, int64_t>> sp;
+    if (!range_rows(ri, s, e, &sp)) return fail(TU_ERR_RANGE, "move %d: source [%lld,%lld) is not live", q,
+                                               (long long)s, (long long)e);
+    for (const auto& x : sp)
+      if (d != s) spans.push_back({x.first, x.second, d - s});
+    src[2 * q] = s;
+    src[2 * q + 1] = e;
+    dst.push_back({d, d + (e - s)});
+    last = std::max(last, d + (e - s));
+    prev_end = e;
+  }
+  if ((int)spans.size() > TU_MAX_RANGES) return fail(TU_ERR_RANGE, "the moves map to more than %d row spans", TU_MAX_RANGES);
+  // destinations: disjoint from each other and from every row that stays
+  std::vector<tu_interval> all = subtract_runs(seq->live, seq->n_live, src.data(), n_moves);
+  all.insert(all.end(), dst.begin(), dst.end());
+  std::sort(all.begin(), all.end(), [](const tu_interval& x, const tu_interval& y) { return x.begin < y.begin; });
+  for (size_t i = 1; i < all.size(); ++i)
+    if (all[i].begin < all[i - 1].end) return fail(TU_ERR_RANGE, "destinations overlap each other or live rows");
+  const std::vector<tu_interval> runs = relabel_runs(seq->live, seq->n_live, moves, n_moves);
+  if ((int64_t)runs.size() > seq->live_cap) return fail(TU_ERR_CAPACITY, "live-interval list would exceed %d", seq->live_cap);
+  std::vector<void*> kbufs(k_layers, k_layers + std::max(0, (int)n_layers));
+  if (int e = run_relocation(spans, kbufs, seq->d_pos, p, static_cast<hipStream_t>(stream))) return e;
+  commit_intervals(seq, runs);
+  seq->next_pos = last;
+  return ok();
+}
+
 int tu_profile_enable(int on) {
   g_prof = on != 0;
   return ok();
@@ -1139,6 +1373,24 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
     plan_attention(&u->attn, items, ws_attn, &ls, &b);
     if (int e = run_attention(ls, u->attn.head_dim, st)) return e;
   }
+  // tail-and-relocate: the stored keys of the tail turn from their computed
+  // positions to the placed ones (values and recurrent state stay as computed)
+  for (int s = 0; s < u->n_seq && sp.n_attn; ++s) {
+    const tu_seq_update& su = u->seqs[s];
+    if (su.placement != TU_PLACE_RELOCATE || su.T == 0) continue;
+    const int64_t L_keep = su.seq->len - sp.rc[s].removed;
+    std::vector<RelocSpan> spans;
+    for (int q = 0, t0 = 0; q < su.n_place_runs; ++q) {
+      const int64_t n = su.place_runs[2 * q + 1] - su.place_runs[2 * q];
+      const int64_t delta = su.place_runs[2 * q] - (su.seq->next_pos + t0);
+      if (delta != 0) spans.push_back({L_keep + t0, n, delta});
+      t0 += (int)n;
+    }
+    std::vector<void*> kbufs;
+    for (int l = 0; l < u->n_layers; ++l)
+      if (u->layers[l].kind == TU_LAYER_ATTN) kbufs.push_back(u->layers[l].k_cache[s]);
+    if (int e = run_relocation(spans, kbufs, su.seq->d_pos, &u->attn, st)) return e;
+  }
   // rows of the tail removed once it is prefilled (maintenance delimiters): their
   // direct KV goes, their effect on the recurrent state and on later rows stays
   if (sp.n_attn && sp.any_post) {
@@ -1157,7 +1409,7 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
     const bool post = sp.n_attn && sp.post_rc[s].removed > 0;
     commit_intervals(seq, post ? sp.post_rc[s].live_after : sp.final_iv[s]);
     seq->len = seq->len - sp.rc[s].removed + u->seqs[s].T - (post ? sp.post_rc[s].removed : 0);
-    seq->next_pos += u->seqs[s].T;
+    seq->next_pos = sp.cursor_after[s];
   }
   return ok();
 }

@@ -142,11 +142,16 @@ struct RopeSeq {
   int32_t L_keep;
   int32_t T;
   int32_t tok_begin;
+  int32_t run_begin;   // slot placement: first entry in RopeArgs::runs (n_runs == 0: cursor + i)
+  int32_t n_runs;
   int32_t pad;
 };
 
+constexpr int kMaxPlaceRunsPerLaunch = 32;   // TU_MAX_PLACE_RUNS
+
 struct RopeArgs {
   RopeSeq seq[kMaxSeqPerLaunch];
+  int32_t runs[kMaxPlaceRunsPerLaunch][2];   // (first position, first tail token) of each placement run
   int32_t n_seq;
   int32_t n_q_heads;
   int32_t n_kv_heads;
@@ -222,6 +227,24 @@ struct DeltaArgs {
   _Float16* ws_kt;       // [chunks][Hv][dk][C]  2^(lg_last - lg) k, transposed
 };
 
+// Key relocation: one workgroup per moved row; every key buffer of the launch gets the
+// row's rotary pairs turned by delta positions, and d_pos (when given) the new label.
+constexpr int kMaxRelocSpans = 64;
+struct RelocArgs {
+  bf16_t* bufs[kMaxBufPerLaunch];              // key caches [cap][Hkv][D]
+  int32_t* pos;                                // d_pos, or null
+  int32_t row[kMaxRelocSpans];                 // first row of each span
+  int32_t delta[kMaxRelocSpans];               // position shift of each span
+  int32_t block_begin[kMaxRelocSpans + 1];     // prefix of the span lengths
+  int32_t n_spans;
+  int32_t n_bufs;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t rotary_dim;
+  int32_t pad;
+  double theta;
+};
+
 // One tensor of a short-convolution launch: x [T][C] bf16, weights [C][W] bf16, state
 // [W-1][C] bf16 (in place), out [T][C] bf16.
 struct ConvJob {
@@ -251,6 +274,7 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 // RoPE + append of the tail tokens and the V^T packing of every key tile, one launch
 hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_relocate(const RelocArgs& a, hipStream_t s);
 int conv_blocks(ConvJob& j, int block_begin);   // sets block_begin / n_cblocks, returns the job's workgroups
 hipError_t launch_short_conv(const ConvArgs& a, int blocks, int width, hipStream_t s);
 hipError_t launch_attention_merge(const MergeArgs& a, int total_rows, int head_dim, hipStream_t s);

@@ -1,7 +1,9 @@
 // True-tail placement (paper Section 4.1, Eq. 3; Section 4.2): the replacement
 // tokens are rotated at their actual new tail positions cursor + i, and their
 // keys and values are appended after the surviving rows. Keys are never rotated
-// back and no placeholder rows are written.
+// back and no placeholder rows are written. For the slot-preserving arm the paper
+// compares (Section 5.2) the rotation uses positions from a short table of runs
+// instead, the rows still being appended after the surviving ones.
 //
 // The same launch also packs every 64-key V tile of the attention into the f16 V^T
 // layout the attention kernel stages (k_stage: the first workgroups rotate tokens, the
@@ -40,7 +42,12 @@ __device__ void rope_token(const RopeArgs& a, int tok) {
   const int Hkv = a.n_kv_heads;
   const int r = a.rotary_dim;
   const int half = r >> 1;
-  const int64_t p = S.cursor + i;
+  int64_t p = S.cursor + i;
+  if (S.n_runs > 0) {   // slot placement: the run holding tail token i
+    int q = S.run_begin;
+    while (q + 1 < S.run_begin + S.n_runs && a.runs[q + 1][1] <= i) ++q;
+    p = (int64_t)a.runs[q][0] + (i - a.runs[q][1]);
+  }
   const long row = (long)S.L_keep + i;
 
   const bf16_t* q = S.q + (long)i * Hq * D;
@@ -175,7 +182,51 @@ __global__ __launch_bounds__(kRopeThreads) void k_stage(RopeArgs r, AttnArgs a, 
   if (b - rope_tokens < a.pack_items) vt_pack_tile<D>(a, b - rope_tokens);
 }
 
+// Key relocation (Section 5.2, tail-and-relocate): one workgroup per moved row. The
+// row's shift delta gives the angles delta * theta^(-2j/r), formed in float64 once per
+// rotary pair into LDS; every key buffer's row is then turned pair by pair in place
+// (float64 rotation of the stored bf16 values, rounded to bf16 nearest even), and the
+// row's position label moves by delta.
+__global__ __launch_bounds__(kRopeThreads) void k_relocate(RelocArgs a) {
+  __shared__ double s_cos[kMaxHalf];
+  __shared__ double s_sin[kMaxHalf];
+  const int b = blockIdx.x;
+  int s = 0;
+  while (s + 1 < a.n_spans && a.block_begin[s + 1] <= b) ++s;
+  const long row = (long)a.row[s] + (b - a.block_begin[s]);
+  const int delta = a.delta[s];
+  const int D = a.head_dim, Hkv = a.n_kv_heads, r = a.rotary_dim, half = r >> 1;
+  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+    const double w = pow(a.theta, -2.0 * (double)j / (double)r);
+    double sn, cs;
+    sincos((double)delta * w, &sn, &cs);
+    s_cos[j] = cs;
+    s_sin[j] = sn;
+  }
+  __syncthreads();
+  for (int bi = 0; bi < a.n_bufs; ++bi) {
+    bf16_t* x = a.bufs[bi] + row * Hkv * D;
+    for (int w = threadIdx.x; w < Hkv * half; w += blockDim.x) {
+      const int h = w / half, j = w - h * half;
+      bf16_t* y = x + (long)h * D;
+      const double av = (double)bf16_to_f32(y[j]);
+      const double bv = (double)bf16_to_f32(y[j + half]);
+      y[j] = (bf16_t)f64_to_bf16_rne(av * s_cos[j] - bv * s_sin[j]);
+      y[j + half] = (bf16_t)f64_to_bf16_rne(bv * s_cos[j] + av * s_sin[j]);
+    }
+  }
+  if (threadIdx.x == 0 && a.pos) a.pos[row] += delta;
+}
+
 }  // namespace
+
+hipError_t launch_relocate(const RelocArgs& a, hipStream_t s) {
+  const int blocks = a.block_begin[a.n_spans];
+  if (blocks <= 0) return hipSuccess;
+  if (a.n_bufs > 0 && a.rotary_dim > 2 * kMaxHalf) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_relocate, dim3(blocks), dim3(kRopeThreads), 0, s, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const AttnArgs& a, int head_dim, hipStream_t s) {
   const int blocks = rope_tokens + a.pack_items;

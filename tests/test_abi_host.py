@@ -208,3 +208,128 @@ def test_commit_tail_advances_cursor_and_intervals(L):
     assert a.intervals() == [(0, 10), (20, 30), (40, 48)] and a.next_pos == 48
     with pytest.raises(tu.TailUpdateError):
         tu.commit_tail(a, 1000)
+
+
+def _runs_of(positions):
+    """Maximal runs of consecutive positions, in the given (row) order."""
+    out = []
+    for p in positions:
+        if out and out[-1][1] == p:
+            out[-1] = (out[-1][0], p + 1)
+        else:
+            out.append((p, p + 1))
+    return out
+
+
+def test_live_runs_in_row_order(L):
+    # rows hold positions in work order: slot-placed rows carry earlier positions
+    rng = np.random.default_rng(8)
+    for trial in range(200):
+        cursor = int(rng.integers(20, 300))
+        live = rng.choice(cursor, size=int(rng.integers(1, cursor)), replace=False)
+        order = np.sort(live)
+        # cut the sorted positions into blocks and shuffle the blocks (row order)
+        cuts = np.sort(rng.choice(np.arange(1, len(order)), size=min(len(order) - 1, int(rng.integers(0, 5))),
+                              replace=False)) if len(order) > 1 else []
+        blocks = np.split(order, cuts)
+        rng.shuffle(blocks)
+        rows = np.concatenate(blocks)
+        ctx = _ctx(_runs_of(rows.tolist()), cursor, live_cap=512)
+        n = int(rng.integers(0, 4))
+        starts = np.sort(rng.integers(0, cursor, size=n))
+        ranges = [(int(a), int(a + rng.integers(1, 6))) for a in starts]
+        try:
+            oracle.validate_ranges(ranges, rows, cursor)
+            expect_ok = True
+        except oracle.RangeError:
+            expect_ok = False
+        if expect_ok:
+            assert ctx.validate_ranges(ranges) == sum(b - a for a, b in ranges)
+        else:
+            with pytest.raises(tu.TailUpdateError):
+                ctx.validate_ranges(ranges)
+    # a run list that is not well formed is rejected
+    for ivs, cursor in [([(0, 5), (5, 9)], 10),      # consecutive runs not merged
+                        ([(0, 5), (3, 9)], 10),      # overlapping runs
+                        ([(6, 9), (0, 3), (2, 4)], 10),
+                        ([(0, 5)], 4)]:              # beyond the cursor
+        ctx = _ctx([(0, 1)], 10)
+        ctx.set_metadata(ivs, cursor)
+        with pytest.raises(tu.TailUpdateError) as ei:
+            ctx.validate_ranges([])
+        assert ei.value.code == B.TU_ERR_ARG
+    # non-adjacent rows may hold adjacent positions: one range covering both is two row spans
+    ctx = _ctx([(0, 10), (50, 60), (10, 20)], 70)
+    assert ctx.validate_ranges([(5, 15)]) == 10
+
+
+def _placed(placement, runs, post=None, T=512, ranges=((100, 228),)):
+    a = _ctx([(0, 1000)], 1000, capacity=1600)
+    attn = tu.attn_params(16, 2, 256)
+    fake = torch.zeros(64, dtype=torch.float32)
+    layers = [tu.LayerIO(B.TU_LAYER_ATTN, fake, fake, fake, fake, k_cache=[fake], v_cache=[fake])]
+    return a, tu.StackUpdate([a], [list(ranges)], [T], layers, attn, None, post_ranges=post,
+                             placement=[placement], place_runs=[runs])
+
+
+def test_validate_placements(L):
+    # slot-preserving: the replacement takes the removed record's slot plus a free range
+    for placement in ("slot", "relocate"):
+        a, up = _placed(placement, [(100, 228), (5000, 5384)])
+        up.validate()
+        assert up.workspace_size() > 0
+        a, up = _placed(placement, [(100, 228), (5000, 5384)], post=[[(100, 111), (5381, 5384)]])
+        up.validate()
+    bad = [
+        ("slot", [(100, 229), (5000, 5383)], B.TU_ERR_RANGE),      # 228 is still live
+        ("slot", [(100, 228), (5000, 5383)], B.TU_ERR_ARG),        # 511 positions for 512 tokens
+        ("relocate", [(100, 228), (150, 534)], B.TU_ERR_RANGE),    # runs overlap each other
+        ("slot", [(-4, 508)], B.TU_ERR_RANGE),
+        ("slot", [(2 ** 31 - 100, 2 ** 31 + 412)], B.TU_ERR_RANGE),
+        ("slot", [(10000 + 16 * i, 10016 + 16 * i) for i in range(32)] + [(9000, 9000)], B.TU_ERR_ARG),  # > 32 runs
+        ("tail", [(5000, 5512)], B.TU_ERR_ARG),                    # runs with a true-tail update
+    ]
+    for placement, runs, code in bad:
+        a, up = _placed(placement, runs)
+        before = (a.intervals(), a.len, a.next_pos)
+        with pytest.raises(tu.TailUpdateError) as ei:
+            up.validate()
+        assert ei.value.code == code, (placement, runs)
+        assert (a.intervals(), a.len, a.next_pos) == before
+    # post-prefill ranges must be made of the tail's final positions
+    a, up = _placed("slot", [(100, 228), (5000, 5384)], post=[[(1000, 1011)]])
+    with pytest.raises(tu.TailUpdateError) as ei:
+        up.validate()
+    assert ei.value.code == B.TU_ERR_RANGE
+    a, up = _placed("slot", [(100, 228), (5000, 5384)], post=[[(90, 105)]])   # starts in surviving rows
+    with pytest.raises(tu.TailUpdateError) as ei:
+        up.validate()
+    assert ei.value.code == B.TU_ERR_RANGE
+    a, up = _placed("tail", None)
+    up.u.seqs[0].placement = 7
+    with pytest.raises(tu.TailUpdateError) as ei:
+        up.validate()
+    assert ei.value.code == B.TU_ERR_ARG
+
+
+def test_relocate_keys_rejects_before_touching_device(L):
+    a = _ctx([(0, 100), (200, 300)], 400, capacity=256)
+    p = tu.attn_params(16, 2, 256)
+    fake = torch.zeros(64, dtype=torch.float32)
+    before = (a.intervals(), a.len, a.next_pos)
+    for moves in ([(50, 150, 1000)],             # source not live
+                  [(50, 60, 95)],                # destination hits a row that stays
+                  [(50, 60, 1000), (55, 65, 2000)],   # overlapping sources
+                  [(60, 70, 1000), (50, 55, 2000)],   # unsorted sources
+                  [(50, 60, 1000), (250, 260, 1005)],  # destinations overlap each other
+                  [(50, 60, -3)], [(50, 60, 2 ** 31 - 5)], [(60, 50, 1000)]):
+        with pytest.raises(tu.TailUpdateError) as ei:
+            tu.relocate_keys(a, [fake], p, moves)
+        assert ei.value.code == B.TU_ERR_RANGE, moves
+        assert (a.intervals(), a.len, a.next_pos) == before
+    with pytest.raises(tu.TailUpdateError) as ei:
+        tu.relocate_keys(a, [fake], tu.attn_params(15, 2, 256), [(50, 60, 1000)])
+    assert ei.value.code == B.TU_ERR_ARG
+    # a move onto its own positions changes nothing and launches nothing
+    tu.relocate_keys(a, [fake], p, [(50, 60, 50)])
+    assert (a.intervals(), a.len, a.next_pos) == before
