@@ -17,7 +17,10 @@ What it computes (paper: Section 4.1, Eq. 2 and Eq. 3; Section 4.2):
     carried state (Section 4.1, Fig. 2: convolution state continues);
   * dense refill and fresh gapped prefill of the final context (Section 5.2);
   * the slot-preserving and tail-and-relocate placements of the replacement and the
-    relocation of stored keys to other positions (Section 5.2, Section 6.3).
+    relocation of stored keys to other positions (Section 5.2, Section 6.3);
+  * the attention diagnostics of Section 5.3: float32 reference-softmax probe
+    distributions, memory-group masses, effective group count, boundary-window share
+    and total variation distance.
 
 Functions with no independent pin are marked "parity unpinned" in their
 docstring; at present there are none.
@@ -29,6 +32,7 @@ from .attention import causal_gqa_attention  # noqa: F401
 from .delta import gated_delta_tokens, gated_delta_chunked  # noqa: F401
 from .short_conv import silu, short_conv_continue  # noqa: F401
 from .placement import check_new_positions, relocate_keys  # noqa: F401
+from .diagnostics import probe_distribution, group_masses, group_summary, tv_distance  # noqa: F401
 from .update import (  # noqa: F401
     attention_layer_update,
     delta_layer_update,
