@@ -309,6 +309,11 @@ def short_conv_row(tu, synth, cfg, T, dev, reps):
             "frac": round(ach / HBM_PEAK_GBS, 4)}
 
 
+def lib_probe_ws(tu, attn_p, length, n_probe):
+    import ctypes
+    return max(256, int(tu.lib().attention_probe_workspace_size(ctypes.byref(attn_p), length, n_probe)))
+
+
 def measured_peaks(dev):
     """Rates this GPU sustains in this run, as a second reference beside the datasheet peaks:
     a plain 1 GiB device copy (bytes read + written per second) and an 8192^3 bf16 GEMM
@@ -629,6 +634,59 @@ def main():
             del copies4, ups4, ws4
         extra["placement"] = place_row
         print(f"[bench] placements: {json.dumps(place_row)}", file=sys.stderr, flush=True)
+
+    # ---- attention diagnostics (Section 5.3): float32 reference-softmax probe of the last
+    # eight tail rows of every attention layer (averaged over layers), masses of 390-token
+    # memory groups with the effective group count, and the total variation between the
+    # probes of the first and the last attention layer, after the first round
+    if kinds.count("attn") and len(chars) == 1:
+        (ctxs, own) = make_copy(tu, chars, layers, dev)
+        up = round_updates(tu, ctxs, own, layers, rounds[:1], attn_p, delta_p)
+        wsd = torch.empty(up[0].workspace_size(), dtype=torch.uint8, device=dev)
+        run_step(up, wsd)
+        torch.cuda.synchronize()
+        ctx = ctxs[0]
+        n_probe = min(8, ctx.len)
+        att = [(L, O) for L, O in zip(layers, own) if L["kind"] == "attn"]
+        qs = [rounds[0]["inputs"][i]["q"][-n_probe:].contiguous() for i, L in enumerate(layers) if L["kind"] == "attn"]
+        probs = torch.zeros(ctx.len, dtype=torch.float32, device=dev)
+        pws = torch.empty(lib_probe_ws(tu, attn_p, ctx.len, n_probe), dtype=torch.uint8, device=dev)
+        first = torch.zeros_like(probs)
+        last = torch.zeros_like(probs)
+
+        def probe_all():
+            probs.zero_()
+            for (L, O), q in zip(att, qs):
+                tu.attention_probe(ctx, O["caches"][0][0], attn_p, q, probs, weight=1.0 / len(att), workspace=pws)
+        probe_all()
+        tu.attention_probe(ctx, att[0][1]["caches"][0][0], attn_p, qs[0], first, workspace=pws)
+        tu.attention_probe(ctx, att[-1][1]["caches"][0][0], attn_p, qs[-1], last, workspace=pws)
+        groups = [(g, min(g + 390, ctx.next_pos)) for g in range(0, ctx.next_pos, 390)]
+        gws = torch.empty(1 << 20, dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        tu.profile_enable(True)      # GPU time of the library's launches (HIP events on the stream)
+        for _ in range(K):
+            probe_all()
+            mass, win, summary = tu.attention_group_mass(ctx, probs, groups, window=8, workspace=gws)
+            tv = tu.attention_tv_distance(first, last, workspace=gws)
+        dp = tu.profile_collect()
+        tu.profile_enable(False)
+        probe_ms = dp["probe"][1] / K
+        group_ms = dp["group_mass"][1] / K
+        tv_ms = dp["tv_distance"][1] / K
+        kbytes = ctx.len * a.n_kv_heads * a.head_dim * 2 * len(att)
+        s = summary.cpu().tolist()
+        extra["attention_diagnostics"] = {
+            "probe_rows": n_probe, "layers": len(att), "live_rows": ctx.len, "probe_ms": round(probe_ms, 5),
+            "probe_key_bytes": kbytes, "bound": "hbm",
+            "achieved": round(kbytes / (probe_ms / 1e3) / 1e9, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
+            "groups": len(groups), "group_mass_ms": round(group_ms, 5), "tv_ms": round(tv_ms, 5),
+            "memory_mass": round(s[0], 6), "effective_group_count": round(s[1], 3), "window_share": round(s[2], 5),
+            "tv_first_last_attention_layer": round(float(tv[0]), 6) if len(att) > 1 else None,
+            "timing": "GPU time of the library's launches (HIP events around each launch)"}
+        print(f"[bench] attention diagnostics: {json.dumps(extra['attention_diagnostics'])}", file=sys.stderr,
+              flush=True)
+        del ctxs, own, up, wsd, pws, gws
 
     # ---- the short-convolution continuation of one delta layer's q, k, v (width 4, SiLU)
     if kinds.count("delta"):

@@ -335,6 +335,48 @@ int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu
                   const int64_t* moves, int32_t n_moves, void* stream);
 
 /*
+ * Attention diagnostics (Section 5.3, Appendix D). The probe queries are the last
+ * n_probe rows of a context; probe query i sees rows 0 .. len - n_probe + i (the
+ * causal rule of the update). Their raw queries are rotated at the rows' positions
+ * (float64 angles, bf16 nearest even, as the cached keys were); scores
+ * softmax_scale * q.k are products of the bf16 values summed in fp32; the reference
+ * softmax over the visible rows is fp32. Holes hold no rows, so they are in no
+ * denominator.
+ *
+ * attention_probe: probs[j] += weight * (mean over the n_probe queries and all query
+ * heads of the softmax probability of row j), for j < seq->len (rows no query sees
+ * get 0). Averaging layers: call once per attention layer with weight 1 / layers.
+ *  k_cache: device bf16 [capacity][n_kv_heads][head_dim] of the layer;
+ *  q:       device bf16 [n_probe][n_q_heads][head_dim] raw queries of the probe rows;
+ *  probs:   device fp32 [>= seq->len], read and written.
+ *  1 <= n_probe <= len, n_probe * n_q_heads / n_kv_heads <= 128. The workspace
+ *  holds the fp32 score rows (n_probe * n_q_heads x len).
+ *
+ * attention_group_mass: memory groups given as host int64 [n_groups][2] position
+ * ranges (sorted, disjoint; one per record). mass[g] = sum of probs over the rows whose
+ * position lies in group g; window_mass[g] (optional) the same over the group's first
+ * `window` positions (the paper uses 8); summary (optional, device fp32 [3]) = {memory
+ * mass M = sum_g mass[g], effective group count exp(-sum_g a_g log a_g) with
+ * a_g = mass[g] / M, boundary-window share sum_g window_mass[g] / M}. Accumulated in
+ * float64 with atomic adds (the summation order, hence the last float64 bits, may
+ * vary between runs), reported as fp32.
+ *
+ * attention_tv_distance: tv[0] = 0.5 * sum_j |p[j] - q[map(j)]| over j < n, where
+ * map = q_row_of_p (device int32 [n], the row of the same token in the other
+ * construction) or the identity when NULL. Float64 partial sums in a fixed order.
+ */
+size_t attention_probe_workspace_size(const tu_attn_params* p, int64_t len, int32_t n_probe);
+int attention_probe(const tu_seq* seq, const void* k_cache, const tu_attn_params* p, const void* q, int32_t n_probe,
+                    float weight, float* probs, void* workspace, size_t workspace_bytes, void* stream);
+size_t attention_group_mass_workspace_size(int32_t n_groups);
+int attention_group_mass(const tu_seq* seq, const float* probs, const int64_t* groups, int32_t n_groups,
+                         int32_t window, float* mass, float* window_mass, float* summary, void* workspace,
+                         size_t workspace_bytes, void* stream);
+size_t attention_tv_workspace_size(int64_t n);
+int attention_tv_distance(const float* p, const float* q, const int32_t* q_row_of_p, int64_t n, float* tv,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Kernel timing (diagnostics, not part of the update). While enabled for the
  * calling thread, every kernel the library launches is bracketed by two HIP
  * events recorded on the launch's stream. tu_profile_collect waits for those
@@ -344,7 +386,7 @@ int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu
  * (or a negative status) and clears the records. Names (one per launch or pair
  * of launches): compact (keep-scan, then gather), rope_vt_pack (RoPE + append of
  * the tail with the V^T packing of the key tiles), attention, attention_merge,
- * delta_prep, delta_chain, short_conv, relocate.
+ * delta_prep, delta_chain, short_conv, relocate, probe, group_mass, tv_distance.
  */
 int tu_profile_enable(int on);
 int tu_profile_collect(char* names, int32_t name_stride, int32_t* counts, double* total_ms, int32_t max_entries);

@@ -6,7 +6,8 @@ compaction, rotary append at the true tail, causal GQA attention over surviving
 + new KV, and the gated delta-rule continuation from the carried state.
 It also continues the recurrent layers' short convolution from its carried state,
 and provides the slot-preserving and tail-and-relocate placements the paper compares
-(Section 5.2) together with the relocation of stored keys.
+(Section 5.2) together with the relocation of stored keys, and the attention
+diagnostics of Section 5.3 (probe distributions, group masses, total variation).
 `binding` is the ctypes layer over its C ABI (include/tailupdate.h).
 """
 from .binding import (  # noqa: F401
@@ -14,6 +15,9 @@ from .binding import (  # noqa: F401
     LayerIO,
     StackUpdate,
     TailUpdateError,
+    attention_group_mass,
+    attention_probe,
+    attention_tv_distance,
     attn_params,
     commit_tail,
     compact_kv,

@@ -101,6 +101,14 @@ _SIGNATURES = {
     "update_layer_stack": (_i32, [ctypes.POINTER(tu_update), _vp, ctypes.c_size_t, _vp]),
     "relocate_keys": (_i32, [ctypes.POINTER(tu_seq), ctypes.POINTER(_vp), _i32, ctypes.POINTER(tu_attn_params),
                              ctypes.POINTER(_i64), _i32, _vp]),
+    "attention_probe_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_attn_params), _i64, _i32]),
+    "attention_probe": (_i32, [ctypes.POINTER(tu_seq), _vp, ctypes.POINTER(tu_attn_params), _vp, _i32, _f32, _vp,
+                               _vp, ctypes.c_size_t, _vp]),
+    "attention_group_mass_workspace_size": (ctypes.c_size_t, [_i32]),
+    "attention_group_mass": (_i32, [ctypes.POINTER(tu_seq), _vp, ctypes.POINTER(_i64), _i32, _i32, _vp, _vp, _vp,
+                                    _vp, ctypes.c_size_t, _vp]),
+    "attention_tv_workspace_size": (ctypes.c_size_t, [_i64]),
+    "attention_tv_distance": (_i32, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
     "tu_profile_enable": (_i32, [_i32]),
     "tu_profile_collect": (_i32, [ctypes.c_char_p, _i32, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double),
                                   _i32]),
@@ -285,6 +293,43 @@ def relocate_keys(ctx: Context, k_layers: Sequence[torch.Tensor], params: Option
     arr, nm = _ranges_array(moves, 3)
     p = params if params is not None else tu_attn_params()
     _check(lib().relocate_keys(ctypes.byref(ctx.c), ks, n, ctypes.byref(p), arr, nm, _stream(stream)))
+
+
+def attention_probe(ctx: Context, k_cache: torch.Tensor, params: tu_attn_params, q: torch.Tensor,
+                    probs: torch.Tensor, weight: float = 1.0, workspace: Optional[torch.Tensor] = None, stream=None):
+    """probs[:len] += weight * the fp32 reference-softmax distribution of the last
+    q.shape[0] rows' queries (raw q [n][Hq][D]) over the rows they see, averaged over
+    those queries and all heads."""
+    n = int(q.shape[0])
+    nbytes = lib().attention_probe_workspace_size(ctypes.byref(params), ctx.len, n)
+    ws = _workspace(nbytes, q.device, workspace)
+    _check(lib().attention_probe(ctypes.byref(ctx.c), _ptr(k_cache), ctypes.byref(params), _ptr(q), n, float(weight),
+                                 _ptr(probs), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def attention_group_mass(ctx: Context, probs: torch.Tensor, groups, window: int = 8,
+                         workspace: Optional[torch.Tensor] = None, stream=None):
+    """Memory-group masses of a token distribution: returns device tensors (mass [m],
+    window mass [m], summary [3] = memory mass, effective group count, window share)."""
+    arr, m = _ranges_array(groups)
+    mass = torch.empty(max(1, m), dtype=torch.float32, device=probs.device)
+    win = torch.empty_like(mass)
+    summary = torch.empty(3, dtype=torch.float32, device=probs.device)
+    ws = _workspace(lib().attention_group_mass_workspace_size(m), probs.device, workspace)
+    _check(lib().attention_group_mass(ctypes.byref(ctx.c), _ptr(probs), arr, m, int(window), _ptr(mass), _ptr(win),
+                                      _ptr(summary), _ptr(ws), ws.numel(), _stream(stream)))
+    return mass[:m], win[:m], summary
+
+
+def attention_tv_distance(p: torch.Tensor, q: torch.Tensor, q_row_of_p: Optional[torch.Tensor] = None,
+                          workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """0.5 * sum |p - q[map]| as a device fp32 tensor [1]."""
+    n = int(p.numel())
+    tv = torch.empty(1, dtype=torch.float32, device=p.device)
+    ws = _workspace(lib().attention_tv_workspace_size(n), p.device, workspace)
+    _check(lib().attention_tv_distance(_ptr(p), _ptr(q), _ptr(q_row_of_p), n, _ptr(tv), _ptr(ws), ws.numel(),
+                                       _stream(stream)))
+    return tv
 
 
 TU_CONV_IDENTITY = 0

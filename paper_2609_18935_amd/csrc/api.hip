@@ -1278,6 +1278,136 @@ int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu
   return ok();
 }
 
+static size_t probe_ws(const tu_attn_params* p, int64_t len, int32_t n_probe, int64_t* ld) {
+  *ld = (len + kProbeKeys - 1) / kProbeKeys * kProbeKeys;
+  const int64_t rows = (int64_t)p->n_q_heads * n_probe;
+  return align_up(sizeof(bf16_t) * rows * p->head_dim) + align_up(sizeof(float) * rows * *ld) +
+         align_up(sizeof(float) * 2 * rows);
+}
+
+size_t attention_probe_workspace_size(const tu_attn_params* p, int64_t len, int32_t n_probe) {
+  if (check_attn(p) || len < 0 || n_probe < 0) return 0;
+  int64_t ld = 0;
+  return std::max<size_t>(probe_ws(p, len, n_probe, &ld), kAlign);
+}
+
+int attention_probe(const tu_seq* seq, const void* k_cache, const tu_attn_params* p, const void* q, int32_t n_probe,
+                    float weight, float* probs, void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_seq(seq)) return e;
+  if (int e = check_attn(p)) return e;
+  const int G = p->n_q_heads / p->n_kv_heads;
+  if (n_probe < 1 || n_probe > seq->len) return fail(TU_ERR_ARG, "n_probe must be in [1, len]");
+  if ((int64_t)n_probe * G > kProbeMaxRows)
+    return fail(TU_ERR_ARG, "n_probe x query heads per KV head must be at most %d", kProbeMaxRows);
+  if ((int64_t)n_probe * p->n_q_heads > 4096) return fail(TU_ERR_ARG, "too many probe rows");
+  if (seq->len > INT32_MAX / 2) return fail(TU_ERR_ARG, "context too long");
+  if (!std::isfinite(weight)) return fail(TU_ERR_ARG, "weight must be finite");
+  if (!k_cache || !q || !probs) return fail(TU_ERR_ARG, "null tensor");
+  if (!aligned16(k_cache) || !aligned16(q)) return fail(TU_ERR_ARG, "tensors must be 16-byte aligned");
+  int64_t ld = 0;
+  const size_t need = probe_ws(p, seq->len, n_probe, &ld);
+  if (!workspace || workspace_bytes < need)
+    return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  Arena ar(workspace);
+  const int64_t rows = (int64_t)p->n_q_heads * n_probe;
+  ProbeArgs a{};
+  a.q = static_cast<const bf16_t*>(q);
+  a.q_hat = static_cast<bf16_t*>(ar.take(sizeof(bf16_t) * rows * p->head_dim));
+  a.scores = static_cast<float*>(ar.take(sizeof(float) * rows * ld));
+  a.stats = static_cast<float*>(ar.take(sizeof(float) * 2 * rows));
+  a.k_cache = static_cast<const bf16_t*>(k_cache);
+  a.pos = seq->d_pos;
+  a.probs = probs;
+  a.len = (int32_t)seq->len;
+  a.n_probe = n_probe;
+  a.ld = (int32_t)ld;
+  a.n_q_heads = p->n_q_heads;
+  a.n_kv_heads = p->n_kv_heads;
+  a.head_dim = p->head_dim;
+  a.rotary_dim = p->rotary_dim;
+  a.theta = p->rope_theta;
+  a.scale = p->softmax_scale;
+  a.weight = weight;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (int e = hip_check(timed("probe", st, [&] { return launch_probe(a, st); }), "probe launch")) return e;
+  return ok();
+}
+
+size_t attention_group_mass_workspace_size(int32_t n_groups) {
+  return align_up(sizeof(double) * 2 * (size_t)std::max(1, (int)n_groups));
+}
+
+int attention_group_mass(const tu_seq* seq, const float* probs, const int64_t* groups, int32_t n_groups,
+                         int32_t window, float* mass, float* window_mass, float* summary, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  if (int e = check_seq(seq)) return e;
+  if (n_groups < 1 || n_groups > (1 << 20) || !groups) return fail(TU_ERR_ARG, "1 .. 2^20 groups");
+  if (window < 0) return fail(TU_ERR_ARG, "negative window");
+  if (!probs || !mass) return fail(TU_ERR_ARG, "null tensor");
+  int64_t prev = INT64_MIN;
+  for (int g = 0; g < n_groups; ++g) {
+    const int64_t a = groups[2 * g], b = groups[2 * g + 1];
+    if (b <= a || a < prev || a < 0 || b > INT32_MAX)
+      return fail(TU_ERR_RANGE, "group %d [%lld,%lld): groups must be non-empty, sorted, disjoint, in [0, 2^31 - 1)", g,
+                  (long long)a, (long long)b);
+    prev = b;
+  }
+  const size_t need = attention_group_mass_workspace_size(n_groups);
+  if (!workspace || workspace_bytes < need)
+    return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  GroupArgs a{};
+  a.pos = seq->d_pos;
+  a.probs = probs;
+  a.acc = static_cast<double*>(workspace);
+  a.mass = mass;
+  a.window_mass = window_mass;
+  a.summary = summary;
+  a.len = (int32_t)seq->len;
+  a.n_total = n_groups;
+  a.window = window;
+  if (int e = hip_check(timed("group_mass", st, [&] { return launch_group_clear(a, st); }), "group clear")) return e;
+  for (int g0 = 0; g0 < n_groups; g0 += kMaxGroupsPerLaunch) {
+    a.g_begin = g0;
+    a.n = std::min(kMaxGroupsPerLaunch, n_groups - g0);
+    for (int g = 0; g < a.n; ++g) {
+      a.range[g][0] = (int32_t)groups[2 * (g0 + g)];
+      a.range[g][1] = (int32_t)groups[2 * (g0 + g) + 1];
+    }
+    if (int e = hip_check(timed("group_mass", st, [&] { return launch_group_mass(a, st); }), "group mass")) return e;
+  }
+  if (int e = hip_check(timed("group_mass", st, [&] { return launch_group_final(a, st); }), "group summary")) return e;
+  return ok();
+}
+
+size_t attention_tv_workspace_size(int64_t n) {
+  if (n < 0) return 0;
+  return align_up(sizeof(double) * (size_t)std::max<int64_t>(1, (n + kTvRowsPerBlock - 1) / kTvRowsPerBlock));
+}
+
+int attention_tv_distance(const float* p, const float* q, const int32_t* q_row_of_p, int64_t n, float* tv,
+                          void* workspace, size_t workspace_bytes, void* stream) {
+  if (n < 0 || n > INT32_MAX) return fail(TU_ERR_ARG, "n outside [0, 2^31 - 1]");
+  if ((n > 0 && (!p || !q)) || !tv) return fail(TU_ERR_ARG, "null tensor");
+  const size_t need = attention_tv_workspace_size(n);
+  if (!workspace || workspace_bytes < need)
+    return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  TvArgs a{};
+  a.p = p;
+  a.q = q;
+  a.map = q_row_of_p;
+  a.partial = static_cast<double*>(workspace);
+  a.tv = tv;
+  a.n = n;
+  a.n_blocks = (int32_t)((n + kTvRowsPerBlock - 1) / kTvRowsPerBlock);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (int e = hip_check(timed("tv_distance", st, [&] { return launch_tv(a, st); }), "tv launch")) return e;
+  return ok();
+}
+
 int tu_profile_enable(int on) {
   g_prof = on != 0;
   return ok();

@@ -245,6 +245,59 @@ struct RelocArgs {
   double theta;
 };
 
+// Attention diagnostics: probe of the last n_probe rows of one layer of one context.
+constexpr int kProbeKeys = 64;       // keys per score workgroup
+constexpr int kProbeMaxRows = 128;   // n_probe x (query heads per KV head)
+struct ProbeArgs {
+  const bf16_t* q;       // [n_probe][Hq][D] raw queries of the probe rows
+  bf16_t* q_hat;         // [n_probe][Hq][D] rotated (workspace)
+  const bf16_t* k_cache; // [cap][Hkv][D]
+  const int32_t* pos;    // d_pos
+  float* scores;         // [Hq * n_probe][ld] (workspace)
+  float* stats;          // [Hq * n_probe][2] (max, 1 / sum) (workspace)
+  float* probs;          // [len] accumulated: probs += weight * mean distribution
+  int32_t len;
+  int32_t n_probe;
+  int32_t ld;            // score row stride, a multiple of kProbeKeys
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t rotary_dim;
+  float scale;
+  float weight;
+  int32_t pad;
+  double theta;
+};
+
+constexpr int kMaxGroupsPerLaunch = 256;
+struct GroupArgs {
+  int32_t range[kMaxGroupsPerLaunch][2];   // this launch's groups: sorted, disjoint position ranges
+  const int32_t* pos;    // d_pos
+  const float* probs;    // [len]
+  double* acc;           // [2][n_total] mass, window mass (workspace)
+  float* mass;           // [n_total]
+  float* window_mass;    // [n_total] or null
+  float* summary;        // [3] or null
+  int32_t len;
+  int32_t n;             // groups in this launch
+  int32_t g_begin;       // index of its first group
+  int32_t n_total;
+  int32_t window;
+  int32_t pad;
+};
+
+constexpr int kTvRowsPerBlock = 4096;
+struct TvArgs {
+  const float* p;
+  const float* q;
+  const int32_t* map;    // row of q for each row of p, or null (identity)
+  double* partial;       // [n_blocks] (workspace)
+  float* tv;             // [1]
+  int64_t n;
+  int32_t n_blocks;
+  int32_t pad;
+};
+
 // One tensor of a short-convolution launch: x [T][C] bf16, weights [C][W] bf16, state
 // [W-1][C] bf16 (in place), out [T][C] bf16.
 struct ConvJob {
@@ -275,6 +328,11 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_relocate(const RelocArgs& a, hipStream_t s);
+hipError_t launch_probe(const ProbeArgs& a, hipStream_t s);
+hipError_t launch_group_clear(const GroupArgs& a, hipStream_t s);
+hipError_t launch_group_mass(const GroupArgs& a, hipStream_t s);
+hipError_t launch_group_final(const GroupArgs& a, hipStream_t s);
+hipError_t launch_tv(const TvArgs& a, hipStream_t s);
 int conv_blocks(ConvJob& j, int block_begin);   // sets block_begin / n_cblocks, returns the job's workgroups
 hipError_t launch_short_conv(const ConvArgs& a, int blocks, int width, hipStream_t s);
 hipError_t launch_attention_merge(const MergeArgs& a, int total_rows, int head_dim, hipStream_t s);

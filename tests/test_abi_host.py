@@ -333,3 +333,26 @@ def test_relocate_keys_rejects_before_touching_device(L):
     # a move onto its own positions changes nothing and launches nothing
     tu.relocate_keys(a, [fake], p, [(50, 60, 50)])
     assert (a.intervals(), a.len, a.next_pos) == before
+
+
+def test_diagnostics_reject_before_touching_device(L):
+    a = _ctx([(0, 100), (200, 300)], 400, capacity=256)
+    p = tu.attn_params(16, 2, 256)
+    fake = torch.zeros(64, dtype=torch.float32)
+    q = torch.zeros(8, 16, 256, dtype=torch.bfloat16)
+    ws = torch.zeros(1 << 20, dtype=torch.uint8)
+    for n, code in [(0, B.TU_ERR_ARG), (201, B.TU_ERR_ARG), (17, B.TU_ERR_ARG)]:   # 17 x 8 rows > 128
+        qq = torch.zeros(max(n, 1), 16, 256, dtype=torch.bfloat16)
+        rc = L.attention_probe(ctypes.byref(a.c), fake.data_ptr(), ctypes.byref(p), qq.data_ptr(), n, 1.0,
+                               fake.data_ptr(), ws.data_ptr(), ws.numel(), None)
+        assert rc == code, n
+    with pytest.raises(tu.TailUpdateError) as ei:   # workspace too small
+        tu.attention_probe(a, fake, p, q, fake, workspace=torch.zeros(256, dtype=torch.uint8))
+    assert ei.value.code == B.TU_ERR_WORKSPACE
+    for groups in ([(10, 20), (15, 30)], [(30, 40), (10, 20)], [(5, 5)], [(-1, 4)]):
+        with pytest.raises(tu.TailUpdateError) as ei:
+            tu.attention_group_mass(a, fake, groups, workspace=ws)
+        assert ei.value.code == B.TU_ERR_RANGE, groups
+    assert L.attention_tv_distance(None, None, None, -1, None, None, 0, None) == B.TU_ERR_ARG
+    assert L.attention_tv_distance(fake.data_ptr(), fake.data_ptr(), None, 10, fake.data_ptr(), None, 0,
+                                   None) == B.TU_ERR_WORKSPACE
