@@ -64,8 +64,11 @@ __device__ __forceinline__ int find_seq_by_chunk(const DeltaArgs& a, int c) {
 }
 
 // ------------------------------------------------------------------ prep
+constexpr int kPrepThreads = 512;   // 8 waves
 template <int DK, int C>
-__global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
+__global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
+  constexpr int NT = kPrepThreads;
+  constexpr int NW = NT / 64;
   constexpr int DV = DK;
   constexpr int NB = C / 16;     // 16-row blocks of the chunk
   constexpr int KP = DK + 8;     // pitch of [C][DK] bf16 tiles
@@ -79,8 +82,8 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
   __shared__ __attribute__((aligned(16))) _Float16 Th[C][CH];
   __shared__ __attribute__((aligned(16))) _Float16 Bt[DK][CH];
   __shared__ __attribute__((aligned(16))) _Float16 Vt[DV][CH];
-  __shared__ float lg[C];
-  __shared__ float bt[C];
+  __shared__ __attribute__((aligned(16))) float lg[C];
+  __shared__ __attribute__((aligned(16))) float bt[C];
 
   const int Hk = a.n_k_heads, Hv = a.n_v_heads;
   const int c = blockIdx.x / Hv;          // global chunk
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
   const int l16 = lane & 15, g4 = lane >> 4;
 
   // ---- phase 0: stage K, Q (bf16), beta, log2 g
-  for (int e = tid; e < C * (DK / 8); e += 256) {
+  for (int e = tid; e < C * (DK / 8); e += NT) {
     const int r = e / (DK / 8), cc = e - r * (DK / 8);
     u32x4 kw = {0, 0, 0, 0}, qw = {0, 0, 0, 0};
     if (r < Cr) {
@@ -106,9 +109,9 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
     *(u32x4*)&Qs[r][cc * 8] = qw;
   }
   // the values this thread converts in phase 5, fetched now so their latency overlaps
-  // phases 1-4 ((C / 4) * (DK / 8) <= 256: one item per thread at most)
+  // phases 1-4 ((C / 4) * (DK / 8) <= NT: one item per thread at most)
   constexpr int NE5 = (C / 4) * (DK / 8);
-  static_assert(NE5 <= 256, "phase 5 maps one item per thread");
+  static_assert(NE5 <= NT, "phase 5 maps one item per thread");
   u32x4 vw[4];
   if (tid < NE5) {
     const int s4 = (tid % (C / 4)) * 4, d0 = (tid / (C / 4)) * 8;
@@ -134,12 +137,12 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
     if (lane < C) lg[lane] = x;
   }
   constexpr int NLB = NB * (NB + 1) / 2;   // lower blocks incl. diagonal
-  constexpr int NPW = (2 * NLB + 3) / 4;   // blocks per wave (KK and QK together)
+  constexpr int NPW = (2 * NLB + NW - 1) / NW;   // blocks per wave (KK and QK together)
   f32x4 acc[NPW];
   int blk_of[NPW];
 #pragma unroll
   for (int j = 0; j < NPW; ++j) {
-    const int idx = wave + 4 * j;
+    const int idx = wave + NW * j;
     blk_of[j] = idx;
     acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (idx < 2 * NLB) {
@@ -148,11 +151,13 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
       int bi = 0;
       while ((bi + 1) * (bi + 2) / 2 <= li) ++bi;
       const int bj = li - bi * (bi + 1) / 2;
+      // transposed product: the lane ends up with row 16 bi + l16 and the 4 consecutive
+      // columns 16 bj + 4 g4 .. (K K^T is symmetric; Q K^T is formed as (K Q^T)^T)
 #pragma unroll
       for (int kk = 0; kk < DK / 32; ++kk) {
-        const bf16x8 av = is_q ? ld_bf16x8(&Qs[16 * bi + l16][32 * kk + 8 * g4])
+        const bf16x8 av = ld_bf16x8(&Ks[16 * bj + l16][32 * kk + 8 * g4]);
+        const bf16x8 bv = is_q ? ld_bf16x8(&Qs[16 * bi + l16][32 * kk + 8 * g4])
                                : ld_bf16x8(&Ks[16 * bi + l16][32 * kk + 8 * g4]);
-        const bf16x8 bv = ld_bf16x8(&Ks[16 * bj + l16][32 * kk + 8 * g4]);
         acc[j] = mfma_bf16(av, bv, acc[j]);
       }
     }
@@ -171,21 +176,28 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
     int bi = 0;
     while ((bi + 1) * (bi + 2) / 2 <= li) ++bi;
     const int bj = li - bi * (bi + 1) / 2;
-    const int i = 16 * bj + l16;
+    const int r = 16 * bi + l16, i0 = 16 * bj + 4 * g4;   // row, first of 4 columns
+    const float lr = lg[r];
+    const f32x4 li4 = *(const f32x4*)&lg[i0];
+    if (is_q) {
+      f16x4 pv;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = 16 * bi + 4 * g4 + e;
-      const float gam = __builtin_amdgcn_exp2f(fminf(lg[r] - lg[i], 0.f));
-      if (is_q)
-        Pg[r * C + i] = (_Float16)(i <= r ? a.scale * gam * acc[j][e] : 0.f);
-      else
-        Mf[r][i] = i < r ? bt[r] * gam * acc[j][e] : 0.f;
+      for (int e = 0; e < 4; ++e)
+        pv[e] = (_Float16)(i0 + e <= r ? a.scale * __builtin_amdgcn_exp2f(fminf(lr - li4[e], 0.f)) * acc[j][e] : 0.f);
+      *(f16x4*)&Pg[r * C + i0] = pv;
+    } else {
+      const float br = bt[r];
+      f32x4 mv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        mv[e] = i0 + e < r ? br * __builtin_amdgcn_exp2f(fminf(lr - li4[e], 0.f)) * acc[j][e] : 0.f;
+      *(f32x4*)&Mf[r][i0] = mv;
     }
   }
   // zero the upper blocks of P
-  for (int e = tid; e < C * C; e += 256) {
-    const int r = e / C, i = e - r * C;
-    if ((i >> 4) > (r >> 4)) Pg[r * C + i] = (_Float16)0.f;
+  for (int e = tid; e < C * C / 8; e += NT) {
+    const int r = e / (C / 8), i = (e - r * (C / 8)) * 8;
+    if ((i >> 4) > (r >> 4)) *(u32x4*)&Pg[r * C + i] = u32x4{0, 0, 0, 0};
   }
   if (tid < C) a.ws_lg[slot * C + tid] = lg[tid];
   lds_barrier();
@@ -206,35 +218,37 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
   }
   lds_barrier();
 
-  // ---- phase 4: off-diagonal blocks, level by level: T_ij = -T_ii sum_{m=j}^{i-1} M_im T_mj
+  // ---- phase 4: off-diagonal blocks, level by level: T_ij = -T_ii sum_{m=j}^{i-1} M_im T_mj.
+  // One wave per block of the level, 16x16x16 products on v_mfma_f32_16x16x4_f32 (fp32
+  // operands and sums); the sum X is staged through the wave's own LDS tile to serve as
+  // the B operand of the second product.
 #pragma unroll
   for (int lev = 1; lev < NB; ++lev) {
     const int nblk = NB - lev;
-    const int q = tid >> 6;            // block of this thread (64 threads per block)
-    const int rr = (tid >> 2) & 15;
-    const int c4 = (tid & 3) * 4;
-    if (q < nblk) {
-      const int j = q, i = q + lev;
+    if (wave < nblk) {
+      const int j = wave, i = wave + lev;
       f32x4 x = {0.f, 0.f, 0.f, 0.f};
       for (int m = j; m < i; ++m)
 #pragma unroll
-        for (int k = 0; k < 16; ++k)
-          x += Mf[16 * i + rr][16 * m + k] * *(const f32x4*)&Tf[16 * m + k][16 * j + c4];
-      *(f32x4*)&Xs[q][rr][c4] = x;
-    }
-    lds_barrier();
-    if (q < nblk) {
-      const int j = q, i = q + lev;
+        for (int s = 0; s < 4; ++s)
+          x = __builtin_amdgcn_mfma_f32_16x16x4f32(Mf[16 * i + l16][16 * m + 4 * s + g4],
+                                                   Tf[16 * m + 4 * s + g4][16 * j + l16], x, 0, 0, 0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Xs[wave][4 * g4 + e][l16] = x[e];
+      __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));   // this wave's LDS writes are done
       f32x4 y = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int k = 0; k < 16; ++k) y += Tf[16 * i + rr][16 * i + k] * *(const f32x4*)&Xs[q][k][c4];
-      *(f32x4*)&Tf[16 * i + rr][16 * j + c4] = -y;
+      for (int s = 0; s < 4; ++s)
+        y = __builtin_amdgcn_mfma_f32_16x16x4f32(Tf[16 * i + l16][16 * i + 4 * s + g4], Xs[wave][4 * s + g4][l16], y,
+                                                 0, 0, 0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Tf[16 * i + 4 * g4 + e][16 * j + l16] = -y[e];
     }
     lds_barrier();
   }
 
   // ---- phase 5: f16 copies: T (lower, zero upper), (beta 2^lg K)^T and (beta V)^T
-  for (int e = tid; e < C * C; e += 256) {
+  for (int e = tid; e < C * C; e += NT) {
     const int r = e / C, i = e - r * C;
     Th[r][i] = (_Float16)((i >> 4) <= (r >> 4) ? Tf[r][i] : 0.f);
   }
@@ -267,7 +281,7 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
     }
   }
   // scale * 2^lg Q as f16 (the chain's Q S^T operand, row decay folded in)
-  for (int e = tid; e < C * (DK / 8); e += 256) {
+  for (int e = tid; e < C * (DK / 8); e += NT) {
     const int r = e / (DK / 8), cc = e - r * (DK / 8);
     const float w = a.scale * __builtin_amdgcn_exp2f(lg[r]);
     const u32x4 qw = *(const u32x4*)&Qs[r][cc * 8];
@@ -285,49 +299,52 @@ __global__ __launch_bounds__(256) void k_delta_prep(DeltaArgs a) {
   _Float16* Wg = a.ws_w + slot * C * DK;
   float* Ug = a.ws_u + slot * C * DV;
   constexpr int NOB = NB * (DK / 16);   // output blocks per matrix
-  for (int idx = wave; idx < 2 * NOB; idx += 4) {
+  for (int idx = wave; idx < 2 * NOB; idx += NW) {
     const bool is_u = idx >= NOB;
     const int b = idx % NOB;
     const int rb = b / (DK / 16), db = b % (DK / 16);
     f32x4 o = {0.f, 0.f, 0.f, 0.f};
+    // transposed product (X^T T^T): the lane ends up with row 16 rb + l16 and the 4
+    // consecutive columns 16 db + 4 g4 .. of W (or U~), stored as one vector
 #pragma unroll
     for (int kk = 0; kk < (C + 31) / 32; ++kk) {
       f16x8 av = zero_f16x8(), bv = zero_f16x8();
       if (C >= 32 || g4 < 2) {
-        av = ld_f16x8(&Th[16 * rb + l16][32 * kk + 8 * g4]);
-        bv = is_u ? ld_f16x8(&Vt[16 * db + l16][32 * kk + 8 * g4]) : ld_f16x8(&Bt[16 * db + l16][32 * kk + 8 * g4]);
+        av = is_u ? ld_f16x8(&Vt[16 * db + l16][32 * kk + 8 * g4]) : ld_f16x8(&Bt[16 * db + l16][32 * kk + 8 * g4]);
+        bv = ld_f16x8(&Th[16 * rb + l16][32 * kk + 8 * g4]);
       }
       o = mfma_f16(av, bv, o);
     }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = 16 * rb + 4 * g4 + e, d = 16 * db + l16;
-      if (is_u)
-        Ug[r * DV + d] = o[e];
-      else
-        Wg[r * DK + d] = (_Float16)o[e];
+    const int r = 16 * rb + l16, d0 = 16 * db + 4 * g4;
+    if (is_u) {
+      *(f32x4*)&Ug[r * DV + d0] = o;
+    } else {
+      const f16x4 wv = {(_Float16)o[0], (_Float16)o[1], (_Float16)o[2], (_Float16)o[3]};
+      *(f16x4*)&Wg[r * DK + d0] = wv;
     }
   }
 }
 
 // ------------------------------------------------------------------ chain
+constexpr int kChainThreads = 1024;  // 16 waves: four per SIMD interleave their latencies
 template <int DK, int C, int DVS>
-__global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
+__global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
+  constexpr int NT = kChainThreads;
+  constexpr int NW = NT / 64;
   constexpr int DV = DK;
   constexpr int KP = DK + 8;
   constexpr int CH = C + 8;
   constexpr int NCB = DVS / 16;                 // column blocks of the slice
   constexpr int NXB = (C / 16) * NCB;           // blocks of W S^T / Q S^T / O
-  constexpr int NXW = (NXB + 3) / 4;            // per wave
+  constexpr int NXW = (NXB + NW - 1) / NW;      // per wave
   constexpr int NSB = (DK / 16) * NCB;          // blocks of S^T
-  constexpr int NSW = NSB / 4;                  // per wave
-  static_assert(NSB % 4 == 0, "state blocks must split over 4 waves");
+  constexpr int NSW = (NSB + NW - 1) / NW;      // per wave (the last ones may own none)
   // per-chunk operands staged from the workspace (all f16 except U~)
   constexpr int VQ = C * DK / 8;                // 16-byte vectors of W and of Qg
   constexpr int VK = DK * C / 8;                // of Kd^T
   constexpr int VP = C * C / 8;                 // of P
   constexpr int VU = C * DVS / 4;               // 16-byte vectors of the U~ slice (fp32)
-  constexpr int RQ = (VQ + 255) / 256, RK = (VK + 255) / 256, RP = (VP + 255) / 256, RU = (VU + 255) / 256;
+  constexpr int RQ = (VQ + NT - 1) / NT, RK = (VK + NT - 1) / NT, RP = (VP + NT - 1) / NT, RU = (VU + NT - 1) / NT;
   __shared__ __attribute__((aligned(16))) _Float16 Ws[C][KP];
   __shared__ __attribute__((aligned(16))) _Float16 Qs[C][KP];
   __shared__ __attribute__((aligned(16))) _Float16 Kdt[DK][CH];
@@ -339,12 +356,27 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
 
   const int Hv = a.n_v_heads;
   const int per_seq = Hv * a.n_slices;
-  const int item = xcd_remap(blockIdx.x, gridDim.x);   // slices of one head share an XCD
-  if (item >= a.n_seq * per_seq) return;
-  const int si = item / per_seq;
-  const int rem = item - si * per_seq;
-  const int h = rem / a.n_slices;
-  const int i0 = (rem - h * a.n_slices) * DVS;
+  int si, h, sl;
+  if ((Hv & 7) == 0) {
+    // workgroup b runs on XCD b % 8 (round-robin dispatch); the prep workgroup of
+    // (chunk, head h) ran on XCD h % 8, so every slice of head h is placed there too and
+    // finds the head's chunk operands in that XCD's L2
+    const int b = blockIdx.x;
+    const int hx = b & 7;                     // h % 8
+    const int rest = b >> 3;                  // (seq, h / 8, slice)
+    sl = rest % a.n_slices;
+    const int hq = (rest / a.n_slices) % (Hv >> 3);
+    si = rest / a.n_slices / (Hv >> 3);
+    h = 8 * hq + hx;
+  } else {
+    const int item = xcd_remap(blockIdx.x, gridDim.x);   // slices of one head share an XCD
+    si = item / per_seq;
+    const int rem = item - si * per_seq;
+    h = rem / a.n_slices;
+    sl = rem - h * a.n_slices;
+  }
+  if (si >= a.n_seq) return;
+  const int i0 = sl * DVS;
   const DeltaSeq S = a.seq[si];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g4 = lane >> 4;
@@ -355,7 +387,8 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
   f32x4 st[NSW];
 #pragma unroll
   for (int j = 0; j < NSW; ++j) {
-    const int b = wave + 4 * j;
+    const int b = wave + NW * j;
+    if (b >= NSB) continue;
     const int db = b / NCB, cb = b % NCB;
     const int i = 16 * cb + l16, d = 16 * db + 4 * g4;
     st[j] = *(const f32x4*)(Sg + (long)(i0 + i) * DK + d);
@@ -375,7 +408,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     const float* U = a.ws_u + slot * C * DV + i0;
 #pragma unroll
     for (int j = 0; j < RQ; ++j) {
-      const int e = tid + 256 * j;
+      const int e = tid + NT * j;
       if (e < VQ) {
         rw[j] = W4[e];
         rq[j] = Q4[e];
@@ -383,13 +416,13 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < RK; ++j)
-      if (tid + 256 * j < VK) rk[j] = K4[tid + 256 * j];
+      if (tid + NT * j < VK) rk[j] = K4[tid + NT * j];
 #pragma unroll
     for (int j = 0; j < RP; ++j)
-      if (tid + 256 * j < VP) rp[j] = P4[tid + 256 * j];
+      if (tid + NT * j < VP) rp[j] = P4[tid + NT * j];
 #pragma unroll
     for (int j = 0; j < RU; ++j) {
-      const int e = tid + 256 * j;
+      const int e = tid + NT * j;
       if (e < VU) {
         const int r = e / (DVS / 4), c4 = e - r * (DVS / 4);
         ru[j] = *(const u32x4*)(U + (long)r * DV + 4 * c4);
@@ -400,7 +433,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
   auto stage = [&]() {
 #pragma unroll
     for (int j = 0; j < RQ; ++j) {
-      const int e = tid + 256 * j;
+      const int e = tid + NT * j;
       if (e < VQ) {
         const int r = e / (DK / 8), c8 = e - r * (DK / 8);
         *(u32x4*)&Ws[r][8 * c8] = rw[j];
@@ -409,7 +442,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < RK; ++j) {
-      const int e = tid + 256 * j;
+      const int e = tid + NT * j;
       if (e < VK) {
         const int d = e / (C / 8), c8 = e - d * (C / 8);
         *(u32x4*)&Kdt[d][8 * c8] = rk[j];
@@ -417,7 +450,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < RP; ++j) {
-      const int e = tid + 256 * j;
+      const int e = tid + NT * j;
       if (e < VP) {
         const int r = e / (C / 8), c8 = e - r * (C / 8);
         *(u32x4*)&Ph[r][8 * c8] = rp[j];
@@ -425,7 +458,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < RU; ++j) {
-      const int e = tid + 256 * j;
+      const int e = tid + NT * j;
       if (e < VU) {
         const int r = e / (DVS / 4), c4 = e - r * (DVS / 4);
         *(u32x4*)&Us[r][4 * c4] = ru[j];
@@ -447,16 +480,18 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     f32x4 oacc[NXW];
 #pragma unroll
     for (int j = 0; j < NXW; ++j) {
-      const int b = wave + 4 * j;
+      const int b = wave + NW * j;
       oacc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
       if (b >= NXB) continue;
       const int rb = b / NCB, cb = b % NCB;
       f32x4 x = {0.f, 0.f, 0.f, 0.f}, y = {0.f, 0.f, 0.f, 0.f};
+      // X in (rows, slice columns) layout for U; Y transposed (S Qg^T) so that the lane
+      // holds one row and 4 consecutive columns of O
 #pragma unroll
       for (int kk = 0; kk < DK / 32; ++kk) {
         const f16x8 sv = ld_f16x8(&Sh[16 * cb + l16][32 * kk + 8 * g4]);
         x = mfma_f16(ld_f16x8(&Ws[16 * rb + l16][32 * kk + 8 * g4]), sv, x);
-        y = mfma_f16(ld_f16x8(&Qs[16 * rb + l16][32 * kk + 8 * g4]), sv, y);
+        y = mfma_f16(sv, ld_f16x8(&Qs[16 * rb + l16][32 * kk + 8 * g4]), y);
       }
       f16x4 uh;
 #pragma unroll
@@ -469,28 +504,27 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
     // ---- O += P U, written out; S^T <- 2^lg_last S^T + Kd^T U; refresh the f16 copy of S
 #pragma unroll
     for (int j = 0; j < NXW; ++j) {
-      const int b = wave + 4 * j;
+      const int b = wave + NW * j;
       if (b >= NXB) continue;
       const int rb = b / NCB, cb = b % NCB;
       f32x4 o = oacc[j];
+      // (P U)^T = U^T P^T: row 16 rb + l16, columns 16 cb + 4 g4 .. + 3 of O
 #pragma unroll
       for (int kk = 0; kk < (C + 31) / 32; ++kk) {
         f16x8 av = zero_f16x8(), bv = zero_f16x8();
         if (kpart) {
-          av = ld_f16x8(&Ph[16 * rb + l16][32 * kk + 8 * g4]);
-          bv = ld_f16x8(&Ut[16 * cb + l16][32 * kk + 8 * g4]);
+          av = ld_f16x8(&Ut[16 * cb + l16][32 * kk + 8 * g4]);
+          bv = ld_f16x8(&Ph[16 * rb + l16][32 * kk + 8 * g4]);
         }
         o = mfma_f16(av, bv, o);
       }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = 16 * rb + 4 * g4 + e;
-        if (r < Cr) S.out[((long)(t0 + r) * Hv + h) * DV + i0 + 16 * cb + l16] = o[e];
-      }
+      const int r = 16 * rb + l16;
+      if (r < Cr) *(f32x4*)(S.out + ((long)(t0 + r) * Hv + h) * DV + i0 + 16 * cb + 4 * g4) = o;
     }
 #pragma unroll
     for (int j = 0; j < NSW; ++j) {
-      const int b = wave + 4 * j;
+      const int b = wave + NW * j;
+      if (b >= NSB) continue;
       const int db = b / NCB, cb = b % NCB;
       f32x4 sacc = st[j] * g_last;
 #pragma unroll
@@ -511,7 +545,8 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
   }
 #pragma unroll
   for (int j = 0; j < NSW; ++j) {
-    const int b = wave + 4 * j;
+    const int b = wave + NW * j;
+    if (b >= NSB) continue;
     const int db = b / NCB, cb = b % NCB;
     *(f32x4*)(Sg + (long)(i0 + 16 * cb + l16) * DK + 16 * db + 4 * g4) = st[j];
   }
@@ -519,7 +554,7 @@ __global__ __launch_bounds__(256) void k_delta_chain(DeltaArgs a) {
 
 template <int DK, int C>
 hipError_t prep_for(const DeltaArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((k_delta_prep<DK, C>), dim3(a.total_chunks * a.n_v_heads), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_delta_prep<DK, C>), dim3(a.total_chunks * a.n_v_heads), dim3(kPrepThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -528,9 +563,9 @@ hipError_t chain_for(const DeltaArgs& a, hipStream_t s) {
   const int blocks = (a.n_seq * a.n_v_heads * a.n_slices + 7) & ~7;   // XCD remap needs a multiple of 8
   const int dvs = DK / a.n_slices;
   if (dvs == 32)
-    hipLaunchKernelGGL((k_delta_chain<DK, C, 32>), dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_delta_chain<DK, C, 32>), dim3(blocks), dim3(kChainThreads), 0, s, a);
   else if (dvs == 64)
-    hipLaunchKernelGGL((k_delta_chain<DK, C, 64>), dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_delta_chain<DK, C, 64>), dim3(blocks), dim3(kChainThreads), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
