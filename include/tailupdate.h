@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define TU_ABI_VERSION 3
+#define TU_ABI_VERSION 4
 
 #define TU_OK 0
 #define TU_ERR_ARG (-1)       /* null pointer, unsupported or inconsistent shape */
@@ -84,8 +84,9 @@ typedef struct tu_seq {
  * Attention-layer shape. Query head h reads KV head h / (n_q_heads / n_kv_heads).
  * head_dim must be 64, 128 or 256; rotary_dim even, 0 <= rotary_dim <= head_dim
  * (rotate-half pairs (j, j + rotary_dim/2), angle pos * rope_theta^(-2j/rotary_dim)).
- * kv_splits = 0 lets the library split the key range for occupancy; a positive
- * value forces that many splits (results are the same up to rounding).
+ * kv_splits = 0 lets the library choose how many workgroups share one key range
+ * (from the waves of workgroups a launch runs in); a positive value forces that many
+ * splits (results are the same up to rounding).
  */
 typedef struct tu_attn_params {
   int32_t n_q_heads;
@@ -114,6 +115,28 @@ typedef struct tu_delta_params {
 /* ABI version (TU_ABI_VERSION) and the calling thread's last error message. */
 int tu_abi_version(void);
 const char* tu_last_error(void);
+
+/*
+ * Device-side checks of the compaction (Section 4.2 keeps the live spans on the
+ * host; the device holds the position labels). While scanning, the kernels check
+ * that every row the deletion ranges keep (by its d_pos label) lies outside the
+ * removed row spans the host derived from its live runs, and every removed row
+ * inside one; and every bounded wait of the in-place move must end in time. A
+ * failed check does not stop the update (the move follows the host's spans and
+ * stays in bounds): it sets a sticky bit in a word held per device:
+ *   TU_FAULT_POSITIONS  d_pos disagrees with the host metadata (`live`, `len`), so
+ *                       the update did not remove exactly the rows whose labels lie
+ *                       in the ranges;
+ *   TU_FAULT_WAIT       a wait of the in-place move expired; moved rows may be wrong.
+ * tu_device_faults enqueues a read of the current device's word on `stream` (and,
+ * if clear != 0, a reset after it), synchronises `stream`, and stores the word in
+ * *faults (host pointer). The word is shared by every stream and context of the
+ * process on that device; a reset can drop bits set meanwhile by work on other
+ * streams. Returns TU_OK, TU_ERR_ARG (faults NULL) or TU_ERR_HIP.
+ */
+#define TU_FAULT_POSITIONS 1
+#define TU_FAULT_WAIT 2
+int tu_device_faults(int32_t* faults, int32_t clear, void* stream);
 
 /*
  * Range verification (Section 4.2; host only, no device access).

@@ -23,6 +23,7 @@ from .binding import (  # noqa: F401
     compact_kv,
     delta_params,
     delta_rule_continue,
+    device_faults,
     lib,
     profile_collect,
     profile_enable,
@@ -31,6 +32,8 @@ from .binding import (  # noqa: F401
     short_conv_continue_batch,
     tail_prefill_attention,
     update_layer_stack,
+    TU_FAULT_POSITIONS,
+    TU_FAULT_WAIT,
     TU_LAYER_ATTN,
     TU_LAYER_DELTA,
     TU_PLACE_RELOCATE,

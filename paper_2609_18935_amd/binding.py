@@ -109,13 +109,14 @@ _SIGNATURES = {
                                     _vp, ctypes.c_size_t, _vp]),
     "attention_tv_workspace_size": (ctypes.c_size_t, [_i64]),
     "attention_tv_distance": (_i32, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tu_device_faults": (_i32, [ctypes.POINTER(_i32), _i32, _vp]),
     "tu_profile_enable": (_i32, [_i32]),
     "tu_profile_collect": (_i32, [ctypes.c_char_p, _i32, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double),
                                   _i32]),
 }
 
 _lib_handle = None
-ABI_VERSION = 3   # TU_ABI_VERSION of include/tailupdate.h that these structures follow
+ABI_VERSION = 4   # TU_ABI_VERSION of include/tailupdate.h that these structures follow
 
 
 def lib():
@@ -423,6 +424,18 @@ class StackUpdate:
 
     def run(self, workspace: torch.Tensor, stream=None):
         _check(lib().update_layer_stack(ctypes.byref(self.u), _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+TU_FAULT_POSITIONS = 1   # device positions disagreed with the host's live runs
+TU_FAULT_WAIT = 2        # a bounded wait of the in-place move expired
+
+
+def device_faults(clear: bool = True, stream=None) -> int:
+    """The current device's sticky fault bits (TU_FAULT_*) set by compaction kernels
+    since the last reset; synchronises `stream` first and resets the word if `clear`."""
+    out = ctypes.c_int32(0)
+    _check(lib().tu_device_faults(ctypes.byref(out), int(bool(clear)), _stream(stream)))
+    return int(out.value)
 
 
 def profile_enable(on: bool = True):

@@ -409,13 +409,11 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
     // gather workgroups claim items in order, so any count works; one grid's worth of
     // resident workgroups suffices (the sizing pass, without a device, takes the cap)
     a.n_workers = std::min({items_total, kMaxGatherWorkers, ws ? std::max(1, max_blocks) : kMaxGatherWorkers});
-    // [claim counter | stripe counters | status words]; counters one 128-byte line apart
+    // [claim counter | stripe counters], one 128-byte line apart
     a.n_counter_words = kFlagStride + a.n_flag_words;
-    int32_t* words = static_cast<int32_t*>(
-        ar.take(sizeof(int32_t) * ((size_t)a.n_counter_words + a.n_scan_blocks + a.n_workers)));
+    int32_t* words = static_cast<int32_t*>(ar.take(sizeof(int32_t) * (size_t)a.n_counter_words));
     a.claim = words;
     a.flags = words ? words + kFlagStride : nullptr;
-    a.status = words ? words + a.n_counter_words : nullptr;
     plan->launches.push_back(a);
   }
   plan->ws_bytes = ar.used;
@@ -453,18 +451,95 @@ struct AttnLaunch {
   RopeArgs rope;
   int rope_tokens;
   AttnArgs attn;
+  AttnOrder order;
   MergeArgs merge;
   int merge_rows;
 };
 
-int choose_splits(const tu_attn_params* p, int64_t L_keep, int64_t T, int64_t base_items_total) {
+// Key-range splits of one context's attention. An attention workgroup holds a whole CU,
+// so a launch runs in waves of kCus workgroups. Alone in its launch, a context takes
+// the split count that minimises (waves) x (time of one workgroup: its key tiles plus a
+// fixed part) plus the merge (a launch, and the partial outputs written and read back
+// once per split); about 2.6 us per 64-key tile at head_dim 256, 5 TB/s. With other
+// contexts in the launch (whose lengths differ, so waves do not line up) it takes
+// enough splits for the launch to fill the CUs. At least 4 key tiles per split, at
+// most 64 splits.
+int choose_splits(const tu_attn_params* p, int64_t L_keep, int64_t T, int64_t base_items_total, bool alone) {
   if (p->kv_splits > 0) return p->kv_splits;
-  const int G = p->n_q_heads / p->n_kv_heads;
-  (void)G;
   const int64_t n_kt = (L_keep + T + kAttnKeys - 1) / kAttnKeys;
-  int want = (int)std::max<int64_t>(1, (256 + base_items_total - 1) / std::max<int64_t>(1, base_items_total));
-  const int max_by_len = (int)std::max<int64_t>(1, n_kt / 4);  // at least 4 key tiles per split
-  return std::max(1, std::min({want, max_by_len, 64}));
+  const int64_t max_s = std::max<int64_t>(1, std::min<int64_t>(64, n_kt / 4));
+  if (!alone) {
+    const int64_t want = std::max<int64_t>(1, (kCus + base_items_total - 1) / std::max<int64_t>(1, base_items_total));
+    return (int)std::min(want, max_s);
+  }
+  const double tile_us = 2.6 * p->head_dim / 256.0;
+  const double split_us = (double)T * p->n_q_heads * p->head_dim * 4.0 / 5e6;
+  double best = 0.0;
+  int best_s = 1;
+  for (int64_t s = 1; s <= max_s; ++s) {
+    const int64_t waves = (base_items_total * s + kCus - 1) / kCus;
+    const double est = (double)waves * ((double)((n_kt + s - 1) / s) * tile_us + 5.0) + (s > 1 ? 5.0 + split_us * s : 0.0);
+    if (s == 1 || est < best) {
+      best = est;
+      best_s = (int)s;
+    }
+  }
+  return best_s;
+}
+
+// Die table of a launch of several contexts: groups (context, kv head, split) cost their
+// items' key tiles plus one each; longest first, each goes to the die with the least
+// cost so far, and each die runs its groups in that order. Launches of one context, and
+// launches with more groups than the table holds, keep the equal-share remap.
+void plan_dies(const AttnArgs& a, int G, AttnOrder* o) {
+  o->n_groups = 0;
+  o->blocks = 0;
+  if (a.n_seq < 2) return;
+  struct Grp {
+    int64_t cost;
+    int32_t item0, count;
+  };
+  std::vector<Grp> gs;
+  for (int si = 0; si < a.n_seq; ++si) {
+    const AttnSeq& s = a.seq[si];
+    for (int sp = 0; sp < s.n_splits; ++sp) {
+      int64_t cost = 0;
+      for (int q = 0; q < s.n_tiles; ++q) {
+        const int64_t r_last = std::min<int64_t>((int64_t)s.T * G, (int64_t)(q + 1) * kAttnRows) - 1;
+        const int64_t n_kt = (s.L_keep + r_last / G + 1 + kAttnKeys - 1) / kAttnKeys;
+        const int64_t tps = (n_kt + s.n_splits - 1) / s.n_splits;
+        cost += std::max<int64_t>(0, std::min(n_kt, sp * tps + tps) - sp * tps) + 1;
+      }
+      for (int h = 0; h < a.n_kv_heads; ++h)
+        gs.push_back({cost, s.item_begin + (h * s.n_splits + sp) * s.n_tiles, s.n_tiles});
+    }
+  }
+  if ((int)gs.size() > kMaxAttnGroups) return;
+  std::stable_sort(gs.begin(), gs.end(), [](const Grp& x, const Grp& y) { return x.cost > y.cost; });
+  int64_t load[kXcds] = {};
+  std::vector<int> die(gs.size());
+  for (size_t g = 0; g < gs.size(); ++g) {
+    int x = 0;
+    for (int y = 1; y < kXcds; ++y)
+      if (load[y] < load[x]) x = y;
+    die[g] = x;
+    load[x] += gs[g].cost;
+  }
+  int n = 0, most = 0;
+  for (int x = 0; x < kXcds; ++x) {
+    o->die_begin[x] = n;
+    int slots = 0;
+    for (size_t g = 0; g < gs.size(); ++g)
+      if (die[g] == x) {
+        o->grp_item0[n] = gs[g].item0;
+        slots += gs[g].count;
+        o->grp_end[n++] = slots;
+      }
+    most = std::max(most, slots);
+  }
+  o->die_begin[kXcds] = n;
+  o->n_groups = n;
+  o->blocks = most * kXcds;
 }
 
 int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* ws, std::vector<AttnLaunch>* out,
@@ -499,7 +574,7 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
       void* qh_ws = ar.take(sizeof(bf16_t) * it.T * Hq * D);
       if (!qh) qh = static_cast<bf16_t*>(qh_ws);
       const int tiles = (int)((it.T * G + kAttnRows - 1) / kAttnRows);
-      const int splits = choose_splits(p, it.L_keep, it.T, base_items);
+      const int splits = choose_splits(p, it.L_keep, it.T, base_items, g1 - g0 == 1);
       const int vt_tiles = (int)((it.L_keep + it.T + kAttnKeys - 1) / kAttnKeys);
       _Float16* vt = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)Hkv * vt_tiles * D * kVtRow));
       _Float16* po = nullptr;
@@ -556,6 +631,7 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
     L.merge.row_begin[L.merge.n_seq] = mrows;
     L.rope_tokens = tok;
     L.attn.total_items = item_total;
+    plan_dies(L.attn, G, &L.order);
     L.attn.pack_items = pack_total;
     L.merge_rows = mrows;
     max_used = std::max(max_used, ar.used);
@@ -592,7 +668,7 @@ int side_stream(SideStream** out) {
 int run_attention(const std::vector<AttnLaunch>& ls, int D, hipStream_t st) {
   for (const auto& L : ls) {
     if (int e = hip_check(timed("rope_vt_pack", st, [&] { return launch_stage(L.rope, L.rope_tokens, L.attn, D, st); }), "RoPE/V^T pack launch")) return e;
-    if (int e = hip_check(timed("attention", st, [&] { return launch_attention(L.attn, D, st); }), "attention launch")) return e;
+    if (int e = hip_check(timed("attention", st, [&] { return launch_attention(L.attn, L.order, D, st); }), "attention launch")) return e;
     if (L.merge_rows > 0)
       if (int e = hip_check(timed("attention_merge", st, [&] { return launch_attention_merge(L.merge, L.merge_rows, D, st); }), "merge launch")) return e;
   }
@@ -972,6 +1048,13 @@ extern "C" {
 int tu_abi_version(void) { return TU_ABI_VERSION; }
 
 const char* tu_last_error(void) { return g_err.c_str(); }
+
+static_assert(TU_FAULT_POSITIONS == tu::kFaultPositions && TU_FAULT_WAIT == tu::kFaultWait, "fault bits");
+
+int tu_device_faults(int32_t* faults, int32_t clear, void* stream) {
+  if (!faults) return fail(TU_ERR_ARG, "faults is null");
+  return hip_check(read_device_faults(faults, clear != 0, (hipStream_t)stream), "reading the device fault word");
+}
 
 int tu_validate_ranges(const tu_seq* seq, const int64_t* ranges, int32_t n_ranges, int64_t* n_removed) {
   if (int e = check_seq(seq)) return e;

@@ -32,8 +32,11 @@
 //
 // For occupancy the key range is split over `n_splits` workgroups; each writes a
 // normalised f16 partial (O / l) with its reference max and sum, and k_attn_merge
-// combines them. Workgroups are ordered (kv head, split, tile) and remapped so that
-// the query tiles of one (head, split) key range share an XCD and its L2.
+// combines them. Workgroups are ordered (context, kv head, split, tile); the query
+// tiles of one (context, head, split) key range go to one die (XCD) and share its L2.
+// A launch of one context gives every die an equal share of the items in this order;
+// a launch of several contexts, whose key ranges differ in length, places the groups
+// by a table: longest first, each on the die with the least work so far.
 #include "common.h"
 
 namespace tu {
@@ -125,13 +128,26 @@ struct IntC {
   static constexpr int value = B;
 };
 
+// The item of this workgroup: by the launch's die table when it has one, else equal
+// shares of the item order per die.
+__device__ __forceinline__ int attn_item(const AttnOrder& o) {
+  if (o.n_groups == 0) return xcd_remap(blockIdx.x, gridDim.x);
+  const int x = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+  const int g0 = o.die_begin[x], g1 = o.die_begin[x + 1];
+  int g = g0;
+  while (g < g1 && o.grp_end[g] <= slot) ++g;
+  if (g == g1) return 0x7fffffff;   // the die's share ends before this slot
+  return o.grp_item0[g] + slot - (g > g0 ? o.grp_end[g - 1] : 0);
+}
+
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_attn(AttnArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_attn(AttnArgs a,
+                                                                                               AttnOrder ord) {
   constexpr int NS = D / 16;                // 16-dim steps of S^T = K Q^T
   constexpr int NDB = D / 32;               // 32-dim blocks of O^T
   constexpr int RC = D / 8;                 // 16-byte chunks of data per K row
 
-  const int item = xcd_remap(blockIdx.x, gridDim.x);
+  const int item = attn_item(ord);
   if (item >= a.total_items) return;
   int si = 0;
   while (si + 1 < a.n_seq && a.seq[si + 1].item_begin <= item) ++si;
@@ -487,16 +503,16 @@ __global__ __launch_bounds__(256) void k_attn_merge(MergeArgs a) {
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s) {
+hipError_t launch_attention(const AttnArgs& a, const AttnOrder& o, int head_dim, hipStream_t s) {
   if (a.total_items <= 0) return hipSuccess;
-  // round the grid up to a multiple of 8 so the XCD remap is a bijection
-  const int blocks = (a.total_items + 7) & ~7;
+  // without a die table the grid is rounded up to a multiple of 8 so the remap is a bijection
+  const int blocks = o.n_groups > 0 ? o.blocks : (a.total_items + kXcds - 1) / kXcds * kXcds;
   if (head_dim == 256)
-    hipLaunchKernelGGL(k_attn<256>, dim3(blocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_attn<256>, dim3(blocks), dim3(kThreads), 0, s, a, o);
   else if (head_dim == 128)
-    hipLaunchKernelGGL(k_attn<128>, dim3(blocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_attn<128>, dim3(blocks), dim3(kThreads), 0, s, a, o);
   else if (head_dim == 64)
-    hipLaunchKernelGGL(k_attn<64>, dim3(blocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_attn<64>, dim3(blocks), dim3(kThreads), 0, s, a, o);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -15,7 +15,7 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
 
-constexpr int kMaxSeqPerLaunch = 16;
+constexpr int kMaxSeqPerLaunch = 32;
 constexpr int kMaxRangesPerLaunch = 128;
 constexpr int kMaxBufPerLaunch = 32;
 constexpr int kMaxSeqPerCompact = 8;
@@ -127,7 +127,6 @@ struct CompactArgs {
   int32_t n_workers;       // gather workgroups
   int32_t* claim;   // next unclaimed gather item (its own 128-byte line), then the flags
   int32_t* flags;   // [n_flag_words] stripe read counters, kFlagStride apart
-  int32_t* status;  // [n_scan_blocks + n_workers]: 0 ok, 2 scan mismatch, 1 wait expired
 };
 
 struct RopeSeq {
@@ -188,6 +187,22 @@ struct AttnArgs {
   int32_t n_q_heads;
   int32_t n_kv_heads;
   float scale_log2;      // softmax_scale * log2(e)
+};
+
+constexpr int kXcds = 8;              // dies of the chip; workgroup b is dispatched to die b % 8
+constexpr int kCus = 256;             // compute units of the chip
+constexpr int kMaxAttnGroups = 256;   // entries of an attention launch's die table
+
+// Placement of the attention workgroups of a launch on the dies. The items of a group
+// (one context, kv head and key split: its query tiles) are consecutive; die x runs
+// the groups [die_begin[x], die_begin[x + 1]) in that order, its workgroup slot s taking
+// item grp_item0[g] + s - (slots of the die's earlier groups).
+struct AttnOrder {
+  int32_t n_groups;                   // 0: equal item counts per die in item order (xcd_remap)
+  int32_t blocks;                     // grid size
+  int32_t die_begin[kXcds + 1];
+  int32_t grp_item0[kMaxAttnGroups];
+  int32_t grp_end[kMaxAttnGroups];    // slots of the die up to and including group g
 };
 
 struct MergeArgs {
@@ -322,11 +337,15 @@ struct ConvArgs {
 // ------------------------------------------------------------------ launchers
 // (defined in the kernel translation units; return a hipError_t)
 int compact_max_blocks();   // resident workgroups of the gather kernel over the device
+// sticky per-device fault bits (the values of TU_FAULT_*)
+constexpr int32_t kFaultPositions = 1;
+constexpr int32_t kFaultWait = 2;
+hipError_t read_device_faults(int32_t* faults, bool clear, hipStream_t s);
 constexpr int kMaxGatherWorkers = 2048;
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 // RoPE + append of the tail tokens and the V^T packing of every key tile, one launch
 hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const AttnArgs& a, int head_dim, hipStream_t s);
-hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, const AttnOrder& o, int head_dim, hipStream_t s);
 hipError_t launch_relocate(const RelocArgs& a, hipStream_t s);
 hipError_t launch_probe(const ProbeArgs& a, hipStream_t s);
 hipError_t launch_group_clear(const GroupArgs& a, hipStream_t s);

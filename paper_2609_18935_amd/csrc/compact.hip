@@ -3,13 +3,13 @@
 // caller's stream. The first scans the old positions (before anything moves them) and
 // clears the move's counters; the second moves the rows.
 //
-// Scan workgroups (k_compact_scan, 4096 rows each): 16 rounds of
+// Scan workgroups (k_compact_scan, kScanRows rows each): rounds of
 // 256 consecutive rows, one row per lane, so every load is coalesced. A lane's keep
 // flag is "position in no deletion range"; the wavefront ballot + mbcnt gives each
 // kept row its rank inside the wave, one wave scans the 64 per-(round, wave) counts,
 // and the rows kept before the workgroup's first row (from the verified spans) give
-// the destination. They write src_index and a status word (2 if a destination differs
-// from the one the host's live spans imply, else 0).
+// the destination. They write src_index; a row whose keep flag disagrees with the
+// host's live spans sets the device's sticky fault word (kFaultPositions).
 //
 // Gather workgroups (k_compact_gather): move whole rows of every attention layer's K and V
 // buffers, and the position array, in place, only from the first removed row on. The
@@ -24,11 +24,15 @@
 // the workgroup holding the smallest unfinished item never waits, so the scheme
 // progresses without any guarantee about which workgroups are resident: an ordinary
 // launch on the caller's stream. One lane polls, with back-off, counters that sit on
-// separate cache lines. Each wait is also bounded: on expiry the workgroup's status
-// word is set to 1 and the item proceeds, so every wave exits.
+// separate cache lines. Each wait is also bounded: on expiry the item proceeds, the
+// device's sticky fault word gets kFaultWait, and every wave exits.
 #include "common.h"
 
 namespace tu {
+
+// Sticky fault bits of this device (one copy per device): set by the compaction
+// kernels, read and cleared by the host through read_device_faults.
+__device__ int32_t g_faults;
 
 namespace {
 
@@ -125,7 +129,7 @@ __device__ void keep_scan(const CompactArgs& a, const ScanSeq& s, int chunk) {
     if ((m[r] >> lane) & 1ull) s.src_index[kept_before + off[r * kScanWaves + wave] + lane_rank(m[r])] = idx;
   }
   bad = __syncthreads_or(bad);
-  if (threadIdx.x == 0) a.status[chunk + s.block_begin] = bad ? 2 : 0;
+  if (threadIdx.x == 0 && bad) atomicOr(&g_faults, kFaultPositions);
 }
 
 __device__ bool gather_items(const CompactArgs& a) {
@@ -137,9 +141,13 @@ __device__ bool gather_items(const CompactArgs& a) {
   const int R = a.rows_per_stripe;
   const int RB = a.row_bytes;
   const int vpr = RB >> 4;  // 16-byte vectors per row
-  stage_spans(a, sp);
-  for (;;) {
+  // with no more items than workgroups every workgroup's single claim gets an item, so
+  // none claims again (a claim is a device-scope round trip, longer when many
+  // workgroups claim at once)
+  const bool one_each = a.n_workers >= a.total_items;
+  for (bool first = true;; first = false) {
     if (tid == 0) s_item = __hip_atomic_fetch_add(a.claim, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (first) stage_spans(a, sp);   // overlaps the first claim's round trip
     __syncthreads();
     const int item = __builtin_amdgcn_readfirstlane(s_item);
     if (item >= a.total_items) break;
@@ -224,6 +232,7 @@ __device__ bool gather_items(const CompactArgs& a) {
         if (t < rows) S.pos[row0 + t] = pv[i];
       }
     }
+    if (one_each) break;
     __syncthreads();   // s_src and s_item are rewritten by the next item
   }
   return expired;
@@ -244,7 +253,7 @@ __global__ __launch_bounds__(kThreads) void k_compact_scan(CompactArgs a) {
 
 __global__ __launch_bounds__(kThreads) void k_compact_gather(CompactArgs a) {
   const bool expired = gather_items(a);
-  if (threadIdx.x == 0) a.status[a.n_scan_blocks + blockIdx.x] = expired ? 1 : 0;
+  if (threadIdx.x == 0 && expired) atomicOr(&g_faults, kFaultWait);
 }
 
 }  // namespace
@@ -260,6 +269,19 @@ int compact_max_blocks() {
     cached = per_cu * cus;
   }
   return cached;
+}
+
+hipError_t read_device_faults(int32_t* faults, bool clear, hipStream_t s) {
+  if (hipError_t e = hipMemcpyFromSymbolAsync(faults, HIP_SYMBOL(g_faults), sizeof(int32_t), 0,
+                                              hipMemcpyDeviceToHost, s); e != hipSuccess)
+    return e;
+  if (clear) {
+    static const int32_t zero = 0;
+    if (hipError_t e = hipMemcpyToSymbolAsync(HIP_SYMBOL(g_faults), &zero, sizeof(int32_t), 0,
+                                              hipMemcpyHostToDevice, s); e != hipSuccess)
+      return e;
+  }
+  return hipStreamSynchronize(s);
 }
 
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s) {

@@ -356,3 +356,13 @@ def test_diagnostics_reject_before_touching_device(L):
     assert L.attention_tv_distance(None, None, None, -1, None, None, 0, None) == B.TU_ERR_ARG
     assert L.attention_tv_distance(fake.data_ptr(), fake.data_ptr(), None, 10, fake.data_ptr(), None, 0,
                                    None) == B.TU_ERR_WORKSPACE
+
+
+def test_device_faults_rejects_null_and_matches_header(L):
+    """tu_device_faults refuses a null output before any device access; the fault bits
+    of the binding are the header's."""
+    assert L.tu_device_faults(None, 1, None) == B.TU_ERR_ARG
+    assert "faults" in L.tu_last_error().decode()
+    hdr = open(HEADER).read()
+    assert int(re.search(r"#define TU_FAULT_POSITIONS (\d+)", hdr).group(1)) == tu.TU_FAULT_POSITIONS
+    assert int(re.search(r"#define TU_FAULT_WAIT (\d+)", hdr).group(1)) == tu.TU_FAULT_WAIT

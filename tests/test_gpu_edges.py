@@ -7,6 +7,10 @@ One update_layer_stack call over four contexts at once, each a degenerate case:
   * a tail and no removals (ordinary continuation);
   * an empty context (fresh prefill from position 0).
 Each context is checked against the float64 oracle on its own.
+
+Also the device-side check of the compaction: position labels that disagree with
+the host's live runs set the device's sticky fault word, which the host reads and
+clears; correct updates leave it clear.
 """
 import numpy as np
 import pytest
@@ -35,6 +39,7 @@ def _ctx_for(case):
 
 
 def test_degenerate_contexts_in_one_call():
+    tu.device_faults(clear=True)
     a = synth.AttnShape(16, 2, 256)
     d = synth.DeltaShape(16, 32, 128, 128, 64)
     specs = [  # (L_old, ranges, T)
@@ -82,3 +87,38 @@ def test_degenerate_contexts_in_one_call():
         assert_close(a_out[int(off[c]): int(off[c + 1])].cpu().numpy(), ref["out"], f"{what}: attention")
         assert_close(d_out[int(off[c]): int(off[c + 1])].cpu().numpy(), o_ref, f"{what}: delta out")
         assert_close(dc.state.cpu().numpy(), S_ref, f"{what}: delta state")
+    assert tu.device_faults() == 0, "an update of consistent contexts raised a device fault"
+
+
+def test_device_fault_on_mislabelled_positions():
+    """The host says rows 0..4095 hold positions 0..4095; the device labels row 1000 with
+    5000 instead. Removing positions [900, 1100) removes rows 900..1099 by the host's
+    spans, but the row labelled 5000 lies in no range: the scan flags the disagreement.
+    The move still follows the host's spans (every access in bounds)."""
+    L = 4096
+    _say = lambda m: print(f"[case] {m}", flush=True)
+    _say("mislabelled row 1000 of 4096, remove [900, 1100)")
+    tu.device_faults(clear=True)
+    k = torch.randn(L, 2, 64, device=DEV).to(torch.bfloat16)
+    v = torch.randn_like(k)
+    k0, v0 = k.clone(), v.clone()
+    ctx = tu.Context(L, device=DEV)
+    labels = torch.arange(L, dtype=torch.int32, device=DEV)
+    labels[1000] = 5000
+    ctx.pos[:L] = labels
+    ctx.set_metadata([(0, L)], L)
+    tu.compact_kv(ctx, [k], [v], np.array([[900, 1100]]))
+    assert tu.device_faults(clear=True) == tu.TU_FAULT_POSITIONS
+    assert tu.device_faults() == 0      # the read above cleared it
+    keep = torch.cat([torch.arange(900), torch.arange(1100, L)]).to(DEV)
+    assert ctx.len == L - 200
+    assert torch.equal(k[: L - 200], k0[keep]) and torch.equal(v[: L - 200], v0[keep])
+    assert torch.equal(ctx.pos[: L - 200], labels[keep])
+    # the same removal with consistent labels raises nothing
+    k, v = k0.clone(), v0.clone()
+    ctx = tu.Context(L, device=DEV)
+    ctx.pos[:L] = torch.arange(L, dtype=torch.int32, device=DEV)
+    ctx.set_metadata([(0, L)], L)
+    tu.compact_kv(ctx, [k], [v], np.array([[900, 1100]]))
+    assert tu.device_faults() == 0
+    assert torch.equal(k[: L - 200], k0[keep])
