@@ -45,6 +45,7 @@ def parse():
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--kv-splits", type=int, default=0)
     ap.add_argument("--no-peaks", action="store_true", help="skip the copy and GEMM rate measurements")
+    ap.add_argument("--no-t-sweep", action="store_true", help="skip the tail-length sweep at 32K rows")
     return ap.parse_args()
 
 
@@ -88,7 +89,7 @@ def build_workload(cfg, seed, device):
     r, and per layer that round's packed tail inputs."""
     import torch
     import synth
-    sc = synth.make_scenario(cfg.index, seed=seed)
+    sc = synth.make_scenario(cfg.index, seed=seed, cfg=cfg)
     rng = DevRng(seed * 1000 + cfg.index, device)
     a, d = cfg.attn, cfg.delta
     kinds = cfg.layer_kinds()
@@ -233,7 +234,7 @@ def cpu_baseline(cfg, seed, budget_s):
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [cores])
     except Exception:
         blas_threads = cores
-    sc = synth.make_scenario(cfg.index, seed=seed)
+    sc = synth.make_scenario(cfg.index, seed=seed, cfg=cfg)
     r = sc.chars[0].rounds[0]
     a, d = cfg.attn, cfg.delta
     kb, vb = synth.gen_attn_cache(seed, cfg.index, 0, r.L_old, a)
@@ -307,6 +308,61 @@ def short_conv_row(tu, synth, cfg, T, dev, reps):
     return {"tokens": T, "channels": chans, "width": W, "launches": 1, "ms": round(ms, 5),
             "bytes": nbytes, "bound": "hbm", "achieved": round(ach, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
             "frac": round(ach / HBM_PEAK_GBS, 4)}
+
+
+def t_sweep_row(tu, synth, dev, attn_p, delta_p, seed, reps, warmup=2):
+    """The update (one attention + one delta layer, one 64-token record removed) at 32,768
+    surviving rows for tails of 1 .. 2048 tokens. Short tails are decode-like: the
+    attention kernel then reads the whole K/V cache for a few queries and is bound by
+    HBM (algorithmic bytes: K and V of the surviving + new rows once); long ones are
+    bound by its MFMA products."""
+    import torch
+    rows = []
+    for T in synth.T_SWEEP:
+        cfg = synth.t_sweep_config(T)
+        _, chars, rounds, layers, _ = build_workload(cfg, seed, dev)
+        copies = [make_copy(tu, chars, layers, dev) for _ in range(warmup + 2 * reps)]
+        ups = [round_updates(tu, c, o, layers, rounds, attn_p, delta_p) for (c, o) in copies]
+        ws = torch.empty(max(u[0].workspace_size() for u in ups), dtype=torch.uint8, device=dev)
+        for u in ups[:warmup]:
+            u[0].run(ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for u in ups[warmup:warmup + reps]:
+            u[0].run(ws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        tu.profile_enable(True)
+        for u in ups[warmup + reps:]:
+            u[0].run(ws)
+        prof = tu.profile_collect()
+        tu.profile_enable(False)
+        kern = {n: t / c for n, (c, t) in prof.items()}
+        a = cfg.attn
+        Lk = rounds[0]["L_keep"][0]
+        kv_bytes = (Lk + T) * a.n_kv_heads * a.head_dim * 2 * 2
+        flops = attention_flops(cfg, rounds)
+        hbm = T * a.n_q_heads / a.n_kv_heads < 312   # below the ridge of 2.5 PFLOP/s over 8 TB/s
+        att = kern.get("attention")
+        row = {"T": T, "L_keep": Lk, "update_ms": round(ms, 5), "tail_tok_s": round(T / (ms / 1e3), 1),
+               "attention_ms": round(att, 5) if att else None,
+               "stage_ms": round(kern["rope_vt_pack"], 5) if "rope_vt_pack" in kern else None,
+               "merge_ms": round(kern["attention_merge"], 5) if "attention_merge" in kern else None,
+               "attention_bound": "hbm" if hbm else "mfma"}
+        if att:
+            if hbm:
+                row.update({"achieved": round(kv_bytes / (att / 1e3) / 1e9, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
+                            "bytes": kv_bytes})
+            else:
+                row.update({"achieved": round(flops / (att / 1e3) / 1e12, 1), "unit": "TFLOP/s",
+                            "peak": MFMA16_PEAK_TFLOPS, "flops": flops})
+            row["frac"] = round(row["achieved"] / row["peak"], 4)
+        rows.append(row)
+        print(f"[bench] t sweep: {json.dumps(row)}", file=sys.stderr, flush=True)
+        del copies, ups, ws, layers, rounds
+    return rows
 
 
 def lib_probe_ws(tu, attn_p, length, n_probe):
@@ -695,6 +751,10 @@ def main():
     if kinds.count("delta"):
         extra["short_conv"] = short_conv_row(tu, synth, cfg, sumT, dev, K)
         print(f"[bench] short conv: {json.dumps(extra['short_conv'])}", file=sys.stderr, flush=True)
+
+    # ---- tail-length sweep at 32K surviving rows, with the single-refresh workload's shapes
+    if cfg.index == 1 and not args.no_t_sweep:
+        extra["t_sweep"] = t_sweep_row(tu, synth, dev, attn_p, delta_p, args.seed, min(K, 10))
 
     # ---- measured peaks of this part in this run: device copy bandwidth and a bf16 GEMM
     peaks = None if args.no_peaks else measured_peaks(dev)

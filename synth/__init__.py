@@ -11,6 +11,8 @@ from .workloads import (  # noqa: F401
     DeltaShape,
     Config,
     CONFIGS,
+    T_SWEEP,
+    t_sweep_config,
     sub_rng,
     to_bf16_bits,
     bf16_bits_to_f32,

@@ -117,6 +117,17 @@ CONFIGS = {
 }
 
 
+# Tail-length sweep at a 32K surviving context (one 64-token record removed): short tails
+# are decode-like and bound by reading the cache, long ones by the attention products.
+T_SWEEP = (1, 8, 32, 128, 512, 2048)
+
+
+def t_sweep_config(T: int) -> Config:
+    return Config(100 + T_SWEEP.index(T), f"tail sweep, T = {T} at 32K surviving rows", _A1, _D1, n_layers=2,
+                  attn_every=2, n_chars=1, n_rounds=1, L_keep=32768, n_records=(1, 1), record_len=(64, 64),
+                  tail=(T, T))
+
+
 def sub_rng(seed: int, cfg: int, layer: int, tensor_id: int, rnd: int = 0, char: int = 0):
     return np.random.default_rng([int(seed), int(cfg), int(layer), int(tensor_id), int(rnd), int(char)])
 
@@ -285,9 +296,12 @@ class Scenario:
 
 
 def make_scenario(cfg_index: int, seed: int = 0, n_rounds: Optional[int] = None,
-                  n_chars: Optional[int] = None) -> Scenario:
-    """Removal ranges and tail lengths for every character and round of a workload."""
-    cfg = CONFIGS[cfg_index]
+                  n_chars: Optional[int] = None, cfg: Optional[Config] = None) -> Scenario:
+    """Removal ranges and tail lengths for every character and round of a workload
+    (CONFIGS[cfg_index], or `cfg` when given, whose index then seeds the draws)."""
+    if cfg is None:
+        cfg = CONFIGS[cfg_index]
+    cfg_index = cfg.index
     R = cfg.n_rounds if n_rounds is None else n_rounds
     C = cfg.n_chars if n_chars is None else n_chars
     chars: List[CharacterPlan] = []
