@@ -463,11 +463,14 @@ struct AttnLaunch {
 // once per split); about 2.6 us per 64-key tile at head_dim 256, 5 TB/s. With other
 // contexts in the launch (whose lengths differ, so waves do not line up) it takes
 // enough splits for the launch to fill the CUs. At least 4 key tiles per split, at
-// most 64 splits.
+// most kMaxAutoSplits (a decode-like tail of one token over 32K rows fills the chip
+// with 128 splits of its two KV heads).
+constexpr int kMaxAutoSplits = 128;
+
 int choose_splits(const tu_attn_params* p, int64_t L_keep, int64_t T, int64_t base_items_total, bool alone) {
   if (p->kv_splits > 0) return p->kv_splits;
   const int64_t n_kt = (L_keep + T + kAttnKeys - 1) / kAttnKeys;
-  const int64_t max_s = std::max<int64_t>(1, std::min<int64_t>(64, n_kt / 4));
+  const int64_t max_s = std::max<int64_t>(1, std::min<int64_t>(kMaxAutoSplits, n_kt / 4));
   if (!alone) {
     const int64_t want = std::max<int64_t>(1, (kCus + base_items_total - 1) / std::max<int64_t>(1, base_items_total));
     return (int)std::min(want, max_s);
@@ -634,6 +637,11 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
     plan_dies(L.attn, G, &L.order);
     L.attn.pack_items = pack_total;
     L.merge_rows = mrows;
+    {   // lanes per row piece: one per batch of 8 splits of the launch's largest split count
+      int most = 1;
+      for (int m = 0; m < L.merge.n_seq; ++m) most = std::max(most, (int)L.merge.seq[m].n_splits);
+      L.merge.split_lanes = most <= 8 ? 1 : most <= 16 ? 2 : most <= 32 ? 4 : 8;
+    }
     max_used = std::max(max_used, ar.used);
     if (L.rope.n_seq > 0) out->push_back(L);
   }

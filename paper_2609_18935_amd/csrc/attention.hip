@@ -444,59 +444,90 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   }
 }
 
-// One thread per 8 output dims of one (token, head) row.
+// Log-sum-exp merge of the split partials: `split_lanes` (1, 2, 4 or 8) consecutive
+// lanes per 8 output dims of one (token, head) row. Lane l of a row's group takes the
+// splits l, l + split_lanes, ... in batches of 8 whose loads are all in flight
+// together (the running max and sums move between batches); the lanes' partial
+// results are then combined by shuffles and the first lane writes the row's 8 outputs.
 template <int D>
 __global__ __launch_bounds__(256) void k_attn_merge(MergeArgs a) {
-  constexpr int TPR = D / 8;  // threads per row
-  const int g = blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
-  const int d8 = threadIdx.x % TPR;
-  if (g >= a.row_begin[a.n_seq]) return;
-  int si = 0;
-  while (si + 1 < a.n_seq && a.row_begin[si + 1] <= g) ++si;
-  const AttnSeq& S = a.seq[si];
-  const long row = g - a.row_begin[si];
-  const long R = (long)S.T * a.n_q_heads;
-  // splits in batches of 8 whose loads are all in flight together; the running max
-  // and sums move between batches
+  constexpr int TPR = D / 8;  // 8-dim pieces per row
+  const int SL = a.split_lanes;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  const int g = t / (TPR * SL);
+  const int d8 = (t / SL) % TPR;
+  const int sl = t % SL;
+  const bool live = g < a.row_begin[a.n_seq];
   float M = -__builtin_inff(), L = 0.f;
   f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-  for (int s0 = 0; s0 < S.n_splits; s0 += 8) {
-    f32x2 ml[8];
-    f16x8 v[8];
+  // (no pointer into the argument struct outlives this block: that would make the
+  // compiler copy the struct to scratch memory)
+  float* orow = nullptr;
+  if (live) {
+    int si = 0;
+    while (si + 1 < a.n_seq && a.row_begin[si + 1] <= g) ++si;
+    const AttnSeq& S = a.seq[si];
+    const long row = g - a.row_begin[si];
+    orow = S.out + row * D + 8 * d8;
+    const long R = (long)S.T * a.n_q_heads;
+    for (int s0 = sl; s0 < S.n_splits; s0 += 8 * SL) {
+      f32x2 ml[8];
+      f16x8 v[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const long at = (long)(s0 + j) * R + row;
-      if (s0 + j < S.n_splits) {
-        ml[j] = *(const f32x2*)(S.part_ml + at * 2);
-        v[j] = *(const f16x8*)(S.part_o + at * D + 8 * d8);
-      } else {
-        ml[j] = f32x2{-__builtin_inff(), 0.f};
-        v[j] = f16x8{};
+      for (int j = 0; j < 8; ++j) {
+        const int sp = s0 + j * SL;
+        const long at = (long)sp * R + row;
+        if (sp < S.n_splits) {
+          ml[j] = *(const f32x2*)(S.part_ml + at * 2);
+          v[j] = *(const f16x8*)(S.part_o + at * D + 8 * d8);
+        } else {
+          ml[j] = f32x2{-__builtin_inff(), 0.f};
+          v[j] = f16x8{};
+        }
       }
-    }
-    float Mb = M;
+      float Mb = M;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) Mb = fmaxf(Mb, ml[j][0]);
-    if (Mb == -__builtin_inff()) continue;
-    const float c = M == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
-    L *= c;
-    acc0 *= c;
-    acc1 *= c;
+      for (int j = 0; j < 8; ++j) Mb = fmaxf(Mb, ml[j][0]);
+      if (Mb == -__builtin_inff()) continue;
+      const float c = M == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(M - Mb);
+      L *= c;
+      acc0 *= c;
+      acc1 *= c;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      if (ml[j][0] == -__builtin_inff()) continue;
-      const float w = __builtin_amdgcn_exp2f(ml[j][0] - Mb) * ml[j][1];
-      L += w;
+      for (int j = 0; j < 8; ++j) {
+        if (ml[j][0] == -__builtin_inff()) continue;
+        const float w = __builtin_amdgcn_exp2f(ml[j][0] - Mb) * ml[j][1];
+        L += w;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc0[e] += w * (float)v[j][e];
-        acc1[e] += w * (float)v[j][4 + e];
+        for (int e = 0; e < 4; ++e) {
+          acc0[e] += w * (float)v[j][e];
+          acc1[e] += w * (float)v[j][4 + e];
+        }
       }
+      M = Mb;
     }
-    M = Mb;
   }
+  // combine the lanes of a row group (every lane of the wave takes part in the shuffles)
+  for (int x = 1; x < SL; x <<= 1) {
+    const float M2 = __shfl_xor(M, x, 64);
+    const float L2 = __shfl_xor(L, x, 64);
+    f32x4 b0, b1;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      b0[e] = __shfl_xor(acc0[e], x, 64);
+      b1[e] = __shfl_xor(acc1[e], x, 64);
+    }
+    const float Mn = fmaxf(M, M2);
+    if (Mn == -__builtin_inff()) continue;
+    const float c1 = M == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
+    const float c2 = M2 == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(M2 - Mn);
+    L = L * c1 + L2 * c2;
+    acc0 = acc0 * c1 + b0 * c2;
+    acc1 = acc1 * c1 + b1 * c2;
+    M = Mn;
+  }
+  if (!live || sl != 0) return;
   const float inv = 1.f / L;
-  float* orow = S.out + row * D + 8 * d8;
   *(f32x4*)orow = acc0 * inv;
   *(f32x4*)(orow + 4) = acc1 * inv;
 }
@@ -520,8 +551,9 @@ hipError_t launch_attention(const AttnArgs& a, const AttnOrder& o, int head_dim,
 
 hipError_t launch_attention_merge(const MergeArgs& a, int total_rows, int head_dim, hipStream_t s) {
   if (total_rows <= 0) return hipSuccess;
-  const int rows_per_block = 256 / (head_dim / 8);
-  const int blocks = (total_rows + rows_per_block - 1) / rows_per_block;
+  if (a.split_lanes != 1 && a.split_lanes != 2 && a.split_lanes != 4 && a.split_lanes != 8) return hipErrorInvalidValue;
+  const long threads = (long)total_rows * (head_dim / 8) * a.split_lanes;
+  const int blocks = (int)((threads + 255) / 256);
   if (head_dim == 256)
     hipLaunchKernelGGL(k_attn_merge<256>, dim3(blocks), dim3(256), 0, s, a);
   else if (head_dim == 128)

@@ -209,6 +209,7 @@ struct MergeArgs {
   AttnSeq seq[kMaxSeqPerLaunch];
   int32_t n_seq;
   int32_t n_q_heads;
+  int32_t split_lanes;   // lanes per 8 output dims of a row (1, 2, 4 or 8), each a share of the splits
   int32_t row_begin[kMaxSeqPerLaunch + 1];  // prefix of T*Hq over contexts
 };
 

@@ -121,7 +121,8 @@ def test_attention_update_parity(cfg):
 
 
 @pytest.mark.parametrize("L_keep,T,splits", [(0, 1, 0), (0, 77, 0), (5, 1, 0), (300, 17, 1), (1000, 200, 3),
-                                             (4000, 64, 0), (2000, 511, 7), (32768, 1, 0), (32768, 8, 0)])
+                                             (4000, 64, 0), (2000, 511, 7), (32768, 1, 0), (32768, 8, 0),
+                                             (3000, 40, 12), (4000, 64, 24), (300, 17, 40)])
 def test_attention_shapes(L_keep, T, splits):
     s = synth.CONFIGS[1].attn
     _say(f"attention shape L_keep={L_keep} T={T} splits={splits}")
