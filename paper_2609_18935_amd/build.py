@@ -4,11 +4,14 @@
 
 Every .hip file under csrc/ is compiled with hipcc for gfx950 and linked into
 paper_2609_18935_amd/libtailupdate.so. Packed-FP32 instructions are disabled
-(-Xclang -target-feature -Xclang -packed-fp32-ops).
+(-Xclang -target-feature -Xclang -packed-fp32-ops). The compiler's per-kernel resource
+report (registers, scratch, LDS, occupancy) is kept in _build/kernel_resources.json.
 """
 import concurrent.futures
 import glob
+import json
 import os
+import re
 import subprocess
 import sys
 
@@ -28,13 +31,32 @@ FLAGS = [
 ]
 
 
-def _compile(src: str) -> str:
+RESOURCES = os.path.join(BUILD, "kernel_resources.json")
+_FIELDS = {"VGPRs": "vgprs", "AGPRs": "agprs", "ScratchSize [bytes/lane]": "scratch_bytes",
+           "Occupancy [waves/SIMD]": "waves_per_simd", "LDS Size [bytes/block]": "lds_bytes"}
+
+
+def _resources(remarks: str) -> dict:
+    """Per-kernel figures from hipcc's kernel-resource-usage remarks."""
+    out, cur = {}, None
+    for line in remarks.splitlines():
+        m = re.search(r"remark:\s+Function Name: (\S+)", line)
+        if m:
+            cur = out.setdefault(m.group(1), {})
+            continue
+        m = re.search(r"remark:\s+([A-Za-z][^:]*): (\d+)", line)
+        if m and cur is not None and m.group(1).strip() in _FIELDS:
+            cur[_FIELDS[m.group(1).strip()]] = int(m.group(2))
+    return out
+
+
+def _compile(src: str):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, "-Rpass-analysis=kernel-resource-usage", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
-    return obj
+    return obj, _resources(r.stderr)
 
 
 def build(verbose: bool = False) -> str:
@@ -42,7 +64,13 @@ def build(verbose: bool = False) -> str:
     sources = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     workers = max(1, min(len(sources), int(os.environ.get("MAX_JOBS", "8"))))
     with concurrent.futures.ThreadPoolExecutor(workers) as ex:
-        objs = list(ex.map(_compile, sources))
+        done = list(ex.map(_compile, sources))
+    objs = [o for o, _ in done]
+    kernels = {}
+    for _, res in done:
+        kernels.update(res)
+    with open(RESOURCES, "w") as f:
+        json.dump(kernels, f, indent=1, sort_keys=True)
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,--no-undefined", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
