@@ -46,6 +46,7 @@ def parse():
     ap.add_argument("--kv-splits", type=int, default=0)
     ap.add_argument("--no-peaks", action="store_true", help="skip the copy and GEMM rate measurements")
     ap.add_argument("--no-t-sweep", action="store_true", help="skip the tail-length sweep at 32K rows")
+    ap.add_argument("--no-paper-trace", action="store_true", help="skip the paper-shaped revision trace")
     return ap.parse_args()
 
 
@@ -363,6 +364,128 @@ def t_sweep_row(tu, synth, dev, attn_p, delta_p, seed, reps, warmup=2):
         print(f"[bench] t sweep: {json.dumps(row)}", file=sys.stderr, flush=True)
         del copies, ups, ws, layers, rounds
     return rows
+
+
+def paper_trace_row(tu, synth, dev, attn_p, delta_p, seed, reps, warmup=1):
+    """Eight revisions shaped like the paper's measured trace (its Section 6.5: an
+    ~11.9K-token prefix of ~390-token records in 10K-position slots; each revision
+    replaces one or two whole records by 214-362 tokens at fresh slots past the cursor,
+    with 11 framing tokens prefilled and removed again) through the 48-layer hybrid
+    stack of the 64K workload (12 attention + 36 delta layers). Reports each revision's
+    update time, the least-squares line time = fixed + per_token * m over the eight
+    revisions (m = replacement-record tokens, the paper's fit variable), and the refill of
+    the final context (contiguous positions, zero states) through the same kernels."""
+    import numpy as np
+    import torch
+    cfg = synth.CONFIGS[4]
+    a, d = cfg.attn, cfg.delta
+    kinds = cfg.layer_kinds()
+    tr = synth.make_paper_trace(seed)
+    L0 = len(tr.positions)
+    cap = max([L0] + [r.L_old + r.T for r in tr.revisions])
+    rng = DevRng(seed * 1000 + 200, dev)
+    layers, inputs = [], [[] for _ in tr.revisions]
+    for kind in kinds:
+        if kind == "attn":
+            layers.append({"kind": "attn", "caches": [(rng.bf16((cap, a.n_kv_heads, a.head_dim)),
+                                                       rng.bf16((cap, a.n_kv_heads, a.head_dim)))]})
+        else:
+            layers.append({"kind": "delta", "states": [rng.normal((d.n_v_heads, d.d_v, d.d_k), std=0.1)]})
+        for r, rv in enumerate(tr.revisions):
+            T = rv.T
+            if kind == "attn":
+                inputs[r].append({"q": rng.bf16((T, a.n_q_heads, a.head_dim)), "k": rng.bf16((T, a.n_kv_heads, a.head_dim)),
+                                  "v": rng.bf16((T, a.n_kv_heads, a.head_dim)),
+                                  "out": torch.empty((T, a.n_q_heads, a.head_dim), dtype=torch.float32, device=dev)})
+            else:
+                inputs[r].append({"q": rng.bf16((T, d.n_k_heads, d.d_k)), "k": rng.unit_bf16((T, d.n_k_heads, d.d_k)),
+                                  "v": rng.bf16((T, d.n_v_heads, d.d_v)), "beta": rng.beta((T, d.n_v_heads)),
+                                  "g": rng.gate((T, d.n_v_heads)),
+                                  "out": torch.empty((T, d.n_v_heads, d.d_v), dtype=torch.float32, device=dev)})
+    pos0 = torch.from_numpy(tr.positions.astype(np.int32)).to(dev)
+
+    def fresh():
+        ctx = tu.Context(cap, device=dev)
+        ctx.pos[:L0] = pos0
+        ctx.set_metadata(tr.intervals, tr.cursor)
+        own = [{"caches": [(k.clone(), v.clone()) for (k, v) in L["caches"]]} if L["kind"] == "attn" else
+               {"states": [x.clone() for x in L["states"]]} for L in layers]
+        return ctx, [stack_update(tu, [ctx], own, layers, inputs[r], [rv.ranges], [rv.T], attn_p, delta_p,
+                                  post=[rv.post], placement=["slot"], place_runs=[rv.runs])
+                     for r, rv in enumerate(tr.revisions)]
+
+    ws = None
+    times = []
+    for rep in range(warmup + reps):
+        ctx, ups = fresh()
+        if ws is None:
+            # the largest workspace any revision needs, each sized on the metadata it will see
+            need = 0
+            for u, rv in zip(ups, tr.revisions):
+                ctx.set_metadata(rv.intervals, rv.cursor)
+                need = max(need, u.workspace_size())
+            ctx.set_metadata(tr.intervals, tr.cursor)
+            ws = torch.empty(need, dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(ups) + 1)]
+        ev[0].record()
+        for i, u in enumerate(ups):
+            u.run(ws)
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        if rep >= warmup:
+            times.append([ev[i].elapsed_time(ev[i + 1]) for i in range(len(ups))])
+        final_rows, final_cursor = ctx.len, ctx.next_pos
+        del ctx, ups
+    per = np.median(np.asarray(times), axis=0)
+    m = np.asarray([rv.m for rv in tr.revisions], dtype=np.float64)
+    per_tok, fixed = np.polyfit(m, per, 1)
+    # refill of the final context through the same stack
+    N = int(final_rows)
+    rin = []
+    for kind in kinds:
+        if kind == "attn":
+            rin.append({"q": rng.bf16((N, a.n_q_heads, a.head_dim)), "k": rng.bf16((N, a.n_kv_heads, a.head_dim)),
+                        "v": rng.bf16((N, a.n_kv_heads, a.head_dim)),
+                        "out": torch.empty((N, a.n_q_heads, a.head_dim), dtype=torch.float32, device=dev)})
+        else:
+            rin.append({"q": rng.bf16((N, d.n_k_heads, d.d_k)), "k": rng.unit_bf16((N, d.n_k_heads, d.d_k)),
+                        "v": rng.bf16((N, d.n_v_heads, d.d_v)), "beta": rng.beta((N, d.n_v_heads)),
+                        "g": rng.gate((N, d.n_v_heads)),
+                        "out": torch.empty((N, d.n_v_heads, d.d_v), dtype=torch.float32, device=dev)})
+    caches = [[(torch.empty((N, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev),
+                torch.empty((N, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev))]
+              if L["kind"] == "attn" else None for L in layers]
+    rt = []
+    for rep in range(warmup + reps):
+        ctx = tu.Context(N, device=dev)
+        ctx.set_metadata([], 0)
+        own = [{"caches": C} if L["kind"] == "attn" else
+               {"states": [torch.zeros((d.n_v_heads, d.d_v, d.d_k), dtype=torch.float32, device=dev)]}
+               for L, C in zip(layers, caches)]
+        u = stack_update(tu, [ctx], own, layers, rin, [np.zeros((0, 2), np.int64)], [N], attn_p, delta_p)
+        rws = torch.empty(u.workspace_size(), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        u.run(rws)
+        e1.record()
+        torch.cuda.synchronize()
+        if rep >= warmup:
+            rt.append(e0.elapsed_time(e1))
+        del u, rws, own, ctx
+    refill_ms = float(np.median(rt))
+    row = {"layers": len(kinds), "attention_layers": kinds.count("attn"), "delta_layers": kinds.count("delta"),
+           "initial_rows": L0, "initial_cursor": tr.cursor, "final_rows": N, "final_cursor": int(final_cursor),
+           "revisions": [{"m": rv.m, "T": rv.T, "removed_rows": int(np.sum(rv.ranges[:, 1] - rv.ranges[:, 0])),
+                          "live_rows_before": rv.L_old, "ms": round(float(t), 5)}
+                         for rv, t in zip(tr.revisions, per)],
+           "total_ms": round(float(per.sum()), 5),
+           "fit_ms": {"fixed": round(float(fixed), 5), "per_token": round(float(per_tok), 7)},
+           "refill_ms": round(refill_ms, 5), "refill_over_mean_revision": round(refill_ms / float(per.mean()), 2),
+           "placement": "each replacement record at a fresh 10K-position slot past the cursor (explicit positions)"}
+    del caches, rin, layers, inputs, ws
+    return row
 
 
 def lib_probe_ws(tu, attn_p, length, n_probe):
@@ -751,6 +874,11 @@ def main():
     if kinds.count("delta"):
         extra["short_conv"] = short_conv_row(tu, synth, cfg, sumT, dev, K)
         print(f"[bench] short conv: {json.dumps(extra['short_conv'])}", file=sys.stderr, flush=True)
+
+    # ---- revisions shaped like the paper's measured trace, through the 48-layer stack
+    if cfg.index == 1 and not args.no_paper_trace:
+        extra["paper_trace"] = paper_trace_row(tu, synth, dev, attn_p, delta_p, args.seed, min(K, 5))
+        print(f"[bench] paper-shaped trace: {json.dumps(extra['paper_trace'])}", file=sys.stderr, flush=True)
 
     # ---- tail-length sweep at 32K surviving rows, with the single-refresh workload's shapes
     if cfg.index == 1 and not args.no_t_sweep:

@@ -29,4 +29,7 @@ from .workloads import (  # noqa: F401
     Round,
     CharacterPlan,
     make_scenario,
+    Revision,
+    PaperTrace,
+    make_paper_trace,
 )

@@ -335,3 +335,85 @@ def make_scenario(cfg_index: int, seed: int = 0, n_rounds: Optional[int] = None,
             cursor += T
         chars.append(CharacterPlan(L_initial=L0, rounds=rounds))
     return Scenario(cfg=cfg, seed=seed, chars=chars)
+
+
+# ----------------------------------------------------------------------------- paper-shaped trace
+
+@dataclass
+class Revision:
+    ranges: np.ndarray                 # int64 [n, 2] position ranges of the records removed
+    runs: List[Tuple[int, int]]        # tail positions as runs, in tail order (framing included)
+    post: np.ndarray                   # int64 [k, 2] framing positions removed after the tail
+    T: int                             # tail tokens: replacement records + framing
+    m: int                             # replacement-record tokens
+    cursor: int                        # next position id before the revision
+    cursor_after: int                  # after it (one past the highest position in use)
+    L_old: int                         # live rows before
+    intervals: List[Tuple[int, int]]   # live position runs (row order) before
+
+
+@dataclass
+class PaperTrace:
+    positions: np.ndarray              # int64 [L0] position of every initial row (row order)
+    intervals: List[Tuple[int, int]]   # initial live runs
+    cursor: int
+    revisions: List[Revision]
+    interval: int
+
+
+def make_paper_trace(seed: int = 0, head: int = 1699, n_records: int = 26, record_len=(330, 450),
+                     interval: int = 10000, n_revisions: int = 8, m_range=(214, 362), framing=(5, 6),
+                     index: int = 200) -> PaperTrace:
+    """A revision trace shaped like the paper's measured one (Section 6.5, Table 1): a common
+    head at positions [0, head), then records of about 390 tokens, record k at the start
+    of its own `interval`-position slot (logical positions, not occupied rows); every
+    revision removes one or two whole records and appends as many replacement records
+    (m tokens in all) at fresh slots past the cursor (the next slot boundary at or above
+    it), framed by `framing` delimiter tokens that are removed again after the tail is
+    processed. The cursor then is one past the highest position in use.
+
+    Draw order per revision: the number of records removed (1 or 2), which live records
+    (uniform, without replacement), m (inclusive range), the split of m over the new
+    records (uniform cut). Positions of the tail: the opening delimiters and the first
+    record share the first fresh slot, each further record takes the next slot, the
+    closing delimiters follow the last record."""
+    rng = sub_rng(seed, index, 0, T_PLAN)
+    lens = rng.integers(record_len[0], record_len[1] + 1, size=n_records)
+    recs = [(interval * (k + 1), interval * (k + 1) + int(lens[k])) for k in range(n_records)]
+    positions = np.concatenate([np.arange(head)] + [np.arange(a, b) for a, b in recs]).astype(np.int64)
+    intervals = [(0, head)] + list(recs)
+    initial = list(intervals)
+    cursor = interval * (n_records + 1)
+    live = len(positions)
+    revisions: List[Revision] = []
+    for _ in range(n_revisions):
+        n = int(rng.integers(1, 3))
+        pick = sorted(int(i) for i in rng.choice(len(recs), size=n, replace=False))
+        gone = [recs[i] for i in pick]
+        m = int(rng.integers(m_range[0], m_range[1] + 1))
+        cuts = sorted(int(c) for c in rng.integers(1, m, size=n - 1)) if n > 1 else []
+        new_lens = [b - a for a, b in zip([0] + cuts, cuts + [m])]
+        runs, new_recs, post = [], [], []
+        base = -(-cursor // interval) * interval      # the next free slot boundary
+        for j, ln in enumerate(new_lens):
+            a = base + interval * j
+            lead = framing[0] if j == 0 else 0
+            trail = framing[1] if j == n - 1 else 0
+            runs.append((a, a + lead + ln + trail))
+            new_recs.append((a + lead, a + lead + ln))
+            if lead:
+                post.append((a, a + lead))
+            if trail:
+                post.append((a + lead + ln, a + lead + ln + trail))
+        T = m + framing[0] + framing[1]
+        cursor_after = runs[-1][1]                     # one past the highest position in use
+        ranges = np.asarray(sorted(gone), dtype=np.int64).reshape(-1, 2)
+        revisions.append(Revision(ranges=ranges, runs=runs, post=np.asarray(post, dtype=np.int64).reshape(-1, 2),
+                                  T=T, m=m, cursor=cursor, cursor_after=cursor_after, L_old=live,
+                                  intervals=list(intervals)))
+        intervals = subtract_ranges(intervals, ranges) + list(new_recs)
+        recs = [r for i, r in enumerate(recs) if i not in pick] + new_recs
+        live = live - sum(b - a for a, b in gone) + m
+        cursor = cursor_after
+    return PaperTrace(positions=positions, intervals=initial, cursor=interval * (n_records + 1),
+                      revisions=revisions, interval=interval)

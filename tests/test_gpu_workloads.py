@@ -313,3 +313,53 @@ def test_zero_removals_equal_fresh_prefill():
     assert_close(st2[vh_t].cpu().numpy(), S_ref, "maintained state vs oracle one pass")
     assert_close(do2[:, vh_t].cpu().numpy(), o_ref[N0:], "maintained delta tail vs oracle")
     assert_close(st2.cpu().numpy(), st1.cpu().numpy().astype(np.float64), "maintained state vs device one pass")
+
+
+def test_paper_shaped_revision_trace():
+    """Revisions shaped like the paper's measured trace (records in 10K-position slots,
+    one or two whole records replaced per revision at fresh slots past the cursor, framing
+    delimiters prefilled and removed again), carried over four revisions of one context
+    with one attention and one delta layer; every revision checked against the oracle
+    chained from the previous one."""
+    A, D = synth.CONFIGS[1].attn, synth.CONFIGS[1].delta
+    tr = synth.make_paper_trace(seed=5, head=700, n_records=10, record_len=(330, 450), n_revisions=4,
+                                m_range=(214, 362), index=201)
+    L0 = len(tr.positions)
+    cap = max([L0] + [r.L_old + r.T for r in tr.revisions])
+    k_bits, v_bits = synth.gen_attn_cache(5, 201, 0, L0, A)
+    S = synth.gen_delta_state(5, 201, 1, D).astype(np.float64)
+    kc, vc = _dev_cache(k_bits, cap), _dev_cache(v_bits, cap)
+    state = torch.from_numpy(S.astype(np.float32)).to(DEV)
+    ctx = tu.Context(cap, device=DEV)
+    ctx.pos[:L0] = torch.from_numpy(tr.positions.astype(np.int32)).to(DEV)
+    ctx.set_metadata(tr.intervals, tr.cursor)
+    pos, kb, vb = tr.positions.copy(), k_bits, v_bits
+    for ri, rv in enumerate(tr.revisions):
+        _say(f"revision {ri}: remove {rv.ranges.tolist()}, tail runs {rv.runs}, framing {rv.post.tolist()}, T {rv.T}")
+        assert ctx.len == rv.L_old and ctx.next_pos == rv.cursor
+        q, k, v = synth.gen_attn_tail(5, 201, 0, rv.T, A, rnd=ri)
+        dq, dk, dv, beta, g = synth.gen_delta_inputs(5, 201, 1, rv.T, D, rnd=ri)
+        a_out = torch.full((rv.T, A.n_q_heads, A.head_dim), float("nan"), dtype=torch.float32, device=DEV)
+        d_out = torch.full((rv.T, D.n_v_heads, D.d_v), float("nan"), dtype=torch.float32, device=DEV)
+        layers = [tu.LayerIO(tu.TU_LAYER_ATTN, to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), a_out, k_cache=[kc],
+                             v_cache=[vc]),
+                  tu.LayerIO(tu.TU_LAYER_DELTA, to_dev_bf16(dq), to_dev_bf16(dk), to_dev_bf16(dv), d_out,
+                             state=[state], beta=torch.from_numpy(beta).to(DEV), g=torch.from_numpy(g).to(DEV))]
+        tu.update_layer_stack([ctx], [rv.ranges], [rv.T], layers, _ap(A), _dp(D), post_ranges=[rv.post],
+                              placement=["slot"], place_runs=[rv.runs])
+        torch.cuda.synchronize()
+        tail_pos = np.concatenate([np.arange(a, b) for a, b in rv.runs])
+        ref = oracle.attention_layer_update(pos, kb, vb, rv.ranges, rv.cursor, q, k, v, A.rdim, A.rope_theta,
+                                            A.softmax_scale, live=pos, post_ranges=rv.post,
+                                            placement="slot", tail_positions=tail_pos)
+        n = len(ref["pos"])
+        assert ctx.len == n and ctx.next_pos == rv.cursor_after
+        assert np.array_equal(ctx.pos[:n].cpu().numpy(), ref["pos"])
+        assert np.array_equal(bits_of(vc[:n]), ref["v_cache"])
+        assert_bf16_close_bits(bits_of(kc[:n]), ref["k_cache"], f"revision {ri}: K cache")
+        assert_close(a_out.cpu().numpy(), ref["out"], f"revision {ri}: attention")
+        o_ref, S = oracle.delta_layer_update(S, dq, dk, dv, beta, g, D.scale)
+        assert_close(d_out.cpu().numpy(), o_ref, f"revision {ri}: delta out")
+        assert_close(state.cpu().numpy(), S, f"revision {ri}: delta state")
+        pos, kb, vb = ref["pos"], ref["k_cache"], ref["v_cache"]
+    assert tu.device_faults() == 0

@@ -177,3 +177,37 @@ def test_placement_bookkeeping_and_rejections():
     with pytest.raises(ValueError):
         oracle.attention_layer_update(pos, kc, vc, ranges, cursor, q, k, v, D, theta, 0.3, placement="slot",
                                       tail_positions=[4, 5, 50], post_ranges=[[30, 31]])
+
+
+def test_paper_shaped_trace_is_consistent():
+    """The seeded revision trace shaped like the paper's (records in 10K-position slots,
+    replacements at fresh slots, framing removed after each tail) is self-consistent and the
+    oracle carries it through every revision: removed ranges are whole live records, tail runs
+    start at slot boundaries at or past the cursor, framing lies inside the tail, and the
+    live-row count and cursor the trace states are the oracle's."""
+    import synth
+    tr = synth.make_paper_trace(seed=3, head=200, n_records=6, record_len=(40, 80), n_revisions=5,
+                                m_range=(30, 60), index=202)
+    pos = tr.positions.copy()
+    assert np.all(np.diff(pos) > 0)
+    assert sum(b - a for a, b in tr.intervals) == len(pos)
+    D = 8
+    kb = np.zeros((len(pos), 1, D), np.uint16)
+    vb = np.zeros_like(kb)
+    for rv in tr.revisions:
+        assert len(pos) == rv.L_old
+        live = set(pos.tolist())
+        for a, b in rv.ranges:
+            assert all(p in live for p in range(a, b))
+        assert rv.runs[0][0] >= rv.cursor and all(a % tr.interval == 0 for a, _ in rv.runs)
+        assert sum(b - a for a, b in rv.runs) == rv.T == rv.m + 11
+        tail = np.concatenate([np.arange(a, b) for a, b in rv.runs])
+        for a, b in rv.post:
+            assert np.all(np.isin(np.arange(a, b), tail))
+        q = np.zeros((rv.T, 1, D), np.uint16)
+        ref = oracle.attention_layer_update(pos, kb, vb, rv.ranges, rv.cursor, q, q, q, D, 1e4, 1.0, live=pos,
+                                            rows=np.zeros(0, np.int64), post_ranges=rv.post, placement="slot",
+                                            tail_positions=tail)
+        assert ref["cursor"] == rv.cursor_after
+        assert len(ref["pos"]) == rv.L_old - int(np.sum(rv.ranges[:, 1] - rv.ranges[:, 0])) + rv.m
+        pos, kb, vb = ref["pos"], ref["k_cache"], ref["v_cache"]
