@@ -367,7 +367,7 @@ def t_sweep_row(tu, synth, dev, attn_p, delta_p, seed, reps, warmup=2):
 
 
 def paper_trace_row(tu, synth, dev, attn_p, delta_p, seed, reps, warmup=1):
-    """Eight revisions shaped like the paper's measured trace (its Section 6.5: an
+    """Eight revisions shaped like the paper's measured trace (its Section 6.6: an
     ~11.9K-token prefix of ~390-token records in 10K-position slots; each revision
     replaces one or two whole records by 214-362 tokens at fresh slots past the cursor,
     with 11 framing tokens prefilled and removed again) through the 48-layer hybrid

@@ -364,7 +364,7 @@ class PaperTrace:
 def make_paper_trace(seed: int = 0, head: int = 1699, n_records: int = 26, record_len=(330, 450),
                      interval: int = 10000, n_revisions: int = 8, m_range=(214, 362), framing=(5, 6),
                      index: int = 200) -> PaperTrace:
-    """A revision trace shaped like the paper's measured one (Section 6.5, Table 1): a common
+    """A revision trace shaped like the paper's measured one (Sections 5.2 and 6.6, Table 1): a common
     head at positions [0, head), then records of about 390 tokens, record k at the start
     of its own `interval`-position slot (logical positions, not occupied rows); every
     revision removes one or two whole records and appends as many replacement records
