@@ -63,6 +63,8 @@ __device__ __forceinline__ int find_seq_by_chunk(const DeltaArgs& a, int c) {
   return si;
 }
 
+constexpr int cmax(size_t x, size_t y) { return (int)(x > y ? x : y); }
+
 // ------------------------------------------------------------------ prep
 constexpr int kPrepThreads = 512;   // 8 waves
 template <int DK, int C>
@@ -74,16 +76,26 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   constexpr int KP = DK + 8;     // pitch of [C][DK] bf16 tiles
   constexpr int CP = C + 4;      // pitch of [C][C] fp32 tiles
   constexpr int CH = C + 8;      // pitch of [*][C] f16 tiles
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[C][KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[C][KP];
-  __shared__ __attribute__((aligned(16))) float Mf[C][CP];
+  // LDS regions shared by arrays whose lifetimes do not overlap, so that two workgroups
+  // fit a CU: K (phases 0-5a) then (beta 2^lg K)^T (5b-6); Q (0-5a) then (beta V)^T
+  // (5b-6); M (1-4) then T in f16 (5a-6). A barrier separates 5a (the last reads of K,
+  // Q and T in fp32) from 5b (the first writes of the transposed copies).
+  constexpr int R1 = cmax(sizeof(bf16_t) * C * KP, sizeof(_Float16) * DK * CH);
+  constexpr int R2 = cmax(sizeof(bf16_t) * C * KP, sizeof(_Float16) * DV * CH);
+  constexpr int R3 = cmax(sizeof(float) * C * CP, sizeof(_Float16) * C * CH);
+  __shared__ __attribute__((aligned(16))) char r1[R1];
+  __shared__ __attribute__((aligned(16))) char r2[R2];
+  __shared__ __attribute__((aligned(16))) char r3[R3];
   __shared__ __attribute__((aligned(16))) float Tf[C][CP];
   __shared__ __attribute__((aligned(16))) float Xs[3][16][20];
-  __shared__ __attribute__((aligned(16))) _Float16 Th[C][CH];
-  __shared__ __attribute__((aligned(16))) _Float16 Bt[DK][CH];
-  __shared__ __attribute__((aligned(16))) _Float16 Vt[DV][CH];
   __shared__ __attribute__((aligned(16))) float lg[C];
   __shared__ __attribute__((aligned(16))) float bt[C];
+  auto& Ks = *reinterpret_cast<bf16_t(*)[C][KP]>(r1);
+  auto& Bt = *reinterpret_cast<_Float16(*)[DK][CH]>(r1);
+  auto& Qs = *reinterpret_cast<bf16_t(*)[C][KP]>(r2);
+  auto& Vt = *reinterpret_cast<_Float16(*)[DV][CH]>(r2);
+  auto& Mf = *reinterpret_cast<float(*)[C][CP]>(r3);
+  auto& Th = *reinterpret_cast<_Float16(*)[C][CH]>(r3);
 
   const int Hk = a.n_k_heads, Hv = a.n_v_heads;
   const int c = blockIdx.x / Hv;          // global chunk
@@ -247,22 +259,42 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
     lds_barrier();
   }
 
-  // ---- phase 5: f16 copies: T (lower, zero upper), (beta 2^lg K)^T and (beta V)^T
+  // ---- phase 5a: T to f16 (lower, zero upper; M is dead), this thread's K rows into
+  // registers, and scale * 2^lg Q as f16 (the chain's Q S^T operand, row decay folded in)
   for (int e = tid; e < C * C; e += NT) {
     const int r = e / C, i = e - r * C;
     Th[r][i] = (_Float16)((i >> 4) <= (r >> 4) ? Tf[r][i] : 0.f);
   }
+  u32x4 kw[4];
+  if (tid < NE5) {
+    const int s4 = (tid % (C / 4)) * 4, d0 = (tid / (C / 4)) * 8;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) kw[j] = *(const u32x4*)&Ks[s4 + j][d0];
+  }
+  for (int e = tid; e < C * (DK / 8); e += NT) {
+    const int r = e / (DK / 8), cc = e - r * (DK / 8);
+    const float w = a.scale * __builtin_amdgcn_exp2f(lg[r]);
+    const u32x4 qw = *(const u32x4*)&Qs[r][cc * 8];
+    f16x8 hq;
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      const uint32_t qb = (d & 1) ? (qw[d >> 1] & 0xFFFF0000u) : (qw[d >> 1] << 16);
+      hq[d] = (_Float16)(w * __uint_as_float(qb));
+    }
+    *(f16x8*)(a.ws_q + slot * C * DK + (long)r * DK + cc * 8) = hq;
+  }
+  lds_barrier();   // K and Q are no longer read: their regions take the transposed copies
+
+  // ---- phase 5b: (beta 2^lg K)^T and (beta V)^T in f16, and the decayed K^T for the chain
   if (tid < NE5) {
     const int s4 = (tid % (C / 4)) * 4, d0 = (tid / (C / 4)) * 8;
     float wk[4], wv[4], wd[4];
-    u32x4 kw[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int s = s4 + j;
       wv[j] = bt[s];
       wk[j] = bt[s] * __builtin_amdgcn_exp2f(lg[s]);
       wd[j] = __builtin_amdgcn_exp2f(lg[C - 1] - lg[s]);
-      kw[j] = *(const u32x4*)&Ks[s][d0];
     }
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
@@ -279,19 +311,6 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
       *(f16x4*)&Vt[d0 + d][s4] = hv;
       *(f16x4*)(a.ws_kt + slot * DK * C + (long)(d0 + d) * C + s4) = hd;
     }
-  }
-  // scale * 2^lg Q as f16 (the chain's Q S^T operand, row decay folded in)
-  for (int e = tid; e < C * (DK / 8); e += NT) {
-    const int r = e / (DK / 8), cc = e - r * (DK / 8);
-    const float w = a.scale * __builtin_amdgcn_exp2f(lg[r]);
-    const u32x4 qw = *(const u32x4*)&Qs[r][cc * 8];
-    f16x8 hq;
-#pragma unroll
-    for (int d = 0; d < 8; ++d) {
-      const uint32_t qb = (d & 1) ? (qw[d >> 1] & 0xFFFF0000u) : (qw[d >> 1] << 16);
-      hq[d] = (_Float16)(w * __uint_as_float(qb));
-    }
-    *(f16x8*)(a.ws_q + slot * C * DK + (long)r * DK + cc * 8) = hq;
   }
   lds_barrier();
 
