@@ -204,6 +204,23 @@ def delta_bytes(cfg, rounds):
     return sum(T * per_tok + state for R in rounds for T in R["T"])
 
 
+def attention_kv_bytes(cfg, rounds):
+    """K and V of every row an attention layer reads (surviving + new), once."""
+    a = cfg.attn
+    return sum((Lk + T) * a.n_kv_heads * a.head_dim * 2 * 2 for R in rounds for T, Lk in zip(R["T"], R["L_keep"]))
+
+
+def stack_ideal_ms(cfg, rounds, mfma_tflops, hbm_gbs):
+    """The step at the roofline: per step of the path its algorithmic work at the peak that
+    bounds it (attention: max of its flops over the matrix peak and its K/V bytes over HBM;
+    delta rule and compaction: bytes over HBM), summed over the layers."""
+    kinds = cfg.layer_kinds()
+    attn = max(attention_flops(cfg, rounds) / (mfma_tflops * 1e12), attention_kv_bytes(cfg, rounds) / (hbm_gbs * 1e9))
+    delta = delta_bytes(cfg, rounds) / (hbm_gbs * 1e9)
+    comp = gather_bytes(cfg, rounds) / (hbm_gbs * 1e9)
+    return 1e3 * (kinds.count("attn") * (attn + comp) + kinds.count("delta") * delta)
+
+
 def gather_bytes(cfg, rounds):
     """Minimum: every surviving row behind the first hole is read and written once."""
     a = cfg.attn
@@ -896,6 +913,17 @@ def main():
                 row["frac_of_measured_copy"] = round(row["achieved"] / peaks["copy_gbs"], 4)
         print(f"[bench] measured peaks: {json.dumps(peaks)}", file=sys.stderr, flush=True)
 
+    # the whole step against its roofline: the summed ideal time of every step of the path
+    # (datasheet peaks; and the rates this part reached in this run, when measured)
+    ideal = stack_ideal_ms(cfg, rounds, MFMA16_PEAK_TFLOPS, HBM_PEAK_GBS)
+    stack_roofline = {"ideal_ms": round(ideal, 5), "measured_ms": round(upd_ms, 5), "frac": round(ideal / upd_ms, 4),
+                      "peaks": {"mfma_tflops": MFMA16_PEAK_TFLOPS, "hbm_gbs": HBM_PEAK_GBS}}
+    if peaks is not None:
+        ideal_m = stack_ideal_ms(cfg, rounds, peaks["bf16_gemm_tflops"], peaks["copy_gbs"])
+        stack_roofline.update({"ideal_ms_measured_peaks": round(ideal_m, 5),
+                               "frac_of_measured_peaks": round(ideal_m / upd_ms, 4)})
+    print(f"[bench] stack roofline: {json.dumps(stack_roofline)}", file=sys.stderr, flush=True)
+
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] cpu oracle leg ...", file=sys.stderr, flush=True)
@@ -921,6 +949,7 @@ def main():
                    "attn": f"{a.n_q_heads}q/{a.n_kv_heads}kv x {a.head_dim}",
                    "delta": f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}"},
         "roofline": roofline,
+        "stack_roofline": stack_roofline,
         "measured_peaks": peaks,
         "extra_rows": extra,
         "stages": stages,
