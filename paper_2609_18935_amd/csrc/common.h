@@ -17,8 +17,8 @@ typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
 
 constexpr int kMaxSeqPerLaunch = 32;
 constexpr int kMaxRangesPerLaunch = 128;
-constexpr int kMaxBufPerLaunch = 32;
-constexpr int kMaxSeqPerCompact = 8;
+constexpr int kMaxBufPerLaunch = 64;
+constexpr int kMaxSeqPerCompact = 32;
 constexpr int kScanRows = 1024;  // rows per keep-scan workgroup (a multiple of 256, at most 16K)
 constexpr int kFlagStride = 32;   // compaction stripe counters sit one per 128-byte line
 constexpr int kGatherStripeBytes = 256 * 16 * 16;  // threads x vectors x 16 B
