@@ -364,3 +364,68 @@ def test_short_conv_batch_matches_single_calls():
     for (st, x, w, out), (ref_y, _, ref_s), (C, T) in zip(items, refs, specs):
         assert_bf16_close_bits(bits_of(out), ref_y, f"batch conv C={C} T={T}")
         assert np.array_equal(bits_of(st), ref_s)
+
+
+def test_stack_equals_per_layer_calls():
+    """One update_layer_stack call over two attention and two delta layers gives, bit for
+    bit, what the separate entry points give layer by layer on copies of the same state
+    (compact_kv over both attention layers' caches, tail_prefill_attention per layer,
+    commit_tail, delta_rule_continue per layer): the stack only batches and orders them."""
+    a = synth.CONFIGS[1].attn
+    d = synth.CONFIGS[1].delta
+    L, T = 3000, 200
+    ranges = np.array([[400, 528], [2000, 2064]])
+    _say(f"stack vs per-layer calls: L {L}, ranges {ranges.tolist()}, T {T}")
+    ap = tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta, a.softmax_scale)
+    dp = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
+    caches, tails, states, dins = [], [], [], []
+    for layer in range(2):
+        kb, vb = synth.gen_attn_cache(7, 1, layer, L, a)
+        kc = np.zeros((L + T, a.n_kv_heads, a.head_dim), np.uint16)
+        vc = np.zeros_like(kc)
+        kc[:L], vc[:L] = kb, vb
+        caches.append((kc, vc))
+        tails.append([to_dev_bf16(x) for x in synth.gen_attn_tail(7, 1, layer, T, a)])
+        states.append(synth.gen_delta_state(7, 1, 2 + layer, d))
+        q, k, v, beta, g = synth.gen_delta_inputs(7, 1, 2 + layer, T, d)
+        dins.append((to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), torch.from_numpy(beta).to(DEV),
+                     torch.from_numpy(g).to(DEV)))
+
+    def fresh():
+        ctx = tu.Context(L + T, device=DEV)
+        ctx.pos[:L] = torch.arange(L, dtype=torch.int32, device=DEV)
+        ctx.set_metadata([(0, L)], L)
+        kv = [(to_dev_bf16(kc), to_dev_bf16(vc)) for kc, vc in caches]
+        st = [torch.from_numpy(S.copy()).to(DEV) for S in states]
+        ao = [torch.full((T, a.n_q_heads, a.head_dim), float("nan"), dtype=torch.float32, device=DEV)
+              for _ in range(2)]
+        do = [torch.full((T, d.n_v_heads, d.d_v), float("nan"), dtype=torch.float32, device=DEV) for _ in range(2)]
+        return ctx, kv, st, ao, do
+
+    # the stack: attention, delta, attention, delta
+    c1, kv1, st1, ao1, do1 = fresh()
+    layers = []
+    for i in range(2):
+        q, k, v = tails[i]
+        layers.append(tu.LayerIO(tu.TU_LAYER_ATTN, q, k, v, ao1[i], k_cache=[kv1[i][0]], v_cache=[kv1[i][1]]))
+        dq, dk, dv, beta, g = dins[i]
+        layers.append(tu.LayerIO(tu.TU_LAYER_DELTA, dq, dk, dv, do1[i], state=[st1[i]], beta=beta, g=g))
+    tu.update_layer_stack([c1], [ranges], [T], layers, ap, dp)
+    # the same through the separate entry points
+    c2, kv2, st2, ao2, do2 = fresh()
+    tu.compact_kv(c2, [k for k, _ in kv2], [v for _, v in kv2], ranges)
+    for i in range(2):
+        q, k, v = tails[i]
+        tu.tail_prefill_attention(c2, kv2[i][0], kv2[i][1], ap, q, k, v, ao2[i])
+    tu.commit_tail(c2, T)
+    for i in range(2):
+        dq, dk, dv, beta, g = dins[i]
+        tu.delta_rule_continue(st2[i], dq, dk, dv, beta, g, dp, do2[i])
+    torch.cuda.synchronize()
+    assert c1.len == c2.len and c1.next_pos == c2.next_pos and c1.intervals() == c2.intervals()
+    n = c1.len
+    assert torch.equal(c1.pos[:n], c2.pos[:n])
+    for i in range(2):
+        assert torch.equal(kv1[i][0][:n], kv2[i][0][:n]) and torch.equal(kv1[i][1][:n], kv2[i][1][:n]), f"layer {i} cache"
+        assert torch.equal(ao1[i], ao2[i]), f"layer {i} attention output"
+        assert torch.equal(do1[i], do2[i]) and torch.equal(st1[i], st2[i]), f"layer {i} delta output and state"
