@@ -85,8 +85,9 @@ typedef struct tu_seq {
  * head_dim must be 64, 128 or 256; rotary_dim even, 0 <= rotary_dim <= head_dim
  * (rotate-half pairs (j, j + rotary_dim/2), angle pos * rope_theta^(-2j/rotary_dim)).
  * kv_splits = 0 lets the library choose how many workgroups share one key range
- * (from the waves of workgroups a launch runs in); a positive value forces that many
- * splits (results are the same up to rounding).
+ * (from the waves of workgroups a launch runs in; up to 128 for short tails over long
+ * contexts); a value in [1, 64] forces that many splits (results are the same up to
+ * rounding). Other values are rejected with TU_ERR_ARG.
  */
 typedef struct tu_attn_params {
   int32_t n_q_heads;
