@@ -122,3 +122,36 @@ def test_device_fault_on_mislabelled_positions():
     tu.compact_kv(ctx, [k], [v], np.array([[900, 1100]]))
     assert tu.device_faults() == 0
     assert torch.equal(k[: L - 200], k0[keep])
+
+
+def test_all_tails_empty():
+    """Pure deletion in every context of a call: caches compacted, states, outputs and
+    cursors untouched, no attention or delta launch needed."""
+    a = synth.AttnShape(16, 2, 256)
+    d = synth.DeltaShape(16, 32, 128, 128, 64)
+    specs = [(2000, np.array([[10, 50], [1900, 2000]])), (900, np.array([[0, 300]]))]
+    print(f"[case] all tails empty: {[(L, r.tolist()) for L, r in specs]}", flush=True)
+    acs = [AttnCase(a, 41, 1, 0, L, 0, char=c) for c, (L, _) in enumerate(specs)]
+    dcs = [DeltaCase(d, 41, 1, 1, 0, char=c) for c in range(len(specs))]
+    ctxs = [_ctx_for(ac) for ac in acs]
+    empty = lambda *s: torch.empty(s, dtype=torch.bfloat16, device=DEV)
+    layers = [tu.LayerIO(tu.TU_LAYER_ATTN, empty(0, 16, 256), empty(0, 2, 256), empty(0, 2, 256),
+                         torch.empty((0, 16, 256), dtype=torch.float32, device=DEV),
+                         k_cache=[c.k_cache for c in acs], v_cache=[c.v_cache for c in acs]),
+              tu.LayerIO(tu.TU_LAYER_DELTA, empty(0, 16, 128), empty(0, 16, 128), empty(0, 32, 128),
+                         torch.empty((0, 32, 128), dtype=torch.float32, device=DEV), state=[c.state for c in dcs],
+                         beta=torch.empty((0, 32), dtype=torch.float32, device=DEV),
+                         g=torch.empty((0, 32), dtype=torch.float32, device=DEV))]
+    tu.update_layer_stack(ctxs, [r for _, r in specs], [0, 0], layers,
+                          tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta),
+                          tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk))
+    torch.cuda.synchronize()
+    for (L, ranges), ac, dc, ctx in zip(specs, acs, dcs, ctxs):
+        ref = ac.oracle(ranges, L)
+        n = len(ref["pos"])
+        assert ctx.len == n and ctx.next_pos == L
+        assert np.array_equal(ctx.pos[:n].cpu().numpy(), ref["pos"])
+        assert np.array_equal(bits_of(ac.v_cache[:n]), ref["v_cache"])
+        assert np.array_equal(bits_of(ac.k_cache[:n]), ref["k_cache"])
+        assert np.array_equal(dc.state.cpu().numpy(), dc.S0)
+    assert tu.device_faults() == 0
