@@ -12,9 +12,16 @@ two device synchronisations.
 Printed: one JSON line with tail tokens/s, the speedup over a full refill of the
 same final context through the same kernels, the roofline fraction of the
 dominant kernel (its duration measured with HIP events on its stream, in a
-second pass over the same steps) and the CPU oracle timed on this host.
+second pass over the same steps, and its HBM traffic from the committed counter
+passes), the whole step against its roofline (stack_roofline), per-stage
+fractions, and the CPU oracle timed on this host. extra_rows adds, for the same
+shapes: delimiter removal after prefill, the slot-preserving and
+tail-and-relocate placements, the attention diagnostics, the short-convolution
+continuation and, for the single-refresh workload, the paper-shaped revision
+trace through the 48-layer stack and the tail-length sweep at 32K rows.
 
     python bench.py [--config 1] [--steps 20] [--warmup 3] [--gpus 1]
+                    [--no-refill] [--no-cpu-baseline] [--no-peaks] [--no-t-sweep] [--no-paper-trace]
 """
 import argparse
 import hashlib
