@@ -135,3 +135,39 @@ def test_relocate_keys_standalone():
     c.pos_h, c.k_h = oracle.relocate_keys(c.pos_h, c.k_h, moves, A.rdim, A.rope_theta)
     c.cursor = max(c.cursor, 7020)
     c.check("after relocate_keys")
+
+
+def test_three_placements_in_one_call():
+    """One stack call over three contexts, one per placement (true tail, slot-preserving,
+    tail-and-relocate with delimiters): the launch carries several contexts' position runs
+    and places their attention work through the die table; each context is checked
+    against its own oracle chain."""
+    specs = [  # (seed, L_old, cap, T, ranges, placement, runs, post)
+        (31, 2200, 2800, 250, np.array([[100, 300]]), "tail", None, None),
+        (32, 3100, 3800, 330, np.array([[500, 628], [2900, 3000]]), "slot",
+         [(500, 628), (2900, 3000), (7000, 7102)], None),
+        (33, 1800, 2400, 180, np.array([[1000, 1100]]), "relocate", [(1000, 1100), (8000, 8080)],
+         np.array([[1000, 1007], [8075, 8080]])),
+    ]
+    _say(f"three placements in one call: {[(s[1], s[5], s[3]) for s in specs]}")
+    cs = [Ctx(seed, L, cap) for seed, L, cap, *_ in specs]
+    qkv = [synth.gen_attn_tail(seed, 1, 0, T, A, rnd=0) for seed, _, _, T, *_ in specs]
+    Ts = [s[3] for s in specs]
+    off = np.concatenate([[0], np.cumsum(Ts)]).astype(int)
+    cat = lambda i: to_dev_bf16(np.concatenate([x[i] for x in qkv]))
+    out = torch.full((off[-1], A.n_q_heads, A.head_dim), float("nan"), dtype=torch.float32, device=DEV)
+    layers = [tu.LayerIO(tu.TU_LAYER_ATTN, cat(0), cat(1), cat(2), out, k_cache=[c.kc for c in cs],
+                         v_cache=[c.vc for c in cs])]
+    tu.update_layer_stack([c.ctx for c in cs], [s[4] for s in specs], Ts, layers,
+                          tu.attn_params(A.n_q_heads, A.n_kv_heads, A.head_dim, A.rdim, A.rope_theta),
+                          post_ranges=[s[7] for s in specs], placement=[s[5] for s in specs],
+                          place_runs=[s[6] for s in specs])
+    torch.cuda.synchronize()
+    for i, (c, (seed, L, cap, T, ranges, placement, runs, post), (q, k, v)) in enumerate(zip(cs, specs, qkv)):
+        tail_pos = None if runs is None else np.concatenate([np.arange(a, b) for a, b in runs])
+        ref = oracle.attention_layer_update(c.pos_h, c.k_h, c.v_h, ranges, c.cursor, q, k, v, A.rdim, A.rope_theta,
+                                            A.softmax_scale, live=c.pos_h.tolist(), post_ranges=post,
+                                            placement=placement, tail_positions=tail_pos)
+        c.pos_h, c.k_h, c.v_h, c.cursor = ref["pos"], ref["k_cache"], ref["v_cache"], ref["cursor"]
+        assert_close(out[off[i]: off[i + 1]].cpu().numpy(), ref["out"], f"context {i} ({placement}) attention")
+        c.check(f"context {i} ({placement})")
