@@ -457,21 +457,22 @@ struct AttnLaunch {
 };
 
 // Key-range splits of one context's attention. An attention workgroup holds a whole CU,
-// so a launch runs in waves of kCus workgroups. Alone in its launch, a context takes
-// the split count that minimises (waves) x (time of one workgroup: its key tiles plus a
-// fixed part) plus the merge (a launch, and the partial outputs written and read back
-// once per split); about 2.6 us per 64-key tile at head_dim 256, 5 TB/s. With other
-// contexts in the launch (whose lengths differ, so waves do not line up) it takes
-// enough splits for the launch to fill the CUs. At least 4 key tiles per split, at
-// most kMaxAutoSplits (a decode-like tail of one token over 32K rows fills the chip
-// with 128 splits of its two KV heads).
+// so a launch runs in waves of kCus workgroups. When every item of the launch has the
+// same surviving rows and tail (one context, or the attention layers of one context's
+// stack), the split count minimises (waves) x (time of one workgroup: its key tiles plus
+// a fixed part) plus the merge (a launch, and the partial outputs written and read back
+// once per split); about 2.6 us per 64-key tile at head_dim 256, 5 TB/s. With items of
+// different lengths in the launch (whose waves do not line up) it takes enough splits
+// for the launch to fill the CUs. At least 4 key tiles per split, at most
+// kMaxAutoSplits (a decode-like tail of one token over 32K rows fills the chip with 128
+// splits of its two KV heads).
 constexpr int kMaxAutoSplits = 128;
 
-int choose_splits(const tu_attn_params* p, int64_t L_keep, int64_t T, int64_t base_items_total, bool alone) {
+int choose_splits(const tu_attn_params* p, int64_t L_keep, int64_t T, int64_t base_items_total, bool uniform) {
   if (p->kv_splits > 0) return p->kv_splits;
   const int64_t n_kt = (L_keep + T + kAttnKeys - 1) / kAttnKeys;
   const int64_t max_s = std::max<int64_t>(1, std::min<int64_t>(kMaxAutoSplits, n_kt / 4));
-  if (!alone) {
+  if (!uniform) {
     const int64_t want = std::max<int64_t>(1, (kCus + base_items_total - 1) / std::max<int64_t>(1, base_items_total));
     return (int)std::min(want, max_s);
   }
@@ -558,7 +559,14 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
       runs += items[g1++].n_place_runs;
     Arena ar(ws);
     int64_t base_items = 0;
-    for (size_t i = g0; i < g1; ++i) base_items += (int64_t)Hkv * ((items[i].T * G + kAttnRows - 1) / kAttnRows);
+    bool uniform = true;   // every item with a tail has the same surviving rows and tail length
+    const AttnItem* first = nullptr;
+    for (size_t i = g0; i < g1; ++i) {
+      base_items += (int64_t)Hkv * ((items[i].T * G + kAttnRows - 1) / kAttnRows);
+      if (items[i].T <= 0) continue;
+      if (!first) first = &items[i];
+      uniform = uniform && items[i].T == first->T && items[i].L_keep == first->L_keep;
+    }
     AttnLaunch L{};
     L.rope.n_q_heads = Hq;
     L.rope.n_kv_heads = Hkv;
@@ -577,7 +585,7 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
       void* qh_ws = ar.take(sizeof(bf16_t) * it.T * Hq * D);
       if (!qh) qh = static_cast<bf16_t*>(qh_ws);
       const int tiles = (int)((it.T * G + kAttnRows - 1) / kAttnRows);
-      const int splits = choose_splits(p, it.L_keep, it.T, base_items, g1 - g0 == 1);
+      const int splits = choose_splits(p, it.L_keep, it.T, base_items, uniform);
       const int vt_tiles = (int)((it.L_keep + it.T + kAttnKeys - 1) / kAttnKeys);
       _Float16* vt = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)Hkv * vt_tiles * D * kVtRow));
       _Float16* po = nullptr;
@@ -1014,6 +1022,31 @@ std::vector<AttnItem> stack_attn_items(const tu_update* u, const StackPlan& sp, 
   return items;
 }
 
+// The (attention layer, context) items of the attention layers in groups that share a set
+// of launches. A layer whose own workgroups (before key splits) do not fill the chip's CUs
+// joins the next ones until the group does: short tails of a deep stack then run as a few
+// launches instead of one set per layer, while layers that fill the chip on their own keep
+// a set each.
+std::vector<std::vector<AttnItem>> stack_attn_groups(const tu_update* u, const StackPlan& sp) {
+  std::vector<std::vector<AttnItem>> groups;
+  std::vector<AttnItem> cur;
+  int64_t cur_wg = 0;
+  const int G = u->attn.n_q_heads / u->attn.n_kv_heads;
+  for (int l = 0; l < u->n_layers; ++l) {
+    if (u->layers[l].kind != TU_LAYER_ATTN) continue;
+    auto items = stack_attn_items(u, sp, u->layers[l]);
+    cur.insert(cur.end(), items.begin(), items.end());
+    for (const auto& it : items) cur_wg += (int64_t)u->attn.n_kv_heads * ((it.T * G + kAttnRows - 1) / kAttnRows);
+    if (cur_wg >= kCus) {
+      groups.push_back(std::move(cur));
+      cur.clear();
+      cur_wg = 0;
+    }
+  }
+  if (!cur.empty()) groups.push_back(std::move(cur));
+  return groups;
+}
+
 void append_delta_items(const tu_update* u, const StackPlan& sp, const tu_layer_io& L,
                         std::vector<DeltaItem>* items) {
   const int64_t krow = (int64_t)u->delta.n_k_heads * u->delta.d_k;
@@ -1298,14 +1331,11 @@ StackWorkspace stack_workspace(const tu_update* u, StackPlan& sp) {
       w.attn = std::max(w.attn, cp.ws_bytes);
     }
   }
-  for (int l = 0; l < u->n_layers; ++l) {
+  for (auto& items : stack_attn_groups(u, sp)) {
     size_t b = 0;
-    if (u->layers[l].kind == TU_LAYER_ATTN) {
-      auto items = stack_attn_items(u, sp, u->layers[l]);
-      std::vector<AttnLaunch> ls;
-      plan_attention(&u->attn, items, nullptr, &ls, &b);
-      w.attn = std::max(w.attn, b);
-    }
+    std::vector<AttnLaunch> ls;
+    plan_attention(&u->attn, items, nullptr, &ls, &b);
+    w.attn = std::max(w.attn, b);
   }
   auto items = stack_delta_items(u, sp);
   if (!items.empty()) {
@@ -1584,12 +1614,10 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
     if (int e = plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, ws_attn, &cp)) return e;
     if (int e = run_compaction(cp, st)) return e;
   }
-  // a4-a5 in layer order
-  for (int l = 0; l < u->n_layers; ++l) {
-    const tu_layer_io& L = u->layers[l];
-    if (L.kind != TU_LAYER_ATTN) continue;
+  // a4-a5: the attention layers are independent of each other once the caches are
+  // compacted; layers too small to fill the chip share a set of launches
+  for (auto& items : stack_attn_groups(u, sp)) {
     size_t b = 0;
-    auto items = stack_attn_items(u, sp, L);
     std::vector<AttnLaunch> ls;
     plan_attention(&u->attn, items, ws_attn, &ls, &b);
     if (int e = run_attention(ls, u->attn.head_dim, st)) return e;

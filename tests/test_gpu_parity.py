@@ -370,13 +370,16 @@ def test_stack_equals_per_layer_calls():
     """One update_layer_stack call over two attention and two delta layers gives, bit for
     bit, what the separate entry points give layer by layer on copies of the same state
     (compact_kv over both attention layers' caches, tail_prefill_attention per layer,
-    commit_tail, delta_rule_continue per layer): the stack only batches and orders them."""
+    commit_tail, delta_rule_continue per layer): the stack only batches and orders them.
+    The key-range split count is forced: left to the library it follows the launch's
+    size, which differs between one layer and two, and with it the rounding."""
     a = synth.CONFIGS[1].attn
     d = synth.CONFIGS[1].delta
     L, T = 3000, 200
     ranges = np.array([[400, 528], [2000, 2064]])
     _say(f"stack vs per-layer calls: L {L}, ranges {ranges.tolist()}, T {T}")
-    ap = tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta, a.softmax_scale)
+    ap = tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta, a.softmax_scale,
+                        kv_splits=3)
     dp = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
     caches, tails, states, dins = [], [], [], []
     for layer in range(2):
