@@ -1023,27 +1023,25 @@ std::vector<AttnItem> stack_attn_items(const tu_update* u, const StackPlan& sp, 
 }
 
 // The (attention layer, context) items of the attention layers in groups that share a set
-// of launches. A layer whose own workgroups (before key splits) do not fill the chip's CUs
-// joins the next ones until the group does: short tails of a deep stack then run as a few
-// launches instead of one set per layer, while layers that fill the chip on their own keep
-// a set each.
+// of launches. A layer whose own workgroups (before key splits) fill the chip's CUs keeps
+// a set of its own: its launch already runs whole waves, and mixing layers of that size
+// spreads the dies over more key/value streams at once. All smaller layers share one set,
+// so a deep stack of short tails runs as a few launches whose splits fill the chip.
 std::vector<std::vector<AttnItem>> stack_attn_groups(const tu_update* u, const StackPlan& sp) {
   std::vector<std::vector<AttnItem>> groups;
-  std::vector<AttnItem> cur;
-  int64_t cur_wg = 0;
+  std::vector<AttnItem> small;
   const int G = u->attn.n_q_heads / u->attn.n_kv_heads;
   for (int l = 0; l < u->n_layers; ++l) {
     if (u->layers[l].kind != TU_LAYER_ATTN) continue;
     auto items = stack_attn_items(u, sp, u->layers[l]);
-    cur.insert(cur.end(), items.begin(), items.end());
-    for (const auto& it : items) cur_wg += (int64_t)u->attn.n_kv_heads * ((it.T * G + kAttnRows - 1) / kAttnRows);
-    if (cur_wg >= kCus) {
-      groups.push_back(std::move(cur));
-      cur.clear();
-      cur_wg = 0;
-    }
+    int64_t wg = 0;
+    for (const auto& it : items) wg += (int64_t)u->attn.n_kv_heads * ((it.T * G + kAttnRows - 1) / kAttnRows);
+    if (wg >= kCus)
+      groups.push_back(std::move(items));
+    else
+      small.insert(small.end(), items.begin(), items.end());
   }
-  if (!cur.empty()) groups.push_back(std::move(cur));
+  if (!small.empty()) groups.push_back(std::move(small));
   return groups;
 }
 
@@ -1615,7 +1613,7 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
     if (int e = run_compaction(cp, st)) return e;
   }
   // a4-a5: the attention layers are independent of each other once the caches are
-  // compacted; layers too small to fill the chip share a set of launches
+  // compacted; the layers too small to fill the chip share one set of launches
   for (auto& items : stack_attn_groups(u, sp)) {
     size_t b = 0;
     std::vector<AttnLaunch> ls;
