@@ -129,9 +129,10 @@ __device__ void rope_token(const RopeArgs& a, int tok) {
 // key_slot order within 16-key groups followed by 8 halves of padding (left
 // unwritten; the attention kernel never reads it). Keys past the cache's data are
 // zero. Thread (c, m) builds chunk c (8 keys) of the 8 rows 8m .. 8m + 7: it loads
-// those 8 keys' dims 8m .. 8m + 7 (16 bytes each, consecutive threads read
-// consecutive bytes of a row), transposes the 8 x 8 block in registers and writes 8
-// chunks.
+// those 8 keys' dims 8m .. 8m + 7 (16 bytes each), transposes the 8 x 8 block in
+// registers and writes 8 chunks. c is the fastest-moving index: a wave's load reads
+// 128 contiguous bytes of each of 8 rows, and its store writes the 8 chunks of each of
+// 8 V^T rows contiguously.
 template <int D>
 __device__ void vt_pack_tile(const AttnArgs& a, int item) {
   constexpr int M = D / 8;                 // 8-dim blocks per row
@@ -150,8 +151,8 @@ __device__ void vt_pack_tile(const AttnArgs& a, int item) {
   const bf16_t* src_new = S.v_new + (long)hkv * D;   // tail row key - L_keep
   _Float16* dst = S.vt + ((long)hkv * S.n_vt_tiles + kt) * (D * kVtRow);
   for (int w = threadIdx.x; w < 8 * M; w += kRopeThreads) {
-    const int m = w % M;        // consecutive threads: consecutive dim blocks
-    const int c = w / M;        // key chunk 0..7
+    const int c = w & 7;        // key chunk 0..7 (consecutive threads)
+    const int m = w >> 3;       // 8-dim block
     u32x4 rowv[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
