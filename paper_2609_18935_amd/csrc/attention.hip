@@ -343,7 +343,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
       __builtin_amdgcn_sched_group_barrier(kValu, 4, 0);
     }
   };
-  // second part: the other score MFMAs and P.V with the exponentials and the tile loads
+  // second part: the other score MFMAs and P.V with the exponentials and the tile loads.
+  // Two vector instructions per score MFMA measured best (2-3 % over 3 to 5; 1 is worse)
   auto sched_tail = [&](int nload) __attribute__((always_inline)) {
     constexpr int kAhead = 4;
     __builtin_amdgcn_sched_group_barrier(kDsRead, kAhead, 0);
@@ -351,7 +352,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     for (int i = 0; i < NS / 2; ++i) {
       __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
       __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(kValu, 5, 0);
+      __builtin_amdgcn_sched_group_barrier(kValu, 2, 0);
     }
 #pragma unroll
     for (int i = 0; i < 2 * NDB; ++i) {
