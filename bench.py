@@ -9,19 +9,26 @@ step runs on its own pristine copy of the contexts (caches, states, positions),
 prepared before the timed region, so the K timed steps run back to back between
 two device synchronisations.
 
-Printed: one JSON line with tail tokens/s, the speedup over a full refill of the
-same final context through the same kernels, the roofline fraction of the
-dominant kernel (its duration measured with HIP events on its stream, in a
-second pass over the same steps, and its HBM traffic from the committed counter
-passes), the whole step against its roofline (stack_roofline), per-stage
-fractions, and the CPU oracle timed on this host. extra_rows adds, for the same
-shapes: delimiter removal after prefill, the slot-preserving and
-tail-and-relocate placements, the attention diagnostics, the short-convolution
-continuation and, for the single-refresh workload, the paper-shaped revision
-trace through the 48-layer stack and the tail-length sweep at 32K rows.
+The headline workload is the 48-layer hybrid stack (12 attention + 36 delta-rule
+layers) on a 65,536-token context: 8 records of 256 tokens removed, 2,048 tail
+tokens appended. Printed: one JSON line with tail tokens/s, the speedup over a
+full refill of the same final context through the same kernels, the roofline
+fraction of the dominant kernel (its duration measured with HIP events on its
+stream, in a second pass over the same steps, and its HBM traffic from the
+committed counter passes), the whole step against its roofline
+(stack_roofline), per-stage fractions, and the CPU oracle timed on this host.
+extra_rows adds: the other workloads (single refresh at 8K, eight rounds over a
+32K context with the refill speedup after every round, 32 contexts in one call),
+delimiter removal after prefill, the slot-preserving and tail-and-relocate
+placements, the attention diagnostics, the short-convolution continuation, the
+paper-shaped revision trace through the 48-layer stack and the tail-length sweep
+at 32K rows.
 
-    python bench.py [--config 1] [--steps 20] [--warmup 3] [--gpus 1]
+    python bench.py [--config 4] [--steps 20] [--warmup 3] [--gpus 1] [--extra-configs 1,2,3]
                     [--no-refill] [--no-cpu-baseline] [--no-peaks] [--no-t-sweep] [--no-paper-trace]
+                    [--only-update]
+    python bench.py --calibrate-copy 256            # counter calibration (a plain device copy)
+    python bench.py --config N --summarize-profile DIR   # rocprofv3 outputs -> profiles/ (CPU)
 """
 import argparse
 import hashlib
@@ -44,7 +51,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=1, choices=[0, 1, 2, 3, 4])
+    ap.add_argument("--config", type=int, default=4, choices=[0, 1, 2, 3, 4],
+                    help="headline workload (default 4: the 48-layer hybrid stack at 64K)")
+    ap.add_argument("--extra-configs", default="1,2,3",
+                    help="comma-separated workloads also measured (update, refill speedup, stage fractions)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--refill-steps", type=int, default=5)
     ap.add_argument("--no-refill", action="store_true")
@@ -54,6 +64,13 @@ def parse():
     ap.add_argument("--no-peaks", action="store_true", help="skip the copy and GEMM rate measurements")
     ap.add_argument("--no-t-sweep", action="store_true", help="skip the tail-length sweep at 32K rows")
     ap.add_argument("--no-paper-trace", action="store_true", help="skip the paper-shaped revision trace")
+    ap.add_argument("--only-update", action="store_true",
+                    help="time the headline update and its profiled pass only (for counter passes)")
+    ap.add_argument("--calibrate-copy", type=int, metavar="MIB", default=0,
+                    help="only copy a MIB-sized device buffer 5 times (calibrates HBM counters), then exit")
+    ap.add_argument("--summarize-profile", metavar="DIR", default=None,
+                    help="CPU only: turn the rocprofv3 outputs under DIR (trace/, calib_*/, pmc_*/) into "
+                         "profiles/update_stack_config<N>.md and profiles/traffic_config<N>.json, then exit")
     return ap.parse_args()
 
 
@@ -557,49 +574,184 @@ def measured_peaks(dev):
             "gemm_shape": [m, m, m], "gemm_launches": reps}
 
 
-def measured_traffic(kernel, workload):
+def measured_traffic(kernel, cfg_index, workload):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE and
-    WRITE_SIZE passes (profiles/traffic_config*.json), or None when there is no record
-    for this workload or the kernel's sources changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", "traffic_config1.json")
+    WRITE_SIZE passes of this workload (profiles/traffic_config<N>.json), or None when
+    there is no record for it or the kernel's sources changed since the counters were
+    taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_config{cfg_index}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
     if rec.get("kernel") != kernel or rec.get("workload") != workload:
         return None
-    h = hashlib.sha256()
-    for src in rec["sources"]:
-        with open(os.path.join(ROOT, src), "rb") as f:
-            h.update(f.read())
-    if h.hexdigest() != rec["sources_sha256"]:
+    if sources_sha256(rec["sources"]) != rec["sources_sha256"]:
         return None
     return {"bytes_per_launch": rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"],
             "read": rec["fetch_bytes_per_launch"], "written": rec["write_bytes_per_launch"],
             "source": rec["summary"]}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the update of one context does not "
-                                   "span devices here (--gpus 1)"}))
-        sys.exit(2)
+def sources_sha256(srcs):
+    h = hashlib.sha256()
+    for src in srcs:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+# sources each kernel's traffic record depends on
+KERNEL_SOURCES = {
+    "attention": ["paper_2609_18935_amd/csrc/attention.hip", "paper_2609_18935_amd/csrc/common.h"],
+}
+KERNEL_SYMBOL = {"attention": "k_attn<256>"}
+
+
+def calibrate_copy(mib):
+    """A plain device copy of `mib` MiB, five times: under rocprofv3 --pmc FETCH_SIZE (then
+    WRITE_SIZE) it shows what the counters report for exactly that many bytes read and
+    written, the factor that scales the library kernels' counters to bytes."""
+    import torch
+    n = mib << 20
+    a = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(f"copied {mib} MiB x 5", flush=True)
+
+
+PROFILE_COMMANDS = """rocprofv3 --kernel-trace --stats -f csv -d <out>/trace -o run -- python3 <repo>/bench.py --config {c} --steps 10 --warmup 2 --only-update
+rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/calib_FETCH_SIZE -o run -- python3 <repo>/bench.py --calibrate-copy 256
+rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/pmc_FETCH_SIZE -o run -- python3 <repo>/bench.py --config {c} --steps 2 --warmup 1 --only-update
+rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/calib_WRITE_SIZE -o run -- python3 <repo>/bench.py --calibrate-copy 256
+rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/pmc_WRITE_SIZE -o run -- python3 <repo>/bench.py --config {c} --steps 2 --warmup 1 --only-update
+python3 <repo>/bench.py --config {c} --summarize-profile <out>"""
+
+
+def describe(cfg):
+    """One line naming a workload's shapes and sizes."""
+    a, d = cfg.attn, cfg.delta
+    kinds = cfg.layer_kinds()
+    if cfg.L_old is not None:
+        pre = f"{cfg.L_old} cached rows"
+    elif cfg.L_keep is not None:
+        pre = f"{cfg.L_keep} surviving rows"
+    else:
+        pre = f"surviving rows uniform in [{cfg.L_keep_range[0]}, {cfg.L_keep_range[1]}]"
+    rec = (f"{cfg.n_records[0]}-{cfg.n_records[1]}" if cfg.n_records[0] != cfg.n_records[1] else f"{cfg.n_records[0]}")
+    rl = (f"{cfg.record_len[0]}-{cfg.record_len[1]}" if cfg.record_len[0] != cfg.record_len[1] else f"{cfg.record_len[0]}")
+    tl = f"{cfg.tail[0]}-{cfg.tail[1]}" if cfg.tail[0] != cfg.tail[1] else f"{cfg.tail[0]}"
+    return (f"{cfg.n_chars} context(s), {cfg.n_rounds} round(s); {pre}; {rec} record(s) of {rl} rows removed and "
+            f"{tl} tail tokens appended per round; {len(kinds)} layers ({kinds.count('attn')} attention "
+            f"{a.n_q_heads}q/{a.n_kv_heads}kv x {a.head_dim}, {kinds.count('delta')} gated delta-rule "
+            f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}).")
+
+
+def summarize_profile(out_dir, cfg_index):
+    """Writes profiles/update_stack_config<N>.md (kernel durations of the traced update,
+    calibrated HBM bytes per dispatch) and profiles/traffic_config<N>.json (the attention
+    kernel's bytes per launch, with the hash of its sources) from rocprofv3 CSV outputs."""
+    import csv
+    import re
+    import statistics
+    import synth
+    cfg = synth.CONFIGS[cfg_index]
+
+    def short(n):
+        n = n.replace("tu::(anonymous namespace)::", "").replace("void ", "")
+        return re.sub(r"\(.*\)$", "", n)
+
+    def rows(sub, name):
+        path = os.path.join(out_dir, sub, name)
+        with open(path) as f:
+            return list(csv.DictReader(f))
+
+    stats = [r for r in rows("trace", "run_kernel_stats.csv") if "tu::" in r["Name"]]
+
+    def pmc(kind):
+        per = {}
+        for r in rows(f"pmc_{kind}", "run_counter_collection.csv"):
+            if "tu::" in r["Kernel_Name"]:
+                per.setdefault(short(r["Kernel_Name"]), []).append(float(r["Counter_Value"]))
+        return {k: statistics.median(v) for k, v in per.items()}
+
+    def calib(kind):
+        vals = [float(r["Counter_Value"]) for r in rows(f"calib_{kind}", "run_counter_collection.csv")]
+        return max(vals)   # the copy dispatches (KiB)
+
+    true_kib = 256 * 1024
+    fr, wr = pmc("FETCH_SIZE"), pmc("WRITE_SIZE")
+    fc, wc = calib("FETCH_SIZE"), calib("WRITE_SIZE")
+    ff, wf = true_kib / fc, true_kib / wc
+    workload = f"config {cfg.index}: {cfg.name}"
+    out = [f"# Update, {workload}: kernel trace and HBM traffic\n",
+           f"Workload: {describe(cfg)}\n",
+           "Commands (repository root on the GPU host; rocprofv3 run from /tmp with TMPDIR=/tmp; each pass in "
+           "its own process; the last line runs here, on the CPU):\n", "```",
+           PROFILE_COMMANDS.format(c=cfg.index), "```\n",
+           "## Kernel durations (rocprofv3 --kernel-trace --stats, every dispatch of the traced command)\n",
+           "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
+        out.append(f"| {short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                   f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    out += ["\n## HBM traffic per dispatch (median over the dispatches, MiB)\n",
+            f"Calibration with a plain 256 MiB device copy: FETCH_SIZE reported {fc:,.1f} KiB for 262,144 KiB read "
+            f"(factor {ff:.3f}), WRITE_SIZE {wc:,.1f} KiB for 262,144 KiB written (factor {wf:.3f}). Values below "
+            "are scaled by those factors.\n", "| kernel | read MiB | written MiB |", "|---|---|---|"]
+    for k in sorted(fr, key=lambda k: -fr[k]):
+        out.append(f"| {k} | {fr[k] * ff / 1024:.2f} | {wr.get(k, 0) * wf / 1024:.2f} |")
+    blog = os.path.join(out_dir, "trace_bench.log")
+    if os.path.exists(blog):
+        lines = [l for l in open(blog) if l.startswith("{")]
+        if lines:
+            out += ["\n## Bench line of the traced run\n", "```json", lines[-1].strip(), "```"]
+    md = f"profiles/update_stack_config{cfg.index}.md"
+    with open(os.path.join(ROOT, md), "w") as f:
+        f.write("\n".join(out) + "\n")
+    sym = KERNEL_SYMBOL["attention"]
+    if sym in fr and sym in wr:
+        rec = {"workload": workload, "kernel": "attention", "kernel_symbol": sym,
+               "sources": KERNEL_SOURCES["attention"], "sources_sha256": sources_sha256(KERNEL_SOURCES["attention"]),
+               "fetch_bytes_per_launch": int(fr[sym] * ff * 1024), "write_bytes_per_launch": int(wr[sym] * wf * 1024),
+               "calibration": {"fetch_factor": round(ff, 4), "write_factor": round(wf, 4)}, "summary": md}
+        with open(os.path.join(ROOT, "profiles", f"traffic_config{cfg.index}.json"), "w") as f:
+            json.dump(rec, f, indent=1)
+    print("\n".join(out[:40]))
+
+
+# ----------------------------------------------------------------------------- one workload
+
+def workload_stage_fracs(cfg, rounds, kern):
+    """Algorithmic work per step of each stage against the summed durations of its kernels."""
+    kinds = cfg.layer_kinds()
+    work = {
+        "attention": (["rope_vt_pack", "attention", "attention_merge"], "mfma",
+                      attention_flops(cfg, rounds) * kinds.count("attn") / 1e12, "TFLOP/s", MFMA16_PEAK_TFLOPS),
+        "delta": (["delta_prep", "delta_chain"], "hbm", delta_bytes(cfg, rounds) * kinds.count("delta") / 1e9,
+                  "GB/s", HBM_PEAK_GBS),
+        "compaction": (["compact"], "hbm", gather_bytes(cfg, rounds) * kinds.count("attn") / 1e9, "GB/s",
+                       HBM_PEAK_GBS),
+    }
+    stages = {}
+    for name, (ks, bound, units, unit, peak) in work.items():
+        ms = sum(kern[k]["ms_per_step"] for k in ks if k in kern)
+        if ms > 0 and units > 0:
+            ach = units / (ms / 1e3)
+            stages[name] = {"kernels": ks, "ms_per_step": round(ms, 5), "bound": bound, "achieved": round(ach, 3),
+                            "peak": peak, "unit": unit, "frac": round(ach / peak, 4)}
+    return stages
+
+
+def measure_update(tu, cfg, seed, dev, attn_p, delta_p, W, K, refill_steps, keep=False):
+    """Times K updates of the workload (each on its own pristine copy, after W warm-ups),
+    then the same steps with per-kernel HIP events, then (refill_steps > 0) the full
+    refill of the live context after every round through the same kernels."""
     import numpy as np
     import torch
-    import synth
-    import paper_2609_18935_amd as tu
-
-    dev = "cuda:0"
-    torch.cuda.set_device(0)
-    tu.lib()
-    cfg = synth.CONFIGS[args.config]
+    sc, chars, rounds, layers, rng = build_workload(cfg, seed, dev)
     a, d = cfg.attn, cfg.delta
-    attn_p = tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta, a.softmax_scale,
-                            kv_splits=args.kv_splits)
-    delta_p = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
-    sc, chars, rounds, layers, rng = build_workload(cfg, args.seed, dev)
-    W, K = args.warmup, args.steps
     n_rounds = len(rounds)
     sumT = sum(sum(R["T"]) for R in rounds)
     print(f"[bench] config {cfg.index} ({cfg.name}): {len(chars)} context(s), {len(layers)} layers, "
@@ -615,12 +767,6 @@ def main():
         for c, ctx in enumerate(ctxs):
             ctx.set_metadata(chars[c]["intervals"], chars[c]["cursor"])
         return n
-
-    def run_step(ups, ws, per_round=None):
-        for i, u in enumerate(ups):
-            u.run(ws)
-            if per_round is not None:
-                per_round[i].record()
 
     # ---- update: one pristine copy per step; a step is every round of the workload
     copies = [make_copy(tu, chars, layers, dev) for _ in range(W + K)]
@@ -638,7 +784,8 @@ def main():
     torch.cuda.synchronize()
     h1 = time.perf_counter()
     upd_ms = ev0.elapsed_time(ev1) / K
-    print(f"[bench] update: {upd_ms:.4f} ms/step (host {1e3 * (h1 - h0) / K:.4f})", file=sys.stderr, flush=True)
+    print(f"[bench] config {cfg.index} update: {upd_ms:.4f} ms/step (host {1e3 * (h1 - h0) / K:.4f})",
+          file=sys.stderr, flush=True)
     del copies, ups
     round_ms = None
     if n_rounds > 1:
@@ -667,53 +814,14 @@ def main():
     tu.profile_enable(False)
     del copies2, ups2
     kern = {n: {"launches_per_step": c / K, "avg_ms": t / c, "ms_per_step": t / K} for n, (c, t) in prof.items()}
-    print(f"[bench] kernels: {json.dumps(kern)}", file=sys.stderr, flush=True)
-
-    kinds = cfg.layer_kinds()
-    # algorithmic work per step of each stage, and the kernels that carry it
-    work = {
-        "attention": (["rope_vt_pack", "attention", "attention_merge"], "mfma",
-                      attention_flops(cfg, rounds) * kinds.count("attn") / 1e12, "TFLOP/s", MFMA16_PEAK_TFLOPS),
-        "delta": (["delta_prep", "delta_chain"], "hbm", delta_bytes(cfg, rounds) * kinds.count("delta") / 1e9,
-                  "GB/s", HBM_PEAK_GBS),
-        "compaction": (["compact"], "hbm", gather_bytes(cfg, rounds) * kinds.count("attn") / 1e9, "GB/s",
-                       HBM_PEAK_GBS),
-    }
-    stages = {}
-    for name, (ks, bound, units, unit, peak) in work.items():
-        ms = sum(kern[k]["ms_per_step"] for k in ks if k in kern)
-        if ms > 0 and units > 0:
-            ach = units / (ms / 1e3)
-            stages[name] = {"kernels": ks, "ms_per_step": round(ms, 5), "bound": bound, "achieved": round(ach, 3),
-                            "peak": peak, "unit": unit, "frac": round(ach / peak, 4)}
-    # the attention kernel carries the workload's dominant work (it is MFMA-bound and on the
-    # caller's stream); side-stream durations include waits for CUs it holds, so they are not
-    # used to pick the dominant kernel
-    dom = "attention" if "attention" in kern else max(kern, key=lambda n: kern[n]["ms_per_step"])
-    work = {"attention": work["attention"][1:]}
-    if dom in work:
-        bound, units, unit, peak = work[dom]
-        launches = kern[dom]["launches_per_step"]
-        ach = units / (kern[dom]["ms_per_step"] / 1e3)
-        roofline = {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
-                    "frac": round(ach / peak, 4), "traffic": None, "kernel": dom,
-                    "per_launch": round(units / launches, 6), "avg_launch_ms": round(kern[dom]["avg_ms"], 5)}
-    else:
-        roofline = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
-                    "kernel": dom}
-    # HBM bytes per launch of the dominant kernel, from the committed counter passes
-    traffic = measured_traffic(dom, f"config {cfg.index}: {cfg.name}")
-    if traffic is not None:
-        roofline["traffic"] = traffic["bytes_per_launch"]
-        roofline["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
-        roofline["traffic_detail"] = traffic
+    print(f"[bench] config {cfg.index} kernels: {json.dumps(kern)}", file=sys.stderr, flush=True)
 
     # ---- full refill, through the same kernels, of the live context after every round
     # (zero recurrent state, contiguous positions from 0, fresh caches); the speedup is
     # the summed refill time over the summed update time
     refill = None
-    if not args.no_refill and args.refill_steps > 0:
-        R_ = args.refill_steps
+    if refill_steps > 0:
+        R_ = refill_steps
         refill_rounds = []
         for ri, R in enumerate(rounds):
             N = [Lk + T for Lk, T in zip(R["L_keep"], R["T"])]
@@ -764,8 +872,213 @@ def main():
             refill["rounds"] = [{"tail": sum(R["T"]), "live_after": x["tokens"], "update_ms": round(um, 5),
                                  "refill_ms": round(x["ms"], 5), "speedup": round(x["ms"] / um, 3)}
                                 for R, x, um in zip(rounds, refill_rounds, round_ms)]
-        print(f"[bench] refill: {refill_ms:.4f} ms ({refill['tokens']} tokens over {n_rounds} round(s)), "
-              f"speedup {refill_ms / upd_ms:.2f}x", file=sys.stderr, flush=True)
+        print(f"[bench] config {cfg.index} refill: {refill_ms:.4f} ms ({refill['tokens']} tokens over {n_rounds} "
+              f"round(s)), speedup {refill_ms / upd_ms:.2f}x", file=sys.stderr, flush=True)
+    res = {"cfg": cfg, "upd_ms": upd_ms, "round_ms": round_ms, "kern": kern, "refill": refill, "sumT": sumT,
+           "stages": workload_stage_fracs(cfg, rounds, kern), "chars": chars, "rounds": rounds}
+    if keep:
+        res.update({"layers": layers, "rng": rng, "ws": ws})
+    else:
+        del layers, ws
+        torch.cuda.empty_cache()
+    return res
+
+
+def config_row(m):
+    """Summary of one measured workload for extra_rows."""
+    cfg, rounds = m["cfg"], m["rounds"]
+    kinds = cfg.layer_kinds()
+    row = {"workload": f"config {cfg.index}: {cfg.name}", "contexts": len(m["chars"]), "layers": len(kinds),
+           "rounds": len(rounds), "tail_tokens": m["sumT"], "update_ms": round(m["upd_ms"], 5),
+           "tail_tok_s": round(m["sumT"] / (m["upd_ms"] / 1e3), 1), "stages": m["stages"],
+           "stack_roofline_frac": round(stack_ideal_ms(cfg, rounds, MFMA16_PEAK_TFLOPS, HBM_PEAK_GBS) / m["upd_ms"], 4),
+           "kernels": {n: {k: (round(v, 6) if isinstance(v, float) else v) for k, v in kv.items()}
+                       for n, kv in m["kern"].items()}}
+    if m["refill"]:
+        row.update({"refill_ms": round(m["refill"]["ms"], 5), "speedup_vs_refill": round(m["refill"]["speedup"], 3)})
+        if "rounds" in m["refill"]:
+            row["refill_rounds"] = m["refill"]["rounds"]
+    return row
+
+
+def run_step(ups, ws, per_round=None):
+    for i, u in enumerate(ups):
+        u.run(ws)
+        if per_round is not None:
+            per_round[i].record()
+
+
+def main():
+    args = parse()
+    if args.summarize_profile:
+        summarize_profile(args.summarize_profile, args.config)
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the update of one context does not "
+                                   "span devices here (--gpus 1)"}))
+        sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
+    import numpy as np
+    import torch
+    import synth
+    import paper_2609_18935_amd as tu
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    tu.lib()
+    cfg = synth.CONFIGS[args.config]
+    a, d = cfg.attn, cfg.delta
+    attn_p = tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta, a.softmax_scale,
+                            kv_splits=args.kv_splits)
+    delta_p = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
+    W, K = args.warmup, args.steps
+    refill_steps = 0 if (args.no_refill or args.only_update) else args.refill_steps
+    m = measure_update(tu, cfg, args.seed, dev, attn_p, delta_p, W, K, refill_steps, keep=not args.only_update)
+    upd_ms, round_ms, kern, refill, sumT = m["upd_ms"], m["round_ms"], m["kern"], m["refill"], m["sumT"]
+    chars, rounds = m["chars"], m["rounds"]
+    n_rounds = len(rounds)
+    stages = m["stages"]
+    kinds = cfg.layer_kinds()
+    # the attention kernel carries the workload's dominant work (it is MFMA-bound and on the
+    # caller's stream); side-stream durations include waits for CUs it holds, so they are not
+    # used to pick the dominant kernel
+    dom = "attention" if "attention" in kern else max(kern, key=lambda n: kern[n]["ms_per_step"])
+    if dom == "attention":
+        units = attention_flops(cfg, rounds) * kinds.count("attn") / 1e12
+        launches = kern[dom]["launches_per_step"]
+        ach = units / (kern[dom]["ms_per_step"] / 1e3)
+        roofline = {"bound": "mfma", "achieved": round(ach, 3), "peak": MFMA16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(ach / MFMA16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
+                    "per_launch": round(units / launches, 6), "per_launch_unit": "TFLOP",
+                    "avg_launch_ms": round(kern[dom]["avg_ms"], 5), "launches_per_step": launches}
+    else:
+        roofline = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
+                    "kernel": dom}
+    # HBM bytes per launch of the dominant kernel, from the committed counter passes
+    traffic = measured_traffic(dom, cfg.index, f"config {cfg.index}: {cfg.name}")
+    if traffic is not None:
+        roofline["traffic"] = traffic["bytes_per_launch"]
+        roofline["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
+        roofline["traffic_detail"] = traffic
+
+    extra = {}
+    if not args.only_update:
+        extra.update(headline_extras(tu, args, cfg, m, attn_p, delta_p, dev))
+    del m
+    torch.cuda.empty_cache()
+
+    # ---- the other workloads: update time, refill speedup (per round for the 8-round
+    # 32K workload, the >= 10x target at 32K contexts) and stage fractions
+    if not args.only_update and args.extra_configs:
+        rows = {}
+        for ci in [int(x) for x in args.extra_configs.split(",") if x.strip() != ""]:
+            if ci == cfg.index:
+                continue
+            c2 = synth.CONFIGS[ci]
+            a2, d2 = c2.attn, c2.delta
+            ap2 = tu.attn_params(a2.n_q_heads, a2.n_kv_heads, a2.head_dim, a2.rdim, a2.rope_theta, a2.softmax_scale,
+                                 kv_splits=args.kv_splits)
+            dp2 = tu.delta_params(d2.n_k_heads, d2.n_v_heads, d2.d_k, d2.d_v, d2.chunk, d2.scale)
+            m2 = measure_update(tu, c2, args.seed, dev, ap2, dp2, min(W, 3), min(K, 10),
+                                0 if args.no_refill else min(args.refill_steps, 3))
+            rows[str(ci)] = config_row(m2)
+            print(f"[bench] config {ci}: {json.dumps({k: v for k, v in rows[str(ci)].items() if k != 'kernels'})}",
+                  file=sys.stderr, flush=True)
+            del m2
+            torch.cuda.empty_cache()
+        extra["configs"] = rows
+
+    # ---- revisions shaped like the paper's measured trace, through the 48-layer stack
+    if not args.only_update and not args.no_paper_trace:
+        a1, d1 = synth.CONFIGS[1].attn, synth.CONFIGS[1].delta
+        ap1 = tu.attn_params(a1.n_q_heads, a1.n_kv_heads, a1.head_dim, a1.rdim, a1.rope_theta, a1.softmax_scale,
+                             kv_splits=args.kv_splits)
+        dp1 = tu.delta_params(d1.n_k_heads, d1.n_v_heads, d1.d_k, d1.d_v, d1.chunk, d1.scale)
+        extra["paper_trace"] = paper_trace_row(tu, synth, dev, ap1, dp1, args.seed, min(K, 5))
+        print(f"[bench] paper-shaped trace: {json.dumps(extra['paper_trace'])}", file=sys.stderr, flush=True)
+        # ---- tail-length sweep at 32K surviving rows, with the single-refresh workload's shapes
+        if not args.no_t_sweep:
+            extra["t_sweep"] = t_sweep_row(tu, synth, dev, ap1, dp1, args.seed, min(K, 10))
+
+    # ---- measured peaks of this part in this run: device copy bandwidth and a bf16 GEMM
+    peaks = None if (args.no_peaks or args.only_update) else measured_peaks(dev)
+    if peaks is not None:
+        meas = peaks["bf16_gemm_tflops"] if roofline.get("bound") == "mfma" else peaks["copy_gbs"]
+        if roofline.get("achieved") is not None and meas:
+            roofline["measured_peak"] = meas
+            roofline["frac_of_measured"] = round(roofline["achieved"] / meas, 4)
+        for row in extra.values():
+            if isinstance(row, dict) and "achieved" in row:
+                row["frac_of_measured_copy"] = round(row["achieved"] / peaks["copy_gbs"], 4)
+        print(f"[bench] measured peaks: {json.dumps(peaks)}", file=sys.stderr, flush=True)
+
+    # the whole step against its roofline: the summed ideal time of every step of the path
+    # (datasheet peaks; and the rates this part reached in this run, when measured)
+    ideal = stack_ideal_ms(cfg, rounds, MFMA16_PEAK_TFLOPS, HBM_PEAK_GBS)
+    stack_roofline = {"ideal_ms": round(ideal, 5), "measured_ms": round(upd_ms, 5), "frac": round(ideal / upd_ms, 4),
+                      "peaks": {"mfma_tflops": MFMA16_PEAK_TFLOPS, "hbm_gbs": HBM_PEAK_GBS}}
+    if peaks is not None:
+        ideal_m = stack_ideal_ms(cfg, rounds, peaks["bf16_gemm_tflops"], peaks["copy_gbs"])
+        stack_roofline.update({"ideal_ms_measured_peaks": round(ideal_m, 5),
+                               "frac_of_measured_peaks": round(ideal_m / upd_ms, 4)})
+    print(f"[bench] stack roofline: {json.dumps(stack_roofline)}", file=sys.stderr, flush=True)
+
+    cpu = None
+    if not args.no_cpu_baseline and not args.only_update:
+        print("[bench] cpu oracle leg ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(cfg, args.seed, args.cpu_budget_s)
+
+    line = {
+        "metric": METRIC,
+        "value": round(sumT / (upd_ms / 1e3), 1),
+        "unit": "tail tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(upd_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"config {cfg.index}: {cfg.name}", "contexts": len(chars), "layers": len(kinds),
+                   "attention_layers": kinds.count("attn"), "delta_layers": kinds.count("delta"),
+                   "rounds": n_rounds, "tail_tokens": sumT, "surviving_rows": rounds[0]["L_keep"][:4],
+                   "removed_rows": sum(o - k for R in rounds for o, k in zip(R["L_old"], R["L_keep"])),
+                   "attn": f"{a.n_q_heads}q/{a.n_kv_heads}kv x {a.head_dim}",
+                   "delta": f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}"},
+        "roofline": roofline,
+        "stack_roofline": stack_roofline,
+        "measured_peaks": peaks,
+        "speedup_vs_refill": round(refill["speedup"], 3) if refill else None,
+        "refill_ms": round(refill["ms"], 5) if refill else None,
+        "refill_rounds": refill.get("rounds") if refill else None,
+        "stages": stages,
+        "extra_rows": extra,
+        "kernels": {n: {k: (round(v, 6) if isinstance(v, float) else v) for k, v in kv.items()}
+                    for n, kv in kern.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def headline_extras(tu, args, cfg, m, attn_p, delta_p, dev):
+    """Rows measured on the headline workload's shapes: delimiter removal after prefill,
+    the slot-preserving and tail-and-relocate placements, the attention diagnostics and the
+    short-convolution continuation."""
+    import numpy as np
+    import torch
+    import synth
+    W, K = args.warmup, args.steps
+    a = cfg.attn
+    chars, rounds, layers = m["chars"], m["rounds"], m["layers"]
+    round_ms, upd_ms = m["round_ms"], m["upd_ms"]
+    kinds = cfg.layer_kinds()
+    sumT = m["sumT"]
+    extra = {}
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
     # ---- the same update with an 11-token opening and a 3-token closing maintenance
     # delimiter in every tail, removed from the caches once the tail is prefilled
@@ -898,76 +1211,7 @@ def main():
     if kinds.count("delta"):
         extra["short_conv"] = short_conv_row(tu, synth, cfg, sumT, dev, K)
         print(f"[bench] short conv: {json.dumps(extra['short_conv'])}", file=sys.stderr, flush=True)
-
-    # ---- revisions shaped like the paper's measured trace, through the 48-layer stack
-    if cfg.index == 1 and not args.no_paper_trace:
-        extra["paper_trace"] = paper_trace_row(tu, synth, dev, attn_p, delta_p, args.seed, min(K, 5))
-        print(f"[bench] paper-shaped trace: {json.dumps(extra['paper_trace'])}", file=sys.stderr, flush=True)
-
-    # ---- tail-length sweep at 32K surviving rows, with the single-refresh workload's shapes
-    if cfg.index == 1 and not args.no_t_sweep:
-        extra["t_sweep"] = t_sweep_row(tu, synth, dev, attn_p, delta_p, args.seed, min(K, 10))
-
-    # ---- measured peaks of this part in this run: device copy bandwidth and a bf16 GEMM
-    peaks = None if args.no_peaks else measured_peaks(dev)
-    if peaks is not None:
-        meas = peaks["bf16_gemm_tflops"] if roofline.get("bound") == "mfma" else peaks["copy_gbs"]
-        if roofline.get("achieved") is not None and meas:
-            roofline["measured_peak"] = meas
-            roofline["frac_of_measured"] = round(roofline["achieved"] / meas, 4)
-        for row in extra.values():
-            if "achieved" in row:
-                row["frac_of_measured_copy"] = round(row["achieved"] / peaks["copy_gbs"], 4)
-        print(f"[bench] measured peaks: {json.dumps(peaks)}", file=sys.stderr, flush=True)
-
-    # the whole step against its roofline: the summed ideal time of every step of the path
-    # (datasheet peaks; and the rates this part reached in this run, when measured)
-    ideal = stack_ideal_ms(cfg, rounds, MFMA16_PEAK_TFLOPS, HBM_PEAK_GBS)
-    stack_roofline = {"ideal_ms": round(ideal, 5), "measured_ms": round(upd_ms, 5), "frac": round(ideal / upd_ms, 4),
-                      "peaks": {"mfma_tflops": MFMA16_PEAK_TFLOPS, "hbm_gbs": HBM_PEAK_GBS}}
-    if peaks is not None:
-        ideal_m = stack_ideal_ms(cfg, rounds, peaks["bf16_gemm_tflops"], peaks["copy_gbs"])
-        stack_roofline.update({"ideal_ms_measured_peaks": round(ideal_m, 5),
-                               "frac_of_measured_peaks": round(ideal_m / upd_ms, 4)})
-    print(f"[bench] stack roofline: {json.dumps(stack_roofline)}", file=sys.stderr, flush=True)
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        print("[bench] cpu oracle leg ...", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(cfg, args.seed, args.cpu_budget_s)
-
-    line = {
-        "metric": METRIC,
-        "value": round(sumT / (upd_ms / 1e3), 1),
-        "unit": "tail tokens/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": W,
-        "ms_per_step": round(upd_ms, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": f"config {cfg.index}: {cfg.name}", "contexts": len(chars), "layers": len(layers),
-                   "attention_layers": kinds.count("attn"), "delta_layers": kinds.count("delta"),
-                   "rounds": n_rounds, "tail_tokens": sumT, "surviving_rows": rounds[0]["L_keep"][:4],
-                   "removed_rows": sum(o - k for R in rounds for o, k in zip(R["L_old"], R["L_keep"])),
-                   "attn": f"{a.n_q_heads}q/{a.n_kv_heads}kv x {a.head_dim}",
-                   "delta": f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}"},
-        "roofline": roofline,
-        "stack_roofline": stack_roofline,
-        "measured_peaks": peaks,
-        "extra_rows": extra,
-        "stages": stages,
-        "speedup_vs_refill":round(refill["speedup"], 3) if refill else None,
-        "refill_ms": round(refill["ms"], 5) if refill else None,
-        "refill_rounds": refill.get("rounds") if refill else None,
-        "kernels": {n: {k: (round(v, 6) if isinstance(v, float) else v) for k, v in kv.items()}
-                    for n, kv in kern.items()},
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(line), flush=True)
+    return extra
 
 
 if __name__ == "__main__":
