@@ -42,6 +42,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# every attention layer keeps a persistent V^T copy beside its caches (refreshed from the
+# first row that moved); --no-vt-copy packs every row into the workspace on every call
+VT_COPIES = True
 MFMA16_PEAK_TFLOPS = 2500.0
 METRIC = "tail-update tokens/s (hybrid layer stack) + speedup vs full refill; % roofline"
 
@@ -64,6 +67,8 @@ def parse():
     ap.add_argument("--no-peaks", action="store_true", help="skip the copy and GEMM rate measurements")
     ap.add_argument("--no-t-sweep", action="store_true", help="skip the tail-length sweep at 32K rows")
     ap.add_argument("--no-paper-trace", action="store_true", help="skip the paper-shaped revision trace")
+    ap.add_argument("--no-vt-copy", action="store_true",
+                    help="no persistent V^T copies: every update packs all value rows into the workspace")
     ap.add_argument("--only-update", action="store_true",
                     help="time the headline update and its profiled pass only (for counter passes)")
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB", default=0,
@@ -106,7 +111,26 @@ class DevRng:
         return self.torch.exp(-self.torch.nn.functional.softplus(self.normal(shape, mean=-4.0)))
 
 
-def build_workload(cfg, seed, device):
+def attach_vt_copies(tu, layers, chars, device):
+    """A V^T copy beside every attention layer's cache of every context, brought up to date
+    with the pristine rows (part of the pristine state each step copies)."""
+    import torch
+    if not VT_COPIES:
+        return
+    for L in layers:
+        if L["kind"] != "attn":
+            continue
+        L["vts"] = []
+        for (k, v), c in zip(L["caches"], chars):
+            vt = tu.new_vt_cache(c["cap"], v.shape[1], v.shape[2], device)
+            ctx = tu.Context(c["cap"], device=device)
+            ctx.set_metadata(c["intervals"], c["cursor"])
+            tu.refresh_vt_cache(ctx, [v], [vt])
+            L["vts"].append(vt)
+    torch.cuda.synchronize()
+
+
+def build_workload(cfg, seed, device, tu=None):
     """Per-context plans plus pristine device buffers and packed tail inputs of every round.
 
     chars[c]: the context's initial state (L_old, intervals, cursor) and capacity;
@@ -153,6 +177,8 @@ def build_workload(cfg, seed, device):
         else:
             layers.append({"kind": "delta",
                            "states": [rng.normal((d.n_v_heads, d.d_v, d.d_k), std=0.1) for _ in chars]})
+    if tu is not None:
+        attach_vt_copies(tu, layers, chars, device)
     return sc, chars, rounds, layers, rng
 
 
@@ -163,12 +189,15 @@ def make_copy(tu, chars, layers, device, pristine=True):
     for c in chars:
         ctx = tu.Context(c["cap"], device=device)
         ctx.pos[: c["L_old"]] = torch.arange(c["L_old"], dtype=torch.int32, device=device)
-        ctx.set_metadata(c["intervals"], c["cursor"])
+        ctx.set_metadata(c["intervals"], c["cursor"], vt_rows=c["L_old"] if VT_COPIES else 0)
         ctxs.append(ctx)
     own = []
     for L in layers:
         if L["kind"] == "attn":
-            own.append({"caches": [(k.clone(), v.clone()) for (k, v) in L["caches"]]})
+            o = {"caches": [(k.clone(), v.clone()) for (k, v) in L["caches"]]}
+            if "vts" in L:
+                o["vts"] = [vt.clone() for vt in L["vts"]]
+            own.append(o)
         else:
             own.append({"states": [s.clone() for s in L["states"]]})
     return ctxs, own
@@ -180,7 +209,8 @@ def stack_update(tu, ctxs, own, layers, inputs, ranges, tails, attn_p, delta_p, 
     for L, O, src in zip(layers, own, inputs):
         if L["kind"] == "attn":
             ios.append(tu.LayerIO(tu.TU_LAYER_ATTN, src["q"], src["k"], src["v"], src["out"],
-                                  k_cache=[k for (k, _) in O["caches"]], v_cache=[v for (_, v) in O["caches"]]))
+                                  k_cache=[k for (k, _) in O["caches"]], v_cache=[v for (_, v) in O["caches"]],
+                                  vt_cache=O.get("vts")))
         else:
             ios.append(tu.LayerIO(tu.TU_LAYER_DELTA, src["q"], src["k"], src["v"], src["out"], state=O["states"],
                                   beta=src["beta"], g=src["g"]))
@@ -362,7 +392,7 @@ def t_sweep_row(tu, synth, dev, attn_p, delta_p, seed, reps, warmup=2):
     rows = []
     for T in synth.T_SWEEP:
         cfg = synth.t_sweep_config(T)
-        _, chars, rounds, layers, _ = build_workload(cfg, seed, dev)
+        _, chars, rounds, layers, _ = build_workload(cfg, seed, dev, tu)
         copies = [make_copy(tu, chars, layers, dev) for _ in range(warmup + 2 * reps)]
         ups = [round_updates(tu, c, o, layers, rounds, attn_p, delta_p) for (c, o) in copies]
         ws = torch.empty(max(u[0].workspace_size() for u in ups), dtype=torch.uint8, device=dev)
@@ -444,13 +474,21 @@ def paper_trace_row(tu, synth, dev, attn_p, delta_p, seed, reps, warmup=1):
                                   "g": rng.gate((T, d.n_v_heads)),
                                   "out": torch.empty((T, d.n_v_heads, d.d_v), dtype=torch.float32, device=dev)})
     pos0 = torch.from_numpy(tr.positions.astype(np.int32)).to(dev)
+    attach_vt_copies(tu, layers, [{"cap": cap, "intervals": tr.intervals, "cursor": tr.cursor}], dev)
 
     def fresh():
         ctx = tu.Context(cap, device=dev)
         ctx.pos[:L0] = pos0
-        ctx.set_metadata(tr.intervals, tr.cursor)
-        own = [{"caches": [(k.clone(), v.clone()) for (k, v) in L["caches"]]} if L["kind"] == "attn" else
-               {"states": [x.clone() for x in L["states"]]} for L in layers]
+        ctx.set_metadata(tr.intervals, tr.cursor, vt_rows=L0 if VT_COPIES else 0)
+        own = []
+        for L in layers:
+            if L["kind"] == "attn":
+                o = {"caches": [(k.clone(), v.clone()) for (k, v) in L["caches"]]}
+                if "vts" in L:
+                    o["vts"] = [vt.clone() for vt in L["vts"]]
+                own.append(o)
+            else:
+                own.append({"states": [x.clone() for x in L["states"]]})
         return ctx, [stack_update(tu, [ctx], own, layers, inputs[r], [rv.ranges], [rv.T], attn_p, delta_p,
                                   post=[rv.post], placement=["slot"], place_runs=[rv.runs])
                      for r, rv in enumerate(tr.revisions)]
@@ -465,7 +503,7 @@ def paper_trace_row(tu, synth, dev, attn_p, delta_p, seed, reps, warmup=1):
             for u, rv in zip(ups, tr.revisions):
                 ctx.set_metadata(rv.intervals, rv.cursor)
                 need = max(need, u.workspace_size())
-            ctx.set_metadata(tr.intervals, tr.cursor)
+            ctx.set_metadata(tr.intervals, tr.cursor, vt_rows=L0 if VT_COPIES else 0)
             ws = torch.empty(need, dtype=torch.uint8, device=dev)
         torch.cuda.synchronize()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(ups) + 1)]
@@ -501,7 +539,8 @@ def paper_trace_row(tu, synth, dev, attn_p, delta_p, seed, reps, warmup=1):
     for rep in range(warmup + reps):
         ctx = tu.Context(N, device=dev)
         ctx.set_metadata([], 0)
-        own = [{"caches": C} if L["kind"] == "attn" else
+        own = [{"caches": C, "vts": [tu.new_vt_cache(N, a.n_kv_heads, a.head_dim, dev)] if VT_COPIES else None}
+               if L["kind"] == "attn" else
                {"states": [torch.zeros((d.n_v_heads, d.d_v, d.d_k), dtype=torch.float32, device=dev)]}
                for L, C in zip(layers, caches)]
         u = stack_update(tu, [ctx], own, layers, rin, [np.zeros((0, 2), np.int64)], [N], attn_p, delta_p)
@@ -750,7 +789,7 @@ def measure_update(tu, cfg, seed, dev, attn_p, delta_p, W, K, refill_steps, keep
     refill of the live context after every round through the same kernels."""
     import numpy as np
     import torch
-    sc, chars, rounds, layers, rng = build_workload(cfg, seed, dev)
+    sc, chars, rounds, layers, rng = build_workload(cfg, seed, dev, tu)
     a, d = cfg.attn, cfg.delta
     n_rounds = len(rounds)
     sumT = sum(sum(R["T"]) for R in rounds)
@@ -760,12 +799,13 @@ def measure_update(tu, cfg, seed, dev, attn_p, delta_p, W, K, refill_steps, keep
     def workspace_for(ctxs, ups):
         """Largest workspace any round of a step needs (each round sized on its own metadata)."""
         n = 0
+        vt0 = [ctx.vt_rows for ctx in ctxs]
         for R, u in zip(rounds, ups):
             for c, ctx in enumerate(ctxs):
                 ctx.set_metadata(R["intervals"][c], R["cursor"][c])
             n = max(n, u.workspace_size())
         for c, ctx in enumerate(ctxs):
-            ctx.set_metadata(chars[c]["intervals"], chars[c]["cursor"])
+            ctx.set_metadata(chars[c]["intervals"], chars[c]["cursor"], vt_rows=vt0[c])
         return n
 
     # ---- update: one pristine copy per step; a step is every round of the workload
@@ -844,6 +884,9 @@ def measure_update(tu, cfg, seed, dev, attn_p, delta_p, W, K, refill_steps, keep
             caches = [[(torch.empty((n, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev),
                         torch.empty((n, a.n_kv_heads, a.head_dim), dtype=torch.bfloat16, device=dev)) for n in N]
                       if L["kind"] == "attn" else None for L in layers]
+            # fresh V^T copies too (the refill packs every row into them)
+            vts = [[tu.new_vt_cache(n, a.n_kv_heads, a.head_dim, dev) for n in N]
+                   if L["kind"] == "attn" and VT_COPIES else None for L in layers]
             rups = []
             for i in range(R_ + 1):
                 ctxs = []
@@ -851,9 +894,9 @@ def measure_update(tu, cfg, seed, dev, attn_p, delta_p, W, K, refill_steps, keep
                     ctx = tu.Context(n, device=dev)
                     ctx.set_metadata([], 0)
                     ctxs.append(ctx)
-                own_i = [{"caches": C} if L["kind"] == "attn" else
+                own_i = [{"caches": C, "vts": V} if L["kind"] == "attn" else
                          {"states": [torch.zeros((d.n_v_heads, d.d_v, d.d_k), dtype=torch.float32, device=dev)
-                                     for _ in N]} for L, C in zip(layers, caches)]
+                                     for _ in N]} for L, C, V in zip(layers, caches, vts)]
                 rups.append(stack_update(tu, ctxs, own_i, layers, rin, [np.zeros((0, 2), np.int64)] * len(N), N,
                                          attn_p, delta_p))
             rws = torch.empty(max(u.workspace_size() for u in rups), dtype=torch.uint8, device=dev)
@@ -920,6 +963,8 @@ def main():
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
         return
+    global VT_COPIES
+    VT_COPIES = not args.no_vt_copy
     import numpy as np
     import torch
     import synth
@@ -1049,6 +1094,7 @@ def main():
                    "removed_rows": sum(o - k for R in rounds for o, k in zip(R["L_old"], R["L_keep"])),
                    "attn": f"{a.n_q_heads}q/{a.n_kv_heads}kv x {a.head_dim}",
                    "delta": f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}"},
+        "layout": {"vt_copies": VT_COPIES},
         "roofline": roofline,
         "stack_roofline": stack_roofline,
         "measured_peaks": peaks,

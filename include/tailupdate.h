@@ -27,6 +27,16 @@
  *    return leaves all device buffers and all host metadata unchanged.
  *  - Status codes: TU_OK (0) or a negative TU_ERR_*; tu_last_error() returns a
  *    thread-local message for the last failure of the calling thread.
+ *  - Checks that only the device can make (see tu_workspace_faults) report into the
+ *    first word of the call's workspace.
+ *  - Input range. Some products take operands rounded to f16 (10 stored mantissa
+ *    bits, largest finite value 65504), because bf16 operands there would exceed the
+ *    accuracy bound: attention values (v), and in the delta rule the state S, the
+ *    pseudo-values U = T (beta v) - W S^T, the decay-scaled q, k and beta v, and the
+ *    WY factors. Inputs whose magnitudes reach 2^16 in these places have no f16
+ *    counterpart: the results are then not meaningful and the call sets
+ *    TU_FAULT_RANGE in its status word. The delta rule expects L2-normalised keys
+ *    (||k_t|| <= 1), beta in [0, 1] and g in [0, 1] (g = 0 is computed as 2^-100).
  */
 #ifndef TAILUPDATE_H
 #define TAILUPDATE_H
@@ -38,7 +48,7 @@
 extern "C" {
 #endif
 
-#define TU_ABI_VERSION 4
+#define TU_ABI_VERSION 5
 
 #define TU_OK 0
 #define TU_ERR_ARG (-1)       /* null pointer, unsupported or inconsistent shape */
@@ -78,6 +88,10 @@ typedef struct tu_seq {
   int32_t n_live;     /* intervals in use */
   int32_t live_cap;   /* intervals allocated */
   int32_t* d_pos;     /* device int32 [capacity]: position id of each cache row */
+  /* Rows [0, vt_rows) of every attention layer's V^T copy (see tu_vt_cache_bytes) hold
+   * the current values of those cache rows. 0 for a new context; the library lowers it
+   * when rows move and raises it to len once every layer's copy is refreshed. */
+  int64_t vt_rows;
 } tu_seq;
 
 /*
@@ -118,26 +132,34 @@ int tu_abi_version(void);
 const char* tu_last_error(void);
 
 /*
- * Device-side checks of the compaction (Section 4.2 keeps the live spans on the
- * host; the device holds the position labels). While scanning, the kernels check
+ * Device-side checks of a call. Section 4.2 keeps the live spans on the host while
+ * the device holds the position labels: while scanning, the compaction kernels check
  * that every row the deletion ranges keep (by its d_pos label) lies outside the
  * removed row spans the host derived from its live runs, and every removed row
- * inside one; and every bounded wait of the in-place move must end in time. A
- * failed check does not stop the update (the move follows the host's spans and
- * stays in bounds): it sets a sticky bit in a word held per device:
+ * inside one; every bounded wait of the in-place move must end in time; and operands
+ * rounded to f16 must be finite (see the input range above). A failed check does not
+ * stop the call (moves follow the host's spans and stay in bounds): it sets a bit in
+ * the status the call keeps in the first 256 bytes of its workspace (compact_kv,
+ * tail_prefill_attention, delta_rule_continue, refresh_vt_cache and
+ * update_layer_stack). Each call is numbered, the bits carry its number and its
+ * kernels record it, so the status never needs clearing and never shows bits of an
+ * earlier call (a call with nothing to enqueue, T = 0, leaves it as it was):
  *   TU_FAULT_POSITIONS  d_pos disagrees with the host metadata (`live`, `len`), so
  *                       the update did not remove exactly the rows whose labels lie
  *                       in the ranges;
- *   TU_FAULT_WAIT       a wait of the in-place move expired; moved rows may be wrong.
- * tu_device_faults enqueues a read of the current device's word on `stream` (and,
- * if clear != 0, a reset after it), synchronises `stream`, and stores the word in
- * *faults (host pointer). The word is shared by every stream and context of the
- * process on that device; a reset can drop bits set meanwhile by work on other
- * streams. Returns TU_OK, TU_ERR_ARG (faults NULL) or TU_ERR_HIP.
+ *   TU_FAULT_WAIT       a wait of the in-place move expired; moved rows may be wrong;
+ *   TU_FAULT_RANGE      a value rounded to f16 overflowed; the results are not
+ *                       meaningful.
+ * tu_workspace_faults enqueues a read of that status on `stream` (the stream the
+ * call ran on), synchronises `stream` and stores the last call's bits in *faults
+ * (host pointer). Each call owns its workspace while it runs, so calls on other
+ * streams with other workspaces never touch it. Returns TU_OK, TU_ERR_ARG (a null
+ * pointer) or TU_ERR_HIP.
  */
 #define TU_FAULT_POSITIONS 1
 #define TU_FAULT_WAIT 2
-int tu_device_faults(int32_t* faults, int32_t clear, void* stream);
+#define TU_FAULT_RANGE 4
+int tu_workspace_faults(const void* workspace, int32_t* faults, void* stream);
 
 /*
  * Range verification (Section 4.2; host only, no device access).
@@ -157,7 +179,8 @@ int tu_validate_ranges(const tu_seq* seq, const int64_t* ranges, int32_t n_range
  *  k_layers, v_layers: host arrays [n_layers] of device bf16 [capacity][n_kv_heads][head_dim].
  *  src_index: optional device int32 [>= seq->len]; on success entry j (< new len)
  *             holds the old row index of the j-th surviving row. May be NULL.
- * On success seq->len and seq->live are updated; seq->next_pos is unchanged.
+ * On success seq->len and seq->live are updated (seq->vt_rows drops to the first
+ * removed row); seq->next_pos is unchanged.
  * The device kernels compute the keep mask from d_pos, turn it into offsets by
  * wavefront prefix sums, and move only the rows behind the first hole, in place.
  */
@@ -165,6 +188,29 @@ size_t compact_kv_workspace_size(int64_t len, int32_t n_layers, int32_t n_kv_hea
 int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_t n_layers,
                int32_t n_kv_heads, int32_t head_dim, const int64_t* ranges, int32_t n_ranges,
                int32_t* src_index, void* workspace, size_t workspace_bytes, void* stream);
+
+
+/*
+ * Persistent V^T copy of one attention layer's value cache (optional, caller-owned):
+ * the values in the f16 transposed tile layout the attention kernel reads (64 keys
+ * per tile; the layout is private to the library). With a copy, a call refreshes only
+ * the tiles from row seq->vt_rows on (the rows a removal moved, and the tail), instead
+ * of packing every row of the cache into the workspace on every call. Bytes of a copy
+ * for `capacity` rows (0 for invalid shapes); 16-byte aligned device memory.
+ */
+size_t tu_vt_cache_bytes(int64_t capacity, int32_t n_kv_heads, int32_t head_dim);
+
+/*
+ * Brings the V^T copies of up to 32 attention layers of one context up to date: rows
+ * [seq->vt_rows, seq->len) of each value cache are packed (with the rest of their
+ * 64-row tiles), then seq->vt_rows = seq->len. For a copy attached to a context that
+ * already holds rows (vt_rows 0 packs every row). v_layers, vt_layers: host arrays
+ * [n_layers] of device pointers (bf16 [capacity][n_kv_heads][head_dim] caches, copies
+ * of tu_vt_cache_bytes(seq->capacity, ...)). The workspace holds only the status word
+ * (256 bytes; TU_FAULT_RANGE for values without an f16 counterpart).
+ */
+int refresh_vt_cache(tu_seq* seq, void* const* v_layers, void* const* vt_layers, int32_t n_layers, int32_t n_kv_heads,
+                     int32_t head_dim, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * True-tail attention of one layer, Eq. 3 (Section 4.1): rotary embedding of the
@@ -177,16 +223,21 @@ int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_
  *     (k before rotation).
  *  out: device fp32 [T][n_q_heads][head_dim].
  *  q_hat: optional device bf16 [T][n_q_heads][head_dim] receiving the rotated queries.
+ *  vt_cache: optional V^T copy of this layer (tu_vt_cache_bytes(seq->capacity, ...));
+ *     tiles from row seq->vt_rows on are refreshed. NULL: every tile is packed into the
+ *     workspace.
  * Does not change `seq` (several layers share one context): call commit_tail once
  * after the last layer, or use update_layer_stack.
  */
 size_t tail_prefill_attention_workspace_size(const tu_attn_params* p, int64_t T, int64_t len);
-int tail_prefill_attention(const tu_seq* seq, void* k_cache, void* v_cache, const tu_attn_params* p,
+int tail_prefill_attention(const tu_seq* seq, void* k_cache, void* v_cache, void* vt_cache, const tu_attn_params* p,
                            const void* q, const void* k, const void* v, int64_t T, float* out,
                            void* q_hat, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Advance a context by T appended tokens: len += T, live gains [next_pos, next_pos+T),
- * next_pos += T (Section 4.2: the cursor grows by every appended token). Host only. */
+ * next_pos += T (Section 4.2: the cursor grows by every appended token); vt_rows
+ * becomes len (every layer's V^T copy, if any, was refreshed by
+ * tail_prefill_attention). Host only. */
 int commit_tail(tu_seq* seq, int64_t T);
 
 /*
@@ -289,8 +340,9 @@ typedef struct tu_seq_update {
 /*
  * One layer of the stack. Tail inputs of all contexts are packed in context
  * order: context s owns rows [sum of earlier T, + T_s).
- *  attention: k_cache[s], v_cache[s] device bf16 caches; q, k, v, out as in
- *             tail_prefill_attention; beta, g, state unused.
+ *  attention: k_cache[s], v_cache[s] device bf16 caches, vt_cache[s] an optional
+ *             V^T copy; q, k, v, out as in tail_prefill_attention; beta, g, state
+ *             unused.
  *  delta:     state[s] device fp32 [Hv][d_v][d_k]; q, k, v, beta, g, out as in
  *             delta_rule_continue; k_cache, v_cache unused.
  */
@@ -298,6 +350,7 @@ typedef struct tu_layer_io {
   int32_t kind;                /* TU_LAYER_ATTN or TU_LAYER_DELTA */
   void* const* k_cache;        /* host array [n_seq] of device pointers */
   void* const* v_cache;
+  void* const* vt_cache;       /* attention: NULL, or host array [n_seq] of V^T copies (entries may be NULL) */
   float* const* state;         /* host array [n_seq] of device pointers */
   const void* q;
   const void* k;
@@ -328,11 +381,15 @@ typedef struct tu_update {
  * says: the positions of post-removed rows become holes, and the recurrent state
  * keeps their influence). A full refill is the same call on empty contexts (len 0)
  * with zero states.
+ * Every context's vt_rows ends at its new len (V^T copies refreshed), or at the first
+ * row the post-prefill removal moved.
  * Delta layers read nothing the attention path writes, so they run concurrently
- * with it on a side stream of the current device (one per calling thread, created on
- * first use, default priority), forked after the work already queued on `stream`
- * and joined back into `stream` before the call returns: all results are ordered on
- * `stream`.
+ * with it on a side stream of the current device, forked after the work already
+ * queued on `stream` and joined back into `stream` before the call returns (also
+ * when a launch fails): all results are ordered on `stream`. The side stream and the
+ * two events of the fork and join are the library's only state besides the
+ * thread-local error message: created on the first such call of a thread on a
+ * device (default priority, non-blocking) and kept for the thread's life.
  * tu_validate_update performs only the host checks (no device access).
  */
 size_t update_layer_stack_workspace_size(const tu_update* u);
@@ -359,7 +416,7 @@ int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu
                   const int64_t* moves, int32_t n_moves, void* stream);
 
 /*
- * Attention diagnostics (Section 5.3, Appendix D). The probe queries are the last
+ * Attention diagnostics (Section 5.3, Appendix C). The probe queries are the last
  * n_probe rows of a context; probe query i sees rows 0 .. len - n_probe + i (the
  * causal rule of the update). Their raw queries are rotated at the rows' positions
  * (float64 angles, bf16 nearest even, as the cached keys were); scores
@@ -381,9 +438,8 @@ int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu
  * position lies in group g; window_mass[g] (optional) the same over the group's first
  * `window` positions (the paper uses 8); summary (optional, device fp32 [3]) = {memory
  * mass M = sum_g mass[g], effective group count exp(-sum_g a_g log a_g) with
- * a_g = mass[g] / M, boundary-window share sum_g window_mass[g] / M}. Accumulated in
- * float64 with atomic adds (the summation order, hence the last float64 bits, may
- * vary between runs), reported as fp32.
+ * a_g = mass[g] / M, boundary-window share sum_g window_mass[g] / M}. Summed in
+ * float64 in a fixed order (the same bits on every run), reported as fp32.
  *
  * attention_tv_distance: tv[0] = 0.5 * sum_j |p[j] - q[map(j)]| over j < n, where
  * map = q_row_of_p (device int32 [n], the row of the same token in the other
@@ -392,7 +448,7 @@ int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu
 size_t attention_probe_workspace_size(const tu_attn_params* p, int64_t len, int32_t n_probe);
 int attention_probe(const tu_seq* seq, const void* k_cache, const tu_attn_params* p, const void* q, int32_t n_probe,
                     float weight, float* probs, void* workspace, size_t workspace_bytes, void* stream);
-size_t attention_group_mass_workspace_size(int32_t n_groups);
+size_t attention_group_mass_workspace_size(int64_t len, int32_t n_groups);
 int attention_group_mass(const tu_seq* seq, const float* probs, const int64_t* groups, int32_t n_groups,
                          int32_t window, float* mass, float* window_mass, float* summary, void* workspace,
                          size_t workspace_bytes, void* stream);

@@ -1,6 +1,6 @@
 """Attention diagnostics of the paper's measurement protocol (test infrastructure only).
 
-Paper Section 5.3 and Appendix D: attention probabilities at a full-attention
+Paper Section 5.3 and Appendix C: attention probabilities at a full-attention
 layer are reconstructed with a float32 reference softmax from the queries and
 keys the model actually holds; the diagnostics average the last eight query
 tokens of a probe, then aggregate over heads (and layers); holes in the position

@@ -23,16 +23,20 @@ from .binding import (  # noqa: F401
     compact_kv,
     delta_params,
     delta_rule_continue,
-    device_faults,
+    new_vt_cache,
+    vt_cache_bytes,
+    workspace_faults,
     lib,
     profile_collect,
     profile_enable,
+    refresh_vt_cache,
     relocate_keys,
     short_conv_continue,
     short_conv_continue_batch,
     tail_prefill_attention,
     update_layer_stack,
     TU_FAULT_POSITIONS,
+    TU_FAULT_RANGE,
     TU_FAULT_WAIT,
     TU_LAYER_ATTN,
     TU_LAYER_DELTA,

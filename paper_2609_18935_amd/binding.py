@@ -44,7 +44,7 @@ class tu_interval(ctypes.Structure):
 class tu_seq(ctypes.Structure):
     _fields_ = [("len", _i64), ("capacity", _i64), ("next_pos", _i64),
                 ("live", ctypes.POINTER(tu_interval)), ("n_live", _i32), ("live_cap", _i32),
-                ("d_pos", _vp)]
+                ("d_pos", _vp), ("vt_rows", _i64)]
 
 
 class tu_attn_params(ctypes.Structure):
@@ -65,7 +65,7 @@ class tu_seq_update(ctypes.Structure):
 
 class tu_layer_io(ctypes.Structure):
     _fields_ = [("kind", _i32), ("k_cache", ctypes.POINTER(_vp)), ("v_cache", ctypes.POINTER(_vp)),
-                ("state", ctypes.POINTER(_vp)), ("q", _vp), ("k", _vp), ("v", _vp), ("beta", _vp), ("g", _vp),
+                ("vt_cache", ctypes.POINTER(_vp)), ("state", ctypes.POINTER(_vp)), ("q", _vp), ("k", _vp), ("v", _vp), ("beta", _vp), ("g", _vp),
                 ("out", _vp)]
 
 
@@ -88,8 +88,11 @@ _SIGNATURES = {
     "compact_kv": (_i32, [ctypes.POINTER(tu_seq), ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _i32, _i32,
                           ctypes.POINTER(_i64), _i32, _vp, _vp, ctypes.c_size_t, _vp]),
     "tail_prefill_attention_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_attn_params), _i64, _i64]),
-    "tail_prefill_attention": (_i32, [ctypes.POINTER(tu_seq), _vp, _vp, ctypes.POINTER(tu_attn_params), _vp, _vp,
-                                      _vp, _i64, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "tu_vt_cache_bytes": (ctypes.c_size_t, [_i64, _i32, _i32]),
+    "refresh_vt_cache": (_i32, [ctypes.POINTER(tu_seq), ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _i32, _i32,
+                                _vp, ctypes.c_size_t, _vp]),
+    "tail_prefill_attention": (_i32, [ctypes.POINTER(tu_seq), _vp, _vp, _vp, ctypes.POINTER(tu_attn_params), _vp,
+                                      _vp, _vp, _i64, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "commit_tail": (_i32, [ctypes.POINTER(tu_seq), _i64]),
     "delta_rule_continue_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_delta_params), _i64]),
     "delta_rule_continue": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i64, ctypes.POINTER(tu_delta_params), _vp, _vp,
@@ -104,19 +107,19 @@ _SIGNATURES = {
     "attention_probe_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_attn_params), _i64, _i32]),
     "attention_probe": (_i32, [ctypes.POINTER(tu_seq), _vp, ctypes.POINTER(tu_attn_params), _vp, _i32, _f32, _vp,
                                _vp, ctypes.c_size_t, _vp]),
-    "attention_group_mass_workspace_size": (ctypes.c_size_t, [_i32]),
+    "attention_group_mass_workspace_size": (ctypes.c_size_t, [_i64, _i32]),
     "attention_group_mass": (_i32, [ctypes.POINTER(tu_seq), _vp, ctypes.POINTER(_i64), _i32, _i32, _vp, _vp, _vp,
                                     _vp, ctypes.c_size_t, _vp]),
     "attention_tv_workspace_size": (ctypes.c_size_t, [_i64]),
     "attention_tv_distance": (_i32, [_vp, _vp, _vp, _i64, _vp, _vp, ctypes.c_size_t, _vp]),
-    "tu_device_faults": (_i32, [ctypes.POINTER(_i32), _i32, _vp]),
+    "tu_workspace_faults": (_i32, [_vp, ctypes.POINTER(_i32), _vp]),
     "tu_profile_enable": (_i32, [_i32]),
     "tu_profile_collect": (_i32, [ctypes.c_char_p, _i32, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double),
                                   _i32]),
 }
 
 _lib_handle = None
-ABI_VERSION = 4   # TU_ABI_VERSION of include/tailupdate.h that these structures follow
+ABI_VERSION = 5   # TU_ABI_VERSION of include/tailupdate.h that these structures follow
 
 
 def lib():
@@ -163,10 +166,28 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]) -> torch.Tensor:
+def _torch_stream(stream, device):
+    """The torch stream object a call runs on (None: the current stream)."""
+    if stream is None:
+        return None
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    return torch.cuda.ExternalStream(handle, device=device)
+
+
+def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor], stream=None) -> torch.Tensor:
+    """The caller's workspace, or a new one. A new one is freed when the call returns,
+    while its kernels may still run on `stream`: when that is not the current stream,
+    the allocation is recorded on it, so that the caching allocator does not hand the
+    memory to another tensor before those kernels are done."""
     if workspace is not None:
         return workspace
-    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    ts = _torch_stream(stream, device)
+    if ts is not None and ts != torch.cuda.current_stream(device):
+        ws.record_stream(ts)
+    return ws
 
 
 def _ranges_array(ranges, width: int = 2) -> tuple:
@@ -201,7 +222,7 @@ class Context:
     def __init__(self, capacity: int, device="cuda", live_cap: int = 4096):
         self.pos = torch.zeros(max(1, capacity), dtype=torch.int32, device=device)
         self._live = (tu_interval * live_cap)()
-        self.c = tu_seq(0, int(capacity), 0, self._live, 0, int(live_cap), self.pos.data_ptr())
+        self.c = tu_seq(0, int(capacity), 0, self._live, 0, int(live_cap), self.pos.data_ptr(), 0)
 
     @property
     def len(self) -> int:
@@ -215,11 +236,16 @@ class Context:
     def next_pos(self) -> int:
         return int(self.c.next_pos)
 
+    @property
+    def vt_rows(self) -> int:
+        return int(self.c.vt_rows)
+
     def intervals(self) -> List[tuple]:
         return [(int(self._live[i].begin), int(self._live[i].end)) for i in range(self.c.n_live)]
 
-    def set_metadata(self, intervals: Sequence[tuple], next_pos: int):
-        """Declare the live positions of a cache the caller filled (pos must match)."""
+    def set_metadata(self, intervals: Sequence[tuple], next_pos: int, vt_rows: int = 0):
+        """Declare the live positions of a cache the caller filled (pos must match);
+        vt_rows: rows of the layers' V^T copies that hold those rows (0: none)."""
         if len(intervals) > self.c.live_cap:
             raise ValueError("too many intervals")
         n = 0
@@ -229,14 +255,17 @@ class Context:
         self.c.n_live = len(intervals)
         self.c.len = n
         self.c.next_pos = int(next_pos)
+        self.c.vt_rows = int(vt_rows)
 
     def snapshot(self):
-        return (self.intervals(), self.next_pos, self.pos.clone())
+        """The context's metadata and positions (Section 4.1 state apart from the caches
+        and recurrent states, which the caller owns and copies itself)."""
+        return (self.intervals(), self.next_pos, self.pos.clone(), self.vt_rows)
 
     def restore(self, snap):
-        iv, nxt, pos = snap
+        iv, nxt, pos, vt_rows = snap
         self.pos.copy_(pos)
-        self.set_metadata(iv, nxt)
+        self.set_metadata(iv, nxt, vt_rows)
 
     def validate_ranges(self, ranges) -> int:
         arr, n = _ranges_array(ranges)
@@ -255,21 +284,46 @@ def compact_kv(ctx: Context, k_layers: Sequence[torch.Tensor], v_layers: Sequenc
     vs = (_vp * max(1, n))(*[_ptr(t) for t in v_layers])
     arr, nr = _ranges_array(ranges)
     nbytes = lib().compact_kv_workspace_size(ctx.len, n, Hkv, D)
-    ws = _workspace(nbytes, ctx.pos.device, workspace)
+    ws = _workspace(nbytes, ctx.pos.device, workspace, stream)
     _check(lib().compact_kv(ctypes.byref(ctx.c), ks, vs, n, Hkv, D, arr, nr, _ptr(src_index), _ptr(ws),
                             ws.numel(), _stream(stream)))
+    return ws
+
+
+def vt_cache_bytes(capacity: int, n_kv_heads: int, head_dim: int) -> int:
+    return int(lib().tu_vt_cache_bytes(int(capacity), int(n_kv_heads), int(head_dim)))
+
+
+def new_vt_cache(capacity: int, n_kv_heads: int, head_dim: int, device="cuda") -> torch.Tensor:
+    """A V^T copy for one attention layer of a context of `capacity` rows (its contents
+    start stale: the context's vt_rows says how many rows are current)."""
+    return torch.empty(vt_cache_bytes(capacity, n_kv_heads, head_dim), dtype=torch.uint8, device=device)
+
+
+def refresh_vt_cache(ctx: Context, v_layers: Sequence[torch.Tensor], vt_layers: Sequence[torch.Tensor],
+                     workspace: Optional[torch.Tensor] = None, stream=None):
+    """Pack rows [ctx.vt_rows, ctx.len) of each value cache into its V^T copy; then
+    ctx.vt_rows == ctx.len. Returns the (status) workspace."""
+    n = len(v_layers)
+    Hkv, D = int(v_layers[0].shape[1]), int(v_layers[0].shape[2])
+    vs = (_vp * max(1, n))(*[_ptr(t) for t in v_layers])
+    ts = (_vp * max(1, n))(*[_ptr(t) for t in vt_layers])
+    ws = _workspace(256, ctx.pos.device, workspace, stream)
+    _check(lib().refresh_vt_cache(ctypes.byref(ctx.c), vs, ts, n, Hkv, D, _ptr(ws), ws.numel(), _stream(stream)))
+    return ws
 
 
 def tail_prefill_attention(ctx: Context, k_cache: torch.Tensor, v_cache: torch.Tensor, params: tu_attn_params,
                            q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: torch.Tensor,
                            q_hat: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
-                           stream=None):
+                           stream=None, vt_cache: Optional[torch.Tensor] = None):
     T = int(q.shape[0])
     nbytes = lib().tail_prefill_attention_workspace_size(ctypes.byref(params), T, ctx.len)
-    ws = _workspace(nbytes, q.device, workspace)
-    _check(lib().tail_prefill_attention(ctypes.byref(ctx.c), _ptr(k_cache), _ptr(v_cache), ctypes.byref(params),
-                                        _ptr(q), _ptr(k), _ptr(v), T, _ptr(out), _ptr(q_hat), _ptr(ws), ws.numel(),
-                                        _stream(stream)))
+    ws = _workspace(nbytes, q.device, workspace, stream)
+    _check(lib().tail_prefill_attention(ctypes.byref(ctx.c), _ptr(k_cache), _ptr(v_cache), _ptr(vt_cache),
+                                        ctypes.byref(params), _ptr(q), _ptr(k), _ptr(v), T, _ptr(out), _ptr(q_hat),
+                                        _ptr(ws), ws.numel(), _stream(stream)))
+    return ws
 
 
 def commit_tail(ctx: Context, T: int):
@@ -280,9 +334,10 @@ def delta_rule_continue(state: torch.Tensor, q, k, v, beta, g, params: tu_delta_
                         workspace: Optional[torch.Tensor] = None, stream=None):
     T = int(q.shape[0])
     nbytes = lib().delta_rule_continue_workspace_size(ctypes.byref(params), T)
-    ws = _workspace(nbytes, state.device, workspace)
+    ws = _workspace(nbytes, state.device, workspace, stream)
     _check(lib().delta_rule_continue(_ptr(state), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(g), T,
                                      ctypes.byref(params), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+    return ws
 
 
 def relocate_keys(ctx: Context, k_layers: Sequence[torch.Tensor], params: Optional[tu_attn_params], moves,
@@ -303,7 +358,7 @@ def attention_probe(ctx: Context, k_cache: torch.Tensor, params: tu_attn_params,
     those queries and all heads."""
     n = int(q.shape[0])
     nbytes = lib().attention_probe_workspace_size(ctypes.byref(params), ctx.len, n)
-    ws = _workspace(nbytes, q.device, workspace)
+    ws = _workspace(nbytes, q.device, workspace, stream)
     _check(lib().attention_probe(ctypes.byref(ctx.c), _ptr(k_cache), ctypes.byref(params), _ptr(q), n, float(weight),
                                  _ptr(probs), _ptr(ws), ws.numel(), _stream(stream)))
 
@@ -316,7 +371,7 @@ def attention_group_mass(ctx: Context, probs: torch.Tensor, groups, window: int 
     mass = torch.empty(max(1, m), dtype=torch.float32, device=probs.device)
     win = torch.empty_like(mass)
     summary = torch.empty(3, dtype=torch.float32, device=probs.device)
-    ws = _workspace(lib().attention_group_mass_workspace_size(m), probs.device, workspace)
+    ws = _workspace(lib().attention_group_mass_workspace_size(ctx.len, m), probs.device, workspace, stream)
     _check(lib().attention_group_mass(ctypes.byref(ctx.c), _ptr(probs), arr, m, int(window), _ptr(mass), _ptr(win),
                                       _ptr(summary), _ptr(ws), ws.numel(), _stream(stream)))
     return mass[:m], win[:m], summary
@@ -327,7 +382,7 @@ def attention_tv_distance(p: torch.Tensor, q: torch.Tensor, q_row_of_p: Optional
     """0.5 * sum |p - q[map]| as a device fp32 tensor [1]."""
     n = int(p.numel())
     tv = torch.empty(1, dtype=torch.float32, device=p.device)
-    ws = _workspace(lib().attention_tv_workspace_size(n), p.device, workspace)
+    ws = _workspace(lib().attention_tv_workspace_size(n), p.device, workspace, stream)
     _check(lib().attention_tv_distance(_ptr(p), _ptr(q), _ptr(q_row_of_p), n, _ptr(tv), _ptr(ws), ws.numel(),
                                        _stream(stream)))
     return tv
@@ -364,10 +419,12 @@ def short_conv_continue_batch(items, activation: str = "silu", stream=None):
 class LayerIO:
     """Inputs and outputs of one layer of a stack update (tail rows packed over contexts)."""
 
-    def __init__(self, kind: int, q, k, v, out, k_cache=None, v_cache=None, state=None, beta=None, g=None):
+    def __init__(self, kind: int, q, k, v, out, k_cache=None, v_cache=None, state=None, beta=None, g=None,
+                 vt_cache=None):
         self.kind = kind
         self.q, self.k, self.v, self.out = q, k, v, out
         self.k_cache, self.v_cache, self.state = k_cache, v_cache, state
+        self.vt_cache = vt_cache   # per context: a V^T copy (new_vt_cache) or None
         self.beta, self.g = beta, g
 
 
@@ -407,7 +464,8 @@ class StackUpdate:
                 a = (_vp * max(1, n))(*[_ptr(t) for t in ts])
                 self._keep.append(a)
                 return a
-            self._layer_arr[l] = tu_layer_io(L.kind, plist(L.k_cache), plist(L.v_cache), plist(L.state), _ptr(L.q),
+            self._layer_arr[l] = tu_layer_io(L.kind, plist(L.k_cache), plist(L.v_cache),
+                                             plist(getattr(L, "vt_cache", None)), plist(L.state), _ptr(L.q),
                                              _ptr(L.k), _ptr(L.v), _ptr(L.beta), _ptr(L.g), _ptr(L.out))
         self.u = tu_update(n, self._seq_arr, len(layers), self._layer_arr,
                            attn if attn is not None else tu_attn_params(),
@@ -428,13 +486,14 @@ class StackUpdate:
 
 TU_FAULT_POSITIONS = 1   # device positions disagreed with the host's live runs
 TU_FAULT_WAIT = 2        # a bounded wait of the in-place move expired
+TU_FAULT_RANGE = 4       # a value rounded to f16 overflowed
 
 
-def device_faults(clear: bool = True, stream=None) -> int:
-    """The current device's sticky fault bits (TU_FAULT_*) set by compaction kernels
-    since the last reset; synchronises `stream` first and resets the word if `clear`."""
+def workspace_faults(workspace: torch.Tensor, stream=None) -> int:
+    """The device-check bits (TU_FAULT_*) of the last call that ran with `workspace`
+    (on `stream`); synchronises `stream`."""
     out = ctypes.c_int32(0)
-    _check(lib().tu_device_faults(ctypes.byref(out), int(bool(clear)), _stream(stream)))
+    _check(lib().tu_workspace_faults(_ptr(workspace), ctypes.byref(out), _stream(stream)))
     return int(out.value)
 
 
@@ -465,6 +524,7 @@ def update_layer_stack(contexts, ranges, tails, layers, attn=None, delta=None, w
     up = StackUpdate(contexts, ranges, tails, layers, attn, delta, src_index, post_ranges, placement, place_runs)
     nbytes = up.workspace_size()
     dev = contexts[0].pos.device if contexts else "cuda"
-    ws = _workspace(nbytes, dev, workspace)
+    ws = _workspace(nbytes, dev, workspace, stream)
     up.run(ws, stream)
+    up.workspace = ws
     return up

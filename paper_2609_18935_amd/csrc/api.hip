@@ -5,9 +5,11 @@
 // host metadata untouched (Section 4.2 of the paper: deletion ranges are verified
 // against the live spans before anything is removed).
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -51,6 +53,26 @@ struct Arena {
   }
 };
 
+// The first kStatusBytes of every workspace hold the call's status: the tagged 64-bit
+// word and, 64 bytes further, the number of the call that last ran there (CallStatus in
+// common.h); the rest is carved by the planners.
+constexpr size_t kStatusBytes = 256;
+constexpr size_t kStatusLastOffset = 64;
+std::atomic<uint32_t> g_calls{0};
+
+// The status of a new call on workspace ws: numbers 1 .. 2^32 - 2, one per call of the process.
+CallStatus call_status(void* ws) {
+  uint32_t n;
+  do n = g_calls.fetch_add(1, std::memory_order_relaxed) + 1;
+  while (n == 0 || n == 0xFFFFFFFFu);
+  CallStatus st{};
+  st.word = static_cast<unsigned long long*>(ws);
+  st.last = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + kStatusLastOffset);
+  st.call = n;
+  return st;
+}
+inline void* after_status(void* ws) { return ws ? static_cast<char*>(ws) + kStatusBytes : nullptr; }
+
 // ------------------------------------------------------------------ metadata checks
 
 int check_seq(const tu_seq* s) {
@@ -61,6 +83,7 @@ int check_seq(const tu_seq* s) {
   if (s->n_live > 0 && !s->live) return fail(TU_ERR_ARG, "null live-interval array");
   if (s->capacity > 0 && !s->d_pos) return fail(TU_ERR_ARG, "null d_pos");
   if (s->next_pos < 0 || s->next_pos > INT32_MAX) return fail(TU_ERR_ARG, "cursor outside the int32 position range");
+  if (s->vt_rows < 0) return fail(TU_ERR_ARG, "negative vt_rows");
   int64_t total = 0, max_end = -1;
   for (int i = 0; i < s->n_live; ++i) {
     const tu_interval& iv = s->live[i];
@@ -259,10 +282,12 @@ struct ProfRec {
 };
 thread_local bool g_prof = false;
 thread_local std::vector<ProfRec> g_recs;
+thread_local uint64_t g_launches = 0;   // kernels this thread has enqueued through timed()
 
 // Runs `launch` (which enqueues one kernel on `st`), bracketed by events when profiling.
 template <class F>
 hipError_t timed(const char* name, hipStream_t st, F&& launch) {
+  ++g_launches;
   if (!g_prof) return launch();
   ProfRec r{name, nullptr, nullptr};
   if (hipEventCreate(&r.start) != hipSuccess) return launch();
@@ -297,7 +322,8 @@ struct CompactPlan {
 
 // Builds the compaction launches for a set of contexts. With ws == nullptr only the
 // workspace size is computed.
-int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, CompactPlan* plan) {
+int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, const CallStatus& status,
+                    CompactPlan* plan) {
   Arena ar(ws);
   const int R = kGatherStripeBytes / row_bytes;
   const int64_t align_rows = std::max(1, 128 / row_bytes);
@@ -414,6 +440,7 @@ int plan_compaction(std::vector<CompactItem>& items, int row_bytes, void* ws, Co
     int32_t* words = static_cast<int32_t*>(ar.take(sizeof(int32_t) * (size_t)a.n_counter_words));
     a.claim = words;
     a.flags = words ? words + kFlagStride : nullptr;
+    a.status = status;
     plan->launches.push_back(a);
   }
   plan->ws_bytes = ar.used;
@@ -445,16 +472,21 @@ struct AttnItem {
   bf16_t* q_hat;            // caller's or null (workspace)
   const int64_t* place_runs = nullptr;   // slot placement: host [n][2] position runs of the tail
   int n_place_runs = 0;
+  void* vt_cache = nullptr;  // persistent V^T copy of the layer, or null (packed into the workspace)
+  int64_t vt_rows = 0;       // rows of the copy that are current (before this call's append)
 };
 
 struct AttnLaunch {
   RopeArgs rope;
   int rope_tokens;
+  PackArgs pack;
   AttnArgs attn;
   AttnOrder order;
   MergeArgs merge;
   int merge_rows;
 };
+
+inline int64_t vt_head_tiles(int64_t rows) { return (rows + kAttnKeys - 1) / kAttnKeys; }
 
 // Key-range splits of one context's attention. An attention workgroup holds a whole CU,
 // so a launch runs in waves of kCus workgroups. When every item of the launch has the
@@ -518,7 +550,7 @@ void plan_dies(const AttnArgs& a, int G, AttnOrder* o) {
         gs.push_back({cost, s.item_begin + (h * s.n_splits + sp) * s.n_tiles, s.n_tiles});
     }
   }
-  if ((int)gs.size() > kMaxAttnGroups) return;
+  if ((int)gs.size() > kMaxAttnGroups || a.total_items > 65535) return;
   std::stable_sort(gs.begin(), gs.end(), [](const Grp& x, const Grp& y) { return x.cost > y.cost; });
   int64_t load[kXcds] = {};
   std::vector<int> die(gs.size());
@@ -535,19 +567,24 @@ void plan_dies(const AttnArgs& a, int G, AttnOrder* o) {
     int slots = 0;
     for (size_t g = 0; g < gs.size(); ++g)
       if (die[g] == x) {
-        o->grp_item0[n] = gs[g].item0;
+        o->grp_item0[n] = (uint16_t)gs[g].item0;
         slots += gs[g].count;
-        o->grp_end[n++] = slots;
+        o->grp_end[n++] = (uint16_t)std::min(slots, 65535);
       }
     most = std::max(most, slots);
+  }
+  if (most > 65535) {   // slot counts are 16-bit: keep the equal-share order
+    o->n_groups = 0;
+    o->blocks = 0;
+    return;
   }
   o->die_begin[kXcds] = n;
   o->n_groups = n;
   o->blocks = most * kXcds;
 }
 
-int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* ws, std::vector<AttnLaunch>* out,
-                   size_t* ws_bytes) {
+int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* ws, const CallStatus& status,
+                   std::vector<AttnLaunch>* out, size_t* ws_bytes) {
   const int Hq = p->n_q_heads, Hkv = p->n_kv_heads, D = p->head_dim, G = Hq / Hkv;
   size_t max_used = 0;
   out->clear();
@@ -586,8 +623,20 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
       if (!qh) qh = static_cast<bf16_t*>(qh_ws);
       const int tiles = (int)((it.T * G + kAttnRows - 1) / kAttnRows);
       const int splits = choose_splits(p, it.L_keep, it.T, base_items, uniform);
-      const int vt_tiles = (int)((it.L_keep + it.T + kAttnKeys - 1) / kAttnKeys);
-      _Float16* vt = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)Hkv * vt_tiles * D * kVtRow));
+      // V^T tiles: refreshed in the layer's own copy from the first row it lacks, or all
+      // packed into the workspace
+      const int vt_end = (int)vt_head_tiles(it.L_keep + it.T);
+      _Float16* vt;
+      int vt_begin, head_tiles;
+      if (it.vt_cache) {
+        vt = static_cast<_Float16*>(it.vt_cache);
+        head_tiles = (int)vt_head_tiles(it.seq->capacity);
+        vt_begin = (int)(std::min(it.vt_rows, it.L_keep) / kAttnKeys);
+      } else {
+        vt = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)Hkv * vt_end * D * kVtRow));
+        head_tiles = vt_end;
+        vt_begin = 0;
+      }
       _Float16* po = nullptr;
       float* pml = nullptr;
       if (splits > 1) {
@@ -615,11 +664,16 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
         ++n_runs;
       }
       tok += (int)it.T;
+      PackSeq& pk = L.pack.seq[L.pack.n_seq++];
+      pk.vt = vt;
+      pk.tile_begin = vt_begin;
+      pk.tile_end = vt_end;
+      pk.head_tiles = head_tiles;
+      pk.pack_begin = pack_total;
+      pack_total += Hkv * (vt_end - vt_begin);
       AttnSeq& s = L.attn.seq[L.attn.n_seq++];
       s.q_hat = qh;
       s.k_cache = static_cast<const bf16_t*>(it.k_cache);
-      s.v_cache = static_cast<const bf16_t*>(it.v_cache);
-      s.v_new = it.v;
       s.vt = vt;
       s.out = it.out;
       s.part_o = po;
@@ -629,10 +683,8 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
       s.n_tiles = tiles;
       s.n_splits = splits;
       s.item_begin = item_total;
-      s.n_vt_tiles = vt_tiles;
-      s.pack_begin = pack_total;
+      s.head_tiles = head_tiles;
       item_total += Hkv * splits * tiles;
-      pack_total += Hkv * vt_tiles;
       if (splits > 1) {
         L.merge.row_begin[L.merge.n_seq] = mrows;
         L.merge.seq[L.merge.n_seq++] = s;
@@ -643,7 +695,8 @@ int plan_attention(const tu_attn_params* p, std::vector<AttnItem>& items, void* 
     L.rope_tokens = tok;
     L.attn.total_items = item_total;
     plan_dies(L.attn, G, &L.order);
-    L.attn.pack_items = pack_total;
+    L.pack.pack_items = pack_total;
+    L.pack.status = status;
     L.merge_rows = mrows;
     {   // lanes per row piece: one per batch of 8 splits of the launch's largest split count
       int most = 1;
@@ -683,7 +736,7 @@ int side_stream(SideStream** out) {
 
 int run_attention(const std::vector<AttnLaunch>& ls, int D, hipStream_t st) {
   for (const auto& L : ls) {
-    if (int e = hip_check(timed("rope_vt_pack", st, [&] { return launch_stage(L.rope, L.rope_tokens, L.attn, D, st); }), "RoPE/V^T pack launch")) return e;
+    if (int e = hip_check(timed("rope_vt_pack", st, [&] { return launch_stage(L.rope, L.rope_tokens, L.pack, D, st); }), "RoPE/V^T pack launch")) return e;
     if (int e = hip_check(timed("attention", st, [&] { return launch_attention(L.attn, L.order, D, st); }), "attention launch")) return e;
     if (L.merge_rows > 0)
       if (int e = hip_check(timed("attention_merge", st, [&] { return launch_attention_merge(L.merge, L.merge_rows, D, st); }), "merge launch")) return e;
@@ -704,8 +757,8 @@ struct DeltaItem {
   int64_t T;
 };
 
-int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, void* ws, std::vector<DeltaArgs>* out,
-               size_t* ws_bytes) {
+int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, void* ws, const CallStatus& status,
+               std::vector<DeltaArgs>* out, size_t* ws_bytes) {
   const int C = p->chunk, Hv = p->n_v_heads, DK = p->d_k;
   size_t max_used = 0;
   out->clear();
@@ -721,6 +774,7 @@ int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, vo
     a.n_v_heads = Hv;
     a.scale = p->scale;
     a.n_slices = DK / dvs;
+    a.status = status;
     int chunks = 0;
     for (size_t i = g0; i < g1; ++i) {
       const auto& it = items[i];
@@ -1013,6 +1067,9 @@ std::vector<AttnItem> stack_attn_items(const tu_update* u, const StackPlan& sp, 
     it.v = static_cast<const bf16_t*>(L.v) + r0 * krow;
     it.out = L.out + r0 * qrow;
     it.q_hat = nullptr;
+    it.vt_cache = L.vt_cache ? L.vt_cache[s] : nullptr;
+    // rows of the copy still current: up to the first row this update's removal moves
+    it.vt_rows = std::min(su.seq->vt_rows, sp.rc[s].removed > 0 ? sp.rc[s].first_row : su.seq->len);
     if (su.placement == TU_PLACE_SLOT) {
       it.place_runs = su.place_runs;
       it.n_place_runs = su.n_place_runs;
@@ -1088,11 +1145,21 @@ int tu_abi_version(void) { return TU_ABI_VERSION; }
 
 const char* tu_last_error(void) { return g_err.c_str(); }
 
-static_assert(TU_FAULT_POSITIONS == tu::kFaultPositions && TU_FAULT_WAIT == tu::kFaultWait, "fault bits");
+static_assert(TU_FAULT_POSITIONS == tu::kFaultPositions && TU_FAULT_WAIT == tu::kFaultWait &&
+                  TU_FAULT_RANGE == tu::kFaultRange, "fault bits");
 
-int tu_device_faults(int32_t* faults, int32_t clear, void* stream) {
-  if (!faults) return fail(TU_ERR_ARG, "faults is null");
-  return hip_check(read_device_faults(faults, clear != 0, (hipStream_t)stream), "reading the device fault word");
+int tu_workspace_faults(const void* workspace, int32_t* faults, void* stream) {
+  if (!faults || !workspace) return fail(TU_ERR_ARG, "null workspace or faults");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint64_t block[(kStatusLastOffset + 8) / 8] = {};
+  if (int e = hip_check(hipMemcpyAsync(block, workspace, sizeof(block), hipMemcpyDeviceToHost, st),
+                        "reading the status words"))
+    return e;
+  if (int e = hip_check(hipStreamSynchronize(st), "stream synchronise")) return e;
+  const uint64_t word = block[0];
+  const uint32_t last = (uint32_t)block[kStatusLastOffset / 8];
+  *faults = (uint32_t)(word >> 32) == last ? (int32_t)(uint32_t)word : 0;
+  return ok();
 }
 
 int tu_validate_ranges(const tu_seq* seq, const int64_t* ranges, int32_t n_ranges, int64_t* n_removed) {
@@ -1119,13 +1186,20 @@ size_t compact_kv_workspace_size(int64_t len, int32_t n_layers, int32_t n_kv_hea
   items[0].bufs.assign(2 * (size_t)n_layers, nullptr);
   fake.len = len + 1;
   CompactPlan plan;
-  plan_compaction(items, row_bytes, nullptr, &plan);
-  return plan.ws_bytes;
+  plan_compaction(items, row_bytes, nullptr, CallStatus{}, &plan);
+  return kStatusBytes + plan.ws_bytes;
 }
 
-int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_t n_layers, int32_t n_kv_heads,
-               int32_t head_dim, const int64_t* ranges, int32_t n_ranges, int32_t* src_index, void* workspace,
-               size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace tu {
+namespace {
+
+// compact_kv with the workspace [base, base + bytes): status block first, unless
+// `status` names a block of its own (then the whole range is the compaction's).
+int compact_with(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_t n_layers, int32_t n_kv_heads,
+                 int32_t head_dim, const int64_t* ranges, int32_t n_ranges, int32_t* src_index, void* base,
+                 size_t bytes, void* status, const char* space, hipStream_t st) {
   if (int e = check_seq(seq)) return e;
   if (n_layers < 0 || (n_layers > 0 && (!k_layers || !v_layers))) return fail(TU_ERR_ARG, "bad layer arrays");
   if (n_kv_heads <= 0 || head_dim <= 0 || ((long)n_kv_heads * head_dim * 2) % 16)
@@ -1150,17 +1224,36 @@ int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_
     items[0].bufs.push_back(v_layers[l]);
   }
   CompactPlan plan;
-  plan_compaction(items, row_bytes, nullptr, &plan);
-  if (!workspace || workspace_bytes < plan.ws_bytes)
-    return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.ws_bytes);
-  if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  plan_compaction(items, row_bytes, nullptr, CallStatus{}, &plan);
+  const size_t need = (status ? 0 : kStatusBytes) + plan.ws_bytes;
+  if (bytes < need) return fail(TU_ERR_WORKSPACE, "%s of %zu bytes, %zu needed", space, bytes, need);
+  if (!base) return fail(TU_ERR_WORKSPACE, "null %s", space);
+  if (!aligned16(base) || (status && !aligned16(status)))
+    return fail(TU_ERR_WORKSPACE, "%s and status must be 16-byte aligned", space);
   items[0].src_index = src_index;
-  if (int e = plan_compaction(items, row_bytes, workspace, &plan)) return e;
-  if (int e = run_compaction(plan, static_cast<hipStream_t>(stream))) return e;
+  const CallStatus cs = call_status(status ? status : base);
+  if (int e = plan_compaction(items, row_bytes, status ? base : after_status(base), cs, &plan)) return e;
+  const uint64_t launches = g_launches;
+  if (int e = run_compaction(plan, st)) return e;
+  if (g_launches == launches)   // nothing to move or scan: record the call all the same
+    if (int e = hip_check(launch_status_mark(cs, st), "status mark")) return e;
   const int64_t removed = items[0].rc.removed;
   commit_intervals(seq, items[0].rc.live_after);
   seq->len -= removed;
+  if (removed > 0) seq->vt_rows = std::min(seq->vt_rows, items[0].rc.first_row);
   return ok();
+}
+
+}  // namespace
+}  // namespace tu
+
+extern "C" {
+
+int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_t n_layers, int32_t n_kv_heads,
+               int32_t head_dim, const int64_t* ranges, int32_t n_ranges, int32_t* src_index, void* workspace,
+               size_t workspace_bytes, void* stream) {
+  return compact_with(seq, k_layers, v_layers, n_layers, n_kv_heads, head_dim, ranges, n_ranges, src_index, workspace,
+                      workspace_bytes, nullptr, "workspace", static_cast<hipStream_t>(stream));
 }
 
 size_t tail_prefill_attention_workspace_size(const tu_attn_params* p, int64_t T, int64_t len) {
@@ -1170,13 +1263,66 @@ size_t tail_prefill_attention_workspace_size(const tu_attn_params* p, int64_t T,
   items[0] = AttnItem{&fake, len, T, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   std::vector<AttnLaunch> ls;
   size_t bytes = 0;
-  plan_attention(p, items, nullptr, &ls, &bytes);
-  return std::max<size_t>(bytes, kAlign);
+  plan_attention(p, items, nullptr, CallStatus{}, &ls, &bytes);
+  return kStatusBytes + bytes;
 }
 
-int tail_prefill_attention(const tu_seq* seq, void* k_cache, void* v_cache, const tu_attn_params* p, const void* q,
-                           const void* k, const void* v, int64_t T, float* out, void* q_hat, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+size_t tu_vt_cache_bytes(int64_t capacity, int32_t n_kv_heads, int32_t head_dim) {
+  if (capacity < 0 || n_kv_heads <= 0 || (head_dim != 64 && head_dim != 128 && head_dim != 256)) return 0;
+  return sizeof(_Float16) * (size_t)n_kv_heads * (size_t)vt_head_tiles(capacity) * head_dim * kVtRow;
+}
+
+int refresh_vt_cache(tu_seq* seq, void* const* v_layers, void* const* vt_layers, int32_t n_layers, int32_t n_kv_heads,
+                     int32_t head_dim, void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_seq(seq)) return e;
+  if (n_layers < 0 || n_layers > kMaxSeqPerLaunch || (n_layers > 0 && (!v_layers || !vt_layers)))
+    return fail(TU_ERR_ARG, "0 .. %d layers with value caches and V^T copies", kMaxSeqPerLaunch);
+  if (tu_vt_cache_bytes(seq->capacity, n_kv_heads, head_dim) == 0 && seq->capacity > 0)
+    return fail(TU_ERR_ARG, "unsupported head shape");
+  for (int l = 0; l < n_layers; ++l)
+    if (!v_layers[l] || !vt_layers[l] || !aligned16(v_layers[l]) || !aligned16(vt_layers[l]))
+      return fail(TU_ERR_ARG, "layer %d: null or misaligned buffer", l);
+  if (!workspace || workspace_bytes < kStatusBytes)
+    return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, kStatusBytes);
+  if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const CallStatus cs = call_status(workspace);
+  const int begin = (int)(std::min(seq->vt_rows, seq->len) / kAttnKeys);
+  const int end = (int)vt_head_tiles(seq->len);
+  if (n_layers > 0 && end > begin) {
+    // the stage kernel with packing workgroups only: one entry per layer, all with no tail
+    RopeArgs r{};
+    PackArgs pk{};
+    r.n_kv_heads = n_kv_heads;
+    r.head_dim = head_dim;
+    for (int l = 0; l < n_layers; ++l) {
+      RopeSeq& rs = r.seq[r.n_seq++];
+      rs.v_cache = static_cast<bf16_t*>(v_layers[l]);
+      rs.v = rs.v_cache;
+      rs.L_keep = (int32_t)seq->len;
+      rs.T = 0;
+      PackSeq& ps = pk.seq[pk.n_seq++];
+      ps.vt = static_cast<_Float16*>(vt_layers[l]);
+      ps.tile_begin = begin;
+      ps.tile_end = end;
+      ps.head_tiles = (int)vt_head_tiles(seq->capacity);
+      ps.pack_begin = pk.pack_items;
+      pk.pack_items += n_kv_heads * (end - begin);
+    }
+    pk.status = cs;
+    if (int e = hip_check(timed("rope_vt_pack", st, [&] { return launch_stage(r, 0, pk, head_dim, st); }),
+                          "V^T pack launch"))
+      return e;
+  } else if (int e = hip_check(launch_status_mark(cs, st), "status mark")) {
+    return e;
+  }
+  seq->vt_rows = seq->len;
+  return ok();
+}
+
+int tail_prefill_attention(const tu_seq* seq, void* k_cache, void* v_cache, void* vt_cache, const tu_attn_params* p,
+                           const void* q, const void* k, const void* v, int64_t T, float* out, void* q_hat,
+                           void* workspace, size_t workspace_bytes, void* stream) {
   if (int e = check_seq(seq)) return e;
   if (int e = check_attn(p)) return e;
   if (T < 0) return fail(TU_ERR_ARG, "negative T");
@@ -1187,20 +1333,24 @@ int tail_prefill_attention(const tu_seq* seq, void* k_cache, void* v_cache, cons
   if (T == 0) return ok();
   if (!k_cache || !v_cache || !q || !k || !v || !out) return fail(TU_ERR_ARG, "null tensor");
   if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(q) || !aligned16(k) || !aligned16(v) ||
-      !aligned16(out) || (q_hat && !aligned16(q_hat)))
+      !aligned16(out) || (q_hat && !aligned16(q_hat)) || (vt_cache && !aligned16(vt_cache)))
     return fail(TU_ERR_ARG, "tensors must be 16-byte aligned");
   std::vector<AttnItem> items(1);
   items[0] = AttnItem{seq, seq->len, T, seq->next_pos, k_cache, v_cache, static_cast<const bf16_t*>(q),
                       static_cast<const bf16_t*>(k), static_cast<const bf16_t*>(v), out,
                       static_cast<bf16_t*>(q_hat)};
+  items[0].vt_cache = vt_cache;
+  items[0].vt_rows = seq->vt_rows;
   std::vector<AttnLaunch> ls;
   size_t need = 0;
-  plan_attention(p, items, nullptr, &ls, &need);
-  if (need > 0 && (!workspace || workspace_bytes < need))
+  plan_attention(p, items, nullptr, CallStatus{}, &ls, &need);
+  need += kStatusBytes;
+  if (!workspace || workspace_bytes < need)
     return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
-  if (workspace && !aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
-  plan_attention(p, items, workspace, &ls, &need);
-  if (int e = run_attention(ls, p->head_dim, static_cast<hipStream_t>(stream))) return e;
+  if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  plan_attention(p, items, after_status(workspace), call_status(workspace), &ls, &need);
+  if (int e = run_attention(ls, p->head_dim, st)) return e;
   return ok();
 }
 
@@ -1215,6 +1365,7 @@ int commit_tail(tu_seq* seq, int64_t T) {
   commit_intervals(seq, iv);
   seq->len += T;
   seq->next_pos += T;
+  seq->vt_rows = seq->len;
   return ok();
 }
 
@@ -1224,8 +1375,8 @@ size_t delta_rule_continue_workspace_size(const tu_delta_params* p, int64_t T) {
   items[0] = DeltaItem{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, T};
   std::vector<DeltaArgs> ls;
   size_t bytes = 0;
-  plan_delta(p, items, nullptr, &ls, &bytes);
-  return std::max<size_t>(bytes, kAlign);
+  plan_delta(p, items, nullptr, CallStatus{}, &ls, &bytes);
+  return kStatusBytes + bytes;
 }
 
 int delta_rule_continue(float* state, const void* q, const void* k, const void* v, const float* beta, const float* g,
@@ -1243,12 +1394,14 @@ int delta_rule_continue(float* state, const void* q, const void* k, const void* 
                        static_cast<const bf16_t*>(v), beta, g, out, T};
   std::vector<DeltaArgs> ls;
   size_t need = 0;
-  plan_delta(p, items, nullptr, &ls, &need);
+  plan_delta(p, items, nullptr, CallStatus{}, &ls, &need);
+  need += kStatusBytes;
   if (!workspace || workspace_bytes < need)
     return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
   if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
-  plan_delta(p, items, workspace, &ls, &need);
-  if (int e = run_delta(ls, p, static_cast<hipStream_t>(stream))) return e;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  plan_delta(p, items, after_status(workspace), call_status(workspace), &ls, &need);
+  if (int e = run_delta(ls, p, st)) return e;
   return ok();
 }
 
@@ -1312,7 +1465,7 @@ int short_conv_continue(void* state, const void* x, const void* weight, int64_t 
 struct StackWorkspace {
   size_t attn = 0;    // compaction and attention layers
   size_t delta = 0;   // delta layers
-  size_t total() const { return align_up(attn) + align_up(delta); }
+  size_t total() const { return kStatusBytes + align_up(attn) + align_up(delta); }
 };
 
 StackWorkspace stack_workspace(const tu_update* u, StackPlan& sp) {
@@ -1321,24 +1474,24 @@ StackWorkspace stack_workspace(const tu_update* u, StackPlan& sp) {
   if (sp.n_attn) {
     auto items = stack_compact_items(u, sp);
     CompactPlan cp;
-    plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, nullptr, &cp);
+    plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, nullptr, CallStatus{}, &cp);
     w.attn = std::max(w.attn, cp.ws_bytes);
     if (sp.any_post) {
       auto post = stack_post_items(u, sp);
-      plan_compaction(post, u->attn.n_kv_heads * u->attn.head_dim * 2, nullptr, &cp);
+      plan_compaction(post, u->attn.n_kv_heads * u->attn.head_dim * 2, nullptr, CallStatus{}, &cp);
       w.attn = std::max(w.attn, cp.ws_bytes);
     }
   }
   for (auto& items : stack_attn_groups(u, sp)) {
     size_t b = 0;
     std::vector<AttnLaunch> ls;
-    plan_attention(&u->attn, items, nullptr, &ls, &b);
+    plan_attention(&u->attn, items, nullptr, CallStatus{}, &ls, &b);
     w.attn = std::max(w.attn, b);
   }
   auto items = stack_delta_items(u, sp);
   if (!items.empty()) {
     std::vector<DeltaArgs> ls;
-    plan_delta(&u->delta, items, nullptr, &ls, &w.delta);
+    plan_delta(&u->delta, items, nullptr, CallStatus{}, &ls, &w.delta);
   }
   return w;
 }
@@ -1453,8 +1606,13 @@ int attention_probe(const tu_seq* seq, const void* k_cache, const tu_attn_params
   return ok();
 }
 
-size_t attention_group_mass_workspace_size(int32_t n_groups) {
-  return align_up(sizeof(double) * 2 * (size_t)std::max(1, (int)n_groups));
+static int group_blocks(int64_t len) {
+  return (int)std::max<int64_t>(1, (len + kGroupRowsPerBlock - 1) / kGroupRowsPerBlock);
+}
+
+size_t attention_group_mass_workspace_size(int64_t len, int32_t n_groups) {
+  if (len < 0) return 0;
+  return align_up(sizeof(double) * 2 * (size_t)group_blocks(len) * (size_t)std::max(1, (int)n_groups));
 }
 
 int attention_group_mass(const tu_seq* seq, const float* probs, const int64_t* groups, int32_t n_groups,
@@ -1472,7 +1630,8 @@ int attention_group_mass(const tu_seq* seq, const float* probs, const int64_t* g
                   (long long)a, (long long)b);
     prev = b;
   }
-  const size_t need = attention_group_mass_workspace_size(n_groups);
+  if (seq->len > INT32_MAX / 2) return fail(TU_ERR_ARG, "context too long");
+  const size_t need = attention_group_mass_workspace_size(seq->len, n_groups);
   if (!workspace || workspace_bytes < need)
     return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
   if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
@@ -1480,14 +1639,14 @@ int attention_group_mass(const tu_seq* seq, const float* probs, const int64_t* g
   GroupArgs a{};
   a.pos = seq->d_pos;
   a.probs = probs;
-  a.acc = static_cast<double*>(workspace);
+  a.partial = static_cast<double*>(workspace);
   a.mass = mass;
   a.window_mass = window_mass;
   a.summary = summary;
   a.len = (int32_t)seq->len;
   a.n_total = n_groups;
   a.window = window;
-  if (int e = hip_check(timed("group_mass", st, [&] { return launch_group_clear(a, st); }), "group clear")) return e;
+  a.n_blocks = group_blocks(seq->len);
   for (int g0 = 0; g0 < n_groups; g0 += kMaxGroupsPerLaunch) {
     a.g_begin = g0;
     a.n = std::min(kMaxGroupsPerLaunch, n_groups - g0);
@@ -1581,9 +1740,19 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
   if (!workspace || workspace_bytes < need)
     return fail(TU_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
   if (!aligned16(workspace)) return fail(TU_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  for (int l = 0; l < u->n_layers; ++l)
+    if (u->layers[l].kind == TU_LAYER_ATTN && u->layers[l].vt_cache)
+      for (int s = 0; s < u->n_seq; ++s) {
+        void* vt = u->layers[l].vt_cache[s];
+        if (vt && !aligned16(vt)) return fail(TU_ERR_ARG, "layer %d context %d: V^T copy must be 16-byte aligned", l, s);
+      }
   hipStream_t st = static_cast<hipStream_t>(stream);
-  void* ws_attn = workspace;
-  void* ws_delta = static_cast<char*>(workspace) + align_up(ws.attn);
+  const CallStatus status = call_status(workspace);
+  void* ws_attn = after_status(workspace);
+  void* ws_delta = static_cast<char*>(ws_attn) + align_up(ws.attn);
+  // the call's number is recorded by the first workgroup of each of its launches (a call
+  // with nothing to launch records it with a one-workgroup kernel, at the end)
+  const uint64_t launches = g_launches;
 
   // Delta layers depend on nothing the attention path writes (the layers' inputs are
   // given), so they run on a side stream of this device, forked after the work
@@ -1598,65 +1767,84 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
     if (int e = hip_check(hipStreamWaitEvent(side->stream, side->fork, 0), "side stream wait")) return e;
   }
   hipStream_t sd = side ? side->stream : st;
-  if (n_delta > 0) {
-    size_t b = 0;
-    auto items = stack_delta_items(u, sp);
-    std::vector<DeltaArgs> ls;
-    plan_delta(&u->delta, items, ws_delta, &ls, &b);
-    if (int e = run_delta(ls, &u->delta, sd)) return e;
-  }
-  // a2-a3: keep-scan and in-place row move over every attention layer of every context
-  if (sp.n_attn) {
-    auto items = stack_compact_items(u, sp);
-    CompactPlan cp;
-    if (int e = plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, ws_attn, &cp)) return e;
-    if (int e = run_compaction(cp, st)) return e;
-  }
-  // a4-a5: the attention layers are independent of each other once the caches are
-  // compacted; the layers too small to fill the chip share one set of launches
-  for (auto& items : stack_attn_groups(u, sp)) {
-    size_t b = 0;
-    std::vector<AttnLaunch> ls;
-    plan_attention(&u->attn, items, ws_attn, &ls, &b);
-    if (int e = run_attention(ls, u->attn.head_dim, st)) return e;
-  }
-  // tail-and-relocate: the stored keys of the tail turn from their computed
-  // positions to the placed ones (values and recurrent state stay as computed)
-  for (int s = 0; s < u->n_seq && sp.n_attn; ++s) {
-    const tu_seq_update& su = u->seqs[s];
-    if (su.placement != TU_PLACE_RELOCATE || su.T == 0) continue;
-    const int64_t L_keep = su.seq->len - sp.rc[s].removed;
-    std::vector<RelocSpan> spans;
-    for (int q = 0, t0 = 0; q < su.n_place_runs; ++q) {
-      const int64_t n = su.place_runs[2 * q + 1] - su.place_runs[2 * q];
-      const int64_t delta = su.place_runs[2 * q] - (su.seq->next_pos + t0);
-      if (delta != 0) spans.push_back({L_keep + t0, n, delta});
-      t0 += (int)n;
+  // Everything from here on is enqueued after the fork; a failing launch still joins
+  // the side stream back into `st` before the error is returned.
+  const int status_code = [&]() -> int {
+    if (n_delta > 0) {
+      size_t b = 0;
+      auto items = stack_delta_items(u, sp);
+      std::vector<DeltaArgs> ls;
+      plan_delta(&u->delta, items, ws_delta, status, &ls, &b);
+      if (int e = run_delta(ls, &u->delta, sd)) return e;
     }
-    std::vector<void*> kbufs;
-    for (int l = 0; l < u->n_layers; ++l)
-      if (u->layers[l].kind == TU_LAYER_ATTN) kbufs.push_back(u->layers[l].k_cache[s]);
-    if (int e = run_relocation(spans, kbufs, su.seq->d_pos, &u->attn, st)) return e;
-  }
-  // rows of the tail removed once it is prefilled (maintenance delimiters): their
-  // direct KV goes, their effect on the recurrent state and on later rows stays
-  if (sp.n_attn && sp.any_post) {
-    auto items = stack_post_items(u, sp);
-    CompactPlan cp;
-    if (int e = plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, ws_attn, &cp)) return e;
-    if (int e = run_compaction(cp, st)) return e;
-  }
+    // a2-a3: keep-scan and in-place row move over every attention layer of every context
+    if (sp.n_attn) {
+      auto items = stack_compact_items(u, sp);
+      CompactPlan cp;
+      if (int e = plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, ws_attn, status, &cp)) return e;
+      if (int e = run_compaction(cp, st)) return e;
+    }
+    // a4-a5: the attention layers are independent of each other once the caches are
+    // compacted; the layers too small to fill the chip share one set of launches
+    for (auto& items : stack_attn_groups(u, sp)) {
+      size_t b = 0;
+      std::vector<AttnLaunch> ls;
+      plan_attention(&u->attn, items, ws_attn, status, &ls, &b);
+      if (int e = run_attention(ls, u->attn.head_dim, st)) return e;
+    }
+    // tail-and-relocate: the stored keys of the tail turn from their computed
+    // positions to the placed ones (values and recurrent state stay as computed)
+    for (int s = 0; s < u->n_seq && sp.n_attn; ++s) {
+      const tu_seq_update& su = u->seqs[s];
+      if (su.placement != TU_PLACE_RELOCATE || su.T == 0) continue;
+      const int64_t L_keep = su.seq->len - sp.rc[s].removed;
+      std::vector<RelocSpan> spans;
+      for (int q = 0, t0 = 0; q < su.n_place_runs; ++q) {
+        const int64_t n = su.place_runs[2 * q + 1] - su.place_runs[2 * q];
+        const int64_t delta = su.place_runs[2 * q] - (su.seq->next_pos + t0);
+        if (delta != 0) spans.push_back({L_keep + t0, n, delta});
+        t0 += (int)n;
+      }
+      std::vector<void*> kbufs;
+      for (int l = 0; l < u->n_layers; ++l)
+        if (u->layers[l].kind == TU_LAYER_ATTN) kbufs.push_back(u->layers[l].k_cache[s]);
+      if (int e = run_relocation(spans, kbufs, su.seq->d_pos, &u->attn, st)) return e;
+    }
+    // rows of the tail removed once it is prefilled (maintenance delimiters): their
+    // direct KV goes, their effect on the recurrent state and on later rows stays
+    if (sp.n_attn && sp.any_post) {
+      auto items = stack_post_items(u, sp);
+      CompactPlan cp;
+      if (int e = plan_compaction(items, u->attn.n_kv_heads * u->attn.head_dim * 2, ws_attn, status, &cp)) return e;
+      if (int e = run_compaction(cp, st)) return e;
+    }
+    return TU_OK;
+  }();
   if (side) {
-    if (int e = hip_check(hipEventRecord(side->join, side->stream), "join event")) return e;
-    if (int e = hip_check(hipStreamWaitEvent(st, side->join, 0), "join wait")) return e;
+    const std::string err = g_err;   // the join must not hide the launch error
+    int e = hip_check(hipEventRecord(side->join, side->stream), "join event");
+    if (!e) e = hip_check(hipStreamWaitEvent(st, side->join, 0), "join wait");
+    if (status_code != TU_OK) {
+      g_err = err;
+      return status_code;
+    }
+    if (e) return e;
   }
+  if (status_code != TU_OK) return status_code;
+  if (g_launches == launches)
+    if (int e = hip_check(launch_status_mark(status, st), "status mark")) return e;
   // a8: commit metadata
   for (int s = 0; s < u->n_seq; ++s) {
     tu_seq* seq = u->seqs[s].seq;
     const bool post = sp.n_attn && sp.post_rc[s].removed > 0;
+    const int64_t L_keep = seq->len - sp.rc[s].removed;
     commit_intervals(seq, post ? sp.post_rc[s].live_after : sp.final_iv[s]);
-    seq->len = seq->len - sp.rc[s].removed + u->seqs[s].T - (post ? sp.post_rc[s].removed : 0);
+    seq->len = L_keep + u->seqs[s].T - (post ? sp.post_rc[s].removed : 0);
     seq->next_pos = sp.cursor_after[s];
+    // the V^T copies now hold every row up to the tail's end, except rows the removal
+    // after the prefill moved
+    if (sp.n_attn) seq->vt_rows = post ? sp.post_rc[s].first_row : seq->len;
+    else seq->vt_rows = std::min(seq->vt_rows, sp.rc[s].removed > 0 ? sp.rc[s].first_row : seq->len);
   }
   return ok();
 }

@@ -16,7 +16,8 @@
 // transposed too, O^T += V^T P^T, on v_mfma_f32_32x32x16_f16 with P in [0, 2^8) rounded to f16
 // (10 stored mantissa bits keep the result inside the accuracy bound; bf16's 7 do
 // not). V^T comes pre-packed per 64-key tile as f16 by k_vt_pack, in exactly the LDS
-// layout, so staging it is a plain copy.
+// layout, so staging it is a plain copy (a copy kept beside the cache, or one packed for
+// this call in the workspace).
 //
 // Tiles move HBM/L2 -> LDS with buffer_load_dwordx4 ... lds (no staging registers;
 // the buffer resource of a tile ends at the cache's data, so rows past it read as
@@ -137,7 +138,7 @@ __device__ __forceinline__ int attn_item(const AttnOrder& o) {
   int g = g0;
   while (g < g1 && o.grp_end[g] <= slot) ++g;
   if (g == g1) return 0x7fffffff;   // the die's share ends before this slot
-  return o.grp_item0[g] + slot - (g > g0 ? o.grp_end[g - 1] : 0);
+  return (int)o.grp_item0[g] + slot - (g > g0 ? (int)o.grp_end[g - 1] : 0);
 }
 
 template <int D>
@@ -210,7 +211,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
 
   const long rs = (long)Hkv * D;  // elements per cache row
   const bf16_t* kbase = S.k_cache + (long)hkv * D;
-  const _Float16* vtbase = S.vt + (long)hkv * S.n_vt_tiles * (D * kVRow);
+  const _Float16* vtbase = S.vt + (long)hkv * S.head_tiles * (D * kVRow);
 
   // ---- tile prefetch. A stage holds K as rows of RC + 1 chunks (16 B each; the last
   // is padding) and V^T as D rows of 9 chunks. LDS chunk q = i * kThreads + tid is
@@ -534,6 +535,9 @@ __global__ __launch_bounds__(256) void k_attn_merge(MergeArgs a) {
 }
 
 }  // namespace
+
+static_assert(sizeof(AttnArgs) + sizeof(AttnOrder) <= kMaxKernargBytes, "attention launch record");
+static_assert(sizeof(MergeArgs) <= kMaxKernargBytes, "merge launch record");
 
 hipError_t launch_attention(const AttnArgs& a, const AttnOrder& o, int head_dim, hipStream_t s) {
   if (a.total_items <= 0) return hipSuccess;

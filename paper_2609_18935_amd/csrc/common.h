@@ -18,7 +18,10 @@ typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
 constexpr int kMaxSeqPerLaunch = 32;
 constexpr int kMaxRangesPerLaunch = 128;
 constexpr int kMaxBufPerLaunch = 64;
-constexpr int kMaxSeqPerCompact = 32;
+constexpr int kMaxSeqPerCompact = 16;
+// Every kernel takes its launch record by value; each record (all arguments of one
+// kernel together) stays within this many bytes.
+constexpr size_t kMaxKernargBytes = 4096;
 constexpr int kScanRows = 1024;  // rows per keep-scan workgroup (a multiple of 256, at most 16K)
 constexpr int kFlagStride = 32;   // compaction stripe counters sit one per 128-byte line
 constexpr int kGatherStripeBytes = 256 * 16 * 16;  // threads x vectors x 16 B
@@ -81,6 +84,38 @@ __device__ __forceinline__ int key_slot(int k) {
   return (k & ~0xC) | ((k & 4) << 1) | ((k & 8) >> 1);
 }
 
+// ------------------------------------------------------------------ call status
+
+// Device-check bits of one call (the kFault* values). The first 256 bytes of a call's
+// workspace hold a 64-bit status word (call number in the high half, bits in the low
+// half) and, 64 bytes further, the 32-bit number of the call that last ran there. Every
+// call has its own number; kernels tag the bits they set with it, and every workgroup 0
+// of the call's launches stores it as the last call's number. A reader takes the bits
+// when the two numbers agree (and none otherwise), so no launch is needed to clear the
+// word and stale bits of earlier calls are never reported.
+struct CallStatus {
+  unsigned long long* word;
+  uint32_t* last;
+  uint32_t call;
+  uint32_t pad;
+};
+
+__device__ __forceinline__ void status_raise(const CallStatus& st, uint32_t bits) {
+  unsigned long long old = __hip_atomic_load(st.word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (;;) {
+    const uint32_t mine = (uint32_t)(old >> 32) == st.call ? (uint32_t)old : 0u;
+    const unsigned long long want = ((unsigned long long)st.call << 32) | (mine | bits);
+    if (want == old) return;
+    const unsigned long long seen = atomicCAS(st.word, old, want);
+    if (seen == old) return;
+    old = seen;
+  }
+}
+
+__device__ __forceinline__ void status_mark(const CallStatus& st) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) *st.last = st.call;
+}
+
 // ------------------------------------------------------------------ launch records
 
 struct ScanSeq {
@@ -127,6 +162,7 @@ struct CompactArgs {
   int32_t n_workers;       // gather workgroups
   int32_t* claim;   // next unclaimed gather item (its own 128-byte line), then the flags
   int32_t* flags;   // [n_flag_words] stripe read counters, kFlagStride apart
+  CallStatus status;
 };
 
 struct RopeSeq {
@@ -160,12 +196,27 @@ struct RopeArgs {
   double theta;
 };
 
+// V^T packing of one context's key tiles [tile_begin, tile_end) (the rows of its V
+// cache and, past L_keep, of the tail's values; RopeArgs::seq[i] of the same index).
+struct PackSeq {
+  _Float16* vt;          // [Hkv][head_tiles][D * kVtRow]
+  int32_t tile_begin;
+  int32_t tile_end;
+  int32_t head_tiles;    // tiles per KV head in vt (its capacity)
+  int32_t pack_begin;    // first packing workgroup of this context
+};
+
+struct PackArgs {
+  PackSeq seq[kMaxSeqPerLaunch];
+  int32_t n_seq;
+  int32_t pack_items;    // packing workgroups
+  CallStatus status;     // kFaultRange when a value exceeds f16
+};
+
 struct AttnSeq {
   const bf16_t* q_hat;   // [T][Hq][D]
   const bf16_t* k_cache; // [cap][Hkv][D]
-  const bf16_t* v_cache;
-  const bf16_t* v_new;   // [T][Hkv][D] the tail's values (rows L_keep .. L_keep + T - 1 of the cache)
-  _Float16* vt;          // [Hkv][n_vt_tiles][D * kVtRow] packed f16 V^T tiles
+  const _Float16* vt;    // [Hkv][head_tiles][D * kVtRow] packed f16 V^T tiles
   float* out;            // [T][Hq][D]
   _Float16* part_o;      // [splits][T*Hq][D] normalised split outputs (unused when splits == 1)
   float* part_ml;        // [splits][T*Hq][2] (reference max in log2 units, sum)
@@ -174,19 +225,17 @@ struct AttnSeq {
   int32_t n_tiles;       // ceil(T*G / kAttnRows)
   int32_t n_splits;
   int32_t item_begin;    // first attention workgroup of this context
-  int32_t n_vt_tiles;    // ceil((L_keep + T) / kAttnKeys)
-  int32_t pack_begin;    // first V^T packing workgroup of this context
-  int32_t pad;
+  int32_t head_tiles;    // tiles per KV head in vt
 };
 
 struct AttnArgs {
   AttnSeq seq[kMaxSeqPerLaunch];
   int32_t n_seq;
   int32_t total_items;   // attention workgroups
-  int32_t pack_items;    // V^T packing workgroups
   int32_t n_q_heads;
   int32_t n_kv_heads;
   float scale_log2;      // softmax_scale * log2(e)
+  int32_t pad;
 };
 
 constexpr int kXcds = 8;              // dies of the chip; workgroup b is dispatched to die b % 8
@@ -196,13 +245,15 @@ constexpr int kMaxAttnGroups = 256;   // entries of an attention launch's die ta
 // Placement of the attention workgroups of a launch on the dies. The items of a group
 // (one context, kv head and key split: its query tiles) are consecutive; die x runs
 // the groups [die_begin[x], die_begin[x + 1]) in that order, its workgroup slot s taking
-// item grp_item0[g] + s - (slots of the die's earlier groups).
+// item grp_item0[g] + s - (slots of the die's earlier groups). Item numbers and slot
+// counts are 16-bit; launches beyond that use the equal-share order.
 struct AttnOrder {
   int32_t n_groups;                   // 0: equal item counts per die in item order (xcd_remap)
   int32_t blocks;                     // grid size
   int32_t die_begin[kXcds + 1];
-  int32_t grp_item0[kMaxAttnGroups];
-  int32_t grp_end[kMaxAttnGroups];    // slots of the die up to and including group g
+  int32_t pad;
+  uint16_t grp_item0[kMaxAttnGroups];
+  uint16_t grp_end[kMaxAttnGroups];   // slots of the die up to and including group g
 };
 
 struct MergeArgs {
@@ -235,6 +286,7 @@ struct DeltaArgs {
   int32_t total_chunks;
   float scale;
   int32_t n_slices;      // d_v slices per value head in the chain kernel
+  CallStatus status;     // kFaultRange when an f16 operand overflows
   _Float16* ws_w;        // [chunks][Hv][C][dk]
   float* ws_u;           // [chunks][Hv][C][dv]
   _Float16* ws_p;        // [chunks][Hv][C][C]
@@ -286,11 +338,12 @@ struct ProbeArgs {
 };
 
 constexpr int kMaxGroupsPerLaunch = 256;
+constexpr int kGroupRowsPerBlock = 8192;   // rows of one group-mass workgroup
 struct GroupArgs {
   int32_t range[kMaxGroupsPerLaunch][2];   // this launch's groups: sorted, disjoint position ranges
   const int32_t* pos;    // d_pos
   const float* probs;    // [len]
-  double* acc;           // [2][n_total] mass, window mass (workspace)
+  double* partial;       // [n_blocks][2][n_total] per-workgroup mass, window mass (workspace)
   float* mass;           // [n_total]
   float* window_mass;    // [n_total] or null
   float* summary;        // [3] or null
@@ -299,7 +352,7 @@ struct GroupArgs {
   int32_t g_begin;       // index of its first group
   int32_t n_total;
   int32_t window;
-  int32_t pad;
+  int32_t n_blocks;      // ceil(len / kGroupRowsPerBlock), at least 1
 };
 
 constexpr int kTvRowsPerBlock = 4096;
@@ -338,18 +391,19 @@ struct ConvArgs {
 // ------------------------------------------------------------------ launchers
 // (defined in the kernel translation units; return a hipError_t)
 int compact_max_blocks();   // resident workgroups of the gather kernel over the device
-// sticky per-device fault bits (the values of TU_FAULT_*)
+// device-check bits of a call's status word (the values of TU_FAULT_*)
 constexpr int32_t kFaultPositions = 1;
 constexpr int32_t kFaultWait = 2;
-hipError_t read_device_faults(int32_t* faults, bool clear, hipStream_t s);
+constexpr int32_t kFaultRange = 4;
+// one workgroup that only records a call's number (for calls that launch nothing else)
+hipError_t launch_status_mark(const CallStatus& st, hipStream_t s);
 constexpr int kMaxGatherWorkers = 2048;
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 // RoPE + append of the tail tokens and the V^T packing of every key tile, one launch
-hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const PackArgs& p, int head_dim, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, const AttnOrder& o, int head_dim, hipStream_t s);
 hipError_t launch_relocate(const RelocArgs& a, hipStream_t s);
 hipError_t launch_probe(const ProbeArgs& a, hipStream_t s);
-hipError_t launch_group_clear(const GroupArgs& a, hipStream_t s);
 hipError_t launch_group_mass(const GroupArgs& a, hipStream_t s);
 hipError_t launch_group_final(const GroupArgs& a, hipStream_t s);
 hipError_t launch_tv(const TvArgs& a, hipStream_t s);

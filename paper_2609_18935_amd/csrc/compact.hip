@@ -9,7 +9,7 @@
 // kept row its rank inside the wave, one wave scans the 64 per-(round, wave) counts,
 // and the rows kept before the workgroup's first row (from the verified spans) give
 // the destination. They write src_index; a row whose keep flag disagrees with the
-// host's live spans sets the device's sticky fault word (kFaultPositions).
+// host's live spans sets kFaultPositions in the call's status word.
 //
 // Gather workgroups (k_compact_gather): move whole rows of every attention layer's K and V
 // buffers, and the position array, in place, only from the first removed row on. The
@@ -25,14 +25,10 @@
 // progresses without any guarantee about which workgroups are resident: an ordinary
 // launch on the caller's stream. One lane polls, with back-off, counters that sit on
 // separate cache lines. Each wait is also bounded: on expiry the item proceeds, the
-// device's sticky fault word gets kFaultWait, and every wave exits.
+// call's status word gets kFaultWait, and every wave exits.
 #include "common.h"
 
 namespace tu {
-
-// Sticky fault bits of this device (one copy per device): set by the compaction
-// kernels, read and cleared by the host through read_device_faults.
-__device__ int32_t g_faults;
 
 namespace {
 
@@ -129,7 +125,7 @@ __device__ void keep_scan(const CompactArgs& a, const ScanSeq& s, int chunk) {
     if ((m[r] >> lane) & 1ull) s.src_index[kept_before + off[r * kScanWaves + wave] + lane_rank(m[r])] = idx;
   }
   bad = __syncthreads_or(bad);
-  if (threadIdx.x == 0 && bad) atomicOr(&g_faults, kFaultPositions);
+  if (threadIdx.x == 0 && bad) status_raise(a.status, kFaultPositions);
 }
 
 __device__ bool gather_items(const CompactArgs& a) {
@@ -238,9 +234,12 @@ __device__ bool gather_items(const CompactArgs& a) {
   return expired;
 }
 
+__global__ __launch_bounds__(64) void k_status_mark(CallStatus st) { status_mark(st); }
+
 // Workgroups 0 .. n_scan_blocks - 1 scan; the last one clears the claim counter and
 // the stripe counters of the move that follows on the same stream.
 __global__ __launch_bounds__(kThreads) void k_compact_scan(CompactArgs a) {
+  status_mark(a.status);
   const int sb = blockIdx.x;
   if (sb == a.n_scan_blocks) {
     for (int i = threadIdx.x; i < a.n_counter_words; i += kThreads) a.claim[i] = 0;
@@ -252,8 +251,9 @@ __global__ __launch_bounds__(kThreads) void k_compact_scan(CompactArgs a) {
 }
 
 __global__ __launch_bounds__(kThreads) void k_compact_gather(CompactArgs a) {
+  status_mark(a.status);
   const bool expired = gather_items(a);
-  if (threadIdx.x == 0 && expired) atomicOr(&g_faults, kFaultWait);
+  if (threadIdx.x == 0 && expired) status_raise(a.status, kFaultWait);
 }
 
 }  // namespace
@@ -271,18 +271,12 @@ int compact_max_blocks() {
   return cached;
 }
 
-hipError_t read_device_faults(int32_t* faults, bool clear, hipStream_t s) {
-  if (hipError_t e = hipMemcpyFromSymbolAsync(faults, HIP_SYMBOL(g_faults), sizeof(int32_t), 0,
-                                              hipMemcpyDeviceToHost, s); e != hipSuccess)
-    return e;
-  if (clear) {
-    static const int32_t zero = 0;
-    if (hipError_t e = hipMemcpyToSymbolAsync(HIP_SYMBOL(g_faults), &zero, sizeof(int32_t), 0,
-                                              hipMemcpyHostToDevice, s); e != hipSuccess)
-      return e;
-  }
-  return hipStreamSynchronize(s);
+hipError_t launch_status_mark(const CallStatus& st, hipStream_t s) {
+  hipLaunchKernelGGL(k_status_mark, dim3(1), dim3(64), 0, s, st);
+  return hipGetLastError();
 }
+
+static_assert(sizeof(CompactArgs) <= kMaxKernargBytes, "compaction launch record");
 
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_compact_scan, dim3(a.n_scan_blocks + 1), dim3(kThreads), 0, s, a);

@@ -46,15 +46,11 @@ __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// 8 bf16 -> 8 f16 (values are well inside the f16 range)
-__device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 w) {
-  f16x8 h;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const uint32_t bits = (e & 1) ? (w[e >> 1] & 0xFFFF0000u) : (w[e >> 1] << 16);
-    h[e] = (_Float16)__uint_as_float(bits);
-  }
-  return __builtin_bit_cast(u32x4, h);
+// Operands rounded to f16 must stay within its range: a larger magnitude rounds to
+// infinity, and the kernels then set kFaultRange in the call's status.
+constexpr float kF16Max = 65504.f;
+__device__ __forceinline__ float max_abs4(f32x4 v) {
+  return fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3])));
 }
 
 __device__ __forceinline__ int find_seq_by_chunk(const DeltaArgs& a, int c) {
@@ -107,6 +103,8 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   const int kh = h / (Hv / Hk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g4 = lane >> 4;
+  float big = 0.f;   // largest magnitude this thread rounds to f16
+  status_mark(a.status);
 
   // ---- phase 0: stage K, Q (bf16), beta, log2 g
   for (int e = tid; e < C * (DK / 8); e += NT) {
@@ -134,7 +132,10 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   if (tid < C) {
     const bool ok = tid < Cr;
     bt[tid] = ok ? S.beta[(long)(t0 + tid) * Hv + h] : 0.f;
-    lg[tid] = ok ? __log2f(S.g[(long)(t0 + tid) * Hv + h]) : 0.f;
+    // log2 g, held at -100 or above: a gate of exactly 0 would give -inf and, in the
+    // differences of the cumulative sums below, NaN; 2^-100 of the state is far below
+    // fp32 rounding of any other term
+    lg[tid] = ok ? fmaxf(__log2f(S.g[(long)(t0 + tid) * Hv + h]), -100.f) : 0.f;
   }
   lds_barrier();
 
@@ -194,8 +195,11 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
     if (is_q) {
       f16x4 pv;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        pv[e] = (_Float16)(i0 + e <= r ? a.scale * __builtin_amdgcn_exp2f(fminf(lr - li4[e], 0.f)) * acc[j][e] : 0.f);
+      for (int e = 0; e < 4; ++e) {
+        const float x = i0 + e <= r ? a.scale * __builtin_amdgcn_exp2f(fminf(lr - li4[e], 0.f)) * acc[j][e] : 0.f;
+        big = fmaxf(big, fabsf(x));
+        pv[e] = (_Float16)x;
+      }
       *(f16x4*)&Pg[r * C + i0] = pv;
     } else {
       const float br = bt[r];
@@ -263,7 +267,9 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   // registers, and scale * 2^lg Q as f16 (the chain's Q S^T operand, row decay folded in)
   for (int e = tid; e < C * C; e += NT) {
     const int r = e / C, i = e - r * C;
-    Th[r][i] = (_Float16)((i >> 4) <= (r >> 4) ? Tf[r][i] : 0.f);
+    const float x = (i >> 4) <= (r >> 4) ? Tf[r][i] : 0.f;
+    big = fmaxf(big, fabsf(x));
+    Th[r][i] = (_Float16)x;
   }
   u32x4 kw[4];
   if (tid < NE5) {
@@ -279,7 +285,9 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
       const uint32_t qb = (d & 1) ? (qw[d >> 1] & 0xFFFF0000u) : (qw[d >> 1] << 16);
-      hq[d] = (_Float16)(w * __uint_as_float(qb));
+      const float x = w * __uint_as_float(qb);
+      big = fmaxf(big, fabsf(x));
+      hq[d] = (_Float16)x;
     }
     *(f16x8*)(a.ws_q + slot * C * DK + (long)r * DK + cc * 8) = hq;
   }
@@ -303,9 +311,12 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
       for (int j = 0; j < 4; ++j) {
         const uint32_t kb = (d & 1) ? (kw[j][d >> 1] & 0xFFFF0000u) : (kw[j][d >> 1] << 16);
         const uint32_t vb = (d & 1) ? (vw[j][d >> 1] & 0xFFFF0000u) : (vw[j][d >> 1] << 16);
-        hk[j] = (_Float16)(wk[j] * __uint_as_float(kb));
-        hv[j] = (_Float16)(wv[j] * __uint_as_float(vb));
-        hd[j] = (_Float16)(wd[j] * __uint_as_float(kb));
+        const float xk = wk[j] * __uint_as_float(kb), xv = wv[j] * __uint_as_float(vb);
+        const float xd = wd[j] * __uint_as_float(kb);
+        big = fmaxf(big, fmaxf(fabsf(xk), fmaxf(fabsf(xv), fabsf(xd))));
+        hk[j] = (_Float16)xk;
+        hv[j] = (_Float16)xv;
+        hd[j] = (_Float16)xd;
       }
       *(f16x4*)&Bt[d0 + d][s4] = hk;
       *(f16x4*)&Vt[d0 + d][s4] = hv;
@@ -338,10 +349,12 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
     if (is_u) {
       *(f32x4*)&Ug[r * DV + d0] = o;
     } else {
+      big = fmaxf(big, fmaxf(fmaxf(fabsf(o[0]), fabsf(o[1])), fmaxf(fabsf(o[2]), fabsf(o[3]))));
       const f16x4 wv = {(_Float16)o[0], (_Float16)o[1], (_Float16)o[2], (_Float16)o[3]};
       *(f16x4*)&Wg[r * DK + d0] = wv;
     }
   }
+  if (big > kF16Max) status_raise(a.status, kFaultRange);
 }
 
 // ------------------------------------------------------------------ chain
@@ -400,6 +413,7 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g4 = lane >> 4;
   const bool kpart = (C >= 32) || (g4 < 2);     // lanes that carry chunk-dim K elements
+  float big = 0.f;   // largest magnitude this thread rounds to f16 (S copy, U)
 
   // ---- load the state slice: S^T blocks (d rows, i cols) in accumulators, f16 copy in LDS
   float* Sg = S.state + (long)h * DV * DK;
@@ -411,6 +425,7 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
     const int db = b / NCB, cb = b % NCB;
     const int i = 16 * cb + l16, d = 16 * db + 4 * g4;
     st[j] = *(const f32x4*)(Sg + (long)(i0 + i) * DK + d);
+    big = fmaxf(big, max_abs4(st[j]));
     f16x4 hv = {(_Float16)st[j][0], (_Float16)st[j][1], (_Float16)st[j][2], (_Float16)st[j][3]};
     *(f16x4*)&Sh[i][d] = hv;
   }
@@ -514,7 +529,11 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
       }
       f16x4 uh;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) uh[e] = (_Float16)(Us[16 * rb + 4 * g4 + e][16 * cb + l16] - x[e]);
+      for (int e = 0; e < 4; ++e) {
+        const float u = Us[16 * rb + 4 * g4 + e][16 * cb + l16] - x[e];
+        big = fmaxf(big, fabsf(u));
+        uh[e] = (_Float16)u;
+      }
       *(f16x4*)&Ut[16 * cb + l16][16 * rb + 4 * g4] = uh;
       oacc[j] = y;
     }
@@ -556,6 +575,7 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
         sacc = mfma_f16(av, bv, sacc);
       }
       st[j] = sacc;
+      big = fmaxf(big, max_abs4(sacc));
       // every read of Sh for this chunk happened before the barrier above
       f16x4 hv = {(_Float16)sacc[0], (_Float16)sacc[1], (_Float16)sacc[2], (_Float16)sacc[3]};
       *(f16x4*)&Sh[16 * cb + l16][16 * db + 4 * g4] = hv;
@@ -569,7 +589,10 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
     const int db = b / NCB, cb = b % NCB;
     *(f32x4*)(Sg + (long)(i0 + 16 * cb + l16) * DK + 16 * db + 4 * g4) = st[j];
   }
+  if (big > kF16Max) status_raise(a.status, kFaultRange);
 }
+
+static_assert(sizeof(DeltaArgs) <= kMaxKernargBytes, "delta launch record");
 
 template <int DK, int C>
 hipError_t prep_for(const DeltaArgs& a, hipStream_t s) {

@@ -1,4 +1,4 @@
-// Attention diagnostics (paper Section 5.3, Appendix D): the float32 reference
+// Attention diagnostics (paper Section 5.3, Appendix C): the float32 reference
 // softmax of the last n query tokens of a context over the rows they see, averaged
 // over tokens and heads into one token distribution, the memory-group masses of that
 // distribution with the effective group count and boundary-window share, and the
@@ -184,49 +184,66 @@ __global__ __launch_bounds__(kThreads) void k_probe_mean(ProbeArgs a) {
   }
 }
 
-// Group masses: clear the float64 accumulators, then one thread per row adds its
-// probability to the group holding its position (binary search over this launch's
-// sorted group ranges) and to the group's boundary window.
-__global__ __launch_bounds__(kThreads) void k_group_clear(GroupArgs a) {
-  const int e = blockIdx.x * kThreads + threadIdx.x;
-  if (e < 2 * a.n_total) a.acc[e] = 0.0;
-}
-
+// Group masses, in a fixed summation order (the same bits on every run): workgroup b
+// takes rows [b * kGroupRowsPerBlock, ...) in rounds of 256; a row adds its probability
+// to the group holding its position (binary search over this launch's sorted group
+// ranges) and to the group's boundary window. Within a wave the rows of one group are
+// summed by a butterfly; each wave accumulates its rounds in order into its own LDS
+// copy of the launch's groups; the four copies are added in wave order and written as
+// the workgroup's partial sums of every group of the launch (zeros included), so no
+// accumulator needs clearing. k_group_final adds the partials in workgroup order.
 __global__ __launch_bounds__(kThreads) void k_group_mass(GroupArgs a) {
-  const int j = blockIdx.x * kThreads + threadIdx.x;
-  const int lane = threadIdx.x & 63;
-  int g = -1;
-  double v = 0.0, w = 0.0;
-  if (j < a.len) {
-    const int p = a.pos[j];
-    int lo = 0, hi = a.n - 1;
-    while (lo <= hi) {
-      const int mid = (lo + hi) >> 1;
-      if (a.range[mid][1] <= p) lo = mid + 1;
-      else if (a.range[mid][0] > p) hi = mid - 1;
-      else { g = mid; break; }
+  __shared__ double acc[kThreads / 64][2][kMaxGroupsPerLaunch];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < (kThreads / 64) * 2 * kMaxGroupsPerLaunch; i += kThreads) (&acc[0][0][0])[i] = 0.0;
+  __syncthreads();
+  const int base = blockIdx.x * kGroupRowsPerBlock;
+  for (int r = 0; r < kGroupRowsPerBlock; r += kThreads) {
+    const int j = base + r + tid;
+    int g = -1;
+    double v = 0.0, w = 0.0;
+    if (j < a.len) {
+      const int p = a.pos[j];
+      int lo = 0, hi = a.n - 1;
+      while (lo <= hi) {
+        const int mid = (lo + hi) >> 1;
+        if (a.range[mid][1] <= p) lo = mid + 1;
+        else if (a.range[mid][0] > p) hi = mid - 1;
+        else { g = mid; break; }
+      }
+      if (g >= 0) {
+        v = (double)a.probs[j];
+        w = p < a.range[g][0] + a.window ? v : 0.0;
+      }
     }
-    if (g >= 0) {
-      v = (double)a.probs[j];
-      w = p < a.range[g][0] + a.window ? v : 0.0;
+    uint64_t left = __ballot(g >= 0);
+    while (left) {
+      const int leader = __builtin_ctzll(left);
+      const int g0 = __shfl(g, leader, 64);
+      const bool mine = g == g0;
+      double s = mine ? v : 0.0, sw = mine ? w : 0.0;
+      for (int o = 32; o > 0; o >>= 1) {
+        s += __shfl_xor(s, o, 64);
+        sw += __shfl_xor(sw, o, 64);
+      }
+      if (lane == leader) {
+        acc[wave][0][g0] += s;
+        acc[wave][1][g0] += sw;
+      }
+      left &= ~__ballot(mine);
     }
   }
-  // the lanes of one group add up first: one pair of atomics per group per wave
-  uint64_t left = __ballot(g >= 0);
-  while (left) {
-    const int leader = __builtin_ctzll(left);
-    const int g0 = __shfl(g, leader, 64);
-    const bool mine = g == g0;
-    double s = mine ? v : 0.0, sw = mine ? w : 0.0;
-    for (int o = 32; o > 0; o >>= 1) {
-      s += __shfl_xor(s, o, 64);
-      sw += __shfl_xor(sw, o, 64);
+  __syncthreads();
+  for (int g = tid; g < a.n; g += kThreads) {
+    double m = 0.0, mw = 0.0;
+#pragma unroll
+    for (int x = 0; x < kThreads / 64; ++x) {
+      m += acc[x][0][g];
+      mw += acc[x][1][g];
     }
-    if (lane == leader) {
-      atomicAdd(&a.acc[a.g_begin + g0], s);
-      atomicAdd(&a.acc[a.n_total + a.g_begin + g0], sw);
-    }
-    left &= ~__ballot(mine);
+    double* out = a.partial + (size_t)blockIdx.x * 2 * a.n_total;
+    out[a.g_begin + g] = m;
+    out[a.n_total + a.g_begin + g] = mw;
   }
 }
 
@@ -235,19 +252,26 @@ __global__ __launch_bounds__(kThreads) void k_group_mass(GroupArgs a) {
 __global__ __launch_bounds__(kThreads) void k_group_final(GroupArgs a) {
   __shared__ double shd[kThreads / 64];
   const int n = a.n_total;
+  // group g's mass and window mass: the workgroups' partials in workgroup order
+  auto group_sum = [&](int g, int which) {
+    double t = 0.0;
+    for (int b = 0; b < a.n_blocks; ++b) t += a.partial[(size_t)b * 2 * n + (size_t)which * n + g];
+    return t;
+  };
   double m = 0.0, w = 0.0;
   for (int g = threadIdx.x; g < n; g += kThreads) {
-    m += a.acc[g];
-    w += a.acc[n + g];
+    const double mg = group_sum(g, 0), wg = group_sum(g, 1);
+    m += mg;
+    w += wg;
+    a.mass[g] = (float)mg;
+    if (a.window_mass) a.window_mass[g] = (float)wg;
   }
   const double M = block_reduce_sum(m, shd);
   const double W = block_reduce_sum(w, shd);
   double h = 0.0;
   for (int g = threadIdx.x; g < n; g += kThreads) {
-    const double x = M > 0.0 ? a.acc[g] / M : 0.0;
+    const double x = M > 0.0 ? group_sum(g, 0) / M : 0.0;
     if (x > 0.0) h -= x * log(x);
-    a.mass[g] = (float)a.acc[g];
-    if (a.window_mass) a.window_mass[g] = (float)a.acc[n + g];
   }
   const double H = block_reduce_sum(h, shd);
   if (threadIdx.x == 0 && a.summary) {
@@ -304,14 +328,12 @@ hipError_t launch_probe(const ProbeArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_group_clear(const GroupArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_group_clear, dim3((2 * a.n_total + kThreads - 1) / kThreads), dim3(kThreads), 0, s, a);
-  return hipGetLastError();
-}
+static_assert(sizeof(GroupArgs) <= kMaxKernargBytes, "group-mass launch record");
+static_assert(sizeof(ProbeArgs) <= kMaxKernargBytes && sizeof(TvArgs) <= kMaxKernargBytes, "probe launch records");
 
 hipError_t launch_group_mass(const GroupArgs& a, hipStream_t s) {
-  if (a.len <= 0 || a.n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_group_mass, dim3((a.len + kThreads - 1) / kThreads), dim3(kThreads), 0, s, a);
+  if (a.n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_group_mass, dim3(a.n_blocks), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

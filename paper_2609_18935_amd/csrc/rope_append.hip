@@ -5,10 +5,12 @@
 // compares (Section 5.2) the rotation uses positions from a short table of runs
 // instead, the rows still being appended after the surviving ones.
 //
-// The same launch also packs every 64-key V tile of the attention into the f16 V^T
+// The same launch also packs the 64-key V tiles of the attention into the f16 V^T
 // layout the attention kernel stages (k_stage: the first workgroups rotate tokens, the
-// rest pack tiles). The pack reads the tail's values from the input rather than from
-// the rows this launch appends, so the two parts never wait on each other.
+// rest pack tiles): every tile, or, with a V^T copy kept beside the cache, only the
+// tiles from the first row that changed since the copy was last refreshed. The pack
+// reads the tail's values from the input rather than from the rows this launch
+// appends, so the two parts never wait on each other.
 //
 // RoPE: one workgroup per tail token (all contexts of a launch packed). The angles
 // (cursor + i) * theta^(-2j/r) and their sines and cosines are formed in float64,
@@ -124,32 +126,36 @@ __device__ void rope_token(const RopeArgs& a, int tok) {
 }
 
 
-// V^T pack: one workgroup per (context, kv head, 64-key tile): V rows -> f16 V^T tile in
-// the attention kernel's LDS layout: D rows (dims) of kVtRow halves, each 64 keys in
-// key_slot order within 16-key groups followed by 8 halves of padding (left
-// unwritten; the attention kernel never reads it). Keys past the cache's data are
-// zero. Thread (c, m) builds chunk c (8 keys) of the 8 rows 8m .. 8m + 7: it loads
-// those 8 keys' dims 8m .. 8m + 7 (16 bytes each), transposes the 8 x 8 block in
-// registers and writes 8 chunks. c is the fastest-moving index: a wave's load reads
-// 128 contiguous bytes of each of 8 rows, and its store writes the 8 chunks of each of
-// 8 V^T rows contiguously.
+// V^T pack: one workgroup per (context, kv head, 64-key tile) of the tiles to refresh:
+// V rows -> f16 V^T tile in the attention kernel's LDS layout: D rows (dims) of kVtRow
+// halves, each 64 keys in key_slot order within 16-key groups followed by 8 halves of
+// padding (left unwritten; the attention kernel never reads it). Keys past the cache's
+// data are zero. Thread (c, m) builds chunk c (8 keys) of the 8 rows 8m .. 8m + 7: it
+// loads those 8 keys' dims 8m .. 8m + 7 (16 bytes each), transposes the 8 x 8 block in
+// registers and writes 8 chunks. c is the fastest-moving index: a wave's load reads 128
+// contiguous bytes of each of 8 rows, and its store writes the 8 chunks of each of 8 V^T
+// rows contiguously. bf16 values of magnitude 2^16 or more (or not finite) have no f16
+// counterpart: the tile then holds infinities and the call's status gets kFaultRange.
 template <int D>
-__device__ void vt_pack_tile(const AttnArgs& a, int item) {
+__device__ void vt_pack_tile(const RopeArgs& r, const PackArgs& pa, int item) {
   constexpr int M = D / 8;                 // 8-dim blocks per row
   constexpr int CPR = kVtRow / 8;          // chunks per V^T row
   int si = 0;
-  while (si + 1 < a.n_seq && a.seq[si + 1].pack_begin <= item) ++si;
-  const AttnSeq& S = a.seq[si];
-  const int local = item - S.pack_begin;
-  const int kt = local % S.n_vt_tiles;
-  const int hkv = local / S.n_vt_tiles;
+  while (si + 1 < pa.n_seq && pa.seq[si + 1].pack_begin <= item) ++si;
+  const PackSeq& P = pa.seq[si];
+  const RopeSeq& S = r.seq[si];
+  const int local = item - P.pack_begin;
+  const int n_tiles = P.tile_end - P.tile_begin;
+  const int kt = P.tile_begin + local % n_tiles;
+  const int hkv = local / n_tiles;
   const int L_keep = S.L_keep;
   const int n_valid = L_keep + S.T;
   const int key0 = kt * kAttnKeys;
-  const long rs = (long)a.n_kv_heads * D;
+  const long rs = (long)r.n_kv_heads * D;
   const bf16_t* src = S.v_cache + (long)hkv * D;
-  const bf16_t* src_new = S.v_new + (long)hkv * D;   // tail row key - L_keep
-  _Float16* dst = S.vt + ((long)hkv * S.n_vt_tiles + kt) * (D * kVtRow);
+  const bf16_t* src_new = S.v + (long)hkv * D;   // tail row key - L_keep
+  _Float16* dst = P.vt + ((long)hkv * P.head_tiles + kt) * (D * kVtRow);
+  uint32_t big = 0;   // largest |bf16| bit pattern converted (two per word)
   for (int w = threadIdx.x; w < 8 * M; w += kRopeThreads) {
     const int c = w & 7;        // key chunk 0..7 (consecutive threads)
     const int m = w >> 3;       // 8-dim block
@@ -159,6 +165,8 @@ __device__ void vt_pack_tile(const AttnArgs& a, int item) {
       const int key = key0 + key_slot(8 * c + j);
       const bf16_t* row = (key < L_keep ? src + (long)key * rs : src_new + (long)(key - L_keep) * rs) + 8 * m;
       rowv[j] = key < n_valid ? *(const u32x4*)row : u32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) big = max(big, max(rowv[j][e] & 0x7FFFu, (rowv[j][e] >> 16) & 0x7FFFu));
     }
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
@@ -171,16 +179,18 @@ __device__ void vt_pack_tile(const AttnArgs& a, int item) {
       *(f16x8*)(dst + ((8 * m + d) * CPR + c) * 8) = h;
     }
   }
+  if (big >= 0x4780u) status_raise(pa.status, kFaultRange);   // 0x4780: bf16 bits of 2^16
 }
 
 template <int D>
-__global__ __launch_bounds__(kRopeThreads) void k_stage(RopeArgs r, AttnArgs a, int rope_tokens) {
+__global__ __launch_bounds__(kRopeThreads) void k_stage(RopeArgs r, PackArgs p, int rope_tokens) {
+  status_mark(p.status);
   const int b = blockIdx.x;
   if (b < rope_tokens) {
     rope_token(r, b);
     return;
   }
-  if (b - rope_tokens < a.pack_items) vt_pack_tile<D>(a, b - rope_tokens);
+  if (b - rope_tokens < p.pack_items) vt_pack_tile<D>(r, p, b - rope_tokens);
 }
 
 // Key relocation (Section 5.2, tail-and-relocate): one workgroup per moved row. The
@@ -229,7 +239,10 @@ hipError_t launch_relocate(const RelocArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const AttnArgs& a, int head_dim, hipStream_t s) {
+static_assert(sizeof(RopeArgs) + sizeof(PackArgs) + sizeof(int) <= kMaxKernargBytes, "stage launch record");
+static_assert(sizeof(RelocArgs) <= kMaxKernargBytes, "relocation launch record");
+
+hipError_t launch_stage(const RopeArgs& r, int rope_tokens, const PackArgs& a, int head_dim, hipStream_t s) {
   const int blocks = rope_tokens + a.pack_items;
   if (blocks <= 0) return hipSuccess;
   if (r.rotary_dim > 2 * kMaxHalf) return hipErrorInvalidValue;

@@ -358,11 +358,55 @@ def test_diagnostics_reject_before_touching_device(L):
                                    None) == B.TU_ERR_WORKSPACE
 
 
-def test_device_faults_rejects_null_and_matches_header(L):
-    """tu_device_faults refuses a null output before any device access; the fault bits
-    of the binding are the header's."""
-    assert L.tu_device_faults(None, 1, None) == B.TU_ERR_ARG
+def test_workspace_faults_rejects_null_and_matches_header(L):
+    """tu_workspace_faults refuses a null workspace or output before any device access;
+    the fault bits of the binding are the header's."""
+    out = ctypes.c_int32(0)
+    assert L.tu_workspace_faults(None, ctypes.byref(out), None) == B.TU_ERR_ARG
+    assert L.tu_workspace_faults(ctypes.c_void_p(16), None, None) == B.TU_ERR_ARG
     assert "faults" in L.tu_last_error().decode()
     hdr = open(HEADER).read()
     assert int(re.search(r"#define TU_FAULT_POSITIONS (\d+)", hdr).group(1)) == tu.TU_FAULT_POSITIONS
     assert int(re.search(r"#define TU_FAULT_WAIT (\d+)", hdr).group(1)) == tu.TU_FAULT_WAIT
+    assert int(re.search(r"#define TU_FAULT_RANGE (\d+)", hdr).group(1)) == tu.TU_FAULT_RANGE
+
+
+def test_new_workspace_is_recorded_on_the_call_stream(monkeypatch):
+    """A workspace the binding allocates for a call on another stream than the current
+    one is recorded on that stream (the caching allocator must not reuse it while the
+    call's kernels run); one for the current stream, or a caller's workspace, is not."""
+    recorded = []
+
+    class FakeTensor:
+        def record_stream(self, st):
+            recorded.append(st)
+
+    class FakeStream:
+        def __init__(self, name):
+            self.name = name
+
+        def __eq__(self, other):
+            return isinstance(other, FakeStream) and other.name == self.name
+
+    current = FakeStream("current")
+    monkeypatch.setattr(B.torch, "empty", lambda *a, **k: FakeTensor())
+    monkeypatch.setattr(B.torch.cuda, "Stream", FakeStream)
+    monkeypatch.setattr(B.torch.cuda, "current_stream", lambda device=None: current)
+    side = FakeStream("side")
+    B._workspace(1024, "cuda", None, side)
+    assert recorded == [side]
+    B._workspace(1024, "cuda", None, current)
+    B._workspace(1024, "cuda", None, None)
+    mine = FakeTensor()
+    assert B._workspace(1024, "cuda", mine, side) is mine
+    assert recorded == [side]
+
+
+def test_vt_cache_bytes(L):
+    """The V^T copy holds Hkv x ceil(capacity / 64) tiles of D rows x 72 f16 (64 keys plus
+    a 16-byte pad); invalid shapes give 0."""
+    assert L.tu_vt_cache_bytes(8192, 2, 256) == 2 * (8192 // 64) * 256 * 72 * 2
+    assert L.tu_vt_cache_bytes(65, 1, 64) == 1 * 2 * 64 * 72 * 2
+    assert L.tu_vt_cache_bytes(0, 2, 256) == 0
+    assert L.tu_vt_cache_bytes(100, 2, 96) == 0
+    assert L.tu_vt_cache_bytes(-1, 2, 256) == 0

@@ -1,4 +1,4 @@
-"""GPU parity of the attention diagnostics (paper Section 5.3, Appendix D) through the
+"""GPU parity of the attention diagnostics (paper Section 5.3, Appendix C) through the
 C ABI against the oracle: the float32 reference-softmax probe of the last eight rows
 of a context after an update (rows in position order, and after a slot-preserving
 update, in work order), averaged over two layers; memory-group and boundary-window

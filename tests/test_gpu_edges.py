@@ -39,7 +39,6 @@ def _ctx_for(case):
 
 
 def test_degenerate_contexts_in_one_call():
-    tu.device_faults(clear=True)
     a = synth.AttnShape(16, 2, 256)
     d = synth.DeltaShape(16, 32, 128, 128, 64)
     specs = [  # (L_old, ranges, T)
@@ -65,9 +64,9 @@ def test_degenerate_contexts_in_one_call():
                          cat([c.v_b for c in dcs]), d_out, state=[c.state for c in dcs],
                          beta=torch.from_numpy(np.concatenate([c.beta for c in dcs])).to(DEV),
                          g=torch.from_numpy(np.concatenate([c.g for c in dcs])).to(DEV))]
-    tu.update_layer_stack(ctxs, [r for _, r, _ in specs], Ts, layers,
-                          tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta),
-                          tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk), src_index=srcs)
+    up = tu.update_layer_stack(ctxs, [r for _, r, _ in specs], Ts, layers,
+                               tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta),
+                               tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk), src_index=srcs)
     torch.cuda.synchronize()
     for c, ((L, ranges, T), ac, dc, ctx) in enumerate(zip(specs, acs, dcs, ctxs)):
         ref = ac.oracle(ranges, L)
@@ -87,18 +86,19 @@ def test_degenerate_contexts_in_one_call():
         assert_close(a_out[int(off[c]): int(off[c + 1])].cpu().numpy(), ref["out"], f"{what}: attention")
         assert_close(d_out[int(off[c]): int(off[c + 1])].cpu().numpy(), o_ref, f"{what}: delta out")
         assert_close(dc.state.cpu().numpy(), S_ref, f"{what}: delta state")
-    assert tu.device_faults() == 0, "an update of consistent contexts raised a device fault"
+    assert tu.workspace_faults(up.workspace) == 0, "an update of consistent contexts raised a device fault"
 
 
 def test_device_fault_on_mislabelled_positions():
     """The host says rows 0..4095 hold positions 0..4095; the device labels row 1000 with
     5000 instead. Removing positions [900, 1100) removes rows 900..1099 by the host's
-    spans, but the row labelled 5000 lies in no range: the scan flags the disagreement.
-    The move still follows the host's spans (every access in bounds)."""
+    spans, but the row labelled 5000 lies in no range: the scan flags the disagreement
+    in the call's status word. The move still follows the host's spans (every access in
+    bounds). A second call on a workspace whose status word holds stale bits (and
+    another workspace untouched meanwhile) starts from a clear word."""
     L = 4096
     _say = lambda m: print(f"[case] {m}", flush=True)
     _say("mislabelled row 1000 of 4096, remove [900, 1100)")
-    tu.device_faults(clear=True)
     k = torch.randn(L, 2, 64, device=DEV).to(torch.bfloat16)
     v = torch.randn_like(k)
     k0, v0 = k.clone(), v.clone()
@@ -107,20 +107,23 @@ def test_device_fault_on_mislabelled_positions():
     labels[1000] = 5000
     ctx.pos[:L] = labels
     ctx.set_metadata([(0, L)], L)
-    tu.compact_kv(ctx, [k], [v], np.array([[900, 1100]]))
-    assert tu.device_faults(clear=True) == tu.TU_FAULT_POSITIONS
-    assert tu.device_faults() == 0      # the read above cleared it
+    nbytes = tu.lib().compact_kv_workspace_size(L, 1, 2, 64)
+    ws = torch.full((nbytes,), 0xFF, dtype=torch.uint8, device=DEV)   # stale bits everywhere
+    other = torch.zeros_like(ws)
+    tu.compact_kv(ctx, [k], [v], np.array([[900, 1100]]), workspace=ws)
+    assert tu.workspace_faults(ws) == tu.TU_FAULT_POSITIONS
+    assert tu.workspace_faults(other) == 0      # another workspace is never touched
     keep = torch.cat([torch.arange(900), torch.arange(1100, L)]).to(DEV)
     assert ctx.len == L - 200
     assert torch.equal(k[: L - 200], k0[keep]) and torch.equal(v[: L - 200], v0[keep])
     assert torch.equal(ctx.pos[: L - 200], labels[keep])
-    # the same removal with consistent labels raises nothing
+    # the same removal with consistent labels raises nothing, on the same workspace
     k, v = k0.clone(), v0.clone()
     ctx = tu.Context(L, device=DEV)
     ctx.pos[:L] = torch.arange(L, dtype=torch.int32, device=DEV)
     ctx.set_metadata([(0, L)], L)
-    tu.compact_kv(ctx, [k], [v], np.array([[900, 1100]]))
-    assert tu.device_faults() == 0
+    tu.compact_kv(ctx, [k], [v], np.array([[900, 1100]]), workspace=ws)
+    assert tu.workspace_faults(ws) == 0
     assert torch.equal(k[: L - 200], k0[keep])
 
 
@@ -142,9 +145,9 @@ def test_all_tails_empty():
                          torch.empty((0, 32, 128), dtype=torch.float32, device=DEV), state=[c.state for c in dcs],
                          beta=torch.empty((0, 32), dtype=torch.float32, device=DEV),
                          g=torch.empty((0, 32), dtype=torch.float32, device=DEV))]
-    tu.update_layer_stack(ctxs, [r for _, r in specs], [0, 0], layers,
-                          tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta),
-                          tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk))
+    up = tu.update_layer_stack(ctxs, [r for _, r in specs], [0, 0], layers,
+                               tu.attn_params(a.n_q_heads, a.n_kv_heads, a.head_dim, a.rdim, a.rope_theta),
+                               tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk))
     torch.cuda.synchronize()
     for (L, ranges), ac, dc, ctx in zip(specs, acs, dcs, ctxs):
         ref = ac.oracle(ranges, L)
@@ -154,4 +157,4 @@ def test_all_tails_empty():
         assert np.array_equal(bits_of(ac.v_cache[:n]), ref["v_cache"])
         assert np.array_equal(bits_of(ac.k_cache[:n]), ref["k_cache"])
         assert np.array_equal(dc.state.cpu().numpy(), dc.S0)
-    assert tu.device_faults() == 0
+    assert tu.workspace_faults(up.workspace) == 0

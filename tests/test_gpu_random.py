@@ -80,8 +80,7 @@ def test_random_stack_update(trial):
     ap = tu.attn_params(A.n_q_heads, A.n_kv_heads, A.head_dim, A.rdim, A.rope_theta, A.softmax_scale,
                         kv_splits=splits)
     dp = tu.delta_params(DSHAPE.n_k_heads, DSHAPE.n_v_heads, DSHAPE.d_k, DSHAPE.d_v, DSHAPE.chunk, DSHAPE.scale)
-    tu.device_faults(clear=True)
-    tu.update_layer_stack(ctxs, [r for _, r, _ in specs], Ts, layers, ap, dp)
+    up = tu.update_layer_stack(ctxs, [r for _, r, _ in specs], Ts, layers, ap, dp)
     torch.cuda.synchronize()
     for c, ((L, ranges, T), (kb, vb, q, k, v, dq, dk, dv, beta, g)) in enumerate(zip(specs, host)):
         what = f"trial {trial} context {c} (L {L}, removed {int(np.sum(ranges[:, 1] - ranges[:, 0]))}, T {T})"
@@ -100,4 +99,4 @@ def test_random_stack_update(trial):
         if T:
             assert_close(d_out[off[c]: off[c + 1]].cpu().numpy(), o_ref, f"{what}: delta out")
         assert_close(states[c][1].cpu().numpy(), S_ref, f"{what}: delta state")
-    assert tu.device_faults() == 0
+    assert tu.workspace_faults(up.workspace) == 0

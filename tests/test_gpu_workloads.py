@@ -345,7 +345,7 @@ def test_paper_shaped_revision_trace():
                              v_cache=[vc]),
                   tu.LayerIO(tu.TU_LAYER_DELTA, to_dev_bf16(dq), to_dev_bf16(dk), to_dev_bf16(dv), d_out,
                              state=[state], beta=torch.from_numpy(beta).to(DEV), g=torch.from_numpy(g).to(DEV))]
-        tu.update_layer_stack([ctx], [rv.ranges], [rv.T], layers, _ap(A), _dp(D), post_ranges=[rv.post],
+        up = tu.update_layer_stack([ctx], [rv.ranges], [rv.T], layers, _ap(A), _dp(D), post_ranges=[rv.post],
                               placement=["slot"], place_runs=[rv.runs])
         torch.cuda.synchronize()
         tail_pos = np.concatenate([np.arange(a, b) for a, b in rv.runs])
@@ -362,4 +362,5 @@ def test_paper_shaped_revision_trace():
         assert_close(d_out.cpu().numpy(), o_ref, f"revision {ri}: delta out")
         assert_close(state.cpu().numpy(), S, f"revision {ri}: delta state")
         pos, kb, vb = ref["pos"], ref["k_cache"], ref["v_cache"]
-    assert tu.device_faults() == 0
+        assert tu.workspace_faults(up.workspace) == 0, f"revision {ri}: device check"
+

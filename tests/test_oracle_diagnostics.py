@@ -1,4 +1,4 @@
-"""Pins for the oracle's attention diagnostics (paper Section 5.3, Appendix D; CPU only).
+"""Pins for the oracle's attention diagnostics (paper Section 5.3, Appendix C; CPU only).
 
 P-G1  library cross-check: the probe distribution equals torch's float32 softmax of
       the masked score matrix (explicit causal mask, heads repeated), averaged.
