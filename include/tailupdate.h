@@ -189,6 +189,24 @@ int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_
                int32_t n_kv_heads, int32_t head_dim, const int64_t* ranges, int32_t n_ranges,
                int32_t* src_index, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * compact_kv for callers that cannot allocate (code under graph capture, serving loops
+ * that forbid allocation): the same removal, with the call's scratch (the index list
+ * when src_index is NULL, the move's counters) in a fixed array the library holds on
+ * every GPU it runs on, TU_NOALLOC_SCRATCH_BYTES (8 MiB) per GPU, kept until the
+ * process ends. No allocation of any kind. A call whose scratch would exceed the array
+ * fails with TU_ERR_WORKSPACE before anything is enqueued (with 1 KB cache rows,
+ * contexts up to about 1.3M rows fit). Calls on one GPU share the array: calls that
+ * overlap in time on that GPU (other streams or threads) race and must not be made.
+ *  status: optional device buffer of 256 bytes (16-byte aligned) that receives the
+ *          call's device-check status (read it with tu_workspace_faults(status, ...));
+ *          NULL keeps the status in the scratch, where it cannot be read.
+ * Every other argument, and the result, as for compact_kv.
+ */
+#define TU_NOALLOC_SCRATCH_BYTES (8u << 20)
+int compact_kv_noalloc(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_t n_layers,
+                       int32_t n_kv_heads, int32_t head_dim, const int64_t* ranges, int32_t n_ranges,
+                       int32_t* src_index, void* status, void* stream);
 
 /*
  * Persistent V^T copy of one attention layer's value cache (optional, caller-owned):

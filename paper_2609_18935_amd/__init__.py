@@ -21,6 +21,7 @@ from .binding import (  # noqa: F401
     attn_params,
     commit_tail,
     compact_kv,
+    compact_kv_noalloc,
     delta_params,
     delta_rule_continue,
     new_vt_cache,

@@ -87,6 +87,8 @@ _SIGNATURES = {
     "compact_kv_workspace_size": (ctypes.c_size_t, [_i64, _i32, _i32, _i32]),
     "compact_kv": (_i32, [ctypes.POINTER(tu_seq), ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _i32, _i32,
                           ctypes.POINTER(_i64), _i32, _vp, _vp, ctypes.c_size_t, _vp]),
+    "compact_kv_noalloc": (_i32, [ctypes.POINTER(tu_seq), ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _i32, _i32,
+                                  ctypes.POINTER(_i64), _i32, _vp, _vp, _vp]),
     "tail_prefill_attention_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(tu_attn_params), _i64, _i64]),
     "tu_vt_cache_bytes": (ctypes.c_size_t, [_i64, _i32, _i32]),
     "refresh_vt_cache": (_i32, [ctypes.POINTER(tu_seq), ctypes.POINTER(_vp), ctypes.POINTER(_vp), _i32, _i32, _i32,
@@ -288,6 +290,22 @@ def compact_kv(ctx: Context, k_layers: Sequence[torch.Tensor], v_layers: Sequenc
     _check(lib().compact_kv(ctypes.byref(ctx.c), ks, vs, n, Hkv, D, arr, nr, _ptr(src_index), _ptr(ws),
                             ws.numel(), _stream(stream)))
     return ws
+
+
+TU_NOALLOC_SCRATCH_BYTES = 8 << 20
+
+
+def compact_kv_noalloc(ctx: Context, k_layers: Sequence[torch.Tensor], v_layers: Sequence[torch.Tensor], ranges,
+                       src_index: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None, stream=None):
+    """compact_kv with its scratch in the library's fixed per-GPU array (no allocation);
+    `status` (256 bytes on the device, optional) receives the call's device checks."""
+    n = len(k_layers)
+    Hkv, D = int(k_layers[0].shape[1]), int(k_layers[0].shape[2])
+    ks = (_vp * max(1, n))(*[_ptr(t) for t in k_layers])
+    vs = (_vp * max(1, n))(*[_ptr(t) for t in v_layers])
+    arr, nr = _ranges_array(ranges)
+    _check(lib().compact_kv_noalloc(ctypes.byref(ctx.c), ks, vs, n, Hkv, D, arr, nr, _ptr(src_index), _ptr(status),
+                                    _stream(stream)))
 
 
 def vt_cache_bytes(capacity: int, n_kv_heads: int, head_dim: int) -> int:

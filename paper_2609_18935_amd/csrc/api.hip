@@ -1192,14 +1192,45 @@ size_t compact_kv_workspace_size(int64_t len, int32_t n_layers, int32_t n_kv_hea
 
 }  // extern "C"
 
+// Fixed scratch of compact_kv_noalloc: each GPU the library runs on holds one copy until
+// the process ends. In host code its name is a stand-in, not a device address; the
+// address comes from hipGetSymbolAddress, once per device, with that device current.
+static __device__ __align__(256) char scratch[TU_NOALLOC_SCRATCH_BYTES];
+
 namespace tu {
 namespace {
 
-// compact_kv with the workspace [base, base + bytes): status block first, unless
-// `status` names a block of its own (then the whole range is the compaction's).
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[64] = {};
+
+int scratch_of_current_device(void** out) {
+  int dev = 0;
+  if (int e = hip_check(hipGetDevice(&dev), "current device")) return e;
+  if (dev < 0 || dev >= 64) return fail(TU_ERR_HIP, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (int e = hip_check(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "scratch address")) return e;
+    if (!p) return fail(TU_ERR_HIP, "no scratch address on device %d", dev);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return TU_OK;
+}
+
+}  // namespace
+}  // namespace tu
+
+namespace tu {
+namespace {
+
+// compact_kv with the workspace [base, base + bytes), or (use_scratch) the fixed scratch
+// of the current device, whose address is fetched once the host checks passed: status
+// block first, unless `status` names a block of its own (then the whole range is the
+// compaction's).
 int compact_with(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_t n_layers, int32_t n_kv_heads,
                  int32_t head_dim, const int64_t* ranges, int32_t n_ranges, int32_t* src_index, void* base,
-                 size_t bytes, void* status, const char* space, hipStream_t st) {
+                 size_t bytes, bool use_scratch, void* status, const char* space, hipStream_t st) {
   if (int e = check_seq(seq)) return e;
   if (n_layers < 0 || (n_layers > 0 && (!k_layers || !v_layers))) return fail(TU_ERR_ARG, "bad layer arrays");
   if (n_kv_heads <= 0 || head_dim <= 0 || ((long)n_kv_heads * head_dim * 2) % 16)
@@ -1227,6 +1258,8 @@ int compact_with(tu_seq* seq, void* const* k_layers, void* const* v_layers, int3
   plan_compaction(items, row_bytes, nullptr, CallStatus{}, &plan);
   const size_t need = (status ? 0 : kStatusBytes) + plan.ws_bytes;
   if (bytes < need) return fail(TU_ERR_WORKSPACE, "%s of %zu bytes, %zu needed", space, bytes, need);
+  if (use_scratch)
+    if (int e = scratch_of_current_device(&base)) return e;
   if (!base) return fail(TU_ERR_WORKSPACE, "null %s", space);
   if (!aligned16(base) || (status && !aligned16(status)))
     return fail(TU_ERR_WORKSPACE, "%s and status must be 16-byte aligned", space);
@@ -1253,7 +1286,14 @@ int compact_kv(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_
                int32_t head_dim, const int64_t* ranges, int32_t n_ranges, int32_t* src_index, void* workspace,
                size_t workspace_bytes, void* stream) {
   return compact_with(seq, k_layers, v_layers, n_layers, n_kv_heads, head_dim, ranges, n_ranges, src_index, workspace,
-                      workspace_bytes, nullptr, "workspace", static_cast<hipStream_t>(stream));
+                      workspace_bytes, false, nullptr, "workspace", static_cast<hipStream_t>(stream));
+}
+
+int compact_kv_noalloc(tu_seq* seq, void* const* k_layers, void* const* v_layers, int32_t n_layers,
+                       int32_t n_kv_heads, int32_t head_dim, const int64_t* ranges, int32_t n_ranges,
+                       int32_t* src_index, void* status, void* stream) {
+  return compact_with(seq, k_layers, v_layers, n_layers, n_kv_heads, head_dim, ranges, n_ranges, src_index, nullptr,
+                      TU_NOALLOC_SCRATCH_BYTES, true, status, "the fixed scratch", static_cast<hipStream_t>(stream));
 }
 
 size_t tail_prefill_attention_workspace_size(const tu_attn_params* p, int64_t T, int64_t len) {
