@@ -17,7 +17,9 @@ from typing import List, Optional, Sequence
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtailupdate.so")
+# TU_LIBRARY may name another build of the same library (e.g. one with host-side
+# sanitizers for the host tests)
+LIB_PATH = os.environ.get("TU_LIBRARY") or os.path.join(_HERE, "libtailupdate.so")
 
 TU_OK = 0
 TU_ERR_ARG = -1
