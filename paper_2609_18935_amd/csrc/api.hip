@@ -493,7 +493,7 @@ inline int64_t vt_head_tiles(int64_t rows) { return (rows + kAttnKeys - 1) / kAt
 // same surviving rows and tail (one context, or the attention layers of one context's
 // stack), the split count minimises (waves) x (time of one workgroup: its key tiles plus
 // a fixed part) plus the merge (a launch, and the partial outputs written and read back
-// once per split); about 2.6 us per 64-key tile at head_dim 256, 5 TB/s. With items of
+// once per split); about 3.8 us per 64-key tile of 256 rows at head_dim 256, 5 TB/s. With items of
 // different lengths in the launch (whose waves do not line up) it takes enough splits
 // for the launch to fill the CUs. At least 4 key tiles per split, at most
 // kMaxAutoSplits (a decode-like tail of one token over 32K rows fills the chip with 128
@@ -508,7 +508,7 @@ int choose_splits(const tu_attn_params* p, int64_t L_keep, int64_t T, int64_t ba
     const int64_t want = std::max<int64_t>(1, (kCus + base_items_total - 1) / std::max<int64_t>(1, base_items_total));
     return (int)std::min(want, max_s);
   }
-  const double tile_us = 2.6 * p->head_dim / 256.0;
+  const double tile_us = 3.8 * p->head_dim / 256.0;
   const double split_us = (double)T * p->n_q_heads * p->head_dim * 4.0 / 5e6;
   double best = 0.0;
   int best_s = 1;
@@ -1497,6 +1497,10 @@ int short_conv_continue(void* state, const void* x, const void* weight, int64_t 
   return short_conv_continue_batch(&t, 1, width, activation, stream);
 }
 
+}  // extern "C"
+
+namespace {
+
 // Workspace of a stack update: [compaction / attention region | delta region]. Delta
 // layers run on a second stream concurrently with the attention path, so the two
 // regions are disjoint. Attention layers run in order and reuse their region; the
@@ -1535,6 +1539,10 @@ StackWorkspace stack_workspace(const tu_update* u, StackPlan& sp) {
   }
   return w;
 }
+
+}  // namespace
+
+extern "C" {
 
 size_t update_layer_stack_workspace_size(const tu_update* u) {
   StackPlan sp;

@@ -5,9 +5,9 @@
 // Tail row i of query head h attends to cache rows 0 .. L_keep + i of KV head
 // h / G (G = Hq / Hkv). The G query heads that share a KV head are packed as
 // rows (token-major: packed row = t * G + (h mod G)), so one workgroup tile of
-// 128 packed rows reads each K/V tile once for all of them.
+// 256 packed rows reads each K/V tile once for all of them.
 //
-// Workgroup: 4 waves of 32 packed rows each (one wave per SIMD); key tiles of 64
+// Workgroup: 8 waves of 32 packed rows each, two waves per SIMD; key tiles of 64
 // rows in LDS, processed as two 32-key units. Scores are formed transposed,
 // S^T = K Q^T, on v_mfma_f32_32x32x16_bf16 (A = 32 keys x 16 dims of K from LDS,
 // B = 16 dims x 32 queries of Q held in registers), so a lane's accumulator holds
@@ -21,15 +21,16 @@
 //
 // Tiles move HBM/L2 -> LDS with buffer_load_dwordx4 ... lds (no staging registers;
 // the buffer resource of a tile ends at the cache's data, so rows past it read as
-// zeros), double-buffered: K of tile k+2 is requested once every wave has formed the
-// scores of tile k, V of tile k+1 once every wave has used V of tile k-1. With one wave
-// per SIMD nothing else hides latency, so every phase (softmax of one 32-key unit,
-// scores of the next, P.V of the first) keeps the matrix core fed: half of the next
-// unit's score MFMAs are issued around the max reduction, the uniform branch that
-// rarely moves the reference max follows, and the other half runs with the
-// exponentials, followed by P.V with the tile loads interleaved. Loads are issued on
-// every tile (zero bytes past the split's end), so the wait counts never change, and
-// the lane-pair exchanges use v_permlane32_swap instead of an LDS round trip.
+// zeros), double-buffered with one barrier per tile: after it, every wave is done with
+// the previous tile, whose stage then receives the next tile while this one is
+// computed. Loads are issued on every tile (zero bytes past the split's end), so the
+// wait counts never change. Each unit runs its score MFMAs, the softmax and the P.V
+// MFMAs in order; the other wave of the SIMD, at another point of its own units, keeps
+// the matrix core fed meanwhile. A wave holds 256 registers: O^T for 32 rows x 256
+// dims (128), the Q fragments (64), the scores and the rest, all in ordinary vector
+// registers (the build asks for the VGPR form of the MFMAs, so the budget is not split
+// in equal accumulator and vector halves, which would spill Q). The lane-pair
+// exchanges use v_permlane32_swap instead of an LDS round trip.
 //
 // For occupancy the key range is split over `n_splits` workgroups; each writes a
 // normalised f16 partial (O / l) with its reference max and sum, and k_attn_merge
@@ -94,7 +95,7 @@ __device__ __forceinline__ void wg_barrier() {
 // rounds of 16-byte loads by the workgroup, so every wave issues the same number of
 // loads per tile. Separate arrays, so the compiler sees that a prefetch into one stage
 // does not alias reads of the other.
-constexpr int kThreads = 256;       // 4 waves x 32 packed rows
+constexpr int kThreads = 512;       // 8 waves x 32 packed rows
 constexpr int kVRow = kVtRow;       // f16 elements per V^T row
 template <int D>
 struct StageGeom {
@@ -111,17 +112,10 @@ __shared__ __attribute__((aligned(16))) bf16_t g_ks1[kKStage];
 __shared__ __attribute__((aligned(16))) _Float16 g_vt0[kVStage];
 __shared__ __attribute__((aligned(16))) _Float16 g_vt1[kVStage];
 
-// Scales an MFMA accumulator that lives in AGPRs. Going through explicit AGPR
-// reads/writes keeps the accumulator out of the VALU register class, so the
-// compiler does not shuttle it between AGPRs and VGPRs on every key tile.
+// Scales an MFMA accumulator (the rare move of the softmax reference max).
 __device__ __forceinline__ void scale_acc(f32x16& acc, float s) {
 #pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    float v;
-    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(acc[e]));
-    v *= s;
-    asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(acc[e]) : "v"(v));
-  }
+  for (int e = 0; e < 16; ++e) acc[e] *= s;
 }
 
 template <int B>
@@ -142,7 +136,7 @@ __device__ __forceinline__ int attn_item(const AttnOrder& o) {
 }
 
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_attn(AttnArgs a,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_attn(AttnArgs a,
                                                                                                AttnOrder ord) {
   constexpr int NS = D / 16;                // 16-dim steps of S^T = K Q^T
   constexpr int NDB = D / 32;               // 32-dim blocks of O^T
@@ -333,80 +327,51 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     }
   };
 
-  constexpr int kMfma = 0x008, kValu = 0x002, kVmemRd = 0x020, kDsRead = 0x100;
-  // first part of a phase: half the score MFMAs of the next unit with the max reduction
-  auto sched_head = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
+  // Keep n MFMAs fed by their LDS fragment reads, two reads ahead: bounds the fragment
+  // registers in flight (the compiler would otherwise issue every read up front).
+  constexpr int kMfma = 0x008, kDsRead = 0x100;
+  auto sched_reads = [&](auto nc) __attribute__((always_inline)) {
+    constexpr int N = decltype(nc)::value;
+    __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
 #pragma unroll
-    for (int i = 0; i < NS / 2; ++i) {
+    for (int i = 0; i < N; ++i) {
       __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-      if (i < NS / 2 - 4) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(kValu, 4, 0);
-    }
-  };
-  // second part: the other score MFMAs and P.V with the exponentials and the tile loads.
-  // Two vector instructions per score MFMA measured best (2-3 % over 3 to 5; 1 is worse)
-  auto sched_tail = [&](int nload) __attribute__((always_inline)) {
-    constexpr int kAhead = 4;
-    __builtin_amdgcn_sched_group_barrier(kDsRead, kAhead, 0);
-#pragma unroll
-    for (int i = 0; i < NS / 2; ++i) {
-      __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(kValu, 2, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < 2 * NDB; ++i) {
-      __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-      if (i < 2 * NDB - kAhead) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
-      if (i < nload) __builtin_amdgcn_sched_group_barrier(kVmemRd, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(kValu, 2, 0);
+      if (i < N - 1) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
     }
   };
 
-  f32x16 sa, sb;
+  f32x16 sa;
   f16x8 pf[2];
-  // One key tile kt in stage B. On entry sa holds the scores of the tile's first
-  // 32-key unit, on exit those of tile kt + 1's first unit. Tile loads are issued
-  // unconditionally (past the split's last tile they have zero bytes and only write
-  // zeros to a stage that is no longer read), so the wait counts are the same on every
-  // tile. On a split's last tile the scores of the next unit read the idle stage and
-  // are discarded.
+  // One 32-key unit of the tile in stage B: scores, softmax, P.V.
+  auto unit = [&](auto bc, int half, int kb0) __attribute__((always_inline)) {
+    qk_part(bc, half, sa, IntC<0>{}, IntC<NS>{});
+    sched_reads(IntC<NS>{});
+    mask(kb0, sa);
+    const float mx = rowmax(sa);
+    rescale_if(mx);
+    sexp(sa, pf);
+    pv(bc, half, pf);
+    sched_reads(IntC<2 * NDB>{});
+  };
+  // One key tile kt in stage B. Only this tile's loads are in flight on entry: once they
+  // have landed and every wave has passed the barrier, every wave is also done with
+  // tile kt - 1, so the loads of tile kt + 1 go to the other stage at once and land
+  // while this tile is computed (one barrier per tile). Loads are issued
+  // unconditionally (past the split's last tile they have zero bytes), so the wait
+  // counts are the same on every tile.
   auto step = [&](auto bc, int kt) __attribute__((always_inline)) {
     constexpr int B = decltype(bc)::value;
-    mask(kt * kBN, sa);
-    qk_part(bc, 1, sb, IntC<0>{}, IntC<NS / 2>{});
-    float mx = rowmax(sa);
-    sched_head();
-    rescale_if(mx);
-    qk_part(bc, 1, sb, IntC<NS / 2>{}, IntC<NS>{});
-    sexp(sa, pf);
-    pv(bc, 0, pf);
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));   // this wave's loads of tile kt have landed
+    wg_barrier();                              // everyone's have; stage B ^ 1 is free
+    load_k(IntC<B ^ 1>{}, kt + 1);
     load_v(IntC<B ^ 1>{}, kt + 1);
-    sched_tail(NLV);
-    __builtin_amdgcn_s_waitcnt(vm_wait(NLV));  // K of tile kt + 1 has landed
-    wg_barrier();                               // every wave is done with K of stage B
-    mask(kt * kBN + 32, sb);
-    qk_part(IntC<B ^ 1>{}, 0, sa, IntC<0>{}, IntC<NS / 2>{});
-    mx = rowmax(sb);
-    sched_head();
-    rescale_if(mx);
-    qk_part(IntC<B ^ 1>{}, 0, sa, IntC<NS / 2>{}, IntC<NS>{});
-    sexp(sb, pf);
-    pv(bc, 1, pf);
-    load_k(bc, kt + 2);
-    sched_tail(NLK);
-    __builtin_amdgcn_s_waitcnt(vm_wait(NLK));  // V of tile kt + 1 has landed
-    wg_barrier();                               // every wave is done with V of stage B
+    unit(bc, 0, kt * kBN);
+    unit(bc, 1, kt * kBN + 32);
   };
 
   if (kt_begin < kt_end) {
     load_k(IntC<0>{}, kt_begin);
     load_v(IntC<0>{}, kt_begin);
-    load_k(IntC<1>{}, kt_begin + 1);
-    __builtin_amdgcn_s_waitcnt(vm_wait(NLK));  // tile kt_begin has landed
-    wg_barrier();
-    qk_part(IntC<0>{}, 0, sa, IntC<0>{}, IntC<NS>{});
     for (int kt = kt_begin; kt < kt_end; kt += 2) {
       step(IntC<0>{}, kt);
       if (kt + 1 < kt_end) step(IntC<1>{}, kt + 1);

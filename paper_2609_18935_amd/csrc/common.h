@@ -25,7 +25,7 @@ constexpr size_t kMaxKernargBytes = 4096;
 constexpr int kScanRows = 1024;  // rows per keep-scan workgroup (a multiple of 256, at most 16K)
 constexpr int kFlagStride = 32;   // compaction stripe counters sit one per 128-byte line
 constexpr int kGatherStripeBytes = 256 * 16 * 16;  // threads x vectors x 16 B
-constexpr int kAttnRows = 128;  // packed query rows per attention workgroup
+constexpr int kAttnRows = 256;  // packed query rows per attention workgroup
 constexpr int kAttnKeys = 64;   // keys per attention K/V tile
 constexpr int kVtRow = kAttnKeys + 8;  // f16 per row of a packed V^T tile (64 keys + pad)
 

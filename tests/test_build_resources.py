@@ -1,8 +1,10 @@
 """The compiler's resource report of every kernel (written by the build next to the
 objects): no kernel keeps anything in scratch memory (a spill, or a kernel-argument
 struct copied to the stack because a pointer into it outlives its use, made the merge
-kernel 15x slower once), every kernel's LDS fits a CU (160 KB on gfx950), and the
-attention kernel's registers fit one wave per SIMD (its design point)."""
+kernel 15x slower once) apart from one bounded exception below, every kernel's LDS fits
+a CU (160 KB on gfx950), and the
+attention kernel's registers fit two waves per SIMD (its design point: 256 per wave,
+so the other wave of the SIMD keeps the matrix core busy through each one's softmax)."""
 import json
 import os
 
@@ -20,9 +22,18 @@ def _report():
     return d
 
 
+# The head_dim-256 attention kernel stores a few loop-invariant values (at most 64 bytes
+# per lane) once before its key loop and reloads them only in the branch that masks a
+# 32-key unit crossing the tail diagonal (a handful of units per workgroup). The
+# spill-free forms of that mask (masking inside the row max and the exponentials of
+# every unit) measured 6-7% slower over the whole update.
+ALLOWED_SCRATCH = {"_ZN2tu12_GLOBAL__N_16k_attnILi256E": 64}
+
+
 def test_no_kernel_uses_scratch():
     for name, r in _report().items():
-        assert r.get("scratch_bytes", 0) == 0, f"{name}: {r['scratch_bytes']} bytes of scratch per lane"
+        limit = max([v for k, v in ALLOWED_SCRATCH.items() if name.startswith(k)], default=0)
+        assert r.get("scratch_bytes", 0) <= limit, f"{name}: {r['scratch_bytes']} bytes of scratch per lane"
 
 
 def test_lds_fits_a_cu():
@@ -30,8 +41,8 @@ def test_lds_fits_a_cu():
         assert r.get("lds_bytes", 0) <= 160 * 1024, f"{name}: {r['lds_bytes']} bytes of LDS"
 
 
-def test_attention_registers_fit_one_wave_per_simd():
+def test_attention_registers_fit_two_waves_per_simd():
     att = {n: r for n, r in _report().items() if "k_attnILi" in n}
     assert len(att) == 3, sorted(att)      # head_dim 64, 128, 256
     for name, r in att.items():
-        assert r["vgprs"] + r["agprs"] <= 512, f"{name}: {r}"
+        assert r["vgprs"] + r["agprs"] <= 256 and r["waves_per_simd"] >= 2, f"{name}: {r}"
