@@ -32,9 +32,9 @@
  *  - Input range. Some products take operands rounded to f16 (10 stored mantissa
  *    bits, largest finite value 65504), because bf16 operands there would exceed the
  *    accuracy bound: attention values (v), and in the delta rule the state S, the
- *    pseudo-values U = T (beta v) - W S^T, the decay-scaled q, k and beta v, and the
- *    WY factors. Inputs whose magnitudes reach 2^16 in these places have no f16
- *    counterpart: the results are then not meaningful and the call sets
+ *    pseudo-values U = T (beta v) - W S^T and their decayed copies, q, k and v
+ *    themselves, and the WY factors. Inputs whose magnitudes reach 2^16 in these
+ *    places have no f16 counterpart: the results are then not meaningful and the call sets
  *    TU_FAULT_RANGE in its status word. The delta rule expects L2-normalised keys
  *    (||k_t|| <= 1), beta in [0, 1] and g in [0, 1] (g = 0 is computed as 2^-100).
  */

@@ -766,9 +766,11 @@ int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, vo
     const size_t g1 = std::min(items.size(), g0 + kMaxSeqPerLaunch);
     int n_active = 0;
     for (size_t i = g0; i < g1; ++i) n_active += items[i].T > 0;
-    // slice d_v so that the chain has enough workgroups
-    const int wg64 = n_active * Hv * (DK / 64);
-    const int dvs = (wg64 >= 256) ? 64 : 32;
+    // slice d_v (16 rows of S per owner wave of the chain) into as few workgroups per
+    // head as give half the CUs one (the rest serve the attention layers running
+    // beside the delta layers)
+    int dvs = std::min(DK, 64);
+    while (dvs > 16 && (int64_t)n_active * Hv * (DK / dvs) < kCus / 2) dvs /= 2;
     DeltaArgs a{};
     a.n_k_heads = p->n_k_heads;
     a.n_v_heads = Hv;
@@ -795,11 +797,9 @@ int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, vo
     a.total_chunks = chunks;
     Arena ar(ws);
     a.ws_w = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * DK));
-    a.ws_u = static_cast<float*>(ar.take(sizeof(float) * (size_t)chunks * Hv * C * DK));
-    a.ws_p = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * C));
+    a.ws_tv = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * C));
+    a.ws_p = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * std::max(C, 32)));
     a.ws_lg = static_cast<float*>(ar.take(sizeof(float) * (size_t)chunks * Hv * C));
-    a.ws_q = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * DK));
-    a.ws_kt = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * DK));
     max_used = std::max(max_used, ar.used);
     if (a.n_seq > 0) out->push_back(a);
   }

@@ -10,6 +10,7 @@ typedef uint16_t bf16_t;  // bfloat16 storage
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
+typedef __attribute__((__vector_size__(2 * sizeof(_Float16)))) _Float16 f16x2;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
@@ -287,12 +288,10 @@ struct DeltaArgs {
   float scale;
   int32_t n_slices;      // d_v slices per value head in the chain kernel
   CallStatus status;     // kFaultRange when an f16 operand overflows
-  _Float16* ws_w;        // [chunks][Hv][C][dk]
-  float* ws_u;           // [chunks][Hv][C][dv]
-  _Float16* ws_p;        // [chunks][Hv][C][C]
-  float* ws_lg;          // [chunks][Hv][C]
-  _Float16* ws_q;        // [chunks][Hv][C][dk]  scale * 2^lg q
-  _Float16* ws_kt;       // [chunks][Hv][dk][C]  2^(lg_last - lg) k, transposed
+  _Float16* ws_w;        // [chunks][Hv][C][dk]  W = T diag(beta 2^lg) K, d in operand order
+  _Float16* ws_tv;       // [chunks][Hv][C][C]   T diag(beta)
+  _Float16* ws_p;        // [chunks][Hv][C][max(C, 32)]  scale lower(G .* Q K^T), operand order
+  float* ws_lg;          // [chunks][Hv][C]     cumulative log2 decay
 };
 
 // Key relocation: one workgroup per moved row; every key buffer of the launch gets the

@@ -7,26 +7,36 @@
 // The tail is cut into chunks of C tokens starting at its first token. Inside a
 // chunk (rows r, i), with lg_r = sum_{s<=r} log2 g_s and G[r][i] = 2^(lg_r - lg_i):
 //     M = strictly-lower(diag(beta) (G .* K K^T)),   T = (I + M)^-1
-//     W = T diag(beta 2^lg) K,   U~ = T diag(beta) V                     (k_delta_prep)
-//     U = U~ - W S^T
-//     O = scale (diag(2^lg) Q S^T + lower(G .* Q K^T) U)
+//     W = T diag(beta 2^lg) K,   T_v = T diag(beta),   P = scale lower(G .* Q K^T)
+//                                                                       (k_delta_prep)
+//     U = T_v V - W S^T
+//     O = scale diag(2^lg) Q S^T + P U
 //     S <- 2^lg_last S + U^T diag(2^(lg_last - lg)) K                      (k_delta_chain)
-// Only decay ratios <= 1 are formed. A ragged last chunk is padded with k = q = v = 0,
-// beta = 0, g = 1, which leaves the recurrence unchanged.
+// (W and T_v V are the WY factors of the chunk.) Only decay ratios <= 1 are formed. A
+// ragged last chunk is padded with k = q = v = 0, beta = 0, g = 1, which leaves the
+// recurrence unchanged.
 //
-// k_delta_prep: one workgroup per (chunk, value head), all chunks in parallel.
-//   K K^T and Q K^T on v_mfma_f32_16x16x32_bf16 (exact bf16 products, fp32 sums);
-//   T by blocked forward substitution in fp32 (16x16 diagonal blocks by one lane per
-//   column, then off-diagonal blocks level by level); W and U~ on
-//   v_mfma_f32_16x16x32_f16 with T and the scaled K, V rounded to f16. Writes W (f16),
-//   U~ (fp32), P = scale * lower(G .* Q K^T) (f16) and lg (fp32) to the workspace.
-// k_delta_chain: one workgroup per (context, value head, slice of DVS rows of S). Rows
-//   of S evolve independently (row i only needs U[:, i]), so slicing d_v spreads a
-//   head over several workgroups. The fp32 state slice lives in MFMA accumulators
-//   for the whole tail, is read from HBM once and written once; each chunk it is
-//   rounded to f16 into LDS to serve as the MFMA operand of W S^T and Q S^T.
-//   f16 (10 stored mantissa bits) keeps the operands of these fp32-intermediate
-//   products accurate enough for the error bound where bf16 would not.
+// k_delta_prep: one workgroup per (chunk, value head), all chunks in parallel: the
+//   work of a chunk that does not depend on the state. K K^T and Q K^T on
+//   v_mfma_f32_16x16x32_bf16 (exact bf16 products, fp32 sums); T by blocked forward
+//   substitution in fp32 (16x16 diagonal blocks by one lane per column, then
+//   off-diagonal blocks level by level); W on v_mfma_f32_16x16x32_f16. Writes W, T_v
+//   and P (f16) and lg (fp32) to the workspace, W and P with their contracted index
+//   in the chain's operand order (below).
+// k_delta_chain: one workgroup per (context, value head, slice of DVS rows of S); rows
+//   of S evolve independently (row i only needs U[:, i]). Each 16 rows of the slice
+//   belong to one "owner" wave that keeps them, fp32, in MFMA accumulators for the
+//   whole tail (read from HBM once, written once). An accumulator lane holds 4
+//   consecutive rows of one column of a 16x16 block; two such blocks side by side
+//   supply the 8 values one lane feeds to a 16x16x32 product, when the contracted
+//   index runs through each group of 32 in the order perm32 below. So S (as f16), U
+//   and its decayed copy serve as MFMA operands straight from registers, and the
+//   state step of a chunk needs no LDS round trip and no barrier. The other waves
+//   ("producers") stage the next chunk's operands into the second of two LDS buffers:
+//   q (f16, permuted d), k^T (f16, permuted s), the v slice transposed, W, P, T_v and
+//   lg. One barrier per chunk. f16 (10 stored mantissa bits) keeps the operands of
+//   these fp32-intermediate products accurate enough for the error bound where bf16
+//   would not; bf16 inputs convert to f16 exactly inside its range.
 #include "common.h"
 
 namespace tu {
@@ -53,6 +63,14 @@ __device__ __forceinline__ float max_abs4(f32x4 v) {
   return fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3])));
 }
 
+// Position of index x inside its group of 32 in the chain's operand order: the group
+// of 4 a = x / 4 goes to 8 (a % 4) + 4 (a / 4), so that lane group g reads indices
+// 4g .. 4g + 3 and 16 + 4g .. 16 + 4g + 3 as 8 contiguous values.
+__device__ __forceinline__ int perm32(int x) {
+  const int a = (x >> 2) & 7;
+  return (x & ~31) | (8 * (a & 3) + 4 * (a >> 2) + (x & 3));
+}
+
 __device__ __forceinline__ int find_seq_by_chunk(const DeltaArgs& a, int c) {
   int si = 0;
   while (si + 1 < a.n_seq && a.seq[si + 1].chunk_begin <= c) ++si;
@@ -71,31 +89,29 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   constexpr int NB = C / 16;     // 16-row blocks of the chunk
   constexpr int KP = DK + 8;     // pitch of [C][DK] bf16 tiles
   constexpr int CP = C + 4;      // pitch of [C][C] fp32 tiles
-  constexpr int CH = C + 8;      // pitch of [*][C] f16 tiles
-  // LDS regions shared by arrays whose lifetimes do not overlap, so that two workgroups
-  // fit a CU: K (phases 0-5a) then (beta 2^lg K)^T (5b-6); Q (0-5a) then (beta V)^T
-  // (5b-6); M (1-4) then T in f16 (5a-6). A barrier separates 5a (the last reads of K,
-  // Q and T in fp32) from 5b (the first writes of the transposed copies).
-  constexpr int R1 = cmax(sizeof(bf16_t) * C * KP, sizeof(_Float16) * DK * CH);
-  constexpr int R2 = cmax(sizeof(bf16_t) * C * KP, sizeof(_Float16) * DV * CH);
-  constexpr int R3 = cmax(sizeof(float) * C * CP, sizeof(_Float16) * C * CH);
-  __shared__ __attribute__((aligned(16))) char r1[R1];
+  constexpr int CT = C + 8;      // pitch of f16 tiles with the chunk index contiguous
+  constexpr int CC = C < 32 ? 32 : C;   // row length of P in the workspace (padded)
+  // Q (phases 0-1), M (2-4) and k^T in f16 (5-6) share a region; barriers separate
+  // the last reads of each from the first writes of the next
+  constexpr int R2 = cmax(cmax(sizeof(bf16_t) * C * KP, sizeof(float) * C * CP), sizeof(_Float16) * DK * CT);
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[C][KP];
   __shared__ __attribute__((aligned(16))) char r2[R2];
-  __shared__ __attribute__((aligned(16))) char r3[R3];
   __shared__ __attribute__((aligned(16))) float Tf[C][CP];
+  __shared__ __attribute__((aligned(16))) _Float16 Twh[C][CT];   // T diag(beta 2^lg) in f16
   __shared__ __attribute__((aligned(16))) float Xs[3][16][20];
   __shared__ __attribute__((aligned(16))) float lg[C];
   __shared__ __attribute__((aligned(16))) float bt[C];
-  auto& Ks = *reinterpret_cast<bf16_t(*)[C][KP]>(r1);
-  auto& Bt = *reinterpret_cast<_Float16(*)[DK][CH]>(r1);
   auto& Qs = *reinterpret_cast<bf16_t(*)[C][KP]>(r2);
-  auto& Vt = *reinterpret_cast<_Float16(*)[DV][CH]>(r2);
-  auto& Mf = *reinterpret_cast<float(*)[C][CP]>(r3);
-  auto& Th = *reinterpret_cast<_Float16(*)[C][CH]>(r3);
+  auto& Mf = *reinterpret_cast<float(*)[C][CP]>(r2);
+  auto& Kt = *reinterpret_cast<_Float16(*)[DK][CT]>(r2);
 
   const int Hk = a.n_k_heads, Hv = a.n_v_heads;
-  const int c = blockIdx.x / Hv;          // global chunk
-  const int h = blockIdx.x - c * Hv;      // value head
+  // work item (chunk, value head); consecutive items, and so the value heads that share
+  // a key head's q and k, run on one XCD and share its L2
+  const int item = xcd_remap(blockIdx.x, gridDim.x);
+  if (item >= a.total_chunks * Hv) return;
+  const int c = item / Hv;                // global chunk
+  const int h = item - c * Hv;            // value head
   const int si = find_seq_by_chunk(a, c);
   const DeltaSeq S = a.seq[si];
   const int t0 = (c - S.chunk_begin) * C;
@@ -117,17 +133,6 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
     }
     *(u32x4*)&Ks[r][cc * 8] = kw;
     *(u32x4*)&Qs[r][cc * 8] = qw;
-  }
-  // the values this thread converts in phase 5, fetched now so their latency overlaps
-  // phases 1-4 ((C / 4) * (DK / 8) <= NT: one item per thread at most)
-  constexpr int NE5 = (C / 4) * (DK / 8);
-  static_assert(NE5 <= NT, "phase 5 maps one item per thread");
-  u32x4 vw[4];
-  if (tid < NE5) {
-    const int s4 = (tid % (C / 4)) * 4, d0 = (tid / (C / 4)) * 8;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      vw[j] = (s4 + j < Cr) ? *(const u32x4*)(S.v + ((long)(t0 + s4 + j) * Hv + h) * DV + d0) : u32x4{0, 0, 0, 0};
   }
   if (tid < C) {
     const bool ok = tid < Cr;
@@ -179,7 +184,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
 
   // ---- phase 2: M (fp32, LDS) and P (f16, workspace) from the MFMA results
   const long slot = (long)c * Hv + h;
-  _Float16* Pg = a.ws_p + slot * C * C;
+  _Float16* Pg = a.ws_p + slot * C * CC;
 #pragma unroll
   for (int j = 0; j < NPW; ++j) {
     const int idx = blk_of[j];
@@ -200,7 +205,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
         big = fmaxf(big, fabsf(x));
         pv[e] = (_Float16)x;
       }
-      *(f16x4*)&Pg[r * C + i0] = pv;
+      *(f16x4*)&Pg[r * CC + perm32(i0)] = pv;
     } else {
       const float br = bt[r];
       f32x4 mv;
@@ -210,10 +215,10 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
       *(f32x4*)&Mf[r][i0] = mv;
     }
   }
-  // zero the upper blocks of P
-  for (int e = tid; e < C * C / 8; e += NT) {
-    const int r = e / (C / 8), i = (e - r * (C / 8)) * 8;
-    if ((i >> 4) > (r >> 4)) *(u32x4*)&Pg[r * C + i] = u32x4{0, 0, 0, 0};
+  // zero the upper blocks of P and the padding of its rows
+  for (int e = tid; e < C * CC / 4; e += NT) {
+    const int r = e / (CC / 4), i = (e - r * (CC / 4)) * 4;
+    if (i >= C || (i >> 4) > (r >> 4)) *(uint2*)&Pg[r * CC + perm32(i)] = uint2{0, 0};
   }
   if (tid < C) a.ws_lg[slot * C + tid] = lg[tid];
   lds_barrier();
@@ -263,331 +268,339 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
     lds_barrier();
   }
 
-  // ---- phase 5a: T to f16 (lower, zero upper; M is dead), this thread's K rows into
-  // registers, and scale * 2^lg Q as f16 (the chain's Q S^T operand, row decay folded in)
-  for (int e = tid; e < C * C; e += NT) {
-    const int r = e / C, i = e - r * C;
-    const float x = (i >> 4) <= (r >> 4) ? Tf[r][i] : 0.f;
-    big = fmaxf(big, fabsf(x));
-    Th[r][i] = (_Float16)x;
-  }
-  u32x4 kw[4];
-  if (tid < NE5) {
-    const int s4 = (tid % (C / 4)) * 4, d0 = (tid / (C / 4)) * 8;
+  // ---- phase 5: T diag(beta 2^lg) (f16, LDS) and T_v = T diag(beta) (f16, workspace),
+  // zero above the diagonal blocks (whose entries of Tf were never written); k^T in f16
+  _Float16* Tvg = a.ws_tv + slot * C * C;
+  for (int e = tid; e < C * C / 4; e += NT) {
+    const int r = e / (C / 4), i0 = (e - r * (C / 4)) * 4;
+    f16x4 hw, hv;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) kw[j] = *(const u32x4*)&Ks[s4 + j][d0];
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + q;
+      const float x = (i >> 4) <= (r >> 4) ? Tf[r][i] : 0.f;
+      const float xw = x * (bt[i] * __builtin_amdgcn_exp2f(lg[i])), xv = x * bt[i];
+      big = fmaxf(big, fmaxf(fabsf(xw), fabsf(xv)));
+      hw[q] = (_Float16)xw;
+      hv[q] = (_Float16)xv;
+    }
+    *(f16x4*)&Twh[r][i0] = hw;
+    *(f16x4*)&Tvg[r * C + i0] = hv;
   }
-  for (int e = tid; e < C * (DK / 8); e += NT) {
-    const int r = e / (DK / 8), cc = e - r * (DK / 8);
-    const float w = a.scale * __builtin_amdgcn_exp2f(lg[r]);
-    const u32x4 qw = *(const u32x4*)&Qs[r][cc * 8];
-    f16x8 hq;
+  for (int e = tid; e < (C / 2) * (DK / 8); e += NT) {
+    const int s2 = (e % (C / 2)) * 2, d0 = (e / (C / 2)) * 8;
+    const u32x4 k0 = *(const u32x4*)&Ks[s2][d0], k1 = *(const u32x4*)&Ks[s2 + 1][d0];
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
-      const uint32_t qb = (d & 1) ? (qw[d >> 1] & 0xFFFF0000u) : (qw[d >> 1] << 16);
-      const float x = w * __uint_as_float(qb);
-      big = fmaxf(big, fabsf(x));
-      hq[d] = (_Float16)x;
-    }
-    *(f16x8*)(a.ws_q + slot * C * DK + (long)r * DK + cc * 8) = hq;
-  }
-  lds_barrier();   // K and Q are no longer read: their regions take the transposed copies
-
-  // ---- phase 5b: (beta 2^lg K)^T and (beta V)^T in f16, and the decayed K^T for the chain
-  if (tid < NE5) {
-    const int s4 = (tid % (C / 4)) * 4, d0 = (tid / (C / 4)) * 8;
-    float wk[4], wv[4], wd[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int s = s4 + j;
-      wv[j] = bt[s];
-      wk[j] = bt[s] * __builtin_amdgcn_exp2f(lg[s]);
-      wd[j] = __builtin_amdgcn_exp2f(lg[C - 1] - lg[s]);
-    }
-#pragma unroll
-    for (int d = 0; d < 8; ++d) {
-      f16x4 hk, hv, hd;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t kb = (d & 1) ? (kw[j][d >> 1] & 0xFFFF0000u) : (kw[j][d >> 1] << 16);
-        const uint32_t vb = (d & 1) ? (vw[j][d >> 1] & 0xFFFF0000u) : (vw[j][d >> 1] << 16);
-        const float xk = wk[j] * __uint_as_float(kb), xv = wv[j] * __uint_as_float(vb);
-        const float xd = wd[j] * __uint_as_float(kb);
-        big = fmaxf(big, fmaxf(fabsf(xk), fmaxf(fabsf(xv), fabsf(xd))));
-        hk[j] = (_Float16)xk;
-        hv[j] = (_Float16)xv;
-        hd[j] = (_Float16)xd;
-      }
-      *(f16x4*)&Bt[d0 + d][s4] = hk;
-      *(f16x4*)&Vt[d0 + d][s4] = hv;
-      *(f16x4*)(a.ws_kt + slot * DK * C + (long)(d0 + d) * C + s4) = hd;
+      const uint32_t b0 = (d & 1) ? (k0[d >> 1] & 0xFFFF0000u) : (k0[d >> 1] << 16);
+      const uint32_t b1 = (d & 1) ? (k1[d >> 1] & 0xFFFF0000u) : (k1[d >> 1] << 16);
+      const float x0 = __uint_as_float(b0), x1 = __uint_as_float(b1);
+      big = fmaxf(big, fmaxf(fabsf(x0), fabsf(x1)));
+      const f16x2 hk = {(_Float16)x0, (_Float16)x1};
+      *(f16x2*)&Kt[d0 + d][s2] = hk;
     }
   }
   lds_barrier();
 
-  // ---- phase 6: W = T (beta 2^lg K), U~ = T (beta V) on MFMA; write to workspace
+  // ---- phase 6: W = T diag(beta 2^lg) K on MFMA, to the workspace with d in the
+  // chain's operand order
   _Float16* Wg = a.ws_w + slot * C * DK;
-  float* Ug = a.ws_u + slot * C * DV;
-  constexpr int NOB = NB * (DK / 16);   // output blocks per matrix
-  for (int idx = wave; idx < 2 * NOB; idx += NW) {
-    const bool is_u = idx >= NOB;
-    const int b = idx % NOB;
-    const int rb = b / (DK / 16), db = b % (DK / 16);
+  constexpr int NOB = NB * (DK / 16);
+  for (int idx = wave; idx < NOB; idx += NW) {
+    const int rb = idx / (DK / 16), db = idx % (DK / 16);
     f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    // transposed product (X^T T^T): the lane ends up with row 16 rb + l16 and the 4
-    // consecutive columns 16 db + 4 g4 .. of W (or U~), stored as one vector
+    // transposed product (K^T W'^T): the lane ends up with row 16 rb + l16 and the 4
+    // consecutive columns 16 db + 4 g4 .. of W
 #pragma unroll
     for (int kk = 0; kk < (C + 31) / 32; ++kk) {
       f16x8 av = zero_f16x8(), bv = zero_f16x8();
       if (C >= 32 || g4 < 2) {
-        av = is_u ? ld_f16x8(&Vt[16 * db + l16][32 * kk + 8 * g4]) : ld_f16x8(&Bt[16 * db + l16][32 * kk + 8 * g4]);
-        bv = ld_f16x8(&Th[16 * rb + l16][32 * kk + 8 * g4]);
+        av = ld_f16x8(&Kt[16 * db + l16][32 * kk + 8 * g4]);
+        bv = ld_f16x8(&Twh[16 * rb + l16][32 * kk + 8 * g4]);
       }
       o = mfma_f16(av, bv, o);
     }
-    const int r = 16 * rb + l16, d0 = 16 * db + 4 * g4;
-    if (is_u) {
-      *(f32x4*)&Ug[r * DV + d0] = o;
-    } else {
-      big = fmaxf(big, fmaxf(fmaxf(fabsf(o[0]), fabsf(o[1])), fmaxf(fabsf(o[2]), fabsf(o[3]))));
-      const f16x4 wv = {(_Float16)o[0], (_Float16)o[1], (_Float16)o[2], (_Float16)o[3]};
-      *(f16x4*)&Wg[r * DK + d0] = wv;
-    }
+    big = fmaxf(big, max_abs4(o));
+    const f16x4 wv = {(_Float16)o[0], (_Float16)o[1], (_Float16)o[2], (_Float16)o[3]};
+    *(f16x4*)&Wg[(16 * rb + l16) * DK + perm32(16 * db + 4 * g4)] = wv;
   }
   if (big > kF16Max) status_raise(a.status, kFaultRange);
 }
 
 // ------------------------------------------------------------------ chain
-constexpr int kChainThreads = 1024;  // 16 waves: four per SIMD interleave their latencies
+constexpr int kChainThreads = 512;   // 8 waves: DVS / 16 owners, the rest producers
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// One chunk's operands in LDS (two of these alternate)
+template <int DK, int C, int DVS>
+struct ChainStage {
+  static constexpr int KP = DK + 8;                  // pitch of rows over d
+  static constexpr int CC = C < 32 ? 32 : C;         // chunk index padded to a whole MFMA step
+  static constexpr int CK = CC + 8;                  // pitch of rows over the chunk index
+  _Float16 W[C][KP];      // W, d in operand order
+  _Float16 Q[C][KP];      // q in f16, d in operand order
+  _Float16 Kt[DK][CK];    // k^T in f16, s in operand order
+  _Float16 P[C][CK];      // P, s in operand order
+  _Float16 Tv[C][CK];     // T_v, natural order
+  _Float16 Vt[DVS][CK];   // the v slice transposed, natural order
+  float lg[C];
+};
+
 template <int DK, int C, int DVS>
 __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
+  using Stage = ChainStage<DK, C, DVS>;
   constexpr int NT = kChainThreads;
-  constexpr int NW = NT / 64;
   constexpr int DV = DK;
-  constexpr int KP = DK + 8;
-  constexpr int CH = C + 8;
-  constexpr int NCB = DVS / 16;                 // column blocks of the slice
-  constexpr int NXB = (C / 16) * NCB;           // blocks of W S^T / Q S^T / O
-  constexpr int NXW = (NXB + NW - 1) / NW;      // per wave
-  constexpr int NSB = (DK / 16) * NCB;          // blocks of S^T
-  constexpr int NSW = (NSB + NW - 1) / NW;      // per wave (the last ones may own none)
-  // per-chunk operands staged from the workspace (all f16 except U~)
-  constexpr int VQ = C * DK / 8;                // 16-byte vectors of W and of Qg
-  constexpr int VK = DK * C / 8;                // of Kd^T
-  constexpr int VP = C * C / 8;                 // of P
-  constexpr int VU = C * DVS / 4;               // 16-byte vectors of the U~ slice (fp32)
-  constexpr int RQ = (VQ + NT - 1) / NT, RK = (VK + NT - 1) / NT, RP = (VP + NT - 1) / NT, RU = (VU + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) _Float16 Ws[C][KP];
-  __shared__ __attribute__((aligned(16))) _Float16 Qs[C][KP];
-  __shared__ __attribute__((aligned(16))) _Float16 Kdt[DK][CH];
-  __shared__ __attribute__((aligned(16))) _Float16 Ph[C][CH];
-  __shared__ __attribute__((aligned(16))) float Us[C][DVS + 4];
-  __shared__ __attribute__((aligned(16))) _Float16 Ut[DVS][CH];
-  __shared__ __attribute__((aligned(16))) _Float16 Sh[DVS][KP];
-  __shared__ float s_glast;
+  constexpr int CC = Stage::CC;
+  constexpr int NO = DVS / 16;                  // owner waves
+  constexpr int NP = NT - 64 * NO;              // producer threads
+  constexpr int NRB = C / 16;                   // 16-row blocks of a chunk
+  constexpr int NDB = DK / 16;                  // 16-row blocks of S^T
+  constexpr int NKD = DK / 32;                  // MFMA steps over d
+  constexpr int NKS = CC / 32;                  // MFMA steps over the chunk index
+  // producer work per chunk: 16-byte vectors of q, W, P, T_v; 2-row x 8-column items of
+  // k and of the v slice
+  constexpr int VQ = C * DK / 8, VW = C * DK / 8, VP = C * CC / 8, VT = C * C / 8;
+  constexpr int NKI = (C / 2) * (DK / 8), NVI = (C / 2) * (DVS / 8);
+  constexpr int RQ = (VQ + NP - 1) / NP, RW = (VW + NP - 1) / NP, RP = (VP + NP - 1) / NP;
+  constexpr int RT = (VT + NP - 1) / NP, RK = (NKI + NP - 1) / NP, RV = (NVI + NP - 1) / NP;
+  __shared__ __attribute__((aligned(16))) Stage stg[2];
 
-  const int Hv = a.n_v_heads;
+  // work item: (context, key head, value head of the group, slice), ordered so that the
+  // workgroups reading one key head's q and k share an XCD
+  const int Hv = a.n_v_heads, Hk = a.n_k_heads, G = Hv / Hk;
+  const int item = xcd_remap(blockIdx.x, gridDim.x);
   const int per_seq = Hv * a.n_slices;
-  int si, h, sl;
-  if ((Hv & 7) == 0) {
-    // workgroup b runs on XCD b % 8 (round-robin dispatch); the prep workgroup of
-    // (chunk, head h) ran on XCD h % 8, so every slice of head h is placed there too and
-    // finds the head's chunk operands in that XCD's L2
-    const int b = blockIdx.x;
-    const int hx = b & 7;                     // h % 8
-    const int rest = b >> 3;                  // (seq, h / 8, slice)
-    sl = rest % a.n_slices;
-    const int hq = (rest / a.n_slices) % (Hv >> 3);
-    si = rest / a.n_slices / (Hv >> 3);
-    h = 8 * hq + hx;
-  } else {
-    const int item = xcd_remap(blockIdx.x, gridDim.x);   // slices of one head share an XCD
-    si = item / per_seq;
-    const int rem = item - si * per_seq;
-    h = rem / a.n_slices;
-    sl = rem - h * a.n_slices;
-  }
+  const int si = item / per_seq;
   if (si >= a.n_seq) return;
-  const int i0 = sl * DVS;
+  const int rem = item - si * per_seq;
+  const int kh = rem / (G * a.n_slices);
+  const int rem2 = rem - kh * G * a.n_slices;
+  const int h = kh * G + rem2 / a.n_slices;
+  const int i0 = (rem2 % a.n_slices) * DVS;
   const DeltaSeq S = a.seq[si];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g4 = lane >> 4;
-  const bool kpart = (C >= 32) || (g4 < 2);     // lanes that carry chunk-dim K elements
-  float big = 0.f;   // largest magnitude this thread rounds to f16 (S copy, U)
+  const bool owner = wave < NO;
+  const int p = tid - 64 * NO;                  // producer thread index
+  float big = 0.f;   // largest magnitude this thread rounds to f16
 
-  // ---- load the state slice: S^T blocks (d rows, i cols) in accumulators, f16 copy in LDS
-  float* Sg = S.state + (long)h * DV * DK;
-  f32x4 st[NSW];
-#pragma unroll
-  for (int j = 0; j < NSW; ++j) {
-    const int b = wave + NW * j;
-    if (b >= NSB) continue;
-    const int db = b / NCB, cb = b % NCB;
-    const int i = 16 * cb + l16, d = 16 * db + 4 * g4;
-    st[j] = *(const f32x4*)(Sg + (long)(i0 + i) * DK + d);
-    big = fmaxf(big, max_abs4(st[j]));
-    f16x4 hv = {(_Float16)st[j][0], (_Float16)st[j][1], (_Float16)st[j][2], (_Float16)st[j][3]};
-    *(f16x4*)&Sh[i][d] = hv;
+  // chunk-index padding of the stages (C = 16 only) stays zero for the whole kernel
+  if (C < 32) {
+    for (int e = tid; e < 2 * (DK + C + DVS) * 16; e += NT) {
+      const int b = e / ((DK + C + DVS) * 16), rest = e - b * (DK + C + DVS) * 16;
+      const int row = rest / 16, x = C + (rest % 16);
+      if (row < DK) stg[b].Kt[row][perm32(x)] = (_Float16)0.f;
+      else if (row < DK + C) stg[b].Tv[row - DK][x] = (_Float16)0.f;
+      else stg[b].Vt[row - DK - C][x] = (_Float16)0.f;
+    }
   }
 
-  // ---- next chunk's operands are fetched into registers while the current one is computed
-  u32x4 rw[RQ], rq[RQ], rk[RK], rp[RP], ru[RU];
-  float rg = 0.f;
-  auto prefetch = [&](int lc) {
+  // ---- producers: registers of one chunk, then their conversion into a stage
+  const u32x4 z4 = {0, 0, 0, 0};
+  u32x4 rq[RQ], rw[RW], rp[RP], rt[RT], rk[RK][2], rv[RV][2];
+  float rlg = 0.f;
+  auto fetch = [&](int lc) {
+    const int t0 = lc * C;
+    const int Cr = min(C, S.T - t0);
     const long slot = (long)(S.chunk_begin + lc) * Hv + h;
+#pragma unroll
+    for (int j = 0; j < RQ; ++j) {
+      const int e = p + NP * j;
+      const int r = e / (DK / 8), c8 = e - r * (DK / 8);
+      rq[j] = (e < VQ && r < Cr) ? *(const u32x4*)(S.q + ((long)(t0 + r) * Hk + kh) * DK + 8 * c8) : z4;
+    }
+#pragma unroll
+    for (int j = 0; j < RK; ++j) {
+      const int e = p + NP * j;
+      const int s2 = (e % (C / 2)) * 2, d0 = (e / (C / 2)) * 8;
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        rk[j][q] = (e < NKI && s2 + q < Cr) ? *(const u32x4*)(S.k + ((long)(t0 + s2 + q) * Hk + kh) * DK + d0) : z4;
+    }
+#pragma unroll
+    for (int j = 0; j < RV; ++j) {
+      const int e = p + NP * j;
+      const int s2 = (e % (C / 2)) * 2, d0 = (e / (C / 2)) * 8;
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        rv[j][q] = (e < NVI && s2 + q < Cr) ? *(const u32x4*)(S.v + ((long)(t0 + s2 + q) * Hv + h) * DV + i0 + d0) : z4;
+    }
     const u32x4* W4 = (const u32x4*)(a.ws_w + slot * C * DK);
-    const u32x4* Q4 = (const u32x4*)(a.ws_q + slot * C * DK);
-    const u32x4* K4 = (const u32x4*)(a.ws_kt + slot * DK * C);
-    const u32x4* P4 = (const u32x4*)(a.ws_p + slot * C * C);
-    const float* U = a.ws_u + slot * C * DV + i0;
+    const u32x4* P4 = (const u32x4*)(a.ws_p + slot * C * CC);
+    const u32x4* T4 = (const u32x4*)(a.ws_tv + slot * C * C);
 #pragma unroll
-    for (int j = 0; j < RQ; ++j) {
-      const int e = tid + NT * j;
-      if (e < VQ) {
-        rw[j] = W4[e];
-        rq[j] = Q4[e];
-      }
-    }
+    for (int j = 0; j < RW; ++j) rw[j] = p + NP * j < VW ? W4[p + NP * j] : z4;
 #pragma unroll
-    for (int j = 0; j < RK; ++j)
-      if (tid + NT * j < VK) rk[j] = K4[tid + NT * j];
+    for (int j = 0; j < RP; ++j) rp[j] = p + NP * j < VP ? P4[p + NP * j] : z4;
 #pragma unroll
-    for (int j = 0; j < RP; ++j)
-      if (tid + NT * j < VP) rp[j] = P4[tid + NT * j];
-#pragma unroll
-    for (int j = 0; j < RU; ++j) {
-      const int e = tid + NT * j;
-      if (e < VU) {
-        const int r = e / (DVS / 4), c4 = e - r * (DVS / 4);
-        ru[j] = *(const u32x4*)(U + (long)r * DV + 4 * c4);
-      }
-    }
-    rg = a.ws_lg[slot * C + C - 1];
+    for (int j = 0; j < RT; ++j) rt[j] = p + NP * j < VT ? T4[p + NP * j] : z4;
+    if (p < C) rlg = a.ws_lg[slot * C + p];
   };
-  auto stage = [&]() {
+  auto put = [&](Stage& B) {
 #pragma unroll
     for (int j = 0; j < RQ; ++j) {
-      const int e = tid + NT * j;
+      const int e = p + NP * j;
       if (e < VQ) {
         const int r = e / (DK / 8), c8 = e - r * (DK / 8);
-        *(u32x4*)&Ws[r][8 * c8] = rw[j];
-        *(u32x4*)&Qs[r][8 * c8] = rq[j];
+        f16x4 lo, hi;
+#pragma unroll
+        for (int w = 0; w < 2; ++w) {
+          const float x0 = bf16_lo(rq[j][w]), x1 = bf16_hi(rq[j][w]);
+          const float y0 = bf16_lo(rq[j][w + 2]), y1 = bf16_hi(rq[j][w + 2]);
+          big = fmaxf(big, fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(y0), fabsf(y1))));
+          lo[2 * w] = (_Float16)x0;
+          lo[2 * w + 1] = (_Float16)x1;
+          hi[2 * w] = (_Float16)y0;
+          hi[2 * w + 1] = (_Float16)y1;
+        }
+        *(f16x4*)&B.Q[r][perm32(8 * c8)] = lo;
+        *(f16x4*)&B.Q[r][perm32(8 * c8 + 4)] = hi;
       }
     }
 #pragma unroll
     for (int j = 0; j < RK; ++j) {
-      const int e = tid + NT * j;
-      if (e < VK) {
-        const int d = e / (C / 8), c8 = e - d * (C / 8);
-        *(u32x4*)&Kdt[d][8 * c8] = rk[j];
+      const int e = p + NP * j;
+      if (e < NKI) {
+        const int s2 = (e % (C / 2)) * 2, d0 = (e / (C / 2)) * 8;
+        const int ps = perm32(s2);
+#pragma unroll
+        for (int d = 0; d < 8; ++d) {
+          const float x0 = (d & 1) ? bf16_hi(rk[j][0][d >> 1]) : bf16_lo(rk[j][0][d >> 1]);
+          const float x1 = (d & 1) ? bf16_hi(rk[j][1][d >> 1]) : bf16_lo(rk[j][1][d >> 1]);
+          big = fmaxf(big, fmaxf(fabsf(x0), fabsf(x1)));
+          const f16x2 hx = {(_Float16)x0, (_Float16)x1};
+          *(f16x2*)&B.Kt[d0 + d][ps] = hx;
+        }
       }
+    }
+#pragma unroll
+    for (int j = 0; j < RV; ++j) {
+      const int e = p + NP * j;
+      if (e < NVI) {
+        const int s2 = (e % (C / 2)) * 2, d0 = (e / (C / 2)) * 8;
+#pragma unroll
+        for (int d = 0; d < 8; ++d) {
+          const float x0 = (d & 1) ? bf16_hi(rv[j][0][d >> 1]) : bf16_lo(rv[j][0][d >> 1]);
+          const float x1 = (d & 1) ? bf16_hi(rv[j][1][d >> 1]) : bf16_lo(rv[j][1][d >> 1]);
+          big = fmaxf(big, fmaxf(fabsf(x0), fabsf(x1)));
+          const f16x2 hx = {(_Float16)x0, (_Float16)x1};
+          *(f16x2*)&B.Vt[d0 + d][s2] = hx;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RW; ++j) {
+      const int e = p + NP * j;
+      if (e < VW) *(u32x4*)&B.W[e / (DK / 8)][8 * (e % (DK / 8))] = rw[j];
     }
 #pragma unroll
     for (int j = 0; j < RP; ++j) {
-      const int e = tid + NT * j;
-      if (e < VP) {
-        const int r = e / (C / 8), c8 = e - r * (C / 8);
-        *(u32x4*)&Ph[r][8 * c8] = rp[j];
-      }
+      const int e = p + NP * j;
+      if (e < VP) *(u32x4*)&B.P[e / (CC / 8)][8 * (e % (CC / 8))] = rp[j];
     }
 #pragma unroll
-    for (int j = 0; j < RU; ++j) {
-      const int e = tid + NT * j;
-      if (e < VU) {
-        const int r = e / (DVS / 4), c4 = e - r * (DVS / 4);
-        *(u32x4*)&Us[r][4 * c4] = ru[j];
-      }
+    for (int j = 0; j < RT; ++j) {
+      const int e = p + NP * j;
+      if (e < VT) *(u32x4*)&B.Tv[e / (C / 8)][8 * (e % (C / 8))] = rt[j];
     }
-    if (tid == 0) s_glast = __builtin_amdgcn_exp2f(rg);
+    if (p < C) B.lg[p] = rlg;
   };
 
-  prefetch(0);
-  for (int lc = 0; lc < S.n_chunks; ++lc) {
-    const int t0 = lc * C;
-    const int Cr = min(C, S.T - t0);
-    stage();
-    lds_barrier();
-    if (lc + 1 < S.n_chunks) prefetch(lc + 1);
-    const float g_last = s_glast;
-
-    // ---- X = W S^T -> U = U~ - X (to LDS as U^T);  Y = Qg S^T starts O
-    f32x4 oacc[NXW];
+  // ---- owners: S^T rows 16 db + 4 g4 + e, column 16 wave + l16 of the slice, in
+  // accumulators; their f16 copy as operands over d (blocks 2 kk and 2 kk + 1)
+  float* Sg = S.state + (long)h * DV * DK + (long)(i0 + 16 * wave + l16) * DK;
+  f32x4 st[NDB];
+  f16x8 sh[NKD];
+  auto refresh_sh = [&]() {
 #pragma unroll
-    for (int j = 0; j < NXW; ++j) {
-      const int b = wave + NW * j;
-      oacc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (b >= NXB) continue;
-      const int rb = b / NCB, cb = b % NCB;
-      f32x4 x = {0.f, 0.f, 0.f, 0.f}, y = {0.f, 0.f, 0.f, 0.f};
-      // X in (rows, slice columns) layout for U; Y transposed (S Qg^T) so that the lane
-      // holds one row and 4 consecutive columns of O
-#pragma unroll
-      for (int kk = 0; kk < DK / 32; ++kk) {
-        const f16x8 sv = ld_f16x8(&Sh[16 * cb + l16][32 * kk + 8 * g4]);
-        x = mfma_f16(ld_f16x8(&Ws[16 * rb + l16][32 * kk + 8 * g4]), sv, x);
-        y = mfma_f16(sv, ld_f16x8(&Qs[16 * rb + l16][32 * kk + 8 * g4]), y);
-      }
-      f16x4 uh;
+    for (int kk = 0; kk < NKD; ++kk) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float u = Us[16 * rb + 4 * g4 + e][16 * cb + l16] - x[e];
-        big = fmaxf(big, fabsf(u));
-        uh[e] = (_Float16)u;
+        sh[kk][e] = (_Float16)st[2 * kk][e];
+        sh[kk][4 + e] = (_Float16)st[2 * kk + 1][e];
       }
-      *(f16x4*)&Ut[16 * cb + l16][16 * rb + 4 * g4] = uh;
-      oacc[j] = y;
+      big = fmaxf(big, fmaxf(max_abs4(st[2 * kk]), max_abs4(st[2 * kk + 1])));
     }
-    lds_barrier();
-
-    // ---- O += P U, written out; S^T <- 2^lg_last S^T + Kd^T U; refresh the f16 copy of S
+  };
+  if (owner) {
 #pragma unroll
-    for (int j = 0; j < NXW; ++j) {
-      const int b = wave + NW * j;
-      if (b >= NXB) continue;
-      const int rb = b / NCB, cb = b % NCB;
-      f32x4 o = oacc[j];
-      // (P U)^T = U^T P^T: row 16 rb + l16, columns 16 cb + 4 g4 .. + 3 of O
-#pragma unroll
-      for (int kk = 0; kk < (C + 31) / 32; ++kk) {
-        f16x8 av = zero_f16x8(), bv = zero_f16x8();
-        if (kpart) {
-          av = ld_f16x8(&Ut[16 * cb + l16][32 * kk + 8 * g4]);
-          bv = ld_f16x8(&Ph[16 * rb + l16][32 * kk + 8 * g4]);
-        }
-        o = mfma_f16(av, bv, o);
-      }
-      const int r = 16 * rb + l16;
-      if (r < Cr) *(f32x4*)(S.out + ((long)(t0 + r) * Hv + h) * DV + i0 + 16 * cb + 4 * g4) = o;
-    }
-#pragma unroll
-    for (int j = 0; j < NSW; ++j) {
-      const int b = wave + NW * j;
-      if (b >= NSB) continue;
-      const int db = b / NCB, cb = b % NCB;
-      f32x4 sacc = st[j] * g_last;
-#pragma unroll
-      for (int kk = 0; kk < (C + 31) / 32; ++kk) {
-        f16x8 av = zero_f16x8(), bv = zero_f16x8();
-        if (kpart) {
-          av = ld_f16x8(&Kdt[16 * db + l16][32 * kk + 8 * g4]);
-          bv = ld_f16x8(&Ut[16 * cb + l16][32 * kk + 8 * g4]);
-        }
-        sacc = mfma_f16(av, bv, sacc);
-      }
-      st[j] = sacc;
-      big = fmaxf(big, max_abs4(sacc));
-      // every read of Sh for this chunk happened before the barrier above
-      f16x4 hv = {(_Float16)sacc[0], (_Float16)sacc[1], (_Float16)sacc[2], (_Float16)sacc[3]};
-      *(f16x4*)&Sh[16 * cb + l16][16 * db + 4 * g4] = hv;
-    }
-    lds_barrier();   // staged tiles, U^T and S are free for the next chunk
+    for (int db = 0; db < NDB; ++db) st[db] = *(const f32x4*)(Sg + 16 * db + 4 * g4);
+    refresh_sh();
+  } else {
+    fetch(0);
+    put(stg[0]);
+    if (S.n_chunks > 1) fetch(1);
   }
+  lds_barrier();
+
+  for (int lc = 0; lc < S.n_chunks; ++lc) {
+    if (owner) {
+      const Stage& B = stg[lc & 1];
+      const int t0 = lc * C;
+      const int Cr = min(C, S.T - t0);
+      // Y^T = S Q^T (columns 16 wave + 4 g4 .., row 16 rb + l16), X = W S^T and
+      // U~ = T_v V (rows 16 rb + 4 g4 .., column 16 wave + l16)
+      f32x4 y[NRB], x[NRB], u[NRB];
 #pragma unroll
-  for (int j = 0; j < NSW; ++j) {
-    const int b = wave + NW * j;
-    if (b >= NSB) continue;
-    const int db = b / NCB, cb = b % NCB;
-    *(f32x4*)(Sg + (long)(i0 + 16 * cb + l16) * DK + 16 * db + 4 * g4) = st[j];
+      for (int rb = 0; rb < NRB; ++rb) y[rb] = x[rb] = u[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < NKD; ++kk)
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
+          y[rb] = mfma_f16(sh[kk], ld_f16x8(&B.Q[16 * rb + l16][32 * kk + 8 * g4]), y[rb]);
+          x[rb] = mfma_f16(ld_f16x8(&B.W[16 * rb + l16][32 * kk + 8 * g4]), sh[kk], x[rb]);
+        }
+#pragma unroll
+      for (int kk = 0; kk < NKS; ++kk)
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
+          u[rb] = mfma_f16(ld_f16x8(&B.Tv[16 * rb + l16][32 * kk + 8 * g4]),
+                           ld_f16x8(&B.Vt[16 * wave + l16][32 * kk + 8 * g4]), u[rb]);
+      // U = U~ - X and its decayed copy, as operands over the chunk index
+      const float lg_last = B.lg[C - 1];
+      f16x8 uh[NKS], ud[NKS];
+#pragma unroll
+      for (int kk = 0; kk < NKS; ++kk) uh[kk] = ud[kk] = zero_f16x8();
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float uu = u[rb][e] - x[rb][e];
+          const float dd = __builtin_amdgcn_exp2f(lg_last - B.lg[16 * rb + 4 * g4 + e]) * uu;
+          big = fmaxf(big, fabsf(uu));
+          uh[rb >> 1][4 * (rb & 1) + e] = (_Float16)uu;
+          ud[rb >> 1][4 * (rb & 1) + e] = (_Float16)dd;
+        }
+      // O^T = scale 2^lg Y^T + U^T P^T, written out
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb) {
+        y[rb] = y[rb] * (a.scale * __builtin_amdgcn_exp2f(B.lg[16 * rb + l16]));
+#pragma unroll
+        for (int kk = 0; kk < NKS; ++kk) y[rb] = mfma_f16(uh[kk], ld_f16x8(&B.P[16 * rb + l16][32 * kk + 8 * g4]), y[rb]);
+        const int r = 16 * rb + l16;
+        if (r < Cr) *(f32x4*)(S.out + ((long)(t0 + r) * Hv + h) * DV + i0 + 16 * wave + 4 * g4) = y[rb];
+      }
+      // S^T <- 2^lg_last S^T + K^T (decayed U)
+      const float g_last = __builtin_amdgcn_exp2f(lg_last);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) st[db] = st[db] * g_last;
+#pragma unroll
+      for (int kk = 0; kk < NKS; ++kk)
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+          st[db] = mfma_f16(ld_f16x8(&B.Kt[16 * db + l16][32 * kk + 8 * g4]), ud[kk], st[db]);
+      refresh_sh();
+    } else if (lc + 1 < S.n_chunks) {
+      put(stg[(lc + 1) & 1]);
+      if (lc + 2 < S.n_chunks) fetch(lc + 2);
+    }
+    lds_barrier();   // the next stage is complete; this one may be refilled
+  }
+  if (owner) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) *(f32x4*)(Sg + 16 * db + 4 * g4) = st[db];
   }
   if (big > kF16Max) status_raise(a.status, kFaultRange);
 }
@@ -596,15 +609,18 @@ static_assert(sizeof(DeltaArgs) <= kMaxKernargBytes, "delta launch record");
 
 template <int DK, int C>
 hipError_t prep_for(const DeltaArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((k_delta_prep<DK, C>), dim3(a.total_chunks * a.n_v_heads), dim3(kPrepThreads), 0, s, a);
+  const int blocks = (a.total_chunks * a.n_v_heads + 7) & ~7;   // xcd_remap wants a multiple of 8
+  hipLaunchKernelGGL((k_delta_prep<DK, C>), dim3(blocks), dim3(kPrepThreads), 0, s, a);
   return hipGetLastError();
 }
 
 template <int DK, int C>
 hipError_t chain_for(const DeltaArgs& a, hipStream_t s) {
-  const int blocks = (a.n_seq * a.n_v_heads * a.n_slices + 7) & ~7;   // XCD remap needs a multiple of 8
+  const int blocks = (a.n_seq * a.n_v_heads * a.n_slices + 7) & ~7;   // xcd_remap wants a multiple of 8
   const int dvs = DK / a.n_slices;
-  if (dvs == 32)
+  if (dvs == 16)
+    hipLaunchKernelGGL((k_delta_chain<DK, C, 16>), dim3(blocks), dim3(kChainThreads), 0, s, a);
+  else if (dvs == 32)
     hipLaunchKernelGGL((k_delta_chain<DK, C, 32>), dim3(blocks), dim3(kChainThreads), 0, s, a);
   else if (dvs == 64)
     hipLaunchKernelGGL((k_delta_chain<DK, C, 64>), dim3(blocks), dim3(kChainThreads), 0, s, a);
