@@ -79,6 +79,14 @@ __device__ __forceinline__ int find_seq_by_chunk(const DeltaArgs& a, int c) {
 
 constexpr int cmax(size_t x, size_t y) { return (int)(x > y ? x : y); }
 
+// Lower-block-triangular C x C fp32 matrix (M, then T): 16x16 blocks (bi, bj), bj <= bi,
+// stored one after another with rows of 20 floats
+constexpr int kTriPitch = 20;
+__device__ __forceinline__ int tri(int r, int c) {
+  const int bi = r >> 4, bj = c >> 4;
+  return ((bi * (bi + 1) / 2 + bj) * 16 + (r & 15)) * kTriPitch + (c & 15);
+}
+
 // ------------------------------------------------------------------ prep
 constexpr int kPrepThreads = 512;   // 8 waves
 template <int DK, int C>
@@ -88,22 +96,26 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   constexpr int DV = DK;
   constexpr int NB = C / 16;     // 16-row blocks of the chunk
   constexpr int KP = DK + 8;     // pitch of [C][DK] bf16 tiles
-  constexpr int CP = C + 4;      // pitch of [C][C] fp32 tiles
   constexpr int CT = C + 8;      // pitch of f16 tiles with the chunk index contiguous
   constexpr int CC = C < 32 ? 32 : C;   // row length of P in the workspace (padded)
-  // Q (phases 0-1), M (2-4) and k^T in f16 (5-6) share a region; barriers separate
-  // the last reads of each from the first writes of the next
-  constexpr int R2 = cmax(cmax(sizeof(bf16_t) * C * KP, sizeof(float) * C * CP), sizeof(_Float16) * DK * CT);
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[C][KP];
-  __shared__ __attribute__((aligned(16))) char r2[R2];
-  __shared__ __attribute__((aligned(16))) float Tf[C][CP];
-  __shared__ __attribute__((aligned(16))) _Float16 Twh[C][CT];   // T diag(beta 2^lg) in f16
+  constexpr int TRI = NB * (NB + 1) / 2 * 16 * kTriPitch;   // floats of a lower-block-triangular matrix
+  // Three regions whose arrays have disjoint lifetimes (barriers separate the last reads
+  // of one from the first writes of the next), 48 KB at C = 64, d = 128, so that three
+  // workgroups fit a CU: k rows (phases 0-1), M (2-4), k^T in f16 (5-6); q rows (0-1),
+  // T (3-5); T diag(beta 2^lg) in f16 (5-6).
+  constexpr int RA = cmax(cmax(sizeof(bf16_t) * C * KP, sizeof(float) * TRI), sizeof(_Float16) * DK * CT);
+  constexpr int RB = cmax(sizeof(bf16_t) * C * KP, sizeof(float) * TRI);
+  __shared__ __attribute__((aligned(16))) char ra[RA];
+  __shared__ __attribute__((aligned(16))) char rb_[RB];
+  __shared__ __attribute__((aligned(16))) _Float16 Twh[C][CT];
   __shared__ __attribute__((aligned(16))) float Xs[3][16][20];
   __shared__ __attribute__((aligned(16))) float lg[C];
   __shared__ __attribute__((aligned(16))) float bt[C];
-  auto& Qs = *reinterpret_cast<bf16_t(*)[C][KP]>(r2);
-  auto& Mf = *reinterpret_cast<float(*)[C][CP]>(r2);
-  auto& Kt = *reinterpret_cast<_Float16(*)[DK][CT]>(r2);
+  auto& Ks = *reinterpret_cast<bf16_t(*)[C][KP]>(ra);
+  float* Mt = reinterpret_cast<float*>(ra);
+  auto& Kt = *reinterpret_cast<_Float16(*)[DK][CT]>(ra);
+  auto& Qs = *reinterpret_cast<bf16_t(*)[C][KP]>(rb_);
+  float* Tt = reinterpret_cast<float*>(rb_);
 
   const int Hk = a.n_k_heads, Hv = a.n_v_heads;
   // work item (chunk, value head); consecutive items, and so the value heads that share
@@ -212,7 +224,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         mv[e] = i0 + e < r ? br * __builtin_amdgcn_exp2f(fminf(lr - li4[e], 0.f)) * acc[j][e] : 0.f;
-      *(f32x4*)&Mf[r][i0] = mv;
+      *(f32x4*)&Mt[tri(r, i0)] = mv;
     }
   }
   // zero the upper blocks of P and the padding of its rows
@@ -223,19 +235,32 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   if (tid < C) a.ws_lg[slot * C + tid] = lg[tid];
   lds_barrier();
 
-  // ---- phase 3: diagonal 16x16 blocks of T = (I + M)^-1, one lane per column
+  // ---- phase 3: diagonal 16x16 blocks of T = (I + M)^-1, one lane per column: forward
+  // substitution, with the next row of M read while the current one is summed
   if (wave == 0 && g4 < NB) {
     const int b = g4, cc = l16;
+    const float* Mrow = &Mt[tri(16 * b, 16 * b)];
     float x[16];
+    f32x4 cur[4], nxt[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) cur[q] = *(const f32x4*)(Mrow + 4 * q);
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) {
-      float s = 0.f;
+      if (rr + 1 < 16) {
 #pragma unroll
-      for (int i = 0; i < rr; ++i) s += Mf[16 * b + rr][16 * b + i] * x[i];
-      x[rr] = rr < cc ? 0.f : (rr == cc ? 1.f : -s);
+        for (int q = 0; q < 4; ++q)
+          if (4 * q < rr + 1) nxt[q] = *(const f32x4*)(Mrow + (rr + 1) * kTriPitch + 4 * q);
+      }
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < rr; ++i) acc[i & 3] += cur[i >> 2][i & 3] * x[i];
+      const float sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+      x[rr] = rr < cc ? 0.f : (rr == cc ? 1.f : -sum);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cur[q] = nxt[q];
     }
 #pragma unroll
-    for (int rr = 0; rr < 16; ++rr) Tf[16 * b + rr][16 * b + cc] = x[rr];
+    for (int rr = 0; rr < 16; ++rr) Tt[tri(16 * b + rr, 16 * b + cc)] = x[rr];
   }
   lds_barrier();
 
@@ -252,24 +277,24 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
       for (int m = j; m < i; ++m)
 #pragma unroll
         for (int s = 0; s < 4; ++s)
-          x = __builtin_amdgcn_mfma_f32_16x16x4f32(Mf[16 * i + l16][16 * m + 4 * s + g4],
-                                                   Tf[16 * m + 4 * s + g4][16 * j + l16], x, 0, 0, 0);
+          x = __builtin_amdgcn_mfma_f32_16x16x4f32(Mt[tri(16 * i + l16, 16 * m + 4 * s + g4)],
+                                                   Tt[tri(16 * m + 4 * s + g4, 16 * j + l16)], x, 0, 0, 0);
 #pragma unroll
       for (int e = 0; e < 4; ++e) Xs[wave][4 * g4 + e][l16] = x[e];
       __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));   // this wave's LDS writes are done
       f32x4 y = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < 4; ++s)
-        y = __builtin_amdgcn_mfma_f32_16x16x4f32(Tf[16 * i + l16][16 * i + 4 * s + g4], Xs[wave][4 * s + g4][l16], y,
-                                                 0, 0, 0);
+        y = __builtin_amdgcn_mfma_f32_16x16x4f32(Tt[tri(16 * i + l16, 16 * i + 4 * s + g4)], Xs[wave][4 * s + g4][l16],
+                                                 y, 0, 0, 0);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) Tf[16 * i + 4 * g4 + e][16 * j + l16] = -y[e];
+      for (int e = 0; e < 4; ++e) Tt[tri(16 * i + 4 * g4 + e, 16 * j + l16)] = -y[e];
     }
     lds_barrier();
   }
 
   // ---- phase 5: T diag(beta 2^lg) (f16, LDS) and T_v = T diag(beta) (f16, workspace),
-  // zero above the diagonal blocks (whose entries of Tf were never written); k^T in f16
+  // zero above the diagonal blocks (whose entries of T were never written); k^T in f16
   _Float16* Tvg = a.ws_tv + slot * C * C;
   for (int e = tid; e < C * C / 4; e += NT) {
     const int r = e / (C / 4), i0 = (e - r * (C / 4)) * 4;
@@ -277,7 +302,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int i = i0 + q;
-      const float x = (i >> 4) <= (r >> 4) ? Tf[r][i] : 0.f;
+      const float x = (i >> 4) <= (r >> 4) ? Tt[tri(r, (i >> 4) <= (r >> 4) ? i : 0)] : 0.f;
       const float xw = x * (bt[i] * __builtin_amdgcn_exp2f(lg[i])), xv = x * bt[i];
       big = fmaxf(big, fmaxf(fabsf(xw), fabsf(xv)));
       hw[q] = (_Float16)xw;
@@ -286,9 +311,12 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
     *(f16x4*)&Twh[r][i0] = hw;
     *(f16x4*)&Tvg[r * C + i0] = hv;
   }
+  // k^T in f16 over the dead M, from the k rows read again (from L2: phase 0 read them)
   for (int e = tid; e < (C / 2) * (DK / 8); e += NT) {
     const int s2 = (e % (C / 2)) * 2, d0 = (e / (C / 2)) * 8;
-    const u32x4 k0 = *(const u32x4*)&Ks[s2][d0], k1 = *(const u32x4*)&Ks[s2 + 1][d0];
+    const u32x4 z4 = {0, 0, 0, 0};
+    const u32x4 k0 = s2 < Cr ? *(const u32x4*)(S.k + ((long)(t0 + s2) * Hk + kh) * DK + d0) : z4;
+    const u32x4 k1 = s2 + 1 < Cr ? *(const u32x4*)(S.k + ((long)(t0 + s2 + 1) * Hk + kh) * DK + d0) : z4;
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
       const uint32_t b0 = (d & 1) ? (k0[d >> 1] & 0xFFFF0000u) : (k0[d >> 1] << 16);
