@@ -226,6 +226,62 @@ def round_updates(tu, ctxs, own, layers, rounds, attn_p, delta_p, post=None, arm
                          place_runs=None if place is None else place(R)) for R in rounds]
 
 
+def layers_of_kind(layers, rounds, kind):
+    """The workload restricted to its layers of one kind (each round's inputs likewise)."""
+    keep = [i for i, L in enumerate(layers) if L["kind"] == kind]
+    rounds_k = [dict(R, inputs=[R["inputs"][i] for i in keep]) for R in rounds]
+    return [layers[i] for i in keep], rounds_k
+
+
+def paths_alone_row(tu, cfg, m, attn_p, delta_p, dev, W, K):
+    """The update with only its delta layers, and with only its attention layers, on
+    pristine copies of the same workload: in the full update the two run side by side and
+    take turns on whole CUs, so the delta kernels' own durations there include waiting for
+    CUs the attention workgroups hold."""
+    import torch
+    chars, rounds, layers = m["chars"], m["rounds"], m["layers"]
+    kinds = cfg.layer_kinds()
+    row = {}
+    for kind in ("delta", "attn"):
+        if not kinds.count(kind):
+            continue
+        lk, rk = layers_of_kind(layers, rounds, kind)
+        copies = [make_copy(tu, chars, lk, dev) for _ in range(W + 2 * K)]
+        ups = [round_updates(tu, ctxs, own, lk, rk, attn_p, delta_p) for (ctxs, own) in copies]
+        ws = torch.empty(max(1, max(u.workspace_size() for u in ups[0])), dtype=torch.uint8, device=dev)
+        for i in range(W):
+            run_step(ups[i], ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(W, W + K):
+            run_step(ups[i], ws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / K
+        tu.profile_enable(True)
+        for i in range(W + K, W + 2 * K):
+            run_step(ups[i], ws)
+        prof = tu.profile_collect()
+        tu.profile_enable(False)
+        kern = {n: round(t / K, 5) for n, (c, t) in prof.items()}
+        if kind == "delta":
+            b = delta_bytes(cfg, rounds) * kinds.count("delta")
+            ach = b / (ms / 1e3) / 1e9
+            row["delta"] = {"layers": kinds.count("delta"), "update_ms": round(ms, 5), "kernels_ms": kern,
+                            "bytes": b, "bound": "hbm", "achieved": round(ach, 1), "unit": "GB/s",
+                            "peak": HBM_PEAK_GBS, "frac": round(ach / HBM_PEAK_GBS, 4)}
+        else:
+            f = attention_flops(cfg, rounds) * kinds.count("attn")
+            att = kern.get("attention")
+            row["attention_path"] = {"layers": kinds.count("attn"), "update_ms": round(ms, 5), "kernels_ms": kern,
+                                     "attention_tflops": round(f / (att / 1e3) / 1e12, 1) if att else None,
+                                     "attention_frac": round(f / (att / 1e3) / 1e12 / MFMA16_PEAK_TFLOPS, 4)
+                                     if att else None}
+        del copies, ups, ws
+    return row
+
+
 def slot_runs(R):
     """Positions of a slot-placed tail: the removed records' slots in order, then a free
     range 10,000 positions past the cursor for the tokens that do not fit."""
@@ -1159,6 +1215,10 @@ def headline_extras(tu, args, cfg, m, attn_p, delta_p, dev):
             "bytes": 2 * 2 * moved * row_b * kinds.count("attn"), "bound": "hbm"}
         print(f"[bench] delimiter removal: {json.dumps(extra['delimiter_removal'])}", file=sys.stderr, flush=True)
         del copies3, ups3, ws3
+
+    # ---- the delta layers alone and the attention path alone
+    extra["paths_alone"] = paths_alone_row(tu, cfg, m, attn_p, delta_p, dev, 1, min(K, 5))
+    print(f"[bench] paths alone: {json.dumps(extra['paths_alone'])}", file=sys.stderr, flush=True)
 
     # ---- the placement arms the paper compares (Section 5.2): slot-preserving (rotated at
     # the removed records' slots) and tail-and-relocate (computed at the true tail, stored

@@ -43,7 +43,6 @@ namespace tu {
 
 namespace {
 
-typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2;
 
 __device__ __forceinline__ f16x8 ld_f16x8(const _Float16* p) { return __builtin_bit_cast(f16x8, *(const u32x4*)p); }
 __device__ __forceinline__ bf16x8 ld_bf16x8(const bf16_t* p) { return __builtin_bit_cast(bf16x8, *(const u32x4*)p); }
