@@ -129,12 +129,13 @@ __device__ void rope_token(const RopeArgs& a, int tok) {
 // V^T pack: one workgroup per (context, kv head, 64-key tile) of the tiles to refresh:
 // V rows -> f16 V^T tile in the attention kernel's LDS layout: D rows (dims) of kVtRow
 // halves, each 64 keys in key_slot order within 16-key groups followed by 8 halves of
-// padding (left unwritten; the attention kernel never reads it). Keys past the cache's
-// data are zero. Thread (c, m) builds chunk c (8 keys) of the 8 rows 8m .. 8m + 7: it
-// loads those 8 keys' dims 8m .. 8m + 7 (16 bytes each), transposes the 8 x 8 block in
-// registers and writes 8 chunks. c is the fastest-moving index: a wave's load reads 128
-// contiguous bytes of each of 8 rows, and its store writes the 8 chunks of each of 8 V^T
-// rows contiguously. bf16 values of magnitude 2^16 or more (or not finite) have no f16
+// padding (zeros; the attention kernel never reads them). Keys past the cache's data are
+// zero. Thread (c, m) builds chunk c (8 keys) of the 8 rows 8m .. 8m + 7: it loads those
+// 8 keys' dims 8m .. 8m + 7 (16 bytes each), transposes the 8 x 8 block in registers and
+// writes 8 chunks; the threads of chunk 7 also write the rows' pads, so every cache line
+// of the tile is written whole (lines written in part cost a read from HBM first). c is
+// the fastest-moving index: a wave's load reads 128 contiguous bytes of each of 8 rows,
+// and its store writes the 8 chunks of each of 8 V^T rows contiguously. bf16 values of magnitude 2^16 or more (or not finite) have no f16
 // counterpart: the tile then holds infinities and the call's status gets kFaultRange.
 template <int D>
 __device__ void vt_pack_tile(const RopeArgs& r, const PackArgs& pa, int item) {
@@ -177,6 +178,7 @@ __device__ void vt_pack_tile(const RopeArgs& r, const PackArgs& pa, int item) {
         h[j] = (_Float16)bf16_to_f32((d & 1) ? (word >> 16) : (word & 0xFFFFu));
       }
       *(f16x8*)(dst + ((8 * m + d) * CPR + c) * 8) = h;
+      if (c == 7) *(u32x4*)(dst + ((8 * m + d) * CPR + 8) * 8) = u32x4{0, 0, 0, 0};
     }
   }
   if (big >= 0x4780u) status_raise(pa.status, kFaultRange);   // 0x4780: bf16 bits of 2^16
