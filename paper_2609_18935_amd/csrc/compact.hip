@@ -64,6 +64,17 @@ __device__ __forceinline__ int removed_before(const int32_t (*sp)[2], int span_b
   return removed;
 }
 
+// Old row that destination row j of a context receives: j plus the lengths of the
+// removed spans whose start, counted in kept rows, is at or before j.
+__device__ __forceinline__ int source_row(const int32_t (*sp)[2], const GatherSeq& S, int j) {
+  int src = j;
+  for (int q = 0; q < S.n_spans; ++q) {
+    if (sp[S.span_begin + q][0] > j) break;
+    src += sp[S.span_begin + q][1];
+  }
+  return src;
+}
+
 // One scan workgroup: kScanRows consecutive old rows of one context.
 __device__ void keep_scan(const CompactArgs& a, const ScanSeq& s, int chunk) {
   __shared__ int32_t rng[kMaxRangesPerLaunch][2];
@@ -158,15 +169,7 @@ __device__ bool gather_items(const CompactArgs& a) {
     const int row0 = S.row_begin + stripe * R;
     const int rows = min(R, S.n_keep - row0);
     // source row of each destination row of the stripe
-    for (int t = tid; t < rows; t += kThreads) {
-      const int j = row0 + t;
-      int src = j;
-      for (int q = 0; q < S.n_spans; ++q) {
-        if (sp[S.span_begin + q][0] > j) break;
-        src += sp[S.span_begin + q][1];
-      }
-      s_src[t] = src;
-    }
+    for (int t = tid; t < rows; t += kThreads) s_src[t] = source_row(sp, S, row0 + t);
     __syncthreads();
     const int n_vec = rows * vpr;
     u32x4 data[kGatherVec];
@@ -193,11 +196,18 @@ __device__ bool gather_items(const CompactArgs& a) {
       if (lane == 0)
         __hip_atomic_fetch_add(a.flags + kFlagStride * (S.flag_begin + stripe), 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
-      // the wave polls up to 64 earlier stripes at once, nearest first
+      // the wave polls up to 64 earlier stripes at once, nearest first; a lane skips a
+      // stripe whose source rows (an increasing function of its destination rows, so
+      // within [source of its first row, source of its last row]) miss this stripe's rows
       const int lo = max(0, stripe - S.window);
       for (int w0 = stripe - 1; w0 >= lo; w0 -= 64) {
         const int w = w0 - lane;
         bool done = w < lo;
+        if (!done) {
+          const int first = S.row_begin + w * R;
+          const int last = min(first + R, S.n_keep) - 1;
+          done = source_row(sp, S, last) < row0 || source_row(sp, S, first) >= row0 + rows;
+        }
         long spins = 0;
         for (;;) {
           if (!done)
