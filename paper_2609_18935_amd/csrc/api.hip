@@ -499,6 +499,7 @@ inline int64_t vt_head_tiles(int64_t rows) { return (rows + kAttnKeys - 1) / kAt
 // kMaxAutoSplits (a decode-like tail of one token over 32K rows fills the chip with 128
 // splits of its two KV heads).
 constexpr int kMaxAutoSplits = 128;
+constexpr int kGateWaves = 4;   // attention launches this many CU-waves long wait for the delta layers
 
 int choose_splits(const tu_attn_params* p, int64_t L_keep, int64_t T, int64_t base_items_total, bool uniform) {
   if (p->kv_splits > 0) return p->kv_splits;
@@ -734,9 +735,14 @@ int side_stream(SideStream** out) {
   return TU_OK;
 }
 
-int run_attention(const std::vector<AttnLaunch>& ls, int D, hipStream_t st) {
+// `gate`, if given, is an event the first attention kernel waits for (after its stage).
+int run_attention(const std::vector<AttnLaunch>& ls, int D, hipStream_t st, hipEvent_t gate = nullptr) {
   for (const auto& L : ls) {
     if (int e = hip_check(timed("rope_vt_pack", st, [&] { return launch_stage(L.rope, L.rope_tokens, L.pack, D, st); }), "RoPE/V^T pack launch")) return e;
+    if (gate) {
+      if (int e = hip_check(hipStreamWaitEvent(st, gate, 0), "attention gate")) return e;
+      gate = nullptr;
+    }
     if (int e = hip_check(timed("attention", st, [&] { return launch_attention(L.attn, L.order, D, st); }), "attention launch")) return e;
     if (L.merge_rows > 0)
       if (int e = hip_check(timed("attention_merge", st, [&] { return launch_attention_merge(L.merge, L.merge_rows, D, st); }), "merge launch")) return e;
@@ -1824,6 +1830,8 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
       std::vector<DeltaArgs> ls;
       plan_delta(&u->delta, items, ws_delta, status, &ls, &b);
       if (int e = run_delta(ls, &u->delta, sd)) return e;
+      if (side)
+        if (int e = hip_check(hipEventRecord(side->join, side->stream), "join event")) return e;
     }
     // a2-a3: keep-scan and in-place row move over every attention layer of every context
     if (sp.n_attn) {
@@ -1833,12 +1841,22 @@ int update_layer_stack(const tu_update* u, void* workspace, size_t workspace_byt
       if (int e = run_compaction(cp, st)) return e;
     }
     // a4-a5: the attention layers are independent of each other once the caches are
-    // compacted; the layers too small to fill the chip share one set of launches
+    // compacted; the layers too small to fill the chip share one set of launches. An
+    // attention workgroup holds a whole CU, and so does a delta-chain workgroup: an
+    // attention launch of kGateWaves or more full waves leaves no CU idle for the delta
+    // layers to use, so it waits for them (they run beside the compaction and the
+    // stage) instead of sharing CUs with them, which would only lengthen it by as much.
+    // Shorter launches leave CUs idle at their ragged end and keep the overlap.
+    hipEvent_t gate = side ? side->join : nullptr;
     for (auto& items : stack_attn_groups(u, sp)) {
       size_t b = 0;
       std::vector<AttnLaunch> ls;
       plan_attention(&u->attn, items, ws_attn, status, &ls, &b);
-      if (int e = run_attention(ls, u->attn.head_dim, st)) return e;
+      int64_t wgs = 0;
+      for (const auto& L : ls) wgs += L.order.blocks > 0 ? L.order.blocks : L.attn.total_items;
+      const bool wait = gate && wgs >= (int64_t)kGateWaves * kCus;
+      if (int e = run_attention(ls, u->attn.head_dim, st, wait ? gate : nullptr)) return e;
+      if (wait) gate = nullptr;
     }
     // tail-and-relocate: the stored keys of the tail turn from their computed
     // positions to the placed ones (values and recurrent state stay as computed)
