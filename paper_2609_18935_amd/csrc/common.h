@@ -292,6 +292,8 @@ struct DeltaArgs {
   _Float16* ws_tv;       // [chunks][Hv][C][C]   T diag(beta)
   _Float16* ws_p;        // [chunks][Hv][C][max(C, 32)]  scale lower(G .* Q K^T), operand order
   float* ws_lg;          // [chunks][Hv][C]     cumulative log2 decay
+  _Float16* ws_q;        // [chunks][Hk][C][dk]  q in f16, d in operand order
+  _Float16* ws_kt;       // [chunks][Hk][dk][max(C, 32)]  k^T in f16, s in operand order
 };
 
 // Key relocation: one workgroup per moved row; every key buffer of the launch gets the

@@ -226,6 +226,28 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
       *(f32x4*)&Mt[tri(r, i0)] = mv;
     }
   }
+  // q in f16 for the chain, d in its operand order, written by the first value head of
+  // each key head: output vector v8 of a row holds the natural d0 .. d0 + 3 and
+  // d0 + 16 .. d0 + 19 of its group of 32 (the inverse of perm32)
+  const int G = Hv / Hk;
+  if (h % G == 0) {
+    _Float16* Qg = a.ws_q + ((long)c * Hk + kh) * C * DK;
+    for (int e = tid; e < C * (DK / 8); e += NT) {
+      const int r = e / (DK / 8), v8 = e - r * (DK / 8);
+      const int d0 = 32 * (v8 >> 2) + 4 * (v8 & 3);
+      const uint2 w[2] = {*(const uint2*)&Qs[r][d0], *(const uint2*)&Qs[r][d0 + 16]};
+      f16x8 hq;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t wq = w[q >> 1][q & 1];
+        const float x0 = __uint_as_float(wq << 16), x1 = __uint_as_float(wq & 0xFFFF0000u);
+        big = fmaxf(big, fmaxf(fabsf(x0), fabsf(x1)));
+        hq[2 * q] = (_Float16)x0;
+        hq[2 * q + 1] = (_Float16)x1;
+      }
+      *(f16x8*)&Qg[r * DK + 8 * v8] = hq;
+    }
+  }
   // zero the upper blocks of P and the padding of its rows
   for (int e = tid; e < C * CC / 4; e += NT) {
     const int r = e / (CC / 4), i = (e - r * (CC / 4)) * 4;
@@ -329,7 +351,19 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   lds_barrier();
 
   // ---- phase 6: W = T diag(beta 2^lg) K on MFMA, to the workspace with d in the
-  // chain's operand order
+  // chain's operand order; k^T (first value head of each key head) with s in that order,
+  // its chunk index padded with zeros to a whole MFMA step
+  if (h % G == 0) {
+    _Float16* Kg = a.ws_kt + ((long)c * Hk + kh) * DK * CC;
+    for (int e = tid; e < DK * (CC / 8); e += NT) {
+      const int d = e / (CC / 8), v8 = e - d * (CC / 8);
+      const int s0 = 32 * (v8 >> 2) + 4 * (v8 & 3);
+      const uint2 z2 = {0, 0};
+      const uint2 lo = s0 < C ? *(const uint2*)&Kt[d][s0] : z2;
+      const uint2 hi = s0 + 16 < C ? *(const uint2*)&Kt[d][s0 + 16] : z2;
+      *(u32x4*)&Kg[d * CC + 8 * v8] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+    }
+  }
   _Float16* Wg = a.ws_w + slot * C * DK;
   constexpr int NOB = NB * (DK / 16);
   for (int idx = wave; idx < NOB; idx += NW) {
@@ -386,12 +420,12 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
   constexpr int NDB = DK / 16;                  // 16-row blocks of S^T
   constexpr int NKD = DK / 32;                  // MFMA steps over d
   constexpr int NKS = CC / 32;                  // MFMA steps over the chunk index
-  // producer work per chunk: 16-byte vectors of q, W, P, T_v; 2-row x 8-column items of
-  // k and of the v slice
-  constexpr int VQ = C * DK / 8, VW = C * DK / 8, VP = C * CC / 8, VT = C * C / 8;
-  constexpr int NKI = (C / 2) * (DK / 8), NVI = (C / 2) * (DVS / 8);
+  // producer work per chunk: 16-byte vectors of q, k^T, W, P, T_v (copied as the prep
+  // wrote them); 2-row x 8-column items of the v slice (converted and transposed)
+  constexpr int VQ = C * DK / 8, VK = DK * CC / 8, VW = C * DK / 8, VP = C * CC / 8, VT = C * C / 8;
+  constexpr int NVI = (C / 2) * (DVS / 8);
   constexpr int RQ = (VQ + NP - 1) / NP, RW = (VW + NP - 1) / NP, RP = (VP + NP - 1) / NP;
-  constexpr int RT = (VT + NP - 1) / NP, RK = (NKI + NP - 1) / NP, RV = (NVI + NP - 1) / NP;
+  constexpr int RT = (VT + NP - 1) / NP, RK = (VK + NP - 1) / NP, RV = (NVI + NP - 1) / NP;
   __shared__ __attribute__((aligned(16))) Stage stg[2];
 
   // work item: (context, key head, value head of the group, slice), ordered so that the
@@ -413,39 +447,32 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
   const int p = tid - 64 * NO;                  // producer thread index
   float big = 0.f;   // largest magnitude this thread rounds to f16
 
-  // chunk-index padding of the stages (C = 16 only) stays zero for the whole kernel
+  // chunk-index padding of T_v and the v slice (C = 16 only) stays zero for the whole
+  // kernel (k^T comes padded from the workspace)
   if (C < 32) {
-    for (int e = tid; e < 2 * (DK + C + DVS) * 16; e += NT) {
-      const int b = e / ((DK + C + DVS) * 16), rest = e - b * (DK + C + DVS) * 16;
+    for (int e = tid; e < 2 * (C + DVS) * 16; e += NT) {
+      const int b = e / ((C + DVS) * 16), rest = e - b * (C + DVS) * 16;
       const int row = rest / 16, x = C + (rest % 16);
-      if (row < DK) stg[b].Kt[row][perm32(x)] = (_Float16)0.f;
-      else if (row < DK + C) stg[b].Tv[row - DK][x] = (_Float16)0.f;
-      else stg[b].Vt[row - DK - C][x] = (_Float16)0.f;
+      if (row < C) stg[b].Tv[row][x] = (_Float16)0.f;
+      else stg[b].Vt[row - C][x] = (_Float16)0.f;
     }
   }
 
   // ---- producers: registers of one chunk, then their conversion into a stage
   const u32x4 z4 = {0, 0, 0, 0};
-  u32x4 rq[RQ], rw[RW], rp[RP], rt[RT], rk[RK][2], rv[RV][2];
+  u32x4 rq[RQ], rw[RW], rp[RP], rt[RT], rk[RK], rv[RV][2];
   float rlg = 0.f;
   auto fetch = [&](int lc) {
     const int t0 = lc * C;
     const int Cr = min(C, S.T - t0);
     const long slot = (long)(S.chunk_begin + lc) * Hv + h;
+    const long slot_k = (long)(S.chunk_begin + lc) * Hk + kh;
+    const u32x4* Q4 = (const u32x4*)(a.ws_q + slot_k * C * DK);
+    const u32x4* K4 = (const u32x4*)(a.ws_kt + slot_k * DK * CC);
 #pragma unroll
-    for (int j = 0; j < RQ; ++j) {
-      const int e = p + NP * j;
-      const int r = e / (DK / 8), c8 = e - r * (DK / 8);
-      rq[j] = (e < VQ && r < Cr) ? *(const u32x4*)(S.q + ((long)(t0 + r) * Hk + kh) * DK + 8 * c8) : z4;
-    }
+    for (int j = 0; j < RQ; ++j) rq[j] = p + NP * j < VQ ? Q4[p + NP * j] : z4;
 #pragma unroll
-    for (int j = 0; j < RK; ++j) {
-      const int e = p + NP * j;
-      const int s2 = (e % (C / 2)) * 2, d0 = (e / (C / 2)) * 8;
-#pragma unroll
-      for (int q = 0; q < 2; ++q)
-        rk[j][q] = (e < NKI && s2 + q < Cr) ? *(const u32x4*)(S.k + ((long)(t0 + s2 + q) * Hk + kh) * DK + d0) : z4;
-    }
+    for (int j = 0; j < RK; ++j) rk[j] = p + NP * j < VK ? K4[p + NP * j] : z4;
 #pragma unroll
     for (int j = 0; j < RV; ++j) {
       const int e = p + NP * j;
@@ -469,38 +496,12 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
 #pragma unroll
     for (int j = 0; j < RQ; ++j) {
       const int e = p + NP * j;
-      if (e < VQ) {
-        const int r = e / (DK / 8), c8 = e - r * (DK / 8);
-        f16x4 lo, hi;
-#pragma unroll
-        for (int w = 0; w < 2; ++w) {
-          const float x0 = bf16_lo(rq[j][w]), x1 = bf16_hi(rq[j][w]);
-          const float y0 = bf16_lo(rq[j][w + 2]), y1 = bf16_hi(rq[j][w + 2]);
-          big = fmaxf(big, fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(y0), fabsf(y1))));
-          lo[2 * w] = (_Float16)x0;
-          lo[2 * w + 1] = (_Float16)x1;
-          hi[2 * w] = (_Float16)y0;
-          hi[2 * w + 1] = (_Float16)y1;
-        }
-        *(f16x4*)&B.Q[r][perm32(8 * c8)] = lo;
-        *(f16x4*)&B.Q[r][perm32(8 * c8 + 4)] = hi;
-      }
+      if (e < VQ) *(u32x4*)&B.Q[e / (DK / 8)][8 * (e % (DK / 8))] = rq[j];
     }
 #pragma unroll
     for (int j = 0; j < RK; ++j) {
       const int e = p + NP * j;
-      if (e < NKI) {
-        const int s2 = (e % (C / 2)) * 2, d0 = (e / (C / 2)) * 8;
-        const int ps = perm32(s2);
-#pragma unroll
-        for (int d = 0; d < 8; ++d) {
-          const float x0 = (d & 1) ? bf16_hi(rk[j][0][d >> 1]) : bf16_lo(rk[j][0][d >> 1]);
-          const float x1 = (d & 1) ? bf16_hi(rk[j][1][d >> 1]) : bf16_lo(rk[j][1][d >> 1]);
-          big = fmaxf(big, fmaxf(fabsf(x0), fabsf(x1)));
-          const f16x2 hx = {(_Float16)x0, (_Float16)x1};
-          *(f16x2*)&B.Kt[d0 + d][ps] = hx;
-        }
-      }
+      if (e < VK) *(u32x4*)&B.Kt[e / (CC / 8)][8 * (e % (CC / 8))] = rk[j];
     }
 #pragma unroll
     for (int j = 0; j < RV; ++j) {
