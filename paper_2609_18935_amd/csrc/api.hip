@@ -805,7 +805,7 @@ int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, vo
     a.ws_w = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * DK));
     a.ws_tv = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * C));
     a.ws_p = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * Hv * C * std::max(C, 32)));
-    a.ws_lg = static_cast<float*>(ar.take(sizeof(float) * (size_t)chunks * Hv * C));
+    a.ws_dec = static_cast<float*>(ar.take(sizeof(float) * (size_t)chunks * Hv * 2 * C));
     a.ws_q = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * p->n_k_heads * C * DK));
     a.ws_kt = static_cast<_Float16*>(ar.take(sizeof(_Float16) * (size_t)chunks * p->n_k_heads * DK * std::max(C, 32)));
     max_used = std::max(max_used, ar.used);

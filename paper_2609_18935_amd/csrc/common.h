@@ -291,7 +291,7 @@ struct DeltaArgs {
   _Float16* ws_w;        // [chunks][Hv][C][dk]  W = T diag(beta 2^lg) K, d in operand order
   _Float16* ws_tv;       // [chunks][Hv][C][C]   T diag(beta)
   _Float16* ws_p;        // [chunks][Hv][C][max(C, 32)]  scale lower(G .* Q K^T), operand order
-  float* ws_lg;          // [chunks][Hv][C]     cumulative log2 decay
+  float* ws_dec;         // [chunks][Hv][2][C]  decay factors 2^(lg_last - lg_s) and 2^lg_s
   _Float16* ws_q;        // [chunks][Hk][C][dk]  q in f16, d in operand order
   _Float16* ws_kt;       // [chunks][Hk][dk][max(C, 32)]  k^T in f16, s in operand order
 };

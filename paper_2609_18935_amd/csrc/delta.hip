@@ -21,8 +21,9 @@
 //   v_mfma_f32_16x16x32_bf16 (exact bf16 products, fp32 sums); T by blocked forward
 //   substitution in fp32 (16x16 diagonal blocks by one lane per column, then
 //   off-diagonal blocks level by level); W on v_mfma_f32_16x16x32_f16. Writes W, T_v
-//   and P (f16) and lg (fp32) to the workspace, W and P with their contracted index
-//   in the chain's operand order (below).
+//   and P (f16) and the decay factors 2^(lg_last - lg) and 2^lg (fp32) to the
+//   workspace, and, once per key head, q and k^T in f16; W, P, q and k^T with their
+//   contracted index in the chain's operand order (below).
 // k_delta_chain: one workgroup per (context, value head, slice of DVS rows of S); rows
 //   of S evolve independently (row i only needs U[:, i]). Each 16 rows of the slice
 //   belong to one "owner" wave that keeps them, fp32, in MFMA accumulators for the
@@ -33,8 +34,8 @@
 //   and its decayed copy serve as MFMA operands straight from registers, and the
 //   state step of a chunk needs no LDS round trip and no barrier. The other waves
 //   ("producers") stage the next chunk's operands into the second of two LDS buffers:
-//   q (f16, permuted d), k^T (f16, permuted s), the v slice transposed, W, P, T_v and
-//   lg. One barrier per chunk. f16 (10 stored mantissa bits) keeps the operands of
+//   q, k^T, W, P, T_v and the decay factors as the prep wrote them, and the v slice
+//   transposed to f16. One barrier per chunk. f16 (10 stored mantissa bits) keeps the operands of
 //   these fp32-intermediate products accurate enough for the error bound where bf16
 //   would not; bf16 inputs convert to f16 exactly inside its range.
 #include "common.h"
@@ -227,8 +228,8 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
     }
   }
   // q in f16 for the chain, d in its operand order, written by the first value head of
-  // each key head: output vector v8 of a row holds the natural d0 .. d0 + 3 and
-  // d0 + 16 .. d0 + 19 of its group of 32 (the inverse of perm32)
+  // each key head (k^T by the last): output vector v8 of a row holds the natural
+  // d0 .. d0 + 3 and d0 + 16 .. d0 + 19 of its group of 32 (the inverse of perm32)
   const int G = Hv / Hk;
   if (h % G == 0) {
     _Float16* Qg = a.ws_q + ((long)c * Hk + kh) * C * DK;
@@ -253,7 +254,11 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
     const int r = e / (CC / 4), i = (e - r * (CC / 4)) * 4;
     if (i >= C || (i >> 4) > (r >> 4)) *(uint2*)&Pg[r * CC + perm32(i)] = uint2{0, 0};
   }
-  if (tid < C) a.ws_lg[slot * C + tid] = lg[tid];
+  // the chain's decay factors: to the chunk's end, and from its start
+  if (tid < C) {
+    a.ws_dec[(2 * slot) * C + tid] = __builtin_amdgcn_exp2f(lg[C - 1] - lg[tid]);
+    a.ws_dec[(2 * slot + 1) * C + tid] = __builtin_amdgcn_exp2f(lg[tid]);
+  }
   lds_barrier();
 
   // ---- phase 3: diagonal 16x16 blocks of T = (I + M)^-1, one lane per column: forward
@@ -351,9 +356,9 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   lds_barrier();
 
   // ---- phase 6: W = T diag(beta 2^lg) K on MFMA, to the workspace with d in the
-  // chain's operand order; k^T (first value head of each key head) with s in that order,
+  // chain's operand order; k^T (last value head of each key head) with s in that order,
   // its chunk index padded with zeros to a whole MFMA step
-  if (h % G == 0) {
+  if (h % G == G - 1) {
     _Float16* Kg = a.ws_kt + ((long)c * Hk + kh) * DK * CC;
     for (int e = tid; e < DK * (CC / 8); e += NT) {
       const int d = e / (CC / 8), v8 = e - d * (CC / 8);
@@ -405,7 +410,7 @@ struct ChainStage {
   _Float16 P[C][CK];      // P, s in operand order
   _Float16 Tv[C][CK];     // T_v, natural order
   _Float16 Vt[DVS][CK];   // the v slice transposed, natural order
-  float lg[C];
+  float dec[2][C];        // 2^(lg_last - lg_s), 2^lg_s
 };
 
 template <int DK, int C, int DVS>
@@ -416,6 +421,7 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
   constexpr int CC = Stage::CC;
   constexpr int NO = DVS / 16;                  // owner waves
   constexpr int NP = NT - 64 * NO;              // producer threads
+  static_assert(NP >= 2 * C, "one decay factor per producer thread");
   constexpr int NRB = C / 16;                   // 16-row blocks of a chunk
   constexpr int NDB = DK / 16;                  // 16-row blocks of S^T
   constexpr int NKD = DK / 32;                  // MFMA steps over d
@@ -461,7 +467,7 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
   // ---- producers: registers of one chunk, then their conversion into a stage
   const u32x4 z4 = {0, 0, 0, 0};
   u32x4 rq[RQ], rw[RW], rp[RP], rt[RT], rk[RK], rv[RV][2];
-  float rlg = 0.f;
+  float rdec = 0.f;   // one of the chunk's 2C decay factors
   auto fetch = [&](int lc) {
     const int t0 = lc * C;
     const int Cr = min(C, S.T - t0);
@@ -490,7 +496,7 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
     for (int j = 0; j < RP; ++j) rp[j] = p + NP * j < VP ? P4[p + NP * j] : z4;
 #pragma unroll
     for (int j = 0; j < RT; ++j) rt[j] = p + NP * j < VT ? T4[p + NP * j] : z4;
-    if (p < C) rlg = a.ws_lg[slot * C + p];
+    if (p < 2 * C) rdec = a.ws_dec[2 * slot * C + p];
   };
   auto put = [&](Stage& B) {
 #pragma unroll
@@ -533,11 +539,12 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
       const int e = p + NP * j;
       if (e < VT) *(u32x4*)&B.Tv[e / (C / 8)][8 * (e % (C / 8))] = rt[j];
     }
-    if (p < C) B.lg[p] = rlg;
+    if (p < 2 * C) B.dec[p / C][p % C] = rdec;
   };
 
   // ---- owners: S^T rows 16 db + 4 g4 + e, column 16 wave + l16 of the slice, in
-  // accumulators; their f16 copy as operands over d (blocks 2 kk and 2 kk + 1)
+  // accumulators; their negated f16 copy as operands over d (blocks 2 kk and 2 kk + 1),
+  // so that -W S^T accumulates onto T_v V in place
   float* Sg = S.state + (long)h * DV * DK + (long)(i0 + 16 * wave + l16) * DK;
   f32x4 st[NDB];
   f16x8 sh[NKD];
@@ -546,8 +553,8 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
     for (int kk = 0; kk < NKD; ++kk) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        sh[kk][e] = (_Float16)st[2 * kk][e];
-        sh[kk][4 + e] = (_Float16)st[2 * kk + 1][e];
+        sh[kk][e] = (_Float16)(-st[2 * kk][e]);
+        sh[kk][4 + e] = (_Float16)(-st[2 * kk + 1][e]);
       }
       big = fmaxf(big, fmaxf(max_abs4(st[2 * kk]), max_abs4(st[2 * kk + 1])));
     }
@@ -568,26 +575,25 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
       const Stage& B = stg[lc & 1];
       const int t0 = lc * C;
       const int Cr = min(C, S.T - t0);
-      // Y^T = S Q^T (columns 16 wave + 4 g4 .., row 16 rb + l16), X = W S^T and
-      // U~ = T_v V (rows 16 rb + 4 g4 .., column 16 wave + l16)
-      f32x4 y[NRB], x[NRB], u[NRB];
+      // -Y^T = (-S) Q^T (columns 16 wave + 4 g4 .., row 16 rb + l16) and
+      // U = T_v V + W (-S)^T (rows 16 rb + 4 g4 .., column 16 wave + l16)
+      f32x4 y[NRB], u[NRB];
 #pragma unroll
-      for (int rb = 0; rb < NRB; ++rb) y[rb] = x[rb] = u[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < NKD; ++kk)
-#pragma unroll
-        for (int rb = 0; rb < NRB; ++rb) {
-          y[rb] = mfma_f16(sh[kk], ld_f16x8(&B.Q[16 * rb + l16][32 * kk + 8 * g4]), y[rb]);
-          x[rb] = mfma_f16(ld_f16x8(&B.W[16 * rb + l16][32 * kk + 8 * g4]), sh[kk], x[rb]);
-        }
+      for (int rb = 0; rb < NRB; ++rb) y[rb] = u[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < NKS; ++kk)
 #pragma unroll
         for (int rb = 0; rb < NRB; ++rb)
           u[rb] = mfma_f16(ld_f16x8(&B.Tv[16 * rb + l16][32 * kk + 8 * g4]),
                            ld_f16x8(&B.Vt[16 * wave + l16][32 * kk + 8 * g4]), u[rb]);
-      // U = U~ - X and its decayed copy, as operands over the chunk index
-      const float lg_last = B.lg[C - 1];
+#pragma unroll
+      for (int kk = 0; kk < NKD; ++kk)
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
+          y[rb] = mfma_f16(sh[kk], ld_f16x8(&B.Q[16 * rb + l16][32 * kk + 8 * g4]), y[rb]);
+          u[rb] = mfma_f16(ld_f16x8(&B.W[16 * rb + l16][32 * kk + 8 * g4]), sh[kk], u[rb]);
+        }
+      // U and its decayed copy, as operands over the chunk index
       f16x8 uh[NKS], ud[NKS];
 #pragma unroll
       for (int kk = 0; kk < NKS; ++kk) uh[kk] = ud[kk] = zero_f16x8();
@@ -595,8 +601,8 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
       for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float uu = u[rb][e] - x[rb][e];
-          const float dd = __builtin_amdgcn_exp2f(lg_last - B.lg[16 * rb + 4 * g4 + e]) * uu;
+          const float uu = u[rb][e];
+          const float dd = B.dec[0][16 * rb + 4 * g4 + e] * uu;
           big = fmaxf(big, fabsf(uu));
           uh[rb >> 1][4 * (rb & 1) + e] = (_Float16)uu;
           ud[rb >> 1][4 * (rb & 1) + e] = (_Float16)dd;
@@ -604,14 +610,14 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
       // O^T = scale 2^lg Y^T + U^T P^T, written out
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb) {
-        y[rb] = y[rb] * (a.scale * __builtin_amdgcn_exp2f(B.lg[16 * rb + l16]));
+        y[rb] = y[rb] * (-a.scale * B.dec[1][16 * rb + l16]);
 #pragma unroll
         for (int kk = 0; kk < NKS; ++kk) y[rb] = mfma_f16(uh[kk], ld_f16x8(&B.P[16 * rb + l16][32 * kk + 8 * g4]), y[rb]);
         const int r = 16 * rb + l16;
         if (r < Cr) *(f32x4*)(S.out + ((long)(t0 + r) * Hv + h) * DV + i0 + 16 * wave + 4 * g4) = y[rb];
       }
       // S^T <- 2^lg_last S^T + K^T (decayed U)
-      const float g_last = __builtin_amdgcn_exp2f(lg_last);
+      const float g_last = B.dec[1][C - 1];
 #pragma unroll
       for (int db = 0; db < NDB; ++db) st[db] = st[db] * g_last;
 #pragma unroll
