@@ -430,8 +430,15 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
   // wrote them); 2-row x 8-column items of the v slice (converted and transposed)
   constexpr int VQ = C * DK / 8, VK = DK * CC / 8, VW = C * DK / 8, VP = C * CC / 8, VT = C * C / 8;
   constexpr int NVI = (C / 2) * (DVS / 8);
-  constexpr int RQ = (VQ + NP - 1) / NP, RW = (VW + NP - 1) / NP, RP = (VP + NP - 1) / NP;
-  constexpr int RT = (VT + NP - 1) / NP, RK = (VK + NP - 1) / NP, RV = (NVI + NP - 1) / NP;
+  // The owners finish their part of a chunk first, so with four owners they copy W, P
+  // and T_v of the next chunk (loads issued before their products, stores after), with
+  // two P and T_v; the producers copy the rest.
+  constexpr bool OW = NO >= 4, OPT = NO >= 2;
+  constexpr int NOT = 64 * NO;                  // owner threads
+  constexpr int RQ = (VQ + NP - 1) / NP, RK = (VK + NP - 1) / NP, RV = (NVI + NP - 1) / NP;
+  constexpr int RW = OW ? (VW + NOT - 1) / NOT : (VW + NP - 1) / NP;
+  constexpr int RP = OPT ? (VP + NOT - 1) / NOT : (VP + NP - 1) / NP;
+  constexpr int RT = OPT ? (VT + NOT - 1) / NOT : (VT + NP - 1) / NP;
   __shared__ __attribute__((aligned(16))) Stage stg[2];
 
   // work item: (context, key head, value head of the group, slice), ordered so that the
@@ -468,6 +475,40 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
   const u32x4 z4 = {0, 0, 0, 0};
   u32x4 rq[RQ], rw[RW], rp[RP], rt[RT], rk[RK], rv[RV][2];
   float rdec = 0.f;   // one of the chunk's 2C decay factors
+  // W, and P and T_v, of chunk lc by thread x of the n that copy them
+  auto fetch_w = [&](int lc, int x, int n) {
+    const u32x4* W4 = (const u32x4*)(a.ws_w + ((long)(S.chunk_begin + lc) * Hv + h) * C * DK);
+#pragma unroll
+    for (int j = 0; j < RW; ++j) rw[j] = x + n * j < VW ? W4[x + n * j] : z4;
+  };
+  auto fetch_pt = [&](int lc, int x, int n) {
+    const long slot = (long)(S.chunk_begin + lc) * Hv + h;
+    const u32x4* P4 = (const u32x4*)(a.ws_p + slot * C * CC);
+    const u32x4* T4 = (const u32x4*)(a.ws_tv + slot * C * C);
+#pragma unroll
+    for (int j = 0; j < RP; ++j) rp[j] = x + n * j < VP ? P4[x + n * j] : z4;
+#pragma unroll
+    for (int j = 0; j < RT; ++j) rt[j] = x + n * j < VT ? T4[x + n * j] : z4;
+  };
+  auto put_w = [&](Stage& B, int x, int n) {
+#pragma unroll
+    for (int j = 0; j < RW; ++j) {
+      const int e = x + n * j;
+      if (e < VW) *(u32x4*)&B.W[e / (DK / 8)][8 * (e % (DK / 8))] = rw[j];
+    }
+  };
+  auto put_pt = [&](Stage& B, int x, int n) {
+#pragma unroll
+    for (int j = 0; j < RP; ++j) {
+      const int e = x + n * j;
+      if (e < VP) *(u32x4*)&B.P[e / (CC / 8)][8 * (e % (CC / 8))] = rp[j];
+    }
+#pragma unroll
+    for (int j = 0; j < RT; ++j) {
+      const int e = x + n * j;
+      if (e < VT) *(u32x4*)&B.Tv[e / (C / 8)][8 * (e % (C / 8))] = rt[j];
+    }
+  };
   auto fetch = [&](int lc) {
     const int t0 = lc * C;
     const int Cr = min(C, S.T - t0);
@@ -487,15 +528,8 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
       for (int q = 0; q < 2; ++q)
         rv[j][q] = (e < NVI && s2 + q < Cr) ? *(const u32x4*)(S.v + ((long)(t0 + s2 + q) * Hv + h) * DV + i0 + d0) : z4;
     }
-    const u32x4* W4 = (const u32x4*)(a.ws_w + slot * C * DK);
-    const u32x4* P4 = (const u32x4*)(a.ws_p + slot * C * CC);
-    const u32x4* T4 = (const u32x4*)(a.ws_tv + slot * C * C);
-#pragma unroll
-    for (int j = 0; j < RW; ++j) rw[j] = p + NP * j < VW ? W4[p + NP * j] : z4;
-#pragma unroll
-    for (int j = 0; j < RP; ++j) rp[j] = p + NP * j < VP ? P4[p + NP * j] : z4;
-#pragma unroll
-    for (int j = 0; j < RT; ++j) rt[j] = p + NP * j < VT ? T4[p + NP * j] : z4;
+    if (!OW) fetch_w(lc, p, NP);
+    if (!OPT) fetch_pt(lc, p, NP);
     if (p < 2 * C) rdec = a.ws_dec[2 * slot * C + p];
   };
   auto put = [&](Stage& B) {
@@ -524,21 +558,8 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
         }
       }
     }
-#pragma unroll
-    for (int j = 0; j < RW; ++j) {
-      const int e = p + NP * j;
-      if (e < VW) *(u32x4*)&B.W[e / (DK / 8)][8 * (e % (DK / 8))] = rw[j];
-    }
-#pragma unroll
-    for (int j = 0; j < RP; ++j) {
-      const int e = p + NP * j;
-      if (e < VP) *(u32x4*)&B.P[e / (CC / 8)][8 * (e % (CC / 8))] = rp[j];
-    }
-#pragma unroll
-    for (int j = 0; j < RT; ++j) {
-      const int e = p + NP * j;
-      if (e < VT) *(u32x4*)&B.Tv[e / (C / 8)][8 * (e % (C / 8))] = rt[j];
-    }
+    if (!OW) put_w(B, p, NP);
+    if (!OPT) put_pt(B, p, NP);
     if (p < 2 * C) B.dec[p / C][p % C] = rdec;
   };
 
@@ -560,9 +581,13 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
     }
   };
   if (owner) {
+    if (OW) fetch_w(0, tid, NOT);
+    if (OPT) fetch_pt(0, tid, NOT);
 #pragma unroll
     for (int db = 0; db < NDB; ++db) st[db] = *(const f32x4*)(Sg + 16 * db + 4 * g4);
     refresh_sh();
+    if (OW) put_w(stg[0], tid, NOT);
+    if (OPT) put_pt(stg[0], tid, NOT);
   } else {
     fetch(0);
     put(stg[0]);
@@ -572,6 +597,9 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
 
   for (int lc = 0; lc < S.n_chunks; ++lc) {
     if (owner) {
+      const bool next = lc + 1 < S.n_chunks;
+      if (OW && next) fetch_w(lc + 1, tid, NOT);
+      if (OPT && next) fetch_pt(lc + 1, tid, NOT);
       const Stage& B = stg[lc & 1];
       const int t0 = lc * C;
       const int Cr = min(C, S.T - t0);
@@ -626,6 +654,8 @@ __global__ __launch_bounds__(kChainThreads) void k_delta_chain(DeltaArgs a) {
         for (int db = 0; db < NDB; ++db)
           st[db] = mfma_f16(ld_f16x8(&B.Kt[16 * db + l16][32 * kk + 8 * g4]), ud[kk], st[db]);
       refresh_sh();
+      if (OW && next) put_w(stg[(lc + 1) & 1], tid, NOT);
+      if (OPT && next) put_pt(stg[(lc + 1) & 1], tid, NOT);
     } else if (lc + 1 < S.n_chunks) {
       put(stg[(lc + 1) & 1]);
       if (lc + 2 < S.n_chunks) fetch(lc + 2);
