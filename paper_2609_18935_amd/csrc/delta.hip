@@ -35,7 +35,8 @@
 //   state step of a chunk needs no LDS round trip and no barrier. The other waves
 //   ("producers") stage the next chunk's operands into the second of two LDS buffers:
 //   q, k^T, W, P, T_v and the decay factors as the prep wrote them, and the v slice
-//   transposed to f16. One barrier per chunk. f16 (10 stored mantissa bits) keeps the operands of
+//   transposed to f16 (with two or four owners, the owners copy P and T_v, or W, P and
+//   T_v, themselves once their products are issued). One barrier per chunk. f16 (10 stored mantissa bits) keeps the operands of
 //   these fp32-intermediate products accurate enough for the error bound where bf16
 //   would not; bf16 inputs convert to f16 exactly inside its range.
 #include "common.h"
