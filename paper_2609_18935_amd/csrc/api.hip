@@ -768,8 +768,8 @@ int plan_delta(const tu_delta_params* p, const std::vector<DeltaItem>& items, vo
   const int C = p->chunk, Hv = p->n_v_heads, DK = p->d_k;
   size_t max_used = 0;
   out->clear();
-  for (size_t g0 = 0; g0 < items.size(); g0 += kMaxSeqPerLaunch) {
-    const size_t g1 = std::min(items.size(), g0 + kMaxSeqPerLaunch);
+  for (size_t g0 = 0; g0 < items.size(); g0 += kMaxSeqPerDelta) {
+    const size_t g1 = std::min(items.size(), g0 + kMaxSeqPerDelta);
     int n_active = 0;
     for (size_t i = g0; i < g1; ++i) n_active += items[i].T > 0;
     // slice d_v (16 rows of S per owner wave of the chain) into as few workgroups per
@@ -1131,7 +1131,7 @@ void append_delta_items(const tu_update* u, const StackPlan& sp, const tu_layer_
 
 // Items of every delta layer of the stack, layer by layer and context by context.
 // Each (layer, context) pair owns its state and its inputs, so all of them are
-// independent and share launches (up to kMaxSeqPerLaunch items each).
+// independent and share launches (up to kMaxSeqPerDelta items each).
 std::vector<DeltaItem> stack_delta_items(const tu_update* u, const StackPlan& sp) {
   std::vector<DeltaItem> items;
   for (int l = 0; l < u->n_layers; ++l) {
@@ -1513,7 +1513,7 @@ namespace {
 // layers run on a second stream concurrently with the attention path, so the two
 // regions are disjoint. Attention layers run in order and reuse their region; the
 // (layer, context) items of all delta layers are planned together into launches of
-// up to kMaxSeqPerLaunch items, which run in order and reuse the delta region.
+// up to kMaxSeqPerDelta items, which run in order and reuse the delta region.
 struct StackWorkspace {
   size_t attn = 0;    // compaction and attention layers
   size_t delta = 0;   // delta layers

@@ -17,6 +17,7 @@ typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
 
 constexpr int kMaxSeqPerLaunch = 32;
+constexpr int kMaxSeqPerDelta = 48;   // (layer, context) items of one delta-rule launch
 constexpr int kMaxRangesPerLaunch = 128;
 constexpr int kMaxBufPerLaunch = 64;
 constexpr int kMaxSeqPerCompact = 16;
@@ -280,7 +281,7 @@ struct DeltaSeq {
 };
 
 struct DeltaArgs {
-  DeltaSeq seq[kMaxSeqPerLaunch];
+  DeltaSeq seq[kMaxSeqPerDelta];
   int32_t n_seq;
   int32_t n_k_heads;
   int32_t n_v_heads;
