@@ -432,3 +432,37 @@ def test_stack_equals_per_layer_calls():
         assert torch.equal(kv1[i][0][:n], kv2[i][0][:n]) and torch.equal(kv1[i][1][:n], kv2[i][1][:n]), f"layer {i} cache"
         assert torch.equal(ao1[i], ao2[i]), f"layer {i} attention output"
         assert torch.equal(do1[i], do2[i]) and torch.equal(st1[i], st2[i]), f"layer {i} delta output and state"
+
+
+def test_stack_of_many_delta_layers_equals_per_layer_calls():
+    """A stack of 50 delta layers (no attention layer) takes two delta launches that reuse
+    one workspace region (at most 48 (layer, context) items per launch); every layer's
+    output and state must equal, bit for bit, a separate delta_rule_continue call on a
+    copy of its state. T = 100 gives a ragged second chunk."""
+    d = synth.CONFIGS[1].delta
+    n_layers, T, L = 50, 100, 256
+    _say(f"stack of {n_layers} delta layers, T {T}")
+    dp = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
+    states, dins = [], []
+    for layer in range(n_layers):
+        states.append(synth.gen_delta_state(9, 1, layer, d))
+        q, k, v, beta, g = synth.gen_delta_inputs(9, 1, layer, T, d)
+        dins.append((to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), torch.from_numpy(beta).to(DEV),
+                     torch.from_numpy(g).to(DEV)))
+    ctx = tu.Context(L + T, device=DEV)
+    ctx.pos[:L] = torch.arange(L, dtype=torch.int32, device=DEV)
+    ctx.set_metadata([(0, L)], L)
+    st1 = [torch.from_numpy(S.copy()).to(DEV) for S in states]
+    st2 = [torch.from_numpy(S.copy()).to(DEV) for S in states]
+    do1 = [torch.full((T, d.n_v_heads, d.d_v), float("nan"), dtype=torch.float32, device=DEV) for _ in range(n_layers)]
+    do2 = [torch.full_like(x, float("nan")) for x in do1]
+    layers = [tu.LayerIO(tu.TU_LAYER_DELTA, *dins[i][:3], do1[i], state=[st1[i]], beta=dins[i][3], g=dins[i][4])
+              for i in range(n_layers)]
+    ap = tu.attn_params(16, 2, 256)
+    tu.update_layer_stack([ctx], [np.zeros((0, 2), np.int64)], [T], layers, ap, dp)
+    for i in range(n_layers):
+        dq, dk, dv, beta, g = dins[i]
+        tu.delta_rule_continue(st2[i], dq, dk, dv, beta, g, dp, do2[i])
+    torch.cuda.synchronize()
+    for i in range(n_layers):
+        assert torch.equal(do1[i], do2[i]) and torch.equal(st1[i], st2[i]), f"layer {i} delta output and state"
