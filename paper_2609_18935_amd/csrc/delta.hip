@@ -94,7 +94,6 @@ template <int DK, int C>
 __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   constexpr int NT = kPrepThreads;
   constexpr int NW = NT / 64;
-  constexpr int DV = DK;
   constexpr int NB = C / 16;     // 16-row blocks of the chunk
   constexpr int KP = DK + 8;     // pitch of [C][DK] bf16 tiles
   constexpr int CT = C + 8;      // pitch of f16 tiles with the chunk index contiguous
