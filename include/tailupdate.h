@@ -449,7 +449,8 @@ int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu
  *  q:       device bf16 [n_probe][n_q_heads][head_dim] raw queries of the probe rows;
  *  probs:   device fp32 [>= seq->len], read and written.
  *  1 <= n_probe <= len, n_probe * n_q_heads / n_kv_heads <= 128. The workspace
- *  holds the fp32 score rows (n_probe * n_q_heads x len).
+ *  holds the rotated queries and per-row and per-key partial sums (about
+ *  (n_probe * n_q_heads / 4 + n_kv_heads) x len floats); no score row is stored.
  *
  * attention_group_mass: memory groups given as host int64 [n_groups][2] position
  * ranges (sorted, disjoint; one per record). mass[g] = sum of probs over the rows whose

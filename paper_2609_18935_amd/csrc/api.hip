@@ -1609,8 +1609,8 @@ int relocate_keys(tu_seq* seq, void* const* k_layers, int32_t n_layers, const tu
 static size_t probe_ws(const tu_attn_params* p, int64_t len, int32_t n_probe, int64_t* ld) {
   *ld = (len + kProbeKeys - 1) / kProbeKeys * kProbeKeys;
   const int64_t rows = (int64_t)p->n_q_heads * n_probe;
-  return align_up(sizeof(bf16_t) * rows * p->head_dim) + align_up(sizeof(float) * rows * *ld) +
-         align_up(sizeof(float) * 2 * rows);
+  return align_up(sizeof(bf16_t) * rows * p->head_dim) + align_up(sizeof(float) * 2 * rows) +
+         align_up(sizeof(float) * 2 * rows * (*ld / 32)) + align_up(sizeof(float) * p->n_kv_heads * *ld);
 }
 
 size_t attention_probe_workspace_size(const tu_attn_params* p, int64_t len, int32_t n_probe) {
@@ -1642,8 +1642,10 @@ int attention_probe(const tu_seq* seq, const void* k_cache, const tu_attn_params
   ProbeArgs a{};
   a.q = static_cast<const bf16_t*>(q);
   a.q_hat = static_cast<bf16_t*>(ar.take(sizeof(bf16_t) * rows * p->head_dim));
-  a.scores = static_cast<float*>(ar.take(sizeof(float) * rows * ld));
   a.stats = static_cast<float*>(ar.take(sizeof(float) * 2 * rows));
+  a.part = static_cast<float*>(ar.take(sizeof(float) * 2 * rows * (ld / 32)));
+  a.key_sum = static_cast<float*>(ar.take(sizeof(float) * p->n_kv_heads * ld));
+  a.n_parts = (int32_t)(ld / 32);
   a.k_cache = static_cast<const bf16_t*>(k_cache);
   a.pos = seq->d_pos;
   a.probs = probs;

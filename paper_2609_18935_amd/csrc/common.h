@@ -323,12 +323,14 @@ struct ProbeArgs {
   bf16_t* q_hat;         // [n_probe][Hq][D] rotated (workspace)
   const bf16_t* k_cache; // [cap][Hkv][D]
   const int32_t* pos;    // d_pos
-  float* scores;         // [Hq * n_probe][ld] (workspace)
   float* stats;          // [Hq * n_probe][2] (max, 1 / sum) (workspace)
+  float* part;           // [Hq * n_probe][n_parts][2] (max, sum of exp) per 32-key block (workspace)
+  float* key_sum;        // [Hkv][ld] normalised scores summed over a KV head's rows (workspace)
+  int32_t n_parts;       // 32-key blocks of a score row: ld / 32
   float* probs;          // [len] accumulated: probs += weight * mean distribution
   int32_t len;
   int32_t n_probe;
-  int32_t ld;            // score row stride, a multiple of kProbeKeys
+  int32_t ld;            // len rounded up to a multiple of kProbeKeys
   int32_t n_q_heads;
   int32_t n_kv_heads;
   int32_t head_dim;

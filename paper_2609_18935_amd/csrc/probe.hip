@@ -7,20 +7,20 @@
 // Probe query i of n is the token in cache row len - n + i; it sees rows
 // 0 .. len - n + i. The raw queries are rotated at the rows' positions (float64
 // angles, bf16 nearest even, as the cached keys were). Scores S = scale * q.k are
-// products of bf16 values summed in fp32 on v_mfma_f32_32x32x16_bf16 (one workgroup
-// per (KV head, 64-key tile), the G query heads of the KV head times the n tokens as
-// rows, both operands staged in LDS), written masked to the workspace; a second
-// kernel forms each row's max and sum of exponentials, a third averages the
-// normalised exponentials per key in a fixed order (deterministic). All of it is
-// HBM-bound: the key cache is read once.
+// products of bf16 values summed in fp32 on v_mfma_f32_32x32x16_bf16. The key cache is
+// read twice and no score is stored: a first pass keeps each 32-key block's max and sum
+// of exponentials per row, a small kernel combines them into each row's max and sum,
+// and a second pass recomputes the scores, normalises them and sums them over the rows
+// of each key. Every sum is taken in a fixed order (deterministic). HBM-bound.
 #include "common.h"
 
 namespace tu {
 
 namespace {
 
+typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2;
+
 constexpr int kThreads = 256;
-constexpr int kMaxHalfP = 128;
 
 __device__ __forceinline__ float block_reduce_max(float v, float* sh) {
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
@@ -44,144 +44,209 @@ __device__ __forceinline__ double block_reduce_sum(double v, double* sh) {
   return r;
 }
 
-// One workgroup per probe token: rotate its query heads at the row's position.
+// One workgroup per (probe token, query head): each thread rotates its own dimension
+// (and computes that dimension's angle), so a workgroup waits on one load.
 __global__ __launch_bounds__(kThreads) void k_probe_rope(ProbeArgs a) {
-  __shared__ double s_cos[kMaxHalfP];
-  __shared__ double s_sin[kMaxHalfP];
-  const int i = blockIdx.x;
+  const int i = blockIdx.x, h = blockIdx.y;
   const int D = a.head_dim, Hq = a.n_q_heads, r = a.rotary_dim, half = r >> 1;
-  const int64_t p = a.pos[a.len - a.n_probe + i];
-  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+  const bf16_t* x = a.q + ((long)i * Hq + h) * D;
+  bf16_t* o = a.q_hat + ((long)i * Hq + h) * D;
+  for (int d = threadIdx.x; d < D; d += blockDim.x) {
+    if (d >= r) {
+      o[d] = x[d];
+      continue;
+    }
+    const int j = d < half ? d : d - half;
+    const double av = (double)bf16_to_f32(x[j]), bv = (double)bf16_to_f32(x[j + half]);
+    const int64_t p = a.pos[a.len - a.n_probe + i];
     const double w = pow(a.theta, -2.0 * (double)j / (double)r);
     double sn, cs;
     sincos((double)p * w, &sn, &cs);
-    s_cos[j] = cs;
-    s_sin[j] = sn;
-  }
-  __syncthreads();
-  const bf16_t* q = a.q + (long)i * Hq * D;
-  bf16_t* o = a.q_hat + (long)i * Hq * D;
-  for (int e = threadIdx.x; e < Hq * D; e += blockDim.x) {
-    const int h = e / D, d = e - h * D;
-    const bf16_t* x = q + (long)h * D;
-    if (d < half) {
-      const double av = (double)bf16_to_f32(x[d]), bv = (double)bf16_to_f32(x[d + half]);
-      o[e] = (bf16_t)f64_to_bf16_rne(av * s_cos[d] - bv * s_sin[d]);
-    } else if (d < r) {
-      const int j = d - half;
-      const double av = (double)bf16_to_f32(x[j]), bv = (double)bf16_to_f32(x[d]);
-      o[e] = (bf16_t)f64_to_bf16_rne(bv * s_cos[j] + av * s_sin[j]);
-    } else {
-      o[e] = x[d];
-    }
+    o[d] = (bf16_t)f64_to_bf16_rne(d < half ? av * cs - bv * sn : bv * cs + av * sn);
   }
 }
 
-// Scores of one (KV head, 64-key tile): rows are (token i, head g of the group) as
-// r = i * G + g, at most kProbeMaxRows; stored as S[(h * n + i) * ld + key].
+// Both score passes work on one (KV head, 64-key tile) per workgroup. Its rows are
+// (token i, head g of the group) as r = i * G + g, at most kProbeMaxRows, in tiles of
+// 32; its keys are two half tiles of 32; a task is one (row tile, half tile) pair, the
+// tasks dealt to the 4 waves in turn (a wave keeps one half tile). The key tile is
+// staged in LDS, a task's query fragments are loaded into registers.
 template <int D>
-__global__ __launch_bounds__(kThreads) void k_probe_scores(ProbeArgs a) {
+__device__ __forceinline__ void stage_keys(const ProbeArgs& a, bf16_t* s_k, int j0, int hkv) {
   constexpr int RC = D / 8 + 1;             // 16-byte chunks per LDS row (one of padding)
+  constexpr int PER = kProbeKeys * (D / 8) / kThreads;
+  static_assert(PER * kThreads == kProbeKeys * (D / 8), "whole chunks per thread");
+  // every load issued before the first LDS write; rows past len repeat row len - 1
+  // (their scores are masked), so no load is conditional
+  u32x4 v[PER];
+#pragma unroll
+  for (int t = 0; t < PER; ++t) {
+    const int c = threadIdx.x + t * kThreads;
+    const int j = min(j0 + c / (D / 8), a.len - 1);
+    v[t] = *(const u32x4*)(a.k_cache + ((long)j * a.n_kv_heads + hkv) * D + (c % (D / 8)) * 8);
+  }
+#pragma unroll
+  for (int t = 0; t < PER; ++t) {
+    const int c = threadIdx.x + t * kThreads;
+    *(u32x4*)(s_k + ((c / (D / 8)) * RC + c % (D / 8)) * 8) = v[t];
+  }
+}
+
+// One MFMA operand of row tile rt: this lane's query row rt * 32 + col, dims
+// 16 s + 8 hl .. + 7 for s < D / 16 (rows past R repeat row 0; their results are
+// masked).
+template <int D>
+__device__ __forceinline__ void load_q(const ProbeArgs& a, bf16x8* qf, int rt, int hkv, int R, int G) {
+  const int lane = threadIdx.x & 63, hl = lane >> 5, col = lane & 31;
+  const int rq = rt * 32 + col < R ? rt * 32 + col : 0;
+  const bf16_t* qrow = a.q_hat + ((long)(rq / G) * a.n_q_heads + hkv * G + rq % G) * D + 8 * hl;
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) qf[s] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qrow + 16 * s));
+}
+
+// Pass 1: each 32-key block's max and sum of exponentials of every row's masked scores,
+// stored as part[(h * n + i) * n_parts + block] = {max, sum}. Keys are the A operand, so
+// a lane holds 16 keys of one row and the pair of lanes l, l ^ 32 the whole block.
+template <int D>
+__global__ __launch_bounds__(kThreads) void k_probe_part(ProbeArgs a) {
+  constexpr int RC = D / 8 + 1;
   constexpr int NS = D / 16;
-  __shared__ __attribute__((aligned(16))) bf16_t s_q[kProbeMaxRows * RC * 8];
   __shared__ __attribute__((aligned(16))) bf16_t s_k[kProbeKeys * RC * 8];
   const int hkv = blockIdx.y;
   const int j0 = blockIdx.x * kProbeKeys;
-  const int Hq = a.n_q_heads, Hkv = a.n_kv_heads, G = Hq / Hkv, n = a.n_probe;
+  const int G = a.n_q_heads / a.n_kv_heads, n = a.n_probe;
   const int R = n * G;
   const int R32 = (R + 31) / 32;
-  const int tid = threadIdx.x;
-  for (int c = tid; c < R32 * 32 * (D / 8); c += kThreads) {
-    const int r = c / (D / 8), ch = c - r * (D / 8);
-    u32x4 v = {0, 0, 0, 0};
-    if (r < R) {
-      const int i = r / G, g = r - i * G;
-      v = *(const u32x4*)(a.q_hat + ((long)i * Hq + hkv * G + g) * D + ch * 8);
-    }
-    *(u32x4*)(s_q + (r * RC + ch) * 8) = v;
-  }
-  for (int c = tid; c < kProbeKeys * (D / 8); c += kThreads) {
-    const int r = c / (D / 8), ch = c - r * (D / 8);
-    const int j = j0 + r;
-    u32x4 v = {0, 0, 0, 0};
-    if (j < a.len) v = *(const u32x4*)(a.k_cache + ((long)j * Hkv + hkv) * D + ch * 8);
-    *(u32x4*)(s_k + (r * RC + ch) * 8) = v;
-  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hl = lane >> 5, col = lane & 31;
+  bf16x8 qf[NS];
+  if (wave < 2 * R32) load_q<D>(a, qf, wave >> 1, hkv, R, G);   // before the staging
+  stage_keys<D>(a, s_k, j0, hkv);
   __syncthreads();
-  const int lane = tid & 63, wave = tid >> 6, hl = lane >> 5, col = lane & 31;
   for (int w = wave; w < 2 * R32; w += kThreads / 64) {
     const int kt = w & 1, rt = w >> 1;
+    if (w != wave) load_q<D>(a, qf, rt, hkv, R, G);
     f32x16 acc;
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[e] = 0.f;
     const bf16_t* ka = s_k + ((kt * 32 + col) * RC + hl) * 8;
-    const bf16_t* qb = s_q + ((rt * 32 + col) * RC + hl) * 8;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const bf16x8 av = __builtin_bit_cast(bf16x8, *(const u32x4*)(ka + 16 * s));
-      const bf16x8 bv = __builtin_bit_cast(bf16x8, *(const u32x4*)(qb + 16 * s));
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc, 0, 0, 0);
+      const bf16x8 kv = __builtin_bit_cast(bf16x8, *(const u32x4*)(ka + 16 * s));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv, qf[s], acc, 0, 0, 0);
     }
     // lane holds keys kt*32 + 8 (e/4) + 4 hl + e%4 of query row rt*32 + col
     const int r = rt * 32 + col;
-    if (r < R) {
-      const int i = r / G, g = r - i * G;
-      const int h = hkv * G + g;
-      const int limit = a.len - n + i;        // last row this probe token sees
-      float* srow = a.scores + ((long)h * n + i) * a.ld;
+    const int i = r / G, g = r - i * G;
+    const int limit = r < R ? a.len - n + i : -1;   // last row this probe token sees
+    float v[16];
 #pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        const int key0 = j0 + kt * 32 + 8 * e4 + 4 * hl;
-        f32x4 v;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) v[c] = key0 + c <= limit ? acc[4 * e4 + c] * a.scale : -__builtin_inff();
-        *(f32x4*)(srow + key0) = v;
-      }
+    for (int e = 0; e < 16; ++e) {
+      const int key = j0 + kt * 32 + 8 * (e >> 2) + 4 * hl + (e & 3);
+      v[e] = key <= limit ? acc[e] * a.scale : -__builtin_inff();
     }
+    float m = -__builtin_inff();
+#pragma unroll
+    for (int e = 0; e < 16; ++e) m = fmaxf(m, v[e]);
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    const float ms = m == -__builtin_inff() ? 0.f : m;
+    float l = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) l += expf(v[e] - ms);
+    l += __shfl_xor(l, 32, 64);
+    if (r < R && hl == 0)
+      *(f32x2*)(a.part + (((long)(hkv * G + g) * n + i) * a.n_parts + 2 * blockIdx.x + kt) * 2) = f32x2{m, l};
   }
 }
 
-// One workgroup per score row: its max and the inverse of its sum of exponentials.
+// One workgroup per score row: its max and the inverse of its sum of exponentials, from
+// the pass-1 pairs, in a fixed order.
 __global__ __launch_bounds__(kThreads) void k_probe_stats(ProbeArgs a) {
   __shared__ float shf[kThreads / 64];
   __shared__ double shd[kThreads / 64];
-  const float* s = a.scores + (long)blockIdx.x * a.ld;
+  const f32x2* pr = reinterpret_cast<const f32x2*>(a.part) + (long)blockIdx.x * a.n_parts;
   float m = -__builtin_inff();
-  for (int j = threadIdx.x; j < a.len; j += kThreads) m = fmaxf(m, s[j]);
+  for (int t = threadIdx.x; t < a.n_parts; t += kThreads) m = fmaxf(m, pr[t][0]);
   m = block_reduce_max(m, shf);
-  float l = 0.f;
-  for (int j = threadIdx.x; j < a.len; j += kThreads) l += expf(s[j] - m);
-  const double L = block_reduce_sum((double)l, shd);
+  double l = 0.0;
+  for (int t = threadIdx.x; t < a.n_parts; t += kThreads) {
+    const f32x2 x = pr[t];
+    if (x[0] != -__builtin_inff()) l += (double)(x[1] * expf(x[0] - m));
+  }
+  const double L = block_reduce_sum(l, shd);
   if (threadIdx.x == 0) {
     a.stats[2 * blockIdx.x] = m;
     a.stats[2 * blockIdx.x + 1] = (float)(1.0 / L);
   }
 }
 
-// 64 keys per workgroup, the score rows split over its 4 waves: each lane adds the
-// normalised probabilities of its key over every fourth row, the waves' partial sums
-// are combined in a fixed order (deterministic), scaled by `weight` and added to probs.
+// Pass 2: the scores again, now with the queries as the A operand, so a lane holds one
+// key and 16 rows; each visible score becomes exp(s - max) / sum with its row's
+// statistics and is added over the rows in a fixed order (a lane's rows, its tasks in
+// turn, the two lane halves, then the waves of one half tile in wave order), giving
+// key_sum[hkv * ld + key].
+template <int D>
+__global__ __launch_bounds__(kThreads) void k_probe_keysum(ProbeArgs a) {
+  constexpr int RC = D / 8 + 1;
+  constexpr int NS = D / 16;
+  __shared__ __attribute__((aligned(16))) bf16_t s_k[kProbeKeys * RC * 8];
+  __shared__ float s_st[2 * kProbeMaxRows];
+  __shared__ float s_sum[kThreads / 64][32];
+  const int hkv = blockIdx.y;
+  const int j0 = blockIdx.x * kProbeKeys;
+  const int G = a.n_q_heads / a.n_kv_heads, n = a.n_probe;
+  const int R = n * G;
+  const int R32 = (R + 31) / 32;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hl = lane >> 5, col = lane & 31;
+  bf16x8 qf[NS];
+  if (wave < 2 * R32) load_q<D>(a, qf, wave >> 1, hkv, R, G);
+  for (int r = threadIdx.x; r < R; r += kThreads) {
+    const int i = r / G, g = r - i * G;
+    const f32x2 st = *(const f32x2*)(a.stats + 2 * ((long)(hkv * G + g) * n + i));
+    s_st[2 * r] = st[0];
+    s_st[2 * r + 1] = st[1];
+  }
+  stage_keys<D>(a, s_k, j0, hkv);
+  __syncthreads();
+  const int kt = wave & 1;                      // the half tile of every task of this wave
+  const int key = j0 + kt * 32 + col;
+  float t = 0.f;
+  for (int w = wave; w < 2 * R32; w += kThreads / 64) {
+    const int rt = w >> 1;
+    if (w != wave) load_q<D>(a, qf, rt, hkv, R, G);
+    f32x16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+    const bf16_t* ka = s_k + ((kt * 32 + col) * RC + hl) * 8;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const bf16x8 kv = __builtin_bit_cast(bf16x8, *(const u32x4*)(ka + 16 * s));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[s], kv, acc, 0, 0, 0);
+    }
+    // lane holds rows rt*32 + 8 (e/4) + 4 hl + e%4 of key `key`
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int r = rt * 32 + 8 * (e >> 2) + 4 * hl + (e & 3);
+      if (r < R && key <= a.len - n + r / G) t += expf(acc[e] * a.scale - s_st[2 * r]) * s_st[2 * r + 1];
+    }
+  }
+  t += __shfl_xor(t, 32, 64);
+  if (hl == 0) s_sum[wave][col] = t;
+  __syncthreads();
+  if (threadIdx.x < kProbeKeys) {
+    const int k2 = threadIdx.x >> 5, c = threadIdx.x & 31;
+    float u = 0.f;
+    for (int w = k2; w < kThreads / 64; w += 2) u += s_sum[w][c];
+    a.key_sum[(long)hkv * a.ld + j0 + threadIdx.x] = u;
+  }
+}
+
+// probs[j] += weight * (sum over the KV heads, in order, of key_sum) / rows.
 __global__ __launch_bounds__(kThreads) void k_probe_mean(ProbeArgs a) {
-  extern __shared__ float s_st[];
-  __shared__ float s_part[kThreads / 64][64];
-  const int rows = a.n_q_heads * a.n_probe;
-  for (int e = threadIdx.x; e < 2 * rows; e += kThreads) s_st[e] = a.stats[e];
-  __syncthreads();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int j = blockIdx.x * 64 + lane;
-  float acc = 0.f;
-  if (j < a.len) {
-#pragma unroll 4
-    for (int r = wave; r < rows; r += kThreads / 64)
-      acc += expf(a.scores[(long)r * a.ld + j] - s_st[2 * r]) * s_st[2 * r + 1];
-  }
-  s_part[wave][lane] = acc;
-  __syncthreads();
-  if (wave == 0 && j < a.len) {
-    float t = s_part[0][lane];
-    for (int w = 1; w < kThreads / 64; ++w) t += s_part[w][lane];
-    a.probs[j] += a.weight * (t / (float)rows);
-  }
+  const int j = blockIdx.x * kThreads + threadIdx.x;
+  if (j >= a.len) return;
+  float t = 0.f;
+  for (int h = 0; h < a.n_kv_heads; ++h) t += a.key_sum[(long)h * a.ld + j];
+  a.probs[j] += a.weight * (t / (float)(a.n_q_heads * a.n_probe));
 }
 
 // Group masses, in a fixed summation order (the same bits on every run): workgroup b
@@ -310,21 +375,27 @@ __global__ __launch_bounds__(kThreads) void k_tv_final(TvArgs a) {
 
 hipError_t launch_probe(const ProbeArgs& a, hipStream_t s) {
   if (a.n_probe <= 0 || a.len <= 0) return hipSuccess;
-  if (a.rotary_dim > 2 * kMaxHalfP || a.n_probe * (a.n_q_heads / a.n_kv_heads) > kProbeMaxRows)
+  if (a.rotary_dim > a.head_dim || a.n_probe * (a.n_q_heads / a.n_kv_heads) > kProbeMaxRows)
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_probe_rope, dim3(a.n_probe), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(k_probe_rope, dim3(a.n_probe, a.n_q_heads), dim3(kThreads), 0, s, a);
   const dim3 grid((a.len + kProbeKeys - 1) / kProbeKeys, a.n_kv_heads);
-  if (a.head_dim == 256)
-    hipLaunchKernelGGL(k_probe_scores<256>, grid, dim3(kThreads), 0, s, a);
-  else if (a.head_dim == 128)
-    hipLaunchKernelGGL(k_probe_scores<128>, grid, dim3(kThreads), 0, s, a);
-  else if (a.head_dim == 64)
-    hipLaunchKernelGGL(k_probe_scores<64>, grid, dim3(kThreads), 0, s, a);
-  else
-    return hipErrorInvalidValue;
   const int rows = a.n_q_heads * a.n_probe;
-  hipLaunchKernelGGL(k_probe_stats, dim3(rows), dim3(kThreads), 0, s, a);
-  hipLaunchKernelGGL(k_probe_mean, dim3((a.len + 63) / 64), dim3(kThreads), sizeof(float) * 2 * rows, s, a);
+  if (a.head_dim == 256) {
+    hipLaunchKernelGGL(k_probe_part<256>, grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_probe_stats, dim3(rows), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_probe_keysum<256>, grid, dim3(kThreads), 0, s, a);
+  } else if (a.head_dim == 128) {
+    hipLaunchKernelGGL(k_probe_part<128>, grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_probe_stats, dim3(rows), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_probe_keysum<128>, grid, dim3(kThreads), 0, s, a);
+  } else if (a.head_dim == 64) {
+    hipLaunchKernelGGL(k_probe_part<64>, grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_probe_stats, dim3(rows), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_probe_keysum<64>, grid, dim3(kThreads), 0, s, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  hipLaunchKernelGGL(k_probe_mean, dim3((a.len + kThreads - 1) / kThreads), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -88,6 +88,33 @@ def test_probe_distribution_two_layers(placement):
     _close(got, p_ref, f"probe distribution ({placement})")
 
 
+@pytest.mark.parametrize("hq,hkv,d,rdim,n,L", [
+    (8, 4, 128, 64, 5, 1000),     # 10 rows per KV head: one ragged row tile
+    (16, 1, 64, 64, 8, 333),      # 128 rows: four row tiles, two tasks per wave
+    (4, 4, 256, 256, 1, 64),      # one row per KV head, one key tile
+])
+def test_probe_shapes(hq, hkv, d, rdim, n, L):
+    """Other head shapes on a context with a hole in its positions, keys and queries
+    scaled so that the softmax rows are peaked."""
+    _say(f"probe shape Hq={hq} Hkv={hkv} D={d} rotary={rdim} n={n} len={L}")
+    rng = np.random.default_rng(50 + d + n)
+    k = synth.to_bf16_bits(rng.normal(0.0, 2.0, (L, hkv, d)))
+    q = synth.to_bf16_bits(rng.normal(0.0, 2.0, (n, hq, d)))
+    cut = L // 3
+    pos = np.concatenate([np.arange(cut), np.arange(cut + 700, cut + 700 + L - cut)])
+    ctx = tu.Context(L, device=DEV)
+    ctx.pos[:L] = torch.from_numpy(pos.astype(np.int32)).to(DEV)
+    ctx.set_metadata([(0, cut), (cut + 700, int(pos[-1]) + 1)], int(pos[-1]) + 1)
+    p = tu.attn_params(hq, hkv, d, rdim, 1.0e6)
+    got = torch.zeros(L, dtype=torch.float32, device=DEV)
+    tu.attention_probe(ctx, to_dev_bf16(k), p, to_dev_bf16(q), got)
+    torch.cuda.synchronize()
+    want = oracle.probe_distribution(q, pos[-n:], k, rdim, 1.0e6, d ** -0.5)
+    got = got.cpu().numpy().astype(np.float64)
+    assert abs(got.sum() - 1.0) < 1e-4
+    _close(got, want, f"probe distribution Hq={hq} Hkv={hkv} D={d} n={n}")
+
+
 def test_group_masses_and_summary():
     ranges = np.array([[100, 228]])
     ctx, kc, q, ref = _updated_layer(31, 0, 3000, ranges, 200)
