@@ -66,31 +66,37 @@ __global__ __launch_bounds__(kThreads) void k_probe_rope(ProbeArgs a) {
   }
 }
 
-// Both score passes work on one (KV head, 64-key tile) per workgroup. Its rows are
-// (token i, head g of the group) as r = i * G + g, at most kProbeMaxRows, in tiles of
-// 32; its keys are two half tiles of 32; a task is one (row tile, half tile) pair, the
-// tasks dealt to the 4 waves in turn (a wave keeps one half tile). The key tile is
-// staged in LDS, a task's query fragments are loaded into registers.
+// Both score passes stream (KV head, 64-key tile) items: a launch holds as many
+// workgroups as fit on the chip at once (a multiple of the KV head count), and workgroup
+// b takes items b, b + grid, ... , all of KV head b % Hkv, prefetching the next item's
+// key tile into registers while it computes on the current one in LDS. Rows are (token
+// i, head g of the group) as r = i * G + g, at most kProbeMaxRows, in R32 row tiles of
+// 32; the keys of a tile are two half tiles of 32. Wave w keeps the query fragments of
+// row tile w % R32 for the whole launch and takes the half tiles w / R32,
+// w / R32 + 4 / R32, ... (R32 <= 4, so every (row tile, half tile) pair has one wave).
 template <int D>
-__device__ __forceinline__ void stage_keys(const ProbeArgs& a, bf16_t* s_k, int j0, int hkv) {
-  constexpr int RC = D / 8 + 1;             // 16-byte chunks per LDS row (one of padding)
-  constexpr int PER = kProbeKeys * (D / 8) / kThreads;
+struct KeyTile {
+  static constexpr int RC = D / 8 + 1;      // 16-byte chunks per LDS row (one of padding)
+  static constexpr int PER = kProbeKeys * (D / 8) / kThreads;
   static_assert(PER * kThreads == kProbeKeys * (D / 8), "whole chunks per thread");
-  // every load issued before the first LDS write; rows past len repeat row len - 1
-  // (their scores are masked), so no load is conditional
   u32x4 v[PER];
+  // rows past len repeat row len - 1 (their scores are masked), so no load is conditional
+  __device__ __forceinline__ void fetch(const ProbeArgs& a, int j0, int hkv) {
 #pragma unroll
-  for (int t = 0; t < PER; ++t) {
-    const int c = threadIdx.x + t * kThreads;
-    const int j = min(j0 + c / (D / 8), a.len - 1);
-    v[t] = *(const u32x4*)(a.k_cache + ((long)j * a.n_kv_heads + hkv) * D + (c % (D / 8)) * 8);
+    for (int t = 0; t < PER; ++t) {
+      const int c = threadIdx.x + t * kThreads;
+      const int j = min(j0 + c / (D / 8), a.len - 1);
+      v[t] = *(const u32x4*)(a.k_cache + ((long)j * a.n_kv_heads + hkv) * D + (c % (D / 8)) * 8);
+    }
   }
+  __device__ __forceinline__ void put(bf16_t* s_k) const {
 #pragma unroll
-  for (int t = 0; t < PER; ++t) {
-    const int c = threadIdx.x + t * kThreads;
-    *(u32x4*)(s_k + ((c / (D / 8)) * RC + c % (D / 8)) * 8) = v[t];
+    for (int t = 0; t < PER; ++t) {
+      const int c = threadIdx.x + t * kThreads;
+      *(u32x4*)(s_k + ((c / (D / 8)) * RC + c % (D / 8)) * 8) = v[t];
+    }
   }
-}
+};
 
 // One MFMA operand of row tile rt: this lane's query row rt * 32 + col, dims
 // 16 s + 8 hl .. + 7 for s < D / 16 (rows past R repeat row 0; their results are
@@ -104,73 +110,112 @@ __device__ __forceinline__ void load_q(const ProbeArgs& a, bf16x8* qf, int rt, i
   for (int s = 0; s < D / 16; ++s) qf[s] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qrow + 16 * s));
 }
 
+// The (row tile, half tiles) share of one wave.
+struct WaveShare {
+  int rt, first, step;
+  bool active;
+  __device__ __forceinline__ WaveShare(int R32) {
+    const int wave = threadIdx.x >> 6;
+    rt = wave % R32;
+    first = wave / R32;
+    step = (kThreads / 64) / R32;
+    active = first < step;
+  }
+  __device__ __forceinline__ bool takes(int kt) const { return active && kt >= first && (kt - first) % step == 0; }
+};
+
 // Pass 1: each 32-key block's max and sum of exponentials of every row's masked scores,
 // stored as part[(h * n + i) * n_parts + block] = {max, sum}. Keys are the A operand, so
 // a lane holds 16 keys of one row and the pair of lanes l, l ^ 32 the whole block.
 template <int D>
 __global__ __launch_bounds__(kThreads) void k_probe_part(ProbeArgs a) {
-  constexpr int RC = D / 8 + 1;
-  constexpr int NS = D / 16;
+  constexpr int RC = KeyTile<D>::RC;
   __shared__ __attribute__((aligned(16))) bf16_t s_k[kProbeKeys * RC * 8];
-  const int hkv = blockIdx.y;
-  const int j0 = blockIdx.x * kProbeKeys;
-  const int G = a.n_q_heads / a.n_kv_heads, n = a.n_probe;
+  const int Hkv = a.n_kv_heads, G = a.n_q_heads / Hkv, n = a.n_probe;
   const int R = n * G;
   const int R32 = (R + 31) / 32;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hl = lane >> 5, col = lane & 31;
-  bf16x8 qf[NS];
-  if (wave < 2 * R32) load_q<D>(a, qf, wave >> 1, hkv, R, G);   // before the staging
-  stage_keys<D>(a, s_k, j0, hkv);
-  __syncthreads();
-  for (int w = wave; w < 2 * R32; w += kThreads / 64) {
-    const int kt = w & 1, rt = w >> 1;
-    if (w != wave) load_q<D>(a, qf, rt, hkv, R, G);
-    f32x16 acc;
+  const int n_items = (a.len + kProbeKeys - 1) / kProbeKeys * Hkv;
+  const int hkv = blockIdx.x % Hkv;
+  const int lane = threadIdx.x & 63, hl = lane >> 5, col = lane & 31;
+  const WaveShare ws(R32);
+  KeyTile<D> kt_regs;
+  kt_regs.fetch(a, (int)blockIdx.x / Hkv * kProbeKeys, hkv);
+  bf16x8 qf[D / 16];
+  if (ws.active) load_q<D>(a, qf, ws.rt, hkv, R, G);
+  // this lane's row and the last key its probe token sees
+  const int r = ws.rt * 32 + col;
+  const int i = r / G, g = r - i * G;
+  const int limit = r < R ? a.len - n + i : -1;
+  float* prow = a.part + ((long)(hkv * G + g) * n + i) * a.n_parts * 2;
+  for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+    const int j0 = it / Hkv * kProbeKeys;
+    __syncthreads();
+    kt_regs.put(s_k);
+    __syncthreads();
+    if (it + (int)gridDim.x < n_items) kt_regs.fetch(a, (it + (int)gridDim.x) / Hkv * kProbeKeys, hkv);
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-    const bf16_t* ka = s_k + ((kt * 32 + col) * RC + hl) * 8;
+    for (int kt = 0; kt < 2; ++kt) {
+      if (!ws.takes(kt)) continue;
+      f32x16 acc;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const bf16x8 kv = __builtin_bit_cast(bf16x8, *(const u32x4*)(ka + 16 * s));
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv, qf[s], acc, 0, 0, 0);
+      for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+      const bf16_t* ka = s_k + ((kt * 32 + col) * RC + hl) * 8;
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        const bf16x8 kv = __builtin_bit_cast(bf16x8, *(const u32x4*)(ka + 16 * s));
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv, qf[s], acc, 0, 0, 0);
+      }
+      // lane holds keys j0 + kt*32 + 4 hl + o, o = 8 (e/4) + e%4, of query row r
+      const int o_max = limit - (j0 + kt * 32 + 4 * hl);
+      float v[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) v[e] = 8 * (e >> 2) + (e & 3) <= o_max ? acc[e] * a.scale : -__builtin_inff();
+      float m = -__builtin_inff();
+#pragma unroll
+      for (int e = 0; e < 16; ++e) m = fmaxf(m, v[e]);
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      const float ms = m == -__builtin_inff() ? 0.f : m;
+      float l = 0.f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) l += expf(v[e] - ms);
+      l += __shfl_xor(l, 32, 64);
+      if (r < R && hl == 0) *(f32x2*)(prow + (2 * (j0 / kProbeKeys) + kt) * 2) = f32x2{m, l};
     }
-    // lane holds keys kt*32 + 8 (e/4) + 4 hl + e%4 of query row rt*32 + col
-    const int r = rt * 32 + col;
-    const int i = r / G, g = r - i * G;
-    const int limit = r < R ? a.len - n + i : -1;   // last row this probe token sees
-    float v[16];
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = j0 + kt * 32 + 8 * (e >> 2) + 4 * hl + (e & 3);
-      v[e] = key <= limit ? acc[e] * a.scale : -__builtin_inff();
-    }
-    float m = -__builtin_inff();
-#pragma unroll
-    for (int e = 0; e < 16; ++e) m = fmaxf(m, v[e]);
-    m = fmaxf(m, __shfl_xor(m, 32, 64));
-    const float ms = m == -__builtin_inff() ? 0.f : m;
-    float l = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) l += expf(v[e] - ms);
-    l += __shfl_xor(l, 32, 64);
-    if (r < R && hl == 0)
-      *(f32x2*)(a.part + (((long)(hkv * G + g) * n + i) * a.n_parts + 2 * blockIdx.x + kt) * 2) = f32x2{m, l};
   }
 }
 
 // One workgroup per score row: its max and the inverse of its sum of exponentials, from
-// the pass-1 pairs, in a fixed order.
+// the pass-1 pairs, in a fixed order. A thread takes pairs tid, tid + 256, ... in batches
+// of kStatsBatch loads issued together; a row of up to kThreads * kStatsBatch pairs
+// (65,536 keys) is read once and kept in registers.
+constexpr int kStatsBatch = 8;
 __global__ __launch_bounds__(kThreads) void k_probe_stats(ProbeArgs a) {
   __shared__ float shf[kThreads / 64];
   __shared__ double shd[kThreads / 64];
   const f32x2* pr = reinterpret_cast<const f32x2*>(a.part) + (long)blockIdx.x * a.n_parts;
+  const int np = a.n_parts;
+  constexpr int B = kThreads * kStatsBatch;
+  f32x2 x[kStatsBatch];
+  auto batch = [&](int t0) {
+#pragma unroll
+    for (int b = 0; b < kStatsBatch; ++b) {
+      const int t = t0 + b * kThreads + (int)threadIdx.x;
+      x[b] = t < np ? pr[t] : f32x2{-__builtin_inff(), 0.f};
+    }
+  };
   float m = -__builtin_inff();
-  for (int t = threadIdx.x; t < a.n_parts; t += kThreads) m = fmaxf(m, pr[t][0]);
+  for (int t0 = 0; t0 < np; t0 += B) {
+    batch(t0);
+#pragma unroll
+    for (int b = 0; b < kStatsBatch; ++b) m = fmaxf(m, x[b][0]);
+  }
   m = block_reduce_max(m, shf);
   double l = 0.0;
-  for (int t = threadIdx.x; t < a.n_parts; t += kThreads) {
-    const f32x2 x = pr[t];
-    if (x[0] != -__builtin_inff()) l += (double)(x[1] * expf(x[0] - m));
+  for (int t0 = (np - 1) / B * B; t0 >= 0; t0 -= B) {   // the last batch is still loaded
+    if (t0 + B < np) batch(t0);
+#pragma unroll
+    for (int b = 0; b < kStatsBatch; ++b)
+      if (x[b][0] != -__builtin_inff()) l += (double)(x[b][1] * expf(x[b][0] - m));
   }
   const double L = block_reduce_sum(l, shd);
   if (threadIdx.x == 0) {
@@ -181,62 +226,75 @@ __global__ __launch_bounds__(kThreads) void k_probe_stats(ProbeArgs a) {
 
 // Pass 2: the scores again, now with the queries as the A operand, so a lane holds one
 // key and 16 rows; each visible score becomes exp(s - max) / sum with its row's
-// statistics and is added over the rows in a fixed order (a lane's rows, its tasks in
-// turn, the two lane halves, then the waves of one half tile in wave order), giving
-// key_sum[hkv * ld + key].
+// statistics and is added over the rows in a fixed order (a lane's rows, the two lane
+// halves, then the waves in wave order), giving key_sum[hkv * ld + key]. Streams items
+// as pass 1 does.
 template <int D>
 __global__ __launch_bounds__(kThreads) void k_probe_keysum(ProbeArgs a) {
-  constexpr int RC = D / 8 + 1;
-  constexpr int NS = D / 16;
+  constexpr int RC = KeyTile<D>::RC;
   __shared__ __attribute__((aligned(16))) bf16_t s_k[kProbeKeys * RC * 8];
   __shared__ float s_st[2 * kProbeMaxRows];
-  __shared__ float s_sum[kThreads / 64][32];
-  const int hkv = blockIdx.y;
-  const int j0 = blockIdx.x * kProbeKeys;
-  const int G = a.n_q_heads / a.n_kv_heads, n = a.n_probe;
+  __shared__ float s_sum[kThreads / 64][2][32];
+  const int Hkv = a.n_kv_heads, G = a.n_q_heads / Hkv, n = a.n_probe;
   const int R = n * G;
   const int R32 = (R + 31) / 32;
+  const int n_items = (a.len + kProbeKeys - 1) / kProbeKeys * Hkv;
+  const int hkv = blockIdx.x % Hkv;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hl = lane >> 5, col = lane & 31;
-  bf16x8 qf[NS];
-  if (wave < 2 * R32) load_q<D>(a, qf, wave >> 1, hkv, R, G);
+  const WaveShare ws(R32);
+  KeyTile<D> kt_regs;
+  kt_regs.fetch(a, (int)blockIdx.x / Hkv * kProbeKeys, hkv);
+  bf16x8 qf[D / 16];
+  if (ws.active) load_q<D>(a, qf, ws.rt, hkv, R, G);
   for (int r = threadIdx.x; r < R; r += kThreads) {
     const int i = r / G, g = r - i * G;
     const f32x2 st = *(const f32x2*)(a.stats + 2 * ((long)(hkv * G + g) * n + i));
     s_st[2 * r] = st[0];
     s_st[2 * r + 1] = st[1];
   }
-  stage_keys<D>(a, s_k, j0, hkv);
-  __syncthreads();
-  const int kt = wave & 1;                      // the half tile of every task of this wave
-  const int key = j0 + kt * 32 + col;
-  float t = 0.f;
-  for (int w = wave; w < 2 * R32; w += kThreads / 64) {
-    const int rt = w >> 1;
-    if (w != wave) load_q<D>(a, qf, rt, hkv, R, G);
-    f32x16 acc;
+  for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+    const int j0 = it / Hkv * kProbeKeys;
+    __syncthreads();
+    kt_regs.put(s_k);
+    __syncthreads();
+    if (it + (int)gridDim.x < n_items) kt_regs.fetch(a, (it + (int)gridDim.x) / Hkv * kProbeKeys, hkv);
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-    const bf16_t* ka = s_k + ((kt * 32 + col) * RC + hl) * 8;
+    for (int kt = 0; kt < 2; ++kt) {
+      float t = 0.f;
+      if (ws.takes(kt)) {
+        f32x16 acc;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const bf16x8 kv = __builtin_bit_cast(bf16x8, *(const u32x4*)(ka + 16 * s));
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[s], kv, acc, 0, 0, 0);
+        for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+        const bf16_t* ka = s_k + ((kt * 32 + col) * RC + hl) * 8;
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) {
+          const bf16x8 kv = __builtin_bit_cast(bf16x8, *(const u32x4*)(ka + 16 * s));
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[s], kv, acc, 0, 0, 0);
+        }
+        // lane holds rows r0 + o, o = 8 (e/4) + e%4, of key j0 + kt*32 + col; row r (token
+        // r / G) sees the key when r / G >= key - (len - n), that is r >= r_min; rows past
+        // R (statistics never written) and unseen rows are selected away
+        const int r0 = ws.rt * 32 + 4 * hl;
+        const int lo = max(0, j0 + kt * 32 + col - (a.len - n)) * G - r0, hi = R - r0;
+        const float* st = s_st + 2 * r0;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int o = 8 * (e >> 2) + (e & 3);
+          const f32x2 mv = *(const f32x2*)(st + 2 * o);
+          const float pe = expf(acc[e] * a.scale - mv[0]) * mv[1];
+          t += o >= lo && o < hi ? pe : 0.f;
+        }
+      }
+      t += __shfl_xor(t, 32, 64);
+      if (hl == 0) s_sum[wave][kt][col] = t;
     }
-    // lane holds rows rt*32 + 8 (e/4) + 4 hl + e%4 of key `key`
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int r = rt * 32 + 8 * (e >> 2) + 4 * hl + (e & 3);
-      if (r < R && key <= a.len - n + r / G) t += expf(acc[e] * a.scale - s_st[2 * r]) * s_st[2 * r + 1];
+    __syncthreads();
+    if (threadIdx.x < kProbeKeys) {
+      const int k2 = threadIdx.x >> 5, c = threadIdx.x & 31;
+      float u = s_sum[0][k2][c];
+      for (int w = 1; w < kThreads / 64; ++w) u += s_sum[w][k2][c];
+      a.key_sum[(long)hkv * a.ld + j0 + threadIdx.x] = u;
     }
-  }
-  t += __shfl_xor(t, 32, 64);
-  if (hl == 0) s_sum[wave][col] = t;
-  __syncthreads();
-  if (threadIdx.x < kProbeKeys) {
-    const int k2 = threadIdx.x >> 5, c = threadIdx.x & 31;
-    float u = 0.f;
-    for (int w = k2; w < kThreads / 64; w += 2) u += s_sum[w][c];
-    a.key_sum[(long)hkv * a.ld + j0 + threadIdx.x] = u;
   }
 }
 
@@ -371,6 +429,26 @@ __global__ __launch_bounds__(kThreads) void k_tv_final(TvArgs a) {
   if (threadIdx.x == 0) a.tv[0] = (float)(0.5 * s);
 }
 
+// A streaming pass: as many workgroups as fit on the chip at once (the kernel's own
+// occupancy, cached per kernel), at most the item count, rounded down to a multiple of
+// the KV head count (item counts are multiples of it).
+template <void (*kernel)(ProbeArgs)>
+hipError_t launch_stream_pass(int n_items, const ProbeArgs& a, hipStream_t s) {
+  static int slots = -1;
+  if (slots < 0) {
+    int dev = 0, per_cu = 0, cus = 0;
+    if (hipError_t e = hipGetDevice(&dev); e != hipSuccess) return e;
+    if (hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0); e != hipSuccess)
+      return e;
+    if (hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev); e != hipSuccess)
+      return e;
+    slots = std::max(1, per_cu) * std::max(1, cus);
+  }
+  const int grid = std::max(a.n_kv_heads, std::min(n_items, slots) / a.n_kv_heads * a.n_kv_heads);
+  hipLaunchKernelGGL(kernel, dim3(grid), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_probe(const ProbeArgs& a, hipStream_t s) {
@@ -378,20 +456,20 @@ hipError_t launch_probe(const ProbeArgs& a, hipStream_t s) {
   if (a.rotary_dim > a.head_dim || a.n_probe * (a.n_q_heads / a.n_kv_heads) > kProbeMaxRows)
     return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_probe_rope, dim3(a.n_probe, a.n_q_heads), dim3(kThreads), 0, s, a);
-  const dim3 grid((a.len + kProbeKeys - 1) / kProbeKeys, a.n_kv_heads);
   const int rows = a.n_q_heads * a.n_probe;
+  const int n_items = (a.len + kProbeKeys - 1) / kProbeKeys * a.n_kv_heads;
   if (a.head_dim == 256) {
-    hipLaunchKernelGGL(k_probe_part<256>, grid, dim3(kThreads), 0, s, a);
+    if (hipError_t e = launch_stream_pass<k_probe_part<256>>(n_items, a, s); e != hipSuccess) return e;
     hipLaunchKernelGGL(k_probe_stats, dim3(rows), dim3(kThreads), 0, s, a);
-    hipLaunchKernelGGL(k_probe_keysum<256>, grid, dim3(kThreads), 0, s, a);
+    if (hipError_t e = launch_stream_pass<k_probe_keysum<256>>(n_items, a, s); e != hipSuccess) return e;
   } else if (a.head_dim == 128) {
-    hipLaunchKernelGGL(k_probe_part<128>, grid, dim3(kThreads), 0, s, a);
+    if (hipError_t e = launch_stream_pass<k_probe_part<128>>(n_items, a, s); e != hipSuccess) return e;
     hipLaunchKernelGGL(k_probe_stats, dim3(rows), dim3(kThreads), 0, s, a);
-    hipLaunchKernelGGL(k_probe_keysum<128>, grid, dim3(kThreads), 0, s, a);
+    if (hipError_t e = launch_stream_pass<k_probe_keysum<128>>(n_items, a, s); e != hipSuccess) return e;
   } else if (a.head_dim == 64) {
-    hipLaunchKernelGGL(k_probe_part<64>, grid, dim3(kThreads), 0, s, a);
+    if (hipError_t e = launch_stream_pass<k_probe_part<64>>(n_items, a, s); e != hipSuccess) return e;
     hipLaunchKernelGGL(k_probe_stats, dim3(rows), dim3(kThreads), 0, s, a);
-    hipLaunchKernelGGL(k_probe_keysum<64>, grid, dim3(kThreads), 0, s, a);
+    if (hipError_t e = launch_stream_pass<k_probe_keysum<64>>(n_items, a, s); e != hipSuccess) return e;
   } else {
     return hipErrorInvalidValue;
   }
