@@ -72,10 +72,16 @@ __device__ __forceinline__ int perm32(int x) {
   return (x & ~31) | (8 * (a & 3) + 4 * (a >> 2) + (x & 3));
 }
 
+// The last sequence whose first chunk is at or before c (chunk_begin is non-decreasing
+// and starts at 0): a binary search, about log2(n_seq) dependent loads.
 __device__ __forceinline__ int find_seq_by_chunk(const DeltaArgs& a, int c) {
-  int si = 0;
-  while (si + 1 < a.n_seq && a.seq[si + 1].chunk_begin <= c) ++si;
-  return si;
+  int lo = 0, hi = a.n_seq - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.seq[mid].chunk_begin <= c) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
 }
 
 constexpr int cmax(size_t x, size_t y) { return (int)(x > y ? x : y); }
@@ -134,25 +140,41 @@ __global__ __launch_bounds__(kPrepThreads) void k_delta_prep(DeltaArgs a) {
   float big = 0.f;   // largest magnitude this thread rounds to f16
   status_mark(a.status);
 
-  // ---- phase 0: stage K, Q (bf16), beta, log2 g
-  for (int e = tid; e < C * (DK / 8); e += NT) {
-    const int r = e / (DK / 8), cc = e - r * (DK / 8);
-    u32x4 kw = {0, 0, 0, 0}, qw = {0, 0, 0, 0};
-    if (r < Cr) {
-      const long off = ((long)(t0 + r) * Hk + kh) * DK + cc * 8;
-      kw = *(const u32x4*)(S.k + off);
-      qw = *(const u32x4*)(S.q + off);
+  // ---- phase 0: stage K, Q (bf16), beta, log2 g. Every load is issued before the first
+  // LDS write; rows past the chunk's end load its last row (Cr >= 1) and are stored as 0.
+  {
+    constexpr int NE = C * (DK / 8);
+    constexpr int PER = (NE + NT - 1) / NT;
+    u32x4 kw[PER], qw[PER];
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int e = min(tid + p * NT, NE - 1);
+      const int r = min(e / (DK / 8), Cr - 1);
+      const long off = ((long)(t0 + r) * Hk + kh) * DK + (e % (DK / 8)) * 8;
+      kw[p] = *(const u32x4*)(S.k + off);
+      qw[p] = *(const u32x4*)(S.q + off);
     }
-    *(u32x4*)&Ks[r][cc * 8] = kw;
-    *(u32x4*)&Qs[r][cc * 8] = qw;
-  }
-  if (tid < C) {
-    const bool ok = tid < Cr;
-    bt[tid] = ok ? S.beta[(long)(t0 + tid) * Hv + h] : 0.f;
-    // log2 g, held at -100 or above: a gate of exactly 0 would give -inf and, in the
-    // differences of the cumulative sums below, NaN; 2^-100 of the state is far below
-    // fp32 rounding of any other term
-    lg[tid] = ok ? fmaxf(__log2f(S.g[(long)(t0 + tid) * Hv + h]), -100.f) : 0.f;
+    const long tr = (long)(t0 + min(tid, Cr - 1)) * Hv + h;
+    const float bv = tid < C ? S.beta[tr] : 0.f;
+    const float gv = tid < C ? S.g[tr] : 1.f;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int e = tid + p * NT;
+      if (NE % NT == 0 || e < NE) {
+        const int r = e / (DK / 8), cc = e - r * (DK / 8);
+        const u32x4 z = {0, 0, 0, 0};
+        *(u32x4*)&Ks[r][cc * 8] = r < Cr ? kw[p] : z;
+        *(u32x4*)&Qs[r][cc * 8] = r < Cr ? qw[p] : z;
+      }
+    }
+    if (tid < C) {
+      const bool ok = tid < Cr;
+      bt[tid] = ok ? bv : 0.f;
+      // log2 g, held at -100 or above: a gate of exactly 0 would give -inf and, in the
+      // differences of the cumulative sums below, NaN; 2^-100 of the state is far below
+      // fp32 rounding of any other term
+      lg[tid] = ok ? fmaxf(__log2f(gv), -100.f) : 0.f;
+    }
   }
   lds_barrier();
 
