@@ -71,8 +71,14 @@ def parse():
                     help="no persistent V^T copies: every update packs all value rows into the workspace")
     ap.add_argument("--only-update", action="store_true",
                     help="time the headline update and its profiled pass only (for counter passes)")
+    ap.add_argument("--only-diagnostics", action="store_true",
+                    help="only the attention diagnostics on the workload (probe, group masses, total variation), "
+                         "one JSON line, then exit (for profiling the probe kernels)")
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB", default=0,
                     help="only copy a MIB-sized device buffer 5 times (calibrates HBM counters), then exit")
+    ap.add_argument("--summarize-diagnostics", metavar="DIR", default=None,
+                    help="CPU only: turn the rocprofv3 outputs of the --only-diagnostics passes under DIR into "
+                         "profiles/attention_diagnostics_config<N>.md, then exit")
     ap.add_argument("--summarize-profile", metavar="DIR", default=None,
                     help="CPU only: turn the rocprofv3 outputs under DIR (trace/, calib_*/, pmc_*/) into "
                          "profiles/update_stack_config<N>.md and profiles/traffic_config<N>.json, then exit")
@@ -744,15 +750,13 @@ def describe(cfg):
             f"{d.n_k_heads}k/{d.n_v_heads}v x {d.d_k}, chunk {d.chunk}).")
 
 
-def summarize_profile(out_dir, cfg_index):
-    """Writes profiles/update_stack_config<N>.md (kernel durations of the traced update,
-    calibrated HBM bytes per dispatch) and profiles/traffic_config<N>.json (the attention
-    kernel's bytes per launch, with the hash of its sources) from rocprofv3 CSV outputs."""
+def _profile_tables(out_dir):
+    """The kernel-duration table and the copy-calibrated HBM traffic per dispatch (MiB) of
+    the rocprofv3 CSV outputs under out_dir (trace/, calib_*/, pmc_*/), as markdown lines,
+    and the calibrated KiB per dispatch by kernel."""
     import csv
     import re
     import statistics
-    import synth
-    cfg = synth.CONFIGS[cfg_index]
 
     def short(n):
         n = n.replace("tu::(anonymous namespace)::", "").replace("void ", "")
@@ -780,13 +784,7 @@ def summarize_profile(out_dir, cfg_index):
     fr, wr = pmc("FETCH_SIZE"), pmc("WRITE_SIZE")
     fc, wc = calib("FETCH_SIZE"), calib("WRITE_SIZE")
     ff, wf = true_kib / fc, true_kib / wc
-    workload = f"config {cfg.index}: {cfg.name}"
-    out = [f"# Update, {workload}: kernel trace and HBM traffic\n",
-           f"Workload: {describe(cfg)}\n",
-           "Commands (repository root on the GPU host; rocprofv3 run from /tmp with TMPDIR=/tmp; each pass in "
-           "its own process; the last line runs here, on the CPU):\n", "```",
-           PROFILE_COMMANDS.format(c=cfg.index), "```\n",
-           "## Kernel durations (rocprofv3 --kernel-trace --stats, every dispatch of the traced command)\n",
+    out = ["## Kernel durations (rocprofv3 --kernel-trace --stats, every dispatch of the traced command)\n",
            "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
     for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
         out.append(f"| {short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
@@ -797,6 +795,24 @@ def summarize_profile(out_dir, cfg_index):
             "are scaled by those factors.\n", "| kernel | read MiB | written MiB |", "|---|---|---|"]
     for k in sorted(fr, key=lambda k: -fr[k]):
         out.append(f"| {k} | {fr[k] * ff / 1024:.2f} | {wr.get(k, 0) * wf / 1024:.2f} |")
+    read_kib = {k: v * ff for k, v in fr.items()}
+    written_kib = {k: v * wf for k, v in wr.items()}
+    return out, read_kib, written_kib, (ff, wf)
+
+
+def summarize_profile(out_dir, cfg_index):
+    """Writes profiles/update_stack_config<N>.md (kernel durations of the traced update,
+    calibrated HBM bytes per dispatch) and profiles/traffic_config<N>.json (the attention
+    kernel's bytes per launch, with the hash of its sources) from rocprofv3 CSV outputs."""
+    import synth
+    cfg = synth.CONFIGS[cfg_index]
+    tables, read_kib, written_kib, (ff, wf) = _profile_tables(out_dir)
+    workload = f"config {cfg.index}: {cfg.name}"
+    out = [f"# Update, {workload}: kernel trace and HBM traffic\n",
+           f"Workload: {describe(cfg)}\n",
+           "Commands (repository root on the GPU host; rocprofv3 run from /tmp with TMPDIR=/tmp; each pass in "
+           "its own process; the last line runs here, on the CPU):\n", "```",
+           PROFILE_COMMANDS.format(c=cfg.index), "```\n"] + tables
     blog = os.path.join(out_dir, "trace_bench.log")
     if os.path.exists(blog):
         lines = [l for l in open(blog) if l.startswith("{")]
@@ -806,14 +822,54 @@ def summarize_profile(out_dir, cfg_index):
     with open(os.path.join(ROOT, md), "w") as f:
         f.write("\n".join(out) + "\n")
     sym = KERNEL_SYMBOL["attention"]
-    if sym in fr and sym in wr:
+    if sym in read_kib and sym in written_kib:
         rec = {"workload": workload, "kernel": "attention", "kernel_symbol": sym,
                "sources": KERNEL_SOURCES["attention"], "sources_sha256": sources_sha256(KERNEL_SOURCES["attention"]),
-               "fetch_bytes_per_launch": int(fr[sym] * ff * 1024), "write_bytes_per_launch": int(wr[sym] * wf * 1024),
+               "fetch_bytes_per_launch": int(read_kib[sym] * 1024), "write_bytes_per_launch": int(written_kib[sym] * 1024),
                "calibration": {"fetch_factor": round(ff, 4), "write_factor": round(wf, 4)}, "summary": md}
         with open(os.path.join(ROOT, "profiles", f"traffic_config{cfg.index}.json"), "w") as f:
             json.dump(rec, f, indent=1)
     print("\n".join(out[:40]))
+
+
+DIAGNOSTICS_COMMANDS = """\
+python3 <repo>/bench.py --config {c} --only-diagnostics --steps 5
+rocprofv3 --kernel-trace --stats -f csv -d <out>/trace -o run -- python3 <repo>/bench.py --config {c} --only-diagnostics --steps 5
+rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/calib_FETCH_SIZE -o run -- python3 <repo>/bench.py --calibrate-copy 256
+rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/pmc_FETCH_SIZE -o run -- python3 <repo>/bench.py --config {c} --only-diagnostics --steps 2
+rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/calib_WRITE_SIZE -o run -- python3 <repo>/bench.py --calibrate-copy 256
+rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/pmc_WRITE_SIZE -o run -- python3 <repo>/bench.py --config {c} --only-diagnostics --steps 2
+python3 <repo>/bench.py --config {c} --summarize-diagnostics <out>"""
+
+
+def summarize_diagnostics(out_dir, cfg_index):
+    """Writes profiles/attention_diagnostics_config<N>.md: the kernel durations and
+    calibrated HBM bytes per dispatch of the attention diagnostics (bench --only-diagnostics),
+    with the row of the plain run (<out>/plain.log) and each score pass's key bytes."""
+    import synth
+    cfg = synth.CONFIGS[cfg_index]
+    a = cfg.attn
+    tables, read_kib, written_kib, _ = _profile_tables(out_dir)
+    workload = f"config {cfg.index}: {cfg.name}"
+    plog = os.path.join(out_dir, "plain.log")
+    plain = [l for l in open(plog) if l.startswith("{")] if os.path.exists(plog) else []
+    live = json.loads(plain[-1])["attention_diagnostics"]["live_rows"] if plain else cfg.L_old
+    key_mib = live * a.n_kv_heads * a.head_dim * 2 / 2 ** 20
+    out = [f"# Attention diagnostics, {workload}: kernel trace and HBM traffic\n",
+           f"Workload: {describe(cfg)} The diagnostics follow the first round: the probe of the last 8 tail rows "
+           "of each of the attention layers (one call per layer), the masses of 390-position memory groups and the "
+           "total variation between the first and the last attention layer's probes.\n",
+           f"Each score pass (`k_probe_part`, `k_probe_keysum`) reads one layer's key cache: {key_mib:.1f} MiB "
+           f"({live:,} live rows, all KV heads, bf16).\n",
+           "Commands (repository root on the GPU host; rocprofv3 run from /tmp with TMPDIR=/tmp; each pass in "
+           "its own process; the last line runs here, on the CPU):\n", "```",
+           DIAGNOSTICS_COMMANDS.format(c=cfg.index), "```\n"] + tables
+    if plain:
+        out += ["\n## Row of the plain run\n", "```json", plain[-1].strip(), "```"]
+    md = f"profiles/attention_diagnostics_config{cfg.index}.md"
+    with open(os.path.join(ROOT, md), "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("\n".join(out))
 
 
 # ----------------------------------------------------------------------------- one workload
@@ -1012,6 +1068,9 @@ def main():
     if args.summarize_profile:
         summarize_profile(args.summarize_profile, args.config)
         return
+    if args.summarize_diagnostics:
+        summarize_diagnostics(args.summarize_diagnostics, args.config)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; the update of one context does not "
                                    "span devices here (--gpus 1)"}))
@@ -1035,6 +1094,14 @@ def main():
                             kv_splits=args.kv_splits)
     delta_p = tu.delta_params(d.n_k_heads, d.n_v_heads, d.d_k, d.d_v, d.chunk, d.scale)
     W, K = args.warmup, args.steps
+    if args.only_diagnostics:
+        sc, chars, rounds, layers, _ = build_workload(cfg, args.seed, dev, tu)
+        if not cfg.layer_kinds().count("attn") or len(chars) != 1:
+            print(json.dumps({"error": "the diagnostics need one context with attention layers"}))
+            sys.exit(2)
+        row = diagnostics_row(tu, cfg, chars, rounds, layers, attn_p, delta_p, dev, K)
+        print(json.dumps({"config": f"config {cfg.index}: {cfg.name}", "attention_diagnostics": row}), flush=True)
+        return
     refill_steps = 0 if (args.no_refill or args.only_update) else args.refill_steps
     m = measure_update(tu, cfg, args.seed, dev, attn_p, delta_p, W, K, refill_steps, keep=not args.only_update)
     upd_ms, round_ms, kern, refill, sumT = m["upd_ms"], m["round_ms"], m["kern"], m["refill"], m["sumT"]
@@ -1166,6 +1233,62 @@ def main():
     print(json.dumps(line), flush=True)
 
 
+def diagnostics_row(tu, cfg, chars, rounds, layers, attn_p, delta_p, dev, K):
+    """Attention diagnostics (Section 5.3) after the workload's first round: the float32
+    reference-softmax probe of the last eight tail rows of every attention layer (averaged
+    over layers), masses of 390-token memory groups with the effective group count, and
+    the total variation between the probes of the first and the last attention layer.
+    GPU time of the library's launches over K repetitions."""
+    import torch
+    a = cfg.attn
+    (ctxs, own) = make_copy(tu, chars, layers, dev)
+    up = round_updates(tu, ctxs, own, layers, rounds[:1], attn_p, delta_p)
+    wsd = torch.empty(up[0].workspace_size(), dtype=torch.uint8, device=dev)
+    run_step(up, wsd)
+    torch.cuda.synchronize()
+    ctx = ctxs[0]
+    n_probe = min(8, ctx.len)
+    att = [(L, O) for L, O in zip(layers, own) if L["kind"] == "attn"]
+    qs = [rounds[0]["inputs"][i]["q"][-n_probe:].contiguous() for i, L in enumerate(layers) if L["kind"] == "attn"]
+    probs = torch.zeros(ctx.len, dtype=torch.float32, device=dev)
+    pws = torch.empty(lib_probe_ws(tu, attn_p, ctx.len, n_probe), dtype=torch.uint8, device=dev)
+    first = torch.zeros_like(probs)
+    last = torch.zeros_like(probs)
+
+    def probe_all():
+        probs.zero_()
+        for (L, O), q in zip(att, qs):
+            tu.attention_probe(ctx, O["caches"][0][0], attn_p, q, probs, weight=1.0 / len(att), workspace=pws)
+    probe_all()
+    tu.attention_probe(ctx, att[0][1]["caches"][0][0], attn_p, qs[0], first, workspace=pws)
+    tu.attention_probe(ctx, att[-1][1]["caches"][0][0], attn_p, qs[-1], last, workspace=pws)
+    groups = [(g, min(g + 390, ctx.next_pos)) for g in range(0, ctx.next_pos, 390)]
+    gws = torch.empty(1 << 20, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    tu.profile_enable(True)      # GPU time of the library's launches (HIP events on the stream)
+    for _ in range(K):
+        probe_all()
+        mass, win, summary = tu.attention_group_mass(ctx, probs, groups, window=8, workspace=gws)
+        tv = tu.attention_tv_distance(first, last, workspace=gws)
+    dp = tu.profile_collect()
+    tu.profile_enable(False)
+    probe_ms = dp["probe"][1] / K
+    group_ms = dp["group_mass"][1] / K
+    tv_ms = dp["tv_distance"][1] / K
+    kbytes = ctx.len * a.n_kv_heads * a.head_dim * 2 * len(att)
+    s = summary.cpu().tolist()
+    row = {
+        "probe_rows": n_probe, "layers": len(att), "live_rows": ctx.len, "probe_ms": round(probe_ms, 5),
+        "probe_key_bytes": kbytes, "bound": "hbm",
+        "achieved": round(kbytes / (probe_ms / 1e3) / 1e9, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
+        "groups": len(groups), "group_mass_ms": round(group_ms, 5), "tv_ms": round(tv_ms, 5),
+        "memory_mass": round(s[0], 6), "effective_group_count": round(s[1], 3), "window_share": round(s[2], 5),
+        "tv_first_last_attention_layer": round(float(tv[0]), 6) if len(att) > 1 else None,
+        "timing": "GPU time of the library's launches (HIP events around each launch)"}
+    del ctxs, own, up, wsd, pws, gws
+    return row
+
+
 def headline_extras(tu, args, cfg, m, attn_p, delta_p, dev):
     """Rows measured on the headline workload's shapes: delimiter removal after prefill,
     the slot-preserving and tail-and-relocate placements, the attention diagnostics and the
@@ -1260,58 +1383,11 @@ def headline_extras(tu, args, cfg, m, attn_p, delta_p, dev):
         extra["placement"] = place_row
         print(f"[bench] placements: {json.dumps(place_row)}", file=sys.stderr, flush=True)
 
-    # ---- attention diagnostics (Section 5.3): float32 reference-softmax probe of the last
-    # eight tail rows of every attention layer (averaged over layers), masses of 390-token
-    # memory groups with the effective group count, and the total variation between the
-    # probes of the first and the last attention layer, after the first round
+    # ---- attention diagnostics (Section 5.3)
     if kinds.count("attn") and len(chars) == 1:
-        (ctxs, own) = make_copy(tu, chars, layers, dev)
-        up = round_updates(tu, ctxs, own, layers, rounds[:1], attn_p, delta_p)
-        wsd = torch.empty(up[0].workspace_size(), dtype=torch.uint8, device=dev)
-        run_step(up, wsd)
-        torch.cuda.synchronize()
-        ctx = ctxs[0]
-        n_probe = min(8, ctx.len)
-        att = [(L, O) for L, O in zip(layers, own) if L["kind"] == "attn"]
-        qs = [rounds[0]["inputs"][i]["q"][-n_probe:].contiguous() for i, L in enumerate(layers) if L["kind"] == "attn"]
-        probs = torch.zeros(ctx.len, dtype=torch.float32, device=dev)
-        pws = torch.empty(lib_probe_ws(tu, attn_p, ctx.len, n_probe), dtype=torch.uint8, device=dev)
-        first = torch.zeros_like(probs)
-        last = torch.zeros_like(probs)
-
-        def probe_all():
-            probs.zero_()
-            for (L, O), q in zip(att, qs):
-                tu.attention_probe(ctx, O["caches"][0][0], attn_p, q, probs, weight=1.0 / len(att), workspace=pws)
-        probe_all()
-        tu.attention_probe(ctx, att[0][1]["caches"][0][0], attn_p, qs[0], first, workspace=pws)
-        tu.attention_probe(ctx, att[-1][1]["caches"][0][0], attn_p, qs[-1], last, workspace=pws)
-        groups = [(g, min(g + 390, ctx.next_pos)) for g in range(0, ctx.next_pos, 390)]
-        gws = torch.empty(1 << 20, dtype=torch.uint8, device=dev)
-        torch.cuda.synchronize()
-        tu.profile_enable(True)      # GPU time of the library's launches (HIP events on the stream)
-        for _ in range(K):
-            probe_all()
-            mass, win, summary = tu.attention_group_mass(ctx, probs, groups, window=8, workspace=gws)
-            tv = tu.attention_tv_distance(first, last, workspace=gws)
-        dp = tu.profile_collect()
-        tu.profile_enable(False)
-        probe_ms = dp["probe"][1] / K
-        group_ms = dp["group_mass"][1] / K
-        tv_ms = dp["tv_distance"][1] / K
-        kbytes = ctx.len * a.n_kv_heads * a.head_dim * 2 * len(att)
-        s = summary.cpu().tolist()
-        extra["attention_diagnostics"] = {
-            "probe_rows": n_probe, "layers": len(att), "live_rows": ctx.len, "probe_ms": round(probe_ms, 5),
-            "probe_key_bytes": kbytes, "bound": "hbm",
-            "achieved": round(kbytes / (probe_ms / 1e3) / 1e9, 1), "unit": "GB/s", "peak": HBM_PEAK_GBS,
-            "groups": len(groups), "group_mass_ms": round(group_ms, 5), "tv_ms": round(tv_ms, 5),
-            "memory_mass": round(s[0], 6), "effective_group_count": round(s[1], 3), "window_share": round(s[2], 5),
-            "tv_first_last_attention_layer": round(float(tv[0]), 6) if len(att) > 1 else None,
-            "timing": "GPU time of the library's launches (HIP events around each launch)"}
+        extra["attention_diagnostics"] = diagnostics_row(tu, cfg, chars, rounds, layers, attn_p, delta_p, dev, K)
         print(f"[bench] attention diagnostics: {json.dumps(extra['attention_diagnostics'])}", file=sys.stderr,
               flush=True)
-        del ctxs, own, up, wsd, pws, gws
 
     # ---- the short-convolution continuation of one delta layer's q, k, v (width 4, SiLU)
     if kinds.count("delta"):

@@ -1665,7 +1665,7 @@ int attention_probe(const tu_seq* seq, const void* k_cache, const tu_attn_params
 }
 
 static int group_blocks(int64_t len) {
-  return (int)std::max<int64_t>(1, (len + kGroupRowsPerBlock - 1) / kGroupRowsPerBlock);
+  return (int)std::min<int64_t>(kGroupMaxBlocks, std::max<int64_t>(1, (len + kGroupMinRows - 1) / kGroupMinRows));
 }
 
 size_t attention_group_mass_workspace_size(int64_t len, int32_t n_groups) {
@@ -1705,6 +1705,7 @@ int attention_group_mass(const tu_seq* seq, const float* probs, const int64_t* g
   a.n_total = n_groups;
   a.window = window;
   a.n_blocks = group_blocks(seq->len);
+  a.block_rows = (int32_t)(((seq->len + a.n_blocks - 1) / a.n_blocks + 255) / 256 * 256);
   for (int g0 = 0; g0 < n_groups; g0 += kMaxGroupsPerLaunch) {
     a.g_begin = g0;
     a.n = std::min(kMaxGroupsPerLaunch, n_groups - g0);

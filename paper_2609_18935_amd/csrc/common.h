@@ -342,7 +342,8 @@ struct ProbeArgs {
 };
 
 constexpr int kMaxGroupsPerLaunch = 256;
-constexpr int kGroupRowsPerBlock = 8192;   // rows of one group-mass workgroup
+constexpr int kGroupMinRows = 1024;      // rows of one group-mass workgroup, at least
+constexpr int kGroupMaxBlocks = 256;     // group-mass workgroups of a launch, at most
 struct GroupArgs {
   int32_t range[kMaxGroupsPerLaunch][2];   // this launch's groups: sorted, disjoint position ranges
   const int32_t* pos;    // d_pos
@@ -356,7 +357,8 @@ struct GroupArgs {
   int32_t g_begin;       // index of its first group
   int32_t n_total;
   int32_t window;
-  int32_t n_blocks;      // ceil(len / kGroupRowsPerBlock), at least 1
+  int32_t n_blocks;      // workgroups: min(kGroupMaxBlocks, ceil(len / kGroupMinRows)), at least 1
+  int32_t block_rows;    // rows of one workgroup, a multiple of 256; n_blocks * block_rows >= len
 };
 
 constexpr int kTvRowsPerBlock = 4096;

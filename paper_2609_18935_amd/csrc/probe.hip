@@ -308,52 +308,70 @@ __global__ __launch_bounds__(kThreads) void k_probe_mean(ProbeArgs a) {
 }
 
 // Group masses, in a fixed summation order (the same bits on every run): workgroup b
-// takes rows [b * kGroupRowsPerBlock, ...) in rounds of 256; a row adds its probability
-// to the group holding its position (binary search over this launch's sorted group
-// ranges) and to the group's boundary window. Within a wave the rows of one group are
-// summed by a butterfly; each wave accumulates its rounds in order into its own LDS
-// copy of the launch's groups; the four copies are added in wave order and written as
-// the workgroup's partial sums of every group of the launch (zeros included), so no
+// takes rows [b * block_rows, ...) in rounds of 256, its position and probability loads
+// issued together, kGroupBatch rounds at a time; a row adds its probability to the group
+// holding its position (binary search over this launch's sorted group ranges, staged in
+// LDS) and to the group's boundary window. Within a wave the rows of one group are summed
+// by a butterfly; each wave accumulates its rounds in order into its own LDS copy of the
+// launch's groups; the four copies are added in wave order and written as the
+// workgroup's partial sums of every group of the launch (zeros included), so no
 // accumulator needs clearing. k_group_final adds the partials in workgroup order.
+constexpr int kGroupBatch = 4;
 __global__ __launch_bounds__(kThreads) void k_group_mass(GroupArgs a) {
   __shared__ double acc[kThreads / 64][2][kMaxGroupsPerLaunch];
+  __shared__ int32_t rng[kMaxGroupsPerLaunch][2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (int i = tid; i < (kThreads / 64) * 2 * kMaxGroupsPerLaunch; i += kThreads) (&acc[0][0][0])[i] = 0.0;
+  for (int i = tid; i < a.n; i += kThreads) {
+    rng[i][0] = a.range[i][0];
+    rng[i][1] = a.range[i][1];
+  }
   __syncthreads();
-  const int base = blockIdx.x * kGroupRowsPerBlock;
-  for (int r = 0; r < kGroupRowsPerBlock; r += kThreads) {
-    const int j = base + r + tid;
-    int g = -1;
-    double v = 0.0, w = 0.0;
-    if (j < a.len) {
-      const int p = a.pos[j];
-      int lo = 0, hi = a.n - 1;
-      while (lo <= hi) {
-        const int mid = (lo + hi) >> 1;
-        if (a.range[mid][1] <= p) lo = mid + 1;
-        else if (a.range[mid][0] > p) hi = mid - 1;
-        else { g = mid; break; }
-      }
-      if (g >= 0) {
-        v = (double)a.probs[j];
-        w = p < a.range[g][0] + a.window ? v : 0.0;
-      }
+  const int base = blockIdx.x * a.block_rows;
+  for (int r0 = 0; r0 < a.block_rows; r0 += kThreads * kGroupBatch) {
+    int pb[kGroupBatch];
+    float vb[kGroupBatch];
+#pragma unroll
+    for (int u = 0; u < kGroupBatch; ++u) {
+      const int j = min(base + r0 + u * kThreads + tid, a.len - 1);   // rows past len: masked below
+      pb[u] = a.pos[j];
+      vb[u] = a.probs[j];
     }
-    uint64_t left = __ballot(g >= 0);
-    while (left) {
-      const int leader = __builtin_ctzll(left);
-      const int g0 = __shfl(g, leader, 64);
-      const bool mine = g == g0;
-      double s = mine ? v : 0.0, sw = mine ? w : 0.0;
-      for (int o = 32; o > 0; o >>= 1) {
-        s += __shfl_xor(s, o, 64);
-        sw += __shfl_xor(sw, o, 64);
+#pragma unroll
+    for (int u = 0; u < kGroupBatch; ++u) {
+      const int j = base + r0 + u * kThreads + tid;
+      int g = -1;
+      double v = 0.0, w = 0.0;
+      if (r0 + u * kThreads < a.block_rows && j < a.len) {
+        const int p = pb[u];
+        int lo = 0, hi = a.n - 1;
+        while (lo <= hi) {
+          const int mid = (lo + hi) >> 1;
+          if (rng[mid][1] <= p) lo = mid + 1;
+          else if (rng[mid][0] > p) hi = mid - 1;
+          else { g = mid; break; }
+        }
+        if (g >= 0) {
+          v = (double)vb[u];
+          w = p < rng[g][0] + a.window ? v : 0.0;
+        }
       }
-      if (lane == leader) {
-        acc[wave][0][g0] += s;
-        acc[wave][1][g0] += sw;
+      uint64_t left = __ballot(g >= 0);
+      while (left) {
+        const int leader = __builtin_ctzll(left);
+        const int g0 = __shfl(g, leader, 64);
+        const bool mine = g == g0;
+        double s = mine ? v : 0.0, sw = mine ? w : 0.0;
+        for (int o = 32; o > 0; o >>= 1) {
+          s += __shfl_xor(s, o, 64);
+          sw += __shfl_xor(sw, o, 64);
+        }
+        if (lane == leader) {
+          acc[wave][0][g0] += s;
+          acc[wave][1][g0] += sw;
+        }
+        left &= ~__ballot(mine);
       }
-      left &= ~__ballot(mine);
     }
   }
   __syncthreads();
@@ -375,10 +393,18 @@ __global__ __launch_bounds__(kThreads) void k_group_mass(GroupArgs a) {
 __global__ __launch_bounds__(kThreads) void k_group_final(GroupArgs a) {
   __shared__ double shd[kThreads / 64];
   const int n = a.n_total;
-  // group g's mass and window mass: the workgroups' partials in workgroup order
+  // group g's mass and window mass: the workgroups' partials in workgroup order, read
+  // eight at a time (independent loads)
   auto group_sum = [&](int g, int which) {
+    const double* pg = a.partial + (size_t)which * n + g;
     double t = 0.0;
-    for (int b = 0; b < a.n_blocks; ++b) t += a.partial[(size_t)b * 2 * n + (size_t)which * n + g];
+    for (int b0 = 0; b0 < a.n_blocks; b0 += 8) {
+      double x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = b0 + u < a.n_blocks ? pg[(size_t)(b0 + u) * 2 * n] : 0.0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t += x[u];
+    }
     return t;
   };
   double m = 0.0, w = 0.0;

@@ -134,6 +134,34 @@ def test_group_masses_and_summary():
     assert float(mass[20:26].sum()) == 0.0      # groups of removed positions hold no rows
 
 
+def test_group_masses_many_workgroups():
+    """300,001 rows in shuffled position order (every group-mass workgroup takes several
+    rounds, the launch its maximum number of workgroups), 300 groups over part of the
+    positions (two launches of groups), window 5: against the
+    oracle, and the same bits on a second call."""
+    rng = np.random.default_rng(60)
+    n = 300_001
+    pos = rng.permutation(n).astype(np.int64) + 7          # one live run, rows in shuffled order
+    ctx = tu.Context(n, device=DEV)
+    ctx.pos[:n] = torch.from_numpy(pos.astype(np.int32)).to(DEV)
+    ctx.set_metadata([(7, n + 7)], n + 7)
+    x = rng.random(n)
+    x = (x / x.sum()).astype(np.float32)
+    cuts = np.sort(rng.choice(np.arange(0, n + 20), size=600, replace=False))
+    groups = [(int(cuts[2 * g]), int(cuts[2 * g + 1])) for g in range(300)]
+    _say(f"group masses of {len(groups)} groups over {n} shuffled rows")
+    p_dev = torch.from_numpy(x).to(DEV)
+    mass, win, summary = tu.attention_group_mass(ctx, p_dev, groups, window=5)
+    mass2, win2, summary2 = tu.attention_group_mass(ctx, p_dev, groups, window=5)
+    torch.cuda.synchronize()
+    m_ref, w_ref = oracle.group_masses(x, pos, groups, window=5)
+    _close(mass.cpu().numpy().astype(np.float64), m_ref, "group masses, many workgroups")
+    _close(win.cpu().numpy().astype(np.float64), w_ref, "boundary-window masses, many workgroups")
+    s_ref = np.array(oracle.group_summary(m_ref, w_ref))
+    _close(summary.cpu().numpy().astype(np.float64), s_ref, "summary, many workgroups")
+    assert torch.equal(mass, mass2) and torch.equal(win, win2) and torch.equal(summary, summary2)
+
+
 def test_total_variation():
     ranges = np.array([[700, 828]])
     ctx_a, kc_a, q_a, ref_a = _updated_layer(32, 0, 2400, ranges, 150)
