@@ -393,23 +393,48 @@ __global__ __launch_bounds__(kThreads) void k_group_mass(GroupArgs a) {
 __global__ __launch_bounds__(kThreads) void k_group_final(GroupArgs a) {
   __shared__ double shd[kThreads / 64];
   const int n = a.n_total;
-  // group g's mass and window mass: the workgroups' partials in workgroup order, read
-  // eight at a time (independent loads)
-  auto group_sum = [&](int g, int which) {
-    const double* pg = a.partial + (size_t)which * n + g;
-    double t = 0.0;
+  // group g's mass and window mass together: the workgroups' partials in workgroup order,
+  // eight workgroups' pairs at a time (independent loads)
+  auto group_sums = [&](int g, double& m, double& w) {
+    const double* pg = a.partial + g;
+    m = 0.0;
+    w = 0.0;
     for (int b0 = 0; b0 < a.n_blocks; b0 += 8) {
-      double x[8];
+      double x[8], y[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) x[u] = b0 + u < a.n_blocks ? pg[(size_t)(b0 + u) * 2 * n] : 0.0;
+      for (int u = 0; u < 8; ++u) {
+        const bool in = b0 + u < a.n_blocks;
+        x[u] = in ? pg[(size_t)(b0 + u) * 2 * n] : 0.0;
+        y[u] = in ? pg[(size_t)(b0 + u) * 2 * n + n] : 0.0;
+      }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) t += x[u];
+      for (int u = 0; u < 8; ++u) {
+        m += x[u];
+        w += y[u];
+      }
     }
-    return t;
   };
+  // a thread's first kKeep groups keep their masses in registers for the entropy sum
+  constexpr int kKeep = 4;
+  double keep[kKeep];
   double m = 0.0, w = 0.0;
-  for (int g = threadIdx.x; g < n; g += kThreads) {
-    const double mg = group_sum(g, 0), wg = group_sum(g, 1);
+#pragma unroll
+  for (int i = 0; i < kKeep; ++i) {
+    const int g = threadIdx.x + i * kThreads;
+    keep[i] = 0.0;
+    if (g < n) {
+      double mg, wg;
+      group_sums(g, mg, wg);
+      keep[i] = mg;
+      m += mg;
+      w += wg;
+      a.mass[g] = (float)mg;
+      if (a.window_mass) a.window_mass[g] = (float)wg;
+    }
+  }
+  for (int g = threadIdx.x + kKeep * kThreads; g < n; g += kThreads) {
+    double mg, wg;
+    group_sums(g, mg, wg);
     m += mg;
     w += wg;
     a.mass[g] = (float)mg;
@@ -418,9 +443,17 @@ __global__ __launch_bounds__(kThreads) void k_group_final(GroupArgs a) {
   const double M = block_reduce_sum(m, shd);
   const double W = block_reduce_sum(w, shd);
   double h = 0.0;
-  for (int g = threadIdx.x; g < n; g += kThreads) {
-    const double x = M > 0.0 ? group_sum(g, 0) / M : 0.0;
+  auto add_entropy = [&](double mg) {
+    const double x = M > 0.0 ? mg / M : 0.0;
     if (x > 0.0) h -= x * log(x);
+  };
+#pragma unroll
+  for (int i = 0; i < kKeep; ++i)
+    if (threadIdx.x + i * kThreads < n) add_entropy(keep[i]);
+  for (int g = threadIdx.x + kKeep * kThreads; g < n; g += kThreads) {
+    double mg, wg;
+    group_sums(g, mg, wg);
+    add_entropy(mg);
   }
   const double H = block_reduce_sum(h, shd);
   if (threadIdx.x == 0 && a.summary) {
@@ -434,14 +467,25 @@ __global__ __launch_bounds__(kThreads) void k_group_final(GroupArgs a) {
 // order), then one workgroup adds the partials in order.
 __global__ __launch_bounds__(kThreads) void k_tv_partial(TvArgs a) {
   __shared__ double shd[kThreads / 64];
+  constexpr int PER = kTvRowsPerBlock / kThreads, B = 8;   // rows of a thread, loaded B at a time
+  static_assert(PER % B == 0, "whole batches");
   double s = 0.0;
   const long base = (long)blockIdx.x * kTvRowsPerBlock;
-  for (int e = threadIdx.x; e < kTvRowsPerBlock; e += kThreads) {
-    const long j = base + e;
-    if (j < a.n) {
-      const long k = a.map ? (long)a.map[j] : j;
-      s += fabs((double)a.p[j] - (double)a.q[k]);
+  for (int b0 = 0; b0 < PER; b0 += B) {
+    float pv[B], qv[B];
+    long kv[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const long j = base + (long)(b0 + u) * kThreads + threadIdx.x;
+      const long jj = j < a.n ? j : 0;   // rows past n read row 0 and are not added
+      pv[u] = a.p[jj];
+      kv[u] = a.map ? (long)a.map[jj] : jj;
     }
+#pragma unroll
+    for (int u = 0; u < B; ++u) qv[u] = a.q[kv[u]];
+#pragma unroll
+    for (int u = 0; u < B; ++u)
+      if (base + (long)(b0 + u) * kThreads + threadIdx.x < a.n) s += fabs((double)pv[u] - (double)qv[u]);
   }
   s = block_reduce_sum(s, shd);
   if (threadIdx.x == 0) a.partial[blockIdx.x] = s;
