@@ -26,6 +26,8 @@
 // launch on the caller's stream. One lane polls, with back-off, counters that sit on
 // separate cache lines. Each wait is also bounded: on expiry the item proceeds, the
 // call's status word gets kFaultWait, and every wave exits.
+#include <atomic>
+
 #include "common.h"
 
 namespace tu {
@@ -269,16 +271,18 @@ __global__ __launch_bounds__(kThreads) void k_compact_gather(CompactArgs a) {
 }  // namespace
 
 int compact_max_blocks() {
-  static int cached = -1;
-  if (cached < 0) {
+  static std::atomic<int> cached{-1};   // queried once; calls from several threads may race to fill it
+  int v = cached.load(std::memory_order_relaxed);
+  if (v < 0) {
     int dev = 0, per_cu = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_compact_gather, kThreads, 0) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return 0;
-    cached = per_cu * cus;
+    v = per_cu * cus;
+    cached.store(v, std::memory_order_relaxed);
   }
-  return cached;
+  return v;
 }
 
 hipError_t launch_status_mark(const CallStatus& st, hipStream_t s) {

@@ -12,6 +12,8 @@
 // of exponentials per row, a small kernel combines them into each row's max and sum,
 // and a second pass recomputes the scores, normalises them and sums them over the rows
 // of each key. Every sum is taken in a fixed order (deterministic). HBM-bound.
+#include <atomic>
+
 #include "common.h"
 
 namespace tu {
@@ -500,19 +502,23 @@ __global__ __launch_bounds__(kThreads) void k_tv_final(TvArgs a) {
 }
 
 // A streaming pass: as many workgroups as fit on the chip at once (the kernel's own
-// occupancy, cached per kernel), at most the item count, rounded down to a multiple of
-// the KV head count (item counts are multiples of it).
+// occupancy, queried once per kernel; two per CU if the query fails), at most the item
+// count, rounded down to a multiple of the KV head count (item counts are multiples of
+// it). Any such grid is correct: a workgroup walks the items b, b + grid, ...
 template <void (*kernel)(ProbeArgs)>
 hipError_t launch_stream_pass(int n_items, const ProbeArgs& a, hipStream_t s) {
-  static int slots = -1;
+  static std::atomic<int> cached{-1};
+  int slots = cached.load(std::memory_order_relaxed);
   if (slots < 0) {
     int dev = 0, per_cu = 0, cus = 0;
-    if (hipError_t e = hipGetDevice(&dev); e != hipSuccess) return e;
-    if (hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0); e != hipSuccess)
-      return e;
-    if (hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev); e != hipSuccess)
-      return e;
-    slots = std::max(1, per_cu) * std::max(1, cus);
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && per_cu > 0 && cus > 0) {
+      slots = per_cu * cus;
+      cached.store(slots, std::memory_order_relaxed);
+    } else {
+      slots = 2 * kCus;
+    }
   }
   const int grid = std::max(a.n_kv_heads, std::min(n_items, slots) / a.n_kv_heads * a.n_kv_heads);
   hipLaunchKernelGGL(kernel, dim3(grid), dim3(kThreads), 0, s, a);
