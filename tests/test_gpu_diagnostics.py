@@ -92,6 +92,7 @@ def test_probe_distribution_two_layers(placement):
     (8, 4, 128, 64, 5, 1000),     # 10 rows per KV head: one ragged row tile
     (16, 1, 64, 64, 8, 333),      # 128 rows: four row tiles, two tasks per wave
     (4, 4, 256, 256, 1, 64),      # one row per KV head, one key tile
+    (8, 2, 64, 32, 5, 5),         # every row a probe row: the first sees only row 0
 ])
 def test_probe_shapes(hq, hkv, d, rdim, n, L):
     """Other head shapes on a context with a hole in its positions, keys and queries
@@ -160,6 +161,30 @@ def test_group_masses_many_workgroups():
     s_ref = np.array(oracle.group_summary(m_ref, w_ref))
     _close(summary.cpu().numpy().astype(np.float64), s_ref, "summary, many workgroups")
     assert torch.equal(mass, mass2) and torch.equal(win, win2) and torch.equal(summary, summary2)
+
+
+def test_group_masses_edge_cases():
+    """Window 0 (no boundary window), a group over the hole in the positions (no row), a
+    group past the last position, and rows in no group (memory mass below 1)."""
+    rng = np.random.default_rng(61)
+    n = 700
+    pos = np.concatenate([np.arange(300), np.arange(900, 1300)]).astype(np.int64)
+    ctx = tu.Context(n, device=DEV)
+    ctx.pos[:n] = torch.from_numpy(pos.astype(np.int32)).to(DEV)
+    ctx.set_metadata([(0, 300), (900, 1300)], 1300)
+    x = rng.random(n)
+    x = (x / x.sum()).astype(np.float32)
+    groups = [(10, 120), (300, 900), (905, 1000), (1000, 1250), (1300, 1400)]
+    p_dev = torch.from_numpy(x).to(DEV)
+    mass, win, summary = tu.attention_group_mass(ctx, p_dev, groups, window=0)
+    torch.cuda.synchronize()
+    m_ref, w_ref = oracle.group_masses(x, pos, groups, window=0)
+    _close(mass.cpu().numpy().astype(np.float64), m_ref, "group masses, edge cases")
+    assert float(mass[1]) == 0.0 and float(mass[4]) == 0.0
+    assert float(win.abs().sum()) == 0.0 and float(summary[2]) == 0.0
+    s_ref = np.array(oracle.group_summary(m_ref, w_ref))
+    assert s_ref[0] < 0.95
+    _close(summary.cpu().numpy().astype(np.float64), s_ref, "summary, edge cases")
 
 
 def test_total_variation():
