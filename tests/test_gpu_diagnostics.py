@@ -93,6 +93,7 @@ def test_probe_distribution_two_layers(placement):
     (16, 1, 64, 64, 8, 333),      # 128 rows: four row tiles, two tasks per wave
     (4, 4, 256, 256, 1, 64),      # one row per KV head, one key tile
     (8, 2, 64, 32, 5, 5),         # every row a probe row: the first sees only row 0
+    (16, 2, 128, 128, 10, 700),   # 80 rows per KV head: three row tiles, one wave idle
 ])
 def test_probe_shapes(hq, hkv, d, rdim, n, L):
     """Other head shapes on a context with a hole in its positions, keys and queries
