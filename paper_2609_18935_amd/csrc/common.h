@@ -316,7 +316,7 @@ struct RelocArgs {
 };
 
 // Attention diagnostics: probe of the last n_probe rows of one layer of one context.
-constexpr int kProbeKeys = 64;       // keys per score workgroup
+constexpr int kProbeKeys = 64;       // keys per item of the probe score passes
 constexpr int kProbeMaxRows = 128;   // n_probe x (query heads per KV head)
 struct ProbeArgs {
   const bf16_t* q;       // [n_probe][Hq][D] raw queries of the probe rows
