@@ -1,6 +1,6 @@
 """Seeded randomized GPU parity of stack updates through the C ABI (MI355X only).
 
-Each trial draws one update_layer_stack call: 1-6 contexts of 0-6,000 live rows with
+Each of 48 trials draws one update_layer_stack call: 1-6 contexts of 0-6,000 live rows with
 0-3 removed records each and 0-700 tail tokens, one attention layer of a drawn shape
 (head dims 64, 128, 256; group sizes 4 and 8) and one small delta layer, and either the
 library's own key-range splits or a forced count. The draws cover single- and
@@ -31,7 +31,7 @@ def _gpu():
     tu.lib()
 
 
-@pytest.mark.parametrize("trial", range(12))
+@pytest.mark.parametrize("trial", range(48))
 def test_random_stack_update(trial):
     rng = np.random.default_rng(9000 + trial)
     A = SHAPES[trial % len(SHAPES)]
@@ -42,7 +42,9 @@ def test_random_stack_update(trial):
         L = int(rng.choice([0, int(rng.integers(1, 6001))], p=[0.15, 0.85]))
         iv = synth.initial_intervals(L) if L else []
         n_rec = int(rng.integers(0, 4)) if L > 400 else 0
-        ranges = synth.draw_records(rng, iv, n_rec, (1, 300)) if n_rec else np.zeros((0, 2), np.int64)
+        # records of up to 300 rows, shorter where n_rec of them would not fit
+        ranges = (synth.draw_records(rng, iv, n_rec, (1, min(300, L // (n_rec + 1)))) if n_rec
+                  else np.zeros((0, 2), np.int64))
         T = int(rng.choice([0, int(rng.integers(1, 701))], p=[0.15, 0.85]))
         specs.append((L, ranges, T))
     if all(T == 0 for _, _, T in specs):
