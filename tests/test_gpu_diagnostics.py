@@ -117,6 +117,44 @@ def test_probe_shapes(hq, hkv, d, rdim, n, L):
     _close(got, want, f"probe distribution Hq={hq} Hkv={hkv} D={d} n={n}")
 
 
+@pytest.mark.parametrize("trial", range(12))
+def test_probe_random(trial):
+    """Seeded draws of the probe's shape: KV heads 1-4, group size 1-16 (at most 128 rows
+    per KV head), head dim 64-256 with full or half rotary, 1-16 probe rows, contexts of
+    up to 3,000 rows in 1-4 live runs, queries and keys of scale 0.5-3."""
+    rng = np.random.default_rng(7000 + trial)
+    d = int(rng.choice([64, 128, 256]))
+    rdim = int(rng.choice([d, d // 2]))
+    hkv = int(rng.choice([1, 2, 4]))
+    G = int(rng.choice([1, 2, 4, 8, 16]))
+    n = int(rng.integers(1, min(16, 128 // G) + 1))
+    L = int(rng.integers(n, 3001))
+    runs = int(rng.integers(1, 5))
+    cuts = np.sort(rng.choice(np.arange(1, L), size=min(runs - 1, L - 1), replace=False)) if L > 1 else []
+    sizes = np.diff(np.concatenate([[0], cuts, [L]])).astype(int)
+    pos, iv, at = [], [], 0
+    for r, sz in enumerate(sizes):
+        at += int(rng.integers(0 if r == 0 else 1, 5000))   # a hole before the run (runs never touch)
+        pos.append(np.arange(at, at + sz))
+        iv.append((at, at + int(sz)))
+        at += int(sz)
+    pos = np.concatenate(pos).astype(np.int64)
+    sc = float(rng.uniform(0.5, 3.0))
+    _say(f"probe trial {trial}: Hq={hkv * G} Hkv={hkv} D={d} rotary={rdim} n={n} len={L} runs={len(iv)}")
+    k = synth.to_bf16_bits(rng.normal(0.0, sc, (L, hkv, d)))
+    q = synth.to_bf16_bits(rng.normal(0.0, sc, (n, hkv * G, d)))
+    ctx = tu.Context(L, device=DEV)
+    ctx.pos[:L] = torch.from_numpy(pos.astype(np.int32)).to(DEV)
+    ctx.set_metadata(iv, at)
+    got = torch.zeros(L, dtype=torch.float32, device=DEV)
+    tu.attention_probe(ctx, to_dev_bf16(k), tu.attn_params(hkv * G, hkv, d, rdim, 1.0e6), to_dev_bf16(q), got)
+    torch.cuda.synchronize()
+    want = oracle.probe_distribution(q, pos[-n:], k, rdim, 1.0e6, d ** -0.5)
+    got = got.cpu().numpy().astype(np.float64)
+    assert abs(got.sum() - 1.0) < 1e-4
+    _close(got, want, f"probe distribution, trial {trial}")
+
+
 def test_group_masses_and_summary():
     ranges = np.array([[100, 228]])
     ctx, kc, q, ref = _updated_layer(31, 0, 3000, ranges, 200)
