@@ -155,6 +155,28 @@ def test_probe_random(trial):
     _close(got, want, f"probe distribution, trial {trial}")
 
 
+def test_probe_long_context():
+    """100,003 rows at the 16/2 x 256 attention shape, 8 probe rows: 3,126 (KV head,
+    key tile) items, several per workgroup of the streaming passes, so the prefetch of
+    the next tile and the walk over items run, with a ragged last tile."""
+    rng = np.random.default_rng(62)
+    L, hq, hkv, d, n = 100_003, 16, 2, 256, 8
+    _say(f"probe over {L} rows, Hq={hq} Hkv={hkv} D={d} n={n}")
+    k = synth.to_bf16_bits(rng.normal(0.0, 1.5, (L, hkv, d)))
+    q = synth.to_bf16_bits(rng.normal(0.0, 1.5, (n, hq, d)))
+    pos = np.concatenate([np.arange(40_000), np.arange(40_500, 40_500 + L - 40_000)]).astype(np.int64)
+    ctx = tu.Context(L, device=DEV)
+    ctx.pos[:L] = torch.from_numpy(pos.astype(np.int32)).to(DEV)
+    ctx.set_metadata([(0, 40_000), (40_500, int(pos[-1]) + 1)], int(pos[-1]) + 1)
+    got = torch.zeros(L, dtype=torch.float32, device=DEV)
+    tu.attention_probe(ctx, to_dev_bf16(k), tu.attn_params(hq, hkv, d, d, 1.0e7), to_dev_bf16(q), got)
+    torch.cuda.synchronize()
+    want = oracle.probe_distribution(q, pos[-n:], k, d, 1.0e7, d ** -0.5)
+    got = got.cpu().numpy().astype(np.float64)
+    assert abs(got.sum() - 1.0) < 1e-4
+    _close(got, want, "probe distribution, 100,003 rows")
+
+
 def test_group_masses_and_summary():
     ranges = np.array([[100, 228]])
     ctx, kc, q, ref = _updated_layer(31, 0, 3000, ranges, 200)
