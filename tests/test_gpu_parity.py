@@ -197,7 +197,8 @@ def test_delta_parity(cfg):
 
 
 @pytest.mark.parametrize("d,chunk,T,hk,hv", [(128, 64, 100, 2, 4), (128, 64, 1, 2, 4), (128, 32, 70, 1, 2),
-                                             (128, 16, 33, 1, 1), (64, 64, 129, 2, 2), (64, 16, 50, 1, 2)])
+                                             (128, 16, 33, 1, 1), (64, 64, 129, 2, 2), (64, 16, 50, 1, 2),
+                                             (64, 32, 45, 2, 4)])
 def test_delta_shapes(d, chunk, T, hk, hv):
     shape = synth.DeltaShape(hk, hv, d, d, chunk)
     _say(f"delta shape d={d} chunk={chunk} T={T} Hk={hk} Hv={hv}")
